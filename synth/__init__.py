@@ -1,0 +1,14 @@
+"""Seeded synthetic FluxBin layers (shared by the tests, the oracle's callers and the benchmark).
+
+This package only draws random inputs of the right shapes and distributions. It holds none of the method's
+arithmetic: no reconstruction, no lookup tables, no scale application.
+"""
+from .layers import (  # noqa: F401
+    LayerSpec,
+    SyntheticLayer,
+    CONFIGS,
+    config_layers,
+    make_layer,
+    make_activations,
+    salient_count,
+)

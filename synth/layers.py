@@ -1,0 +1,180 @@
+"""Synthetic Llama-shaped FluxBin layers.
+
+The paper measures on LLaMA-2/3.1 and Qwen3 layers (Sec. 4, App. E.4). No weights or datasets are available, so
+these seeded layers stand in for them, with the same shapes and with the format of Sec. 3.1:
+  * ``signs``      uint32 [Kb, M, W]  canonical packed sign planes B^(k), W = ceil(N/32); bit t of word w is column
+                   32w+t, a set bit means +1. Bits past column N-1 are zero.
+  * ``alpha_r``    uint16 [Kb, M, G_r] fp16 row scales, one per (row, group of g_r columns), G_r = ceil(N/g_r).
+  * ``alpha_c``    uint16 [Kb, N]      fp16 column scales.
+  * ``sal_idx``    int32  [S]          salient column indices, strictly increasing.
+  * ``sal_signs``  uint32 [Ks, M, W]   full-width salient sign planes B_s^(k) (bits off the salient set are random
+                   and must be ignored).
+  * ``alpha_sr``   uint16 [Ks, M, G_s] fp16 salient row scales, one per (row, group of g_s salient columns).
+  * ``alpha_sc``   uint16 [Ks, N]      fp16 full-width salient column scales.
+  * ``x``          uint16 [B, N]       fp16 activations.
+
+Distributions: signs Bernoulli(1/2); row scales fp16(|N(0, 0.05)|); column scales fp16(lognormal(0, 0.3));
+activations fp16(N(0, 1)) with an optional fraction of outlier channels multiplied by 20 before rounding; salient
+columns drawn uniformly without replacement. fp16 values are produced by round-to-nearest-even.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List
+
+import numpy as np
+
+
+def _round_half_up(v: float) -> int:
+    return int(math.floor(v + 0.5))
+
+
+def salient_count(N: int, frac: float) -> int:
+    """Number of salient columns for a fraction of N (fractional counts round half up)."""
+    return _round_half_up(frac * N)
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerSpec:
+    name: str
+    M: int            # output channels (rows of W)
+    N: int            # input channels (columns of W)
+    Kb: int           # global binary bases
+    Ks: int           # salient binary bases
+    mu: int           # LUT sub-vector length (4 or 8)
+    S: int            # number of salient columns
+    g_r: int          # row-scale group (columns) of the global branch
+    g_s: int          # row-scale group (salient columns) of the salient branch
+    outlier_frac: float = 0.0
+    seed: int = 0
+    layer_id: int = 0
+
+    @property
+    def G_r(self) -> int:
+        return -(-self.N // self.g_r)
+
+    @property
+    def G_s(self) -> int:
+        return -(-self.S // self.g_s) if self.S > 0 else 0
+
+    @property
+    def W(self) -> int:
+        return -(-self.N // 32)
+
+    def with_(self, **kw) -> "LayerSpec":
+        return dataclasses.replace(self, **kw)
+
+
+@dataclasses.dataclass
+class SyntheticLayer:
+    spec: LayerSpec
+    signs: np.ndarray
+    alpha_r: np.ndarray
+    alpha_c: np.ndarray
+    sal_idx: np.ndarray
+    sal_signs: np.ndarray
+    alpha_sr: np.ndarray
+    alpha_sc: np.ndarray
+    outliers: np.ndarray
+
+
+def _f16_bits(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(a.astype(np.float16)).view(np.uint16)
+
+
+def _random_sign_words(rng: np.random.Generator, planes: int, M: int, N: int) -> np.ndarray:
+    nbytes = -(-N // 8)
+    W = -(-N // 32)
+    raw = rng.integers(0, 256, size=(planes, M, nbytes), dtype=np.uint8)
+    buf = np.zeros((planes, M, W * 4), dtype=np.uint8)
+    buf[:, :, :nbytes] = raw
+    if N % 8:
+        buf[:, :, nbytes - 1] &= np.uint8((1 << (N % 8)) - 1)
+    return buf.view("<u4").reshape(planes, M, W).astype(np.uint32)
+
+
+def make_layer(spec: LayerSpec) -> SyntheticLayer:
+    """Draw one layer. The draw order is fixed: global signs, alpha_r, alpha_c, salient set, salient signs,
+    alpha_sr, alpha_sc, outlier channels."""
+    rng = np.random.default_rng([spec.seed, spec.layer_id])
+    M, N, Kb, Ks, S = spec.M, spec.N, spec.Kb, spec.Ks, spec.S
+    signs = _random_sign_words(rng, Kb, M, N)
+    alpha_r = _f16_bits(np.abs(rng.normal(0.0, 0.05, size=(Kb, M, spec.G_r))))
+    alpha_c = _f16_bits(rng.lognormal(0.0, 0.3, size=(Kb, N)))
+    sal_idx = np.sort(rng.choice(N, size=S, replace=False)).astype(np.int32) if S > 0 else np.zeros(0, np.int32)
+    sal_signs = _random_sign_words(rng, Ks, M, N)
+    alpha_sr = _f16_bits(np.abs(rng.normal(0.0, 0.05, size=(Ks, M, spec.G_s))))
+    alpha_sc = _f16_bits(rng.lognormal(0.0, 0.3, size=(Ks, N)))
+    n_out = _round_half_up(spec.outlier_frac * N)
+    outliers = np.sort(rng.choice(N, size=n_out, replace=False)).astype(np.int64) if n_out else np.zeros(0, np.int64)
+    return SyntheticLayer(spec, signs, alpha_r, alpha_c, sal_idx, sal_signs, alpha_sr, alpha_sc, outliers)
+
+
+def make_activations(layer: SyntheticLayer, B: int, draw: int = 0) -> np.ndarray:
+    """fp16 activations [B, N] (as uint16 bits); outlier channels scaled by 20 before rounding."""
+    spec = layer.spec
+    rng = np.random.default_rng([spec.seed, spec.layer_id, 1000 + B, draw])
+    x = rng.normal(0.0, 1.0, size=(B, spec.N))
+    if layer.outliers.size:
+        x[:, layer.outliers] *= 20.0
+    return _f16_bits(x)
+
+
+def _attn_mlp(name, M, N, Kb, frac, seed, layer_id, mu=8, g_r=128, outlier_frac=0.0):
+    S = salient_count(N, frac)
+    return LayerSpec(name=name, M=M, N=N, Kb=Kb, Ks=1, mu=mu, S=S, g_r=g_r, g_s=max(S, 1),
+                     outlier_frac=outlier_frac, seed=seed, layer_id=layer_id)
+
+
+def config_layers(cfg: str, g_r: str = "128") -> List[LayerSpec]:
+    """Layers of one workload. ``g_r`` is "128" (one row scale per 128 columns) or "N" (one per row)."""
+    specs = CONFIGS[cfg]["layers"]
+    out = []
+    for s in specs:
+        gr = s.g_r if g_r == "128" else s.N
+        out.append(s.with_(g_r=gr))
+    return out
+
+
+def _build_configs() -> Dict[str, dict]:
+    c = {}
+    c["c1_tiny"] = dict(
+        desc="tiny single linear 512x256 (out x in), 2 bases + 1 salient base on 8 columns, mu=4, batch 1",
+        batches=[1],
+        layers=[LayerSpec("tiny", M=512, N=256, Kb=2, Ks=1, mu=4, S=8, g_r=128, g_s=8, seed=0, layer_id=0)],
+    )
+    c["c2_attn7b"] = dict(
+        desc="Llama-7B attention projection 4096x4096, 2 bases + 1 on 2% salient columns, mu=8, batch 1",
+        batches=[1],
+        layers=[_attn_mlp("attn_proj", 4096, 4096, 2, 0.02, seed=1, layer_id=0)],
+    )
+    c["c3_mlp7b"] = dict(
+        desc="Llama-7B MLP gate/up 11008x4096 and down 4096x11008, 2 bases + 1 on 3% salient, mu=8, batch 1-8",
+        batches=[1, 2, 4, 8],
+        layers=[_attn_mlp("gate_up", 11008, 4096, 2, 0.03, seed=2, layer_id=0),
+                _attn_mlp("down", 4096, 11008, 2, 0.03, seed=2, layer_id=1)],
+    )
+    c["c4_mlp70b"] = dict(
+        desc="70B-shaped MLP up 28672x8192 and down 8192x28672, 3 bases + 1 on 5% salient, mu=8, batch 1, "
+             "0.1% outlier channels x20",
+        batches=[1],
+        layers=[_attn_mlp("up", 28672, 8192, 3, 0.05, seed=3, layer_id=0, outlier_frac=0.001),
+                _attn_mlp("down", 8192, 28672, 3, 0.05, seed=3, layer_id=1, outlier_frac=0.001)],
+    )
+    layers5 = []
+    lid = 0
+    for variant, Kb, frac in (("2b1pct", 2, 0.01), ("3b5pct", 3, 0.05)):
+        for nm, M, N in (("q", 8192, 8192), ("k", 1024, 8192), ("v", 1024, 8192), ("o", 8192, 8192),
+                         ("gate", 28672, 8192), ("up", 28672, 8192), ("down", 8192, 28672)):
+            layers5.append(_attn_mlp(f"{variant}_{nm}", M, N, Kb, frac, seed=4, layer_id=lid, outlier_frac=0.001))
+            lid += 1
+    c["c5_layer70b"] = dict(
+        desc="70B decoder-layer linears (q,k,v,o with GQA, gate, up, down), 2b/1% and 3b/5% hybrid, batch 1/4/16",
+        batches=[1, 4, 16],
+        layers=layers5,
+    )
+    return c
+
+
+CONFIGS = _build_configs()
