@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Benchmark of the FluxBin LUT-GEMV hot path on one MI355X.
+
+Step = one pass of the hot path over one batch: the batch-1 LUT-GEMV of the 70B-shaped MLP layers up (28672x8192,
+out x in) and down (8192x28672), 3 global bases + 1 salient base on 5% of the columns, mu = 8, one row scale per 128
+columns, fp16 activations with 0.1% outlier channels. Synthetic seeded data (no weights are available); inputs are
+packed and resident in HBM before timing. Several packed copies of each layer (> 2x the 256 MB Infinity Cache in
+total) are rotated so that every launch streams its signs from HBM.
+
+value = algorithmic bytes of the K steps / time of the K steps (GB/s). Algorithmic bytes per call:
+  Kb*M*N/8 + Ks*M*S/8 (sign bits) + 2*Kb*M*ceil(N/g_r) + 2*Ks*M*ceil(S/g_s) (fp16 row scales)
+  + 2*Kb*N + 2*Ks*S (fp16 column scales) + 2*S (16-bit salient indices) + 2*B*N (x) + 2*B*M (fp16 y).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "achieved HBM GB/s (% of peak) + µs per LUT-GEMV, batch 1, 4096² and 8192×28672"
+WORKLOAD = ("70B MLP up 28672x8192 + down 8192x28672 (out x in), Kb=3 + Ks=1 on 5% salient columns, mu=8, "
+            "g_r=128, batch 1")
+
+
+def algorithmic_bytes(spec, B: int = 1) -> int:
+    M, N, Kb, Ks, S = spec.M, spec.N, spec.Kb, spec.Ks, spec.S
+    sal = S if Ks > 0 else 0
+    G_r = -(-N // spec.g_r)
+    G_s = -(-S // spec.g_s) if sal else 0
+    return (Kb * M * N // 8 + Ks * M * sal // 8 + 2 * Kb * M * G_r + 2 * Ks * M * G_s + 2 * Kb * N + 2 * Ks * sal
+            + 2 * S + 2 * B * N + 2 * B * M)
+
+
+def lookups(spec, B: int = 1) -> int:
+    return B * spec.M * (spec.Kb * -(-spec.N // spec.mu) + spec.Ks * -(-spec.S // spec.mu))
+
+
+class Bench:
+    def __init__(self, layer_specs, B: int, copies_target_bytes: float):
+        import numpy as np
+        import torch
+        from paper_2608_15602_amd import fluxbin as fb
+        from synth import make_activations, make_layer
+        self.fb = fb
+        self.specs = layer_specs
+        self.B = B
+        self.items = []
+        for spec in layer_specs:
+            L = make_layer(spec)
+            dev = {}
+            for name in ("signs", "alpha_r", "alpha_c", "sal_idx", "sal_signs", "alpha_sr", "alpha_sc"):
+                a = getattr(L, name)
+                dt = {np.dtype(np.uint32): np.int32, np.dtype(np.uint16): np.int16, np.dtype(np.int32): np.int32}[
+                    a.dtype]
+                dev[name] = torch.from_numpy(np.ascontiguousarray(a).view(dt)).cuda()
+            shape = fb.make_shape(spec.M, spec.N, spec.Kb, spec.Ks, spec.mu, spec.g_r, spec.S, spec.g_s)
+            one = fb.fluxbin_pack_query(shape)
+            n_copies = max(1, math.ceil(copies_target_bytes / (one * len(layer_specs))))
+            packs = [fb.fluxbin_pack(shape, dev) for _ in range(n_copies)]
+            del dev
+            x = torch.from_numpy(make_activations(L, B).view(np.float16)).cuda()
+            y = torch.empty(B, spec.M, dtype=torch.float16, device="cuda")
+            ws = fb.make_workspace(packs[0], B)
+            self.items.append(dict(spec=spec, L=L, packs=packs, x=x, y=y, ws=ws,
+                                   bytes=algorithmic_bytes(spec, B), lookups=lookups(spec, B)))
+        torch.cuda.synchronize()
+
+    def launch(self, it, step):
+        p = it["packs"][step % len(it["packs"])]
+        if self.B == 1:
+            self.fb.fluxbin_lut_gemv(p, it["x"][0], y=it["y"][0], workspace=it["ws"])
+        else:
+            self.fb.fluxbin_lut_gemm_smallbatch(p, it["x"], y=it["y"], workspace=it["ws"])
+
+    def run(self, steps: int, warmup: int):
+        import torch
+        for s in range(warmup):
+            for it in self.items:
+                self.launch(it, s)
+        torch.cuda.synchronize()
+        evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+               for _ in self.items]
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        t0.record()
+        for s in range(steps):
+            for li, it in enumerate(self.items):
+                evs[li][s][0].record()
+                self.launch(it, warmup + s)
+                evs[li][s][1].record()
+        t1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        total_ms = t0.elapsed_time(t1)
+        per = []
+        for li, it in enumerate(self.items):
+            ms = [a.elapsed_time(b) for a, b in evs[li]]
+            per.append(sum(ms) / len(ms))
+        return total_ms, per, wall
+
+
+def cpu_baseline(bench, budget_s: float):
+    """The fp64 oracle (explicit reconstruction + matvec, untuned) on a bounded contiguous row sample of each layer;
+    throughput scaled to the same algorithmic bytes per row as the GPU figure."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    done_bytes = 0.0
+    t_total = 0.0
+    parts = []
+    for it in bench.items:
+        spec = it["spec"]
+        x = it["x"].cpu().numpy().view(np.uint16)
+        # one 256-row probe to size the sample to the time budget
+        t = time.perf_counter()
+        oracle.gemv_dense(it["L"], x, row_range=(0, min(256, spec.M)))
+        per_row = (time.perf_counter() - t) / min(256, spec.M)
+        rows = int(min(spec.M, max(256, budget_s / len(bench.items) / per_row)))
+        t = time.perf_counter()
+        oracle.gemv_dense(it["L"], x, row_range=(0, rows))
+        dt = time.perf_counter() - t
+        t_total += dt
+        done_bytes += it["bytes"] * rows / spec.M
+        parts.append(f"{spec.name}: rows 0..{rows - 1} of {spec.M}")
+    return {"value": round(done_bytes / t_total / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": "; ".join(parts) + f" (fp64 reconstruct + matvec, {t_total:.1f} s)"}
+
+
+def small_layer_us(spec, steps=200):
+    """Per-call microseconds of a small layer (4096x4096), launches captured in a HIP graph to take the CPU launch
+    cost out; distinct packed copies rotate so the signs come from HBM."""
+    import torch
+    b = Bench([spec], 1, 512e6)
+    for s in range(5):
+        b.launch(b.items[0], s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for k in range(steps):
+                b.launch(b.items[0], k)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(5):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1000.0 / steps)
+    times.sort()
+    us = times[len(times) // 2]
+    return us, b.items[0]["bytes"]
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--g-r", choices=["128", "N"], default="128")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 per-call figure")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is design-only (DESIGN.md)",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from synth import config_layers
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    print(f"# device {torch.cuda.get_device_name(0)}", file=sys.stderr, flush=True)
+    specs = config_layers("c4_mlp70b", args.g_r)
+    bench = Bench(specs, 1, 600e6)
+    print("# packed " + ", ".join(f"{it['spec'].name} x{len(it['packs'])}" for it in bench.items), file=sys.stderr,
+          flush=True)
+    total_ms, per_ms, wall = bench.run(args.steps, args.warmup)
+    step_bytes = sum(it["bytes"] for it in bench.items)
+    value = step_bytes * args.steps / (total_ms * 1e-3) / 1e9
+    kern_us = [m * 1000.0 for m in per_ms]
+    achieved = step_bytes / (sum(per_ms) * 1e-3) / 1e9
+    per_layer = {}
+    for it, us in zip(bench.items, kern_us):
+        s = it["spec"]
+        per_layer[s.name] = {
+            "shape_out_x_in": f"{s.M}x{s.N}", "us_per_gemv": round(us, 3),
+            "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
+            "pct_of_8TBps": round(100 * it["bytes"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 1),
+            "tflop_eq": round(2.0 * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
+            "bytes": it["bytes"], "lookups": it["lookups"],
+        }
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(total_ms / args.steps, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded Llama-70B-shaped MLP layers; no trained weights)",
+        "config": {"workload": WORKLOAD, "global_batch": 1, "g_r": args.g_r, "layers": per_layer},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "k_gemv_mu8_b1 (per-launch HIP events on the launch stream)",
+                     "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}},
+        "wall_s_timed": round(wall, 3),
+    }
+    if not args.no_small:
+        spec2 = config_layers("c2_attn7b", args.g_r)[0]
+        us, b2 = small_layer_us(spec2)
+        out["config"]["attn_4096x4096_us_per_gemv"] = round(us, 3)
+        out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,209 @@
+/*
+ * fluxbin.h - C ABI of the FluxBin LUT-GEMV hot path on AMD Instinct MI355X (gfx950).
+ *
+ * FluxBin (arXiv 2608.15602) stores a weight matrix W (M output rows x N input columns) as hybrid binary bases
+ * (Sec. 3.1, Eqs. 3 and 9):
+ *
+ *   W-hat = sum_{k<Kb} (alpha_r^(k) alpha_c^(k)^T) .* B^(k)                       global bases
+ *         + sum_{k<Ks} ((B_s^(k) .* Mask) .* (alpha_sr^(k) alpha_sc^(k)^T))          salient refinement
+ *
+ * with B in {-1,+1}, one row scale per (row, group of columns), one column scale per column, and the salient bases
+ * restricted to a set I_sal of salient columns. The hot path computes Y = X W-hat^T for a batch of fp16 activation
+ * rows X (Eq. 10) without dequantizing W: column scales are folded into the activations (Eq. 11), the salient columns
+ * are remapped into a dense block (VCM, Eqs. 12-13), per mu-column sub-vector a table of all 2^mu signed partial sums
+ * of (x * alpha_c) is built (LUT-BSF, Eq. 14), every mu-bit weight pattern indexes its table, and the row scales are
+ * applied to the summed lookups (Eq. 15).
+ *
+ * Conventions for every entry point:
+ *   - fp16 values are IEEE binary16 bit patterns passed as uint16_t.
+ *   - Device pointers are HIP device memory of the current device; host pointers are ordinary host memory.
+ *   - The caller owns every buffer. The library keeps no state between calls and allocates no device memory that
+ *     outlives a call (fluxbin_pack with host inputs stages them in a temporary device buffer).
+ *   - Device work is enqueued on the given stream and is asynchronous; no call synchronizes the device unless stated.
+ *   - Every call validates its arguments on the host before any launch and returns a status; on failure nothing is
+ *     launched and fluxbin_last_error_message() (thread-local) describes the problem.
+ *   - Results are deterministic: the same inputs on the same device give bitwise identical outputs (no float atomics).
+ *   - Calls that share a workspace must not overlap in time (same stream, or ordered by the caller).
+ */
+#ifndef FLUXBIN_H_
+#define FLUXBIN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FLUXBIN_OK = 0,
+  FLUXBIN_ERR_INVALID_ARG = 1,      /* null pointer, inconsistent sizes, unsorted salient set, ... */
+  FLUXBIN_ERR_UNSUPPORTED = 2,      /* valid per the paper but outside what this library implements */
+  FLUXBIN_ERR_BUFFER_TOO_SMALL = 3, /* packed buffer or workspace smaller than the query said */
+  FLUXBIN_ERR_HIP = 4               /* a HIP runtime call failed; the message names it */
+} fluxbin_status;
+
+/* Static description of a status code. Never NULL. */
+const char* fluxbin_status_string(fluxbin_status s);
+/* Detail of the last failed call on this thread ("" if none). Valid until the next call on this thread. */
+const char* fluxbin_last_error_message(void);
+
+/*
+ * Logical shape of one layer (paper notation, Sec. 3.1 and App. C.2).
+ *   M    output channels (rows of W), 1 <= M <= 2^31 - 1.
+ *   N    input channels (columns of W), 1 <= N <= 65535 (salient and activation indices are stored in 16 bits, as in
+ *        App. C.2).
+ *   Kb   global bases, 1..4.            Ks   salient bases, 0..4 (the paper uses Ks = Kb; the hybrid configs here 1).
+ *   mu   LUT sub-vector length, 4 or 8 (Sec. 3.2 and App. E.2 use both; 8 is the paper's default).
+ *   g_r  global row-scale group in columns: one row scale per (row, base, group of g_r consecutive columns)
+ *        ("one row scale per weight group", Sec. 3.1). Supported: a multiple of 128, or g_r >= N (one per row).
+ *   S    number of salient columns, 0..N (N_sal in the paper).
+ *   g_s  salient row-scale group in VCM dense columns: one salient row scale per (row, salient base, group of g_s
+ *        consecutive dense columns). Supported: a multiple of 128, or g_s >= S. Ignored when S == 0 or Ks == 0.
+ */
+typedef struct {
+  int64_t M, N;
+  int32_t Kb, Ks;
+  int32_t mu;
+  int32_t reserved0;
+  int64_t g_r;
+  int64_t S;
+  int64_t g_s;
+} fluxbin_shape;
+
+/*
+ * Canonical (unpacked-layout) weights, read-only, all host or all device (inputs_on_device).
+ *   signs      uint32 [Kb][M][W], W = ceil(N/32): bit t of word w is B^(k)[i, 32w+t] == +1 (a clear bit is -1, the
+ *              (2b-1) map of Eq. 14). Bits past column N-1 are ignored.
+ *   alpha_r    fp16 [Kb][M][G_r], G_r = ceil(N/g_r).
+ *   alpha_c    fp16 [Kb][N].
+ *   sal_idx    int32 [S], strictly increasing, each in [0, N) (I_sal, Eq. 8). May be NULL when S == 0.
+ *   sal_signs  uint32 [Ks][M][W], FULL WIDTH like signs; only the bits of salient columns are read (B_s .* Mask).
+ *   alpha_sr   fp16 [Ks][M][G_s], G_s = ceil(S/g_s).
+ *   alpha_sc   fp16 [Ks][N], FULL WIDTH; the VCM gather (Eq. 13) is done at pack time.
+ * Salient pointers may be NULL when S == 0 or Ks == 0.
+ */
+typedef struct {
+  const uint32_t* signs;
+  const uint16_t* alpha_r;
+  const uint16_t* alpha_c;
+  const int32_t* sal_idx;
+  const uint32_t* sal_signs;
+  const uint16_t* alpha_sr;
+  const uint16_t* alpha_sc;
+  int32_t inputs_on_device; /* 0: host pointers, 1: device pointers */
+} fluxbin_weights;
+
+/*
+ * Packed layer: a POD descriptor of a caller-owned device buffer written by fluxbin_pack. It may be copied freely;
+ * it stays valid as long as the buffer does. The same fields are stored in the buffer's 256-byte header, so the
+ * buffer bytes alone are a serializable artifact (see fluxbin_layer_from_header).
+ */
+typedef struct {
+  fluxbin_shape shape;
+  void* d_base;         /* start of the packed device buffer */
+  uint64_t bytes;       /* its size as returned by fluxbin_pack_query */
+  uint32_t format_version;
+  uint32_t reserved1;
+  /* derived sizes (see PACKED FORMAT below) */
+  int64_t Npad, Sv, NC, NSC, Mp, Gr, Gs, NRP;
+  /* byte offsets of the sections from d_base */
+  uint64_t off_signs, off_rscale, off_colscale, off_xidx, off_chunk_plane, off_sal_idx;
+} fluxbin_layer;
+
+/*
+ * PACKED FORMAT (version 1). Written by fluxbin_pack, read by the GEMV kernels.
+ *
+ * Virtual columns. The global bases' columns and the salient bases' VCM dense columns (Def. VCM, Eq. 12: salient
+ * column t of the dense block is input column I_sal[t]) are laid end to end in chunks of 128 columns:
+ *   Npad = ceil(N/128)*128 and ncg = Npad/128 chunks per global base;
+ *   Sv = ceil(S/128)*128 (0 if S == 0 or Ks == 0) and ncs = Sv/128 chunks per salient base;
+ *   NC = Kb*ncg + Ks*ncs chunks, NSC = ceil(NC/2) super-chunks of two chunks, NCP = 2*NSC (an odd NC gets one
+ *   all-zero pad chunk), V = 128*NCP virtual columns.
+ * Chunk c < Kb*ncg is global base k = c / ncg, input columns ((c % ncg)*128 + r); chunk Kb*ncg <= c < NC is salient
+ * base k = (c - Kb*ncg) / ncs, dense columns t = ((c - Kb*ncg) % ncs)*128 + r, input column I_sal[t]. A virtual column
+ * with no source (r past N, t past S, the pad chunk) has sign bit 0, column scale 0 and activation index 0xFFFF; it
+ * contributes exactly zero.
+ *
+ * Sections (each starts at a multiple of 256 bytes, in this order after the 256-byte header):
+ *   signs       [NSC][2][Mp][16] bytes, Mp = ceil(M/64)*64. Each 16-byte entry is one chunk of one row: 128 sign
+ *               bits, split into sub-vectors of mu bits (bit n of a sub-vector is its n-th column; set = +1).
+ *               mu = 8: slot h of super-chunk sc for row i holds chunk 2*sc + (h XOR [i mod 32 >= 16]); its byte q is
+ *               the chunk's sub-vector u = (q + i) mod 16.
+ *               mu = 4: slot h holds chunk 2*sc + h; its nibble q (byte q/2, low nibble first) is the chunk's
+ *               sub-vector u = (q + i) mod 32.
+ *               Rows i >= M are zero. (The rotation by the row index lets the 32 lanes of a half-wavefront read 32
+ *               different tables at the same step, so every LDS bank is hit once.)
+ *   rscale      fp16 [NRP][Mp], NRP = Kb*G_r + Ks*G_s: plane k*G_r + g holds alpha_r^(k)[:, g]; plane
+ *               Kb*G_r + k*G_s + g holds alpha_sr^(k)[:, g]; rows >= M are zero.
+ *   colscale    fp16 [V]: alpha_c^(k)[j] for global columns, alpha_sc^(k)[I_sal[t]] (= alpha_scd, Eq. 13) for salient
+ *               dense columns, 0 for columns without a source.
+ *   xidx        uint16 [V]: the input column j whose activation the virtual column reads, 0xFFFF for none.
+ *   chunk_plane int32 [NCP]: rscale plane of each chunk (the pad chunk has 0).
+ *   sal_idx     uint16 [max(S,1)]: I_sal as 16-bit indices (App. C.2); a single 0 when S == 0.
+ */
+#define FLUXBIN_FORMAT_VERSION 1u
+#define FLUXBIN_HEADER_BYTES 256u
+
+/* Bytes of the packed buffer for a shape. Host only; validates the shape. */
+fluxbin_status fluxbin_pack_query(const fluxbin_shape* shape, size_t* packed_bytes);
+
+/*
+ * Pack canonical weights into the device format (relayout of the sign planes, VCM extraction of the salient columns
+ * and gather of their column scales, Eqs. 12-13). d_packed: caller-allocated device buffer of at least
+ * fluxbin_pack_query bytes. Fills *out. With host inputs the call copies them to a temporary device buffer and
+ * returns after the packing kernels complete; with device inputs it is asynchronous on `stream`.
+ * The salient index set is validated on the host (host inputs) or copied to the host first (device inputs).
+ */
+fluxbin_status fluxbin_pack(const fluxbin_shape* shape, const fluxbin_weights* w, void* d_packed, size_t packed_bytes,
+                            fluxbin_layer* out, hipStream_t stream);
+
+/* Rebuild a layer descriptor from the 256-byte header of a packed buffer (copied to host memory by the caller) and
+ * the device address where the packed bytes now live. Checks magic, version and sizes. */
+fluxbin_status fluxbin_layer_from_header(const void* header_host, void* d_packed, size_t packed_bytes,
+                                         fluxbin_layer* out);
+
+/*
+ * Workspace for split reductions of one GEMV/GEMM call with batch B (1..16): partial sums of output rows and one
+ * 32-bit counter per row tile. Before its first use the workspace must be zero-filled (fluxbin_workspace_init); every
+ * call leaves the counters at zero again. Calls sharing a workspace must not overlap in time.
+ */
+fluxbin_status fluxbin_workspace_query(const fluxbin_layer* layer, int32_t B, size_t* bytes);
+fluxbin_status fluxbin_workspace_init(void* d_workspace, size_t bytes, hipStream_t stream);
+
+/*
+ * y = W-hat x for one fp16 activation vector (batch 1), Eqs. 10-15.
+ *   d_x  fp16 [N] device.   d_y  [M] device, fp16 (y_is_fp32 = 0) or fp32 (y_is_fp32 = 1); must not alias d_x.
+ * Sums are accumulated in fp32: x*alpha_c is exact in fp32, LUT entries and row sums are fp32, the fp16 output is
+ * rounded to nearest even.
+ */
+fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x, void* d_y, int32_t y_is_fp32,
+                                void* d_workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Y[b, :] = W-hat X[b, :] for b < B (1..16), reading every packed sign word once per call and using it for all B rows
+ * (one set of LUTs per batch row, App. E.2). d_x fp16 with row stride ldx >= N (elements); d_y with row stride
+ * ldy >= M (elements of the output type). B = 1 gives the same result as fluxbin_lut_gemv.
+ */
+fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx,
+                                           void* d_y, int64_t ldy, int32_t y_is_fp32, void* d_workspace,
+                                           size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Test support. fluxbin_debug_indices writes the LUT index p read for every (chunk c < NCP, row i < M, sub-vector
+ * u < 128/mu) into d_p[(c*M + i)*(128/mu) + u] (uint8), extracted from the packed signs by the same device code as the
+ * kernels. fluxbin_unpack_canonical writes the global sign planes back in canonical form [Kb][M][W] (bits past N
+ * zero) and, if d_dense_out is not NULL, the VCM dense salient planes [Ks][M][ceil(S/32)] (bit t of word w is dense
+ * column 32w + t).
+ */
+fluxbin_status fluxbin_debug_indices(const fluxbin_layer* layer, uint8_t* d_p, hipStream_t stream);
+fluxbin_status fluxbin_unpack_canonical(const fluxbin_layer* layer, uint32_t* d_signs_out, uint32_t* d_dense_out,
+                                        hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLUXBIN_H_ */

@@ -84,19 +84,22 @@ def reconstruct_rows(L, r0: int, r1: int) -> np.ndarray:
     return W
 
 
-def gemv_dense(L, x_bits: np.ndarray, rows: Optional[Iterable[int]] = None, block: int = 256) -> np.ndarray:
+def gemv_dense(L, x_bits: np.ndarray, rows: Optional[Iterable[int]] = None, block: int = 256,
+               row_range: Optional[Tuple[int, int]] = None) -> np.ndarray:
     """y*[b, i] = sum_j W-hat[i, j] x[b, j] in float64 (Eq. 10), by explicit reconstruction in row blocks.
 
-    ``rows`` restricts the output to a sorted subset of rows (the result then has one column per listed row)."""
+    ``rows`` restricts the output to a sorted subset of rows (the result then has one column per listed row);
+    ``row_range`` = (r0, r1) to the contiguous rows r0 <= i < r1."""
     x = f16_to_f64(x_bits)
     if x.ndim == 1:
         x = x[None, :]
     M = L.spec.M
     if rows is None:
-        out = np.zeros((x.shape[0], M), dtype=np.float64)
-        for r0 in range(0, M, block):
-            r1 = min(M, r0 + block)
-            out[:, r0:r1] = (reconstruct_rows(L, r0, r1) @ x.T).T
+        lo, hi = row_range if row_range is not None else (0, M)
+        out = np.zeros((x.shape[0], hi - lo), dtype=np.float64)
+        for r0 in range(lo, hi, block):
+            r1 = min(hi, r0 + block)
+            out[:, r0 - lo:r1 - lo] = (reconstruct_rows(L, r0, r1) @ x.T).T
         return out
     rows = np.asarray(list(rows), dtype=np.int64)
     out = np.zeros((x.shape[0], rows.size), dtype=np.float64)

@@ -1,0 +1,395 @@
+// Host side of libfluxbin: argument validation, format sizes, launch planning and the C ABI entry points.
+// Every check runs before any HIP call so that invalid input never reaches a kernel.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "fluxbin_internal.h"
+
+namespace fluxbin {
+
+static thread_local char g_msg[512] = "";
+
+fluxbin_status fail(fluxbin_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_msg, sizeof(g_msg), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+fluxbin_status hip_fail(int err, const char* what) {
+  return fail(FLUXBIN_ERR_HIP, "%s failed: %s", what, hipGetErrorString(static_cast<hipError_t>(err)));
+}
+
+int device_cu_count() {
+  static std::mutex mu;
+  static std::vector<int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  std::lock_guard<std::mutex> lock(mu);
+  if (dev >= static_cast<int>(cache.size())) cache.resize(dev + 1, 0);
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return -1;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+static fluxbin_status check_shape(const fluxbin_shape* s) {
+  if (!s) return fail(FLUXBIN_ERR_INVALID_ARG, "shape is NULL");
+  if (s->M < 1 || s->M > (int64_t(1) << 30))
+    return fail(FLUXBIN_ERR_INVALID_ARG, "M = %lld out of range [1, 2^30]", (long long)s->M);
+  if (s->N < 1) return fail(FLUXBIN_ERR_INVALID_ARG, "N = %lld must be >= 1", (long long)s->N);
+  if (s->N > 65535)
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "N = %lld exceeds 65535 (16-bit column indices)", (long long)s->N);
+  if (s->Kb < 1 || s->Kb > 4) return fail(FLUXBIN_ERR_INVALID_ARG, "Kb = %d out of range [1, 4]", s->Kb);
+  if (s->Ks < 0 || s->Ks > 4) return fail(FLUXBIN_ERR_INVALID_ARG, "Ks = %d out of range [0, 4]", s->Ks);
+  if (s->mu < 1 || s->mu > 16) return fail(FLUXBIN_ERR_INVALID_ARG, "mu = %d out of range", s->mu);
+  if (s->mu != 4 && s->mu != 8) return fail(FLUXBIN_ERR_UNSUPPORTED, "mu = %d (supported: 4, 8)", s->mu);
+  if (s->g_r < 1) return fail(FLUXBIN_ERR_INVALID_ARG, "g_r = %lld must be >= 1", (long long)s->g_r);
+  if (s->g_r < s->N && s->g_r % s->mu != 0)
+    return fail(FLUXBIN_ERR_INVALID_ARG, "g_r = %lld must hold whole sub-vectors of mu = %d", (long long)s->g_r, s->mu);
+  if (s->g_r < s->N && s->g_r % kChunk != 0)
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "g_r = %lld: supported are multiples of 128 or g_r >= N", (long long)s->g_r);
+  if (s->S < 0 || s->S > s->N)
+    return fail(FLUXBIN_ERR_INVALID_ARG, "S = %lld out of range [0, N]", (long long)s->S);
+  if (s->S > 0 && s->Ks > 0) {
+    if (s->g_s < 1) return fail(FLUXBIN_ERR_INVALID_ARG, "g_s = %lld must be >= 1", (long long)s->g_s);
+    if (s->g_s < s->S && s->g_s % s->mu != 0)
+      return fail(FLUXBIN_ERR_INVALID_ARG, "g_s = %lld must hold whole sub-vectors of mu = %d", (long long)s->g_s,
+                  s->mu);
+    if (s->g_s < s->S && s->g_s % kChunk != 0)
+      return fail(FLUXBIN_ERR_UNSUPPORTED, "g_s = %lld: supported are multiples of 128 or g_s >= S",
+                  (long long)s->g_s);
+  }
+  return FLUXBIN_OK;
+}
+
+static void fill_layer(const fluxbin_shape& s, void* d_base, uint64_t bytes, fluxbin_layer* L) {
+  const Derived d = derive(s);
+  const Offsets o = offsets(s, d);
+  std::memset(L, 0, sizeof(*L));
+  L->shape = s;
+  L->d_base = d_base;
+  L->bytes = bytes;
+  L->format_version = FLUXBIN_FORMAT_VERSION;
+  L->Npad = d.Npad;
+  L->Sv = d.Sv;
+  L->NC = d.NC;
+  L->NSC = d.NSC;
+  L->Mp = d.Mp;
+  L->Gr = d.Gr;
+  L->Gs = d.Gs;
+  L->NRP = d.NRP;
+  L->off_signs = o.signs;
+  L->off_rscale = o.rscale;
+  L->off_colscale = o.colscale;
+  L->off_xidx = o.xidx;
+  L->off_chunk_plane = o.chunk_plane;
+  L->off_sal_idx = o.sal_idx;
+}
+
+static fluxbin_status check_layer(const fluxbin_layer* L) {
+  if (!L) return fail(FLUXBIN_ERR_INVALID_ARG, "layer is NULL");
+  if (L->format_version != FLUXBIN_FORMAT_VERSION)
+    return fail(FLUXBIN_ERR_INVALID_ARG, "layer format version %u (expected %u)", L->format_version,
+                FLUXBIN_FORMAT_VERSION);
+  if (!L->d_base) return fail(FLUXBIN_ERR_INVALID_ARG, "layer has no device buffer");
+  fluxbin_status st = check_shape(&L->shape);
+  if (st != FLUXBIN_OK) return st;
+  fluxbin_layer ref;
+  fill_layer(L->shape, L->d_base, L->bytes, &ref);
+  if (std::memcmp(&ref, L, sizeof(ref)) != 0)
+    return fail(FLUXBIN_ERR_INVALID_ARG, "layer descriptor is inconsistent with its shape");
+  if (L->bytes < offsets(L->shape, derive(L->shape)).total)
+    return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "layer buffer is smaller than its format needs");
+  return FLUXBIN_OK;
+}
+
+static int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  return std::atoi(v);
+}
+
+fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
+  const int cus = device_cu_count();
+  if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
+  std::memset(p, 0, sizeof(*p));
+  const int per_cu = env_int("FLUXBIN_BLOCKS_PER_CU", 2);
+  const int64_t target = int64_t(cus) * (per_cu >= 1 && per_cu <= 8 ? per_cu : 2);
+  const int force_generic = env_int("FLUXBIN_GENERIC", 0);
+  const int rpt_env = env_int("FLUXBIN_RPT", 0);
+  p->nt = 256;
+  if (L.shape.mu == 8 && B == 1 && !force_generic) {
+    p->kernel = 0;
+    p->bg = 1;
+    p->n_groups = 1;
+  } else {
+    p->kernel = 1;
+    p->bg = B == 1 ? 1 : (B == 2 ? 2 : 4);
+    p->n_groups = int((B + p->bg - 1) / p->bg);
+    if (p->n_groups == 3) p->n_groups = 4;  // instantiated batch paddings: 1, 2, 4, 8, 16
+  }
+  p->bpad = p->bg * p->n_groups;
+  const int64_t steps = (p->kernel == 0) ? L.NSC : (2 * L.NSC) * p->n_groups;
+  // instantiated rows per thread: 4 only for the batch-1 kernel and the mu=8 generic kernel with <= 2 batch rows
+  const int rpt_max = (p->kernel == 0 || (L.shape.mu == 8 && p->bpad <= 2)) ? 4 : 2;
+  int chosen = 1;
+  if (rpt_env == 1 || rpt_env == 2 || rpt_env == 4) {
+    chosen = rpt_env > rpt_max ? rpt_max : rpt_env;
+  } else {
+    for (int rpt = rpt_max; rpt >= 1; rpt /= 2) {
+      const int64_t tiles = ceil_div(L.shape.M, int64_t(p->nt) * rpt);
+      if (tiles * steps >= 2 * target || rpt == 1) {
+        chosen = rpt;
+        break;
+      }
+    }
+  }
+  p->rpt = chosen;
+  p->rows = p->nt * p->rpt;
+  p->n_tiles = ceil_div(L.shape.M, p->rows);
+  p->units = p->n_tiles * steps;
+  p->blocks = p->units < target ? p->units : target;
+  p->ws_counters_off = 0;
+  p->ws_partials_off = round_up256(uint64_t(p->n_tiles) * 4u);
+  p->ws_bytes = p->ws_partials_off + uint64_t(p->blocks) * 2u * uint64_t(p->rows) * uint64_t(p->bpad) * 4u;
+  return FLUXBIN_OK;
+}
+
+static bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const char* pa = static_cast<const char*>(a);
+  const char* pb = static_cast<const char*>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+// Copies an array to a fresh device allocation (host-input packing path).
+static fluxbin_status stage(const void* h, size_t bytes, void** d, std::vector<void*>& owned) {
+  *d = nullptr;
+  if (!h || bytes == 0) return FLUXBIN_OK;
+  hipError_t e = hipMalloc(d, bytes);
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc (pack staging)");
+  owned.push_back(*d);
+  e = hipMemcpy(*d, h, bytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy (pack staging)");
+  return FLUXBIN_OK;
+}
+
+}  // namespace fluxbin
+
+using namespace fluxbin;
+
+extern "C" {
+
+const char* fluxbin_status_string(fluxbin_status s) {
+  switch (s) {
+    case FLUXBIN_OK: return "ok";
+    case FLUXBIN_ERR_INVALID_ARG: return "invalid argument";
+    case FLUXBIN_ERR_UNSUPPORTED: return "unsupported";
+    case FLUXBIN_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+    case FLUXBIN_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* fluxbin_last_error_message(void) { return g_msg; }
+
+fluxbin_status fluxbin_pack_query(const fluxbin_shape* shape, size_t* packed_bytes) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_shape(shape);
+  if (st != FLUXBIN_OK) return st;
+  if (!packed_bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "packed_bytes is NULL");
+  *packed_bytes = static_cast<size_t>(offsets(*shape, derive(*shape)).total);
+  return FLUXBIN_OK;
+}
+
+fluxbin_status fluxbin_pack(const fluxbin_shape* shape, const fluxbin_weights* w, void* d_packed, size_t packed_bytes,
+                            fluxbin_layer* out, hipStream_t stream) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_shape(shape);
+  if (st != FLUXBIN_OK) return st;
+  if (!w) return fail(FLUXBIN_ERR_INVALID_ARG, "weights is NULL");
+  if (!out) return fail(FLUXBIN_ERR_INVALID_ARG, "out is NULL");
+  if (!d_packed) return fail(FLUXBIN_ERR_INVALID_ARG, "d_packed is NULL");
+  const fluxbin_shape& s = *shape;
+  const Derived d = derive(s);
+  const Offsets o = offsets(s, d);
+  if (packed_bytes < o.total)
+    return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "packed buffer has %zu bytes, needs %llu", packed_bytes,
+                (unsigned long long)o.total);
+  if (!w->signs || !w->alpha_r || !w->alpha_c) return fail(FLUXBIN_ERR_INVALID_ARG, "global weight pointer is NULL");
+  const bool sal = s.S > 0 && s.Ks > 0;
+  if (s.S > 0 && !w->sal_idx) return fail(FLUXBIN_ERR_INVALID_ARG, "sal_idx is NULL with S > 0");
+  if (sal && (!w->sal_signs || !w->alpha_sr || !w->alpha_sc))
+    return fail(FLUXBIN_ERR_INVALID_ARG, "salient weight pointer is NULL with S > 0 and Ks > 0");
+  if (w->inputs_on_device != 0 && w->inputs_on_device != 1)
+    return fail(FLUXBIN_ERR_INVALID_ARG, "inputs_on_device must be 0 or 1");
+
+  const int64_t W = ceil_div(s.N, 32);
+  const size_t n_signs = size_t(s.Kb) * s.M * W * 4;
+  const size_t n_ar = size_t(s.Kb) * s.M * d.Gr * 2;
+  const size_t n_ac = size_t(s.Kb) * s.N * 2;
+  const size_t n_idx = size_t(s.S) * 4;
+  const size_t n_ss = sal ? size_t(s.Ks) * s.M * W * 4 : 0;
+  const size_t n_asr = sal ? size_t(s.Ks) * s.M * d.Gs * 2 : 0;
+  const size_t n_asc = sal ? size_t(s.Ks) * s.N * 2 : 0;
+
+  // The salient set must be strictly increasing and in range: checked on the host before any kernel reads it.
+  std::vector<int32_t> idx(size_t(s.S));
+  if (s.S > 0) {
+    if (w->inputs_on_device) {
+      hipError_t e = hipMemcpyAsync(idx.data(), w->sal_idx, n_idx, hipMemcpyDeviceToHost, stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) return hip_fail(e, "copying sal_idx to the host");
+    } else {
+      std::memcpy(idx.data(), w->sal_idx, n_idx);
+    }
+    for (int64_t t = 0; t < s.S; ++t) {
+      if (idx[t] < 0 || idx[t] >= s.N)
+        return fail(FLUXBIN_ERR_INVALID_ARG, "sal_idx[%lld] = %d out of range [0, N)", (long long)t, idx[t]);
+      if (t > 0 && idx[t] <= idx[t - 1])
+        return fail(FLUXBIN_ERR_INVALID_ARG, "sal_idx is not strictly increasing at %lld", (long long)t);
+    }
+  }
+
+  fluxbin_layer L;
+  fill_layer(s, d_packed, packed_bytes, &L);
+
+  if (w->inputs_on_device) {
+    st = launch_pack(L, *w, w->sal_idx, stream);
+    if (st != FLUXBIN_OK) return st;
+  } else {
+    std::vector<void*> owned;
+    fluxbin_weights dw = *w;
+    void* p = nullptr;
+    auto release = [&]() {
+      for (void* q : owned) (void)hipFree(q);
+    };
+    st = stage(w->signs, n_signs, &p, owned); dw.signs = (const uint32_t*)p;
+    if (st == FLUXBIN_OK) { st = stage(w->alpha_r, n_ar, &p, owned); dw.alpha_r = (const uint16_t*)p; }
+    if (st == FLUXBIN_OK) { st = stage(w->alpha_c, n_ac, &p, owned); dw.alpha_c = (const uint16_t*)p; }
+    if (st == FLUXBIN_OK) { st = stage(w->sal_idx, n_idx, &p, owned); dw.sal_idx = (const int32_t*)p; }
+    if (st == FLUXBIN_OK && sal) { st = stage(w->sal_signs, n_ss, &p, owned); dw.sal_signs = (const uint32_t*)p; }
+    if (st == FLUXBIN_OK && sal) { st = stage(w->alpha_sr, n_asr, &p, owned); dw.alpha_sr = (const uint16_t*)p; }
+    if (st == FLUXBIN_OK && sal) { st = stage(w->alpha_sc, n_asc, &p, owned); dw.alpha_sc = (const uint16_t*)p; }
+    dw.inputs_on_device = 1;
+    if (st == FLUXBIN_OK) st = launch_pack(L, dw, dw.sal_idx, stream);
+    if (st == FLUXBIN_OK) {
+      hipError_t e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) st = hip_fail(e, "hipStreamSynchronize (pack)");
+    } else {
+      (void)hipStreamSynchronize(stream);
+    }
+    release();
+    if (st != FLUXBIN_OK) return st;
+  }
+  *out = L;
+  return FLUXBIN_OK;
+}
+
+fluxbin_status fluxbin_layer_from_header(const void* header_host, void* d_packed, size_t packed_bytes,
+                                         fluxbin_layer* out) {
+  g_msg[0] = 0;
+  if (!header_host || !d_packed || !out) return fail(FLUXBIN_ERR_INVALID_ARG, "NULL argument");
+  Header h;
+  std::memcpy(&h, header_host, sizeof(h));
+  if (h.magic != kMagic) return fail(FLUXBIN_ERR_INVALID_ARG, "bad magic 0x%08x", h.magic);
+  if (h.version != FLUXBIN_FORMAT_VERSION) return fail(FLUXBIN_ERR_UNSUPPORTED, "format version %u", h.version);
+  fluxbin_status st = check_shape(&h.shape);
+  if (st != FLUXBIN_OK) return st;
+  const Derived d = derive(h.shape);
+  const Offsets o = offsets(h.shape, d);
+  if (h.total != o.total || h.off_signs != o.signs || h.NSC != d.NSC || h.Mp != d.Mp)
+    return fail(FLUXBIN_ERR_INVALID_ARG, "header sizes are inconsistent with its shape");
+  if (packed_bytes < o.total) return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "packed buffer is too small");
+  fill_layer(h.shape, d_packed, packed_bytes, out);
+  return FLUXBIN_OK;
+}
+
+fluxbin_status fluxbin_workspace_query(const fluxbin_layer* layer, int32_t B, size_t* bytes) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_layer(layer);
+  if (st != FLUXBIN_OK) return st;
+  if (!bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "bytes is NULL");
+  if (B < 1 || B > kMaxBatch) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, 16]", B);
+  Plan p;
+  st = make_plan(*layer, B, &p);
+  if (st != FLUXBIN_OK) return st;
+  *bytes = static_cast<size_t>(p.ws_bytes);
+  return FLUXBIN_OK;
+}
+
+fluxbin_status fluxbin_workspace_init(void* d_workspace, size_t bytes, hipStream_t stream) {
+  g_msg[0] = 0;
+  if (!d_workspace && bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "workspace is NULL");
+  if (bytes % 4) return fail(FLUXBIN_ERR_INVALID_ARG, "workspace size must be a multiple of 4");
+  if (bytes == 0) return FLUXBIN_OK;
+  return launch_fill_zero(d_workspace, bytes, stream);
+}
+
+static fluxbin_status gemm_common(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx, void* d_y,
+                                  int64_t ldy, int32_t y_is_fp32, void* d_ws, size_t ws_bytes, hipStream_t stream) {
+  fluxbin_status st = check_layer(layer);
+  if (st != FLUXBIN_OK) return st;
+  const fluxbin_shape& s = layer->shape;
+  if (B < 1 || B > kMaxBatch) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, 16]", B);
+  if (!d_x || !d_y) return fail(FLUXBIN_ERR_INVALID_ARG, "x or y is NULL");
+  if (y_is_fp32 != 0 && y_is_fp32 != 1) return fail(FLUXBIN_ERR_INVALID_ARG, "y_is_fp32 must be 0 or 1");
+  if (ldx < s.N) return fail(FLUXBIN_ERR_INVALID_ARG, "ldx = %lld < N", (long long)ldx);
+  if (ldy < s.M) return fail(FLUXBIN_ERR_INVALID_ARG, "ldy = %lld < M", (long long)ldy);
+  const size_t xb = (size_t(B - 1) * ldx + s.N) * 2;
+  const size_t yb = (size_t(B - 1) * ldy + s.M) * (y_is_fp32 ? 4 : 2);
+  if (ranges_overlap(d_x, xb, d_y, yb)) return fail(FLUXBIN_ERR_INVALID_ARG, "x and y overlap");
+  Plan p;
+  st = make_plan(*layer, B, &p);
+  if (st != FLUXBIN_OK) return st;
+  if (!d_ws) return fail(FLUXBIN_ERR_INVALID_ARG, "workspace is NULL");
+  if (ws_bytes < p.ws_bytes)
+    return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "workspace has %zu bytes, needs %llu", ws_bytes,
+                (unsigned long long)p.ws_bytes);
+  if (ranges_overlap(d_ws, ws_bytes, d_y, yb) || ranges_overlap(d_ws, ws_bytes, d_x, xb))
+    return fail(FLUXBIN_ERR_INVALID_ARG, "workspace overlaps x or y");
+  return launch_gemm(*layer, p, B, d_x, ldx, d_y, ldy, y_is_fp32, d_ws, stream);
+}
+
+fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x, void* d_y, int32_t y_is_fp32,
+                                void* d_workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_msg[0] = 0;
+  const int64_t M = layer ? layer->shape.M : 0;
+  const int64_t N = layer ? layer->shape.N : 0;
+  return gemm_common(layer, 1, d_x, N, d_y, M, y_is_fp32, d_workspace, workspace_bytes, stream);
+}
+
+fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx,
+                                           void* d_y, int64_t ldy, int32_t y_is_fp32, void* d_workspace,
+                                           size_t workspace_bytes, hipStream_t stream) {
+  g_msg[0] = 0;
+  return gemm_common(layer, B, d_x, ldx, d_y, ldy, y_is_fp32, d_workspace, workspace_bytes, stream);
+}
+
+fluxbin_status fluxbin_debug_indices(const fluxbin_layer* layer, uint8_t* d_p, hipStream_t stream) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_layer(layer);
+  if (st != FLUXBIN_OK) return st;
+  if (!d_p) return fail(FLUXBIN_ERR_INVALID_ARG, "d_p is NULL");
+  return launch_debug_indices(*layer, d_p, stream);
+}
+
+fluxbin_status fluxbin_unpack_canonical(const fluxbin_layer* layer, uint32_t* d_signs_out, uint32_t* d_dense_out,
+                                        hipStream_t stream) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_layer(layer);
+  if (st != FLUXBIN_OK) return st;
+  if (!d_signs_out) return fail(FLUXBIN_ERR_INVALID_ARG, "d_signs_out is NULL");
+  return launch_unpack(*layer, d_signs_out, d_dense_out, stream);
+}
+
+}  // extern "C"

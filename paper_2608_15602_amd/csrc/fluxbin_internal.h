@@ -1,0 +1,100 @@
+// Internal declarations shared by the host code and the HIP kernels of libfluxbin.
+#pragma once
+
+#include <cstdint>
+#include <cstddef>
+
+#include "fluxbin.h"
+
+namespace fluxbin {
+
+constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes of signs per row)
+constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
+constexpr int kMaxBatch = 16;
+
+struct Derived {
+  int64_t Npad, ncg, Sv, ncs, NC, NSC, NCP, V, Mp, Gr, Gs, NRP;
+};
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline uint64_t round_up256(uint64_t v) { return (v + 255u) & ~uint64_t(255u); }
+
+inline Derived derive(const fluxbin_shape& s) {
+  Derived d{};
+  d.Npad = ceil_div(s.N, kChunk) * kChunk;
+  d.ncg = d.Npad / kChunk;
+  const bool sal = s.S > 0 && s.Ks > 0;
+  d.Sv = sal ? ceil_div(s.S, kChunk) * kChunk : 0;
+  d.ncs = d.Sv / kChunk;
+  d.NC = s.Kb * d.ncg + s.Ks * d.ncs;
+  d.NSC = ceil_div(d.NC, 2);
+  d.NCP = 2 * d.NSC;
+  d.V = kChunk * d.NCP;
+  d.Mp = ceil_div(s.M, 64) * 64;
+  d.Gr = ceil_div(s.N, s.g_r);
+  d.Gs = sal ? ceil_div(s.S, s.g_s) : 0;
+  d.NRP = s.Kb * d.Gr + s.Ks * d.Gs;
+  return d;
+}
+
+struct Offsets {
+  uint64_t signs, rscale, colscale, xidx, chunk_plane, sal_idx, total;
+};
+
+inline Offsets offsets(const fluxbin_shape& s, const Derived& d) {
+  Offsets o{};
+  uint64_t off = FLUXBIN_HEADER_BYTES;
+  o.signs = off;       off += round_up256(uint64_t(d.NSC) * 2u * uint64_t(d.Mp) * 16u);
+  o.rscale = off;      off += round_up256(uint64_t(d.NRP) * uint64_t(d.Mp) * 2u);
+  o.colscale = off;    off += round_up256(uint64_t(d.V) * 2u);
+  o.xidx = off;        off += round_up256(uint64_t(d.V) * 2u);
+  o.chunk_plane = off; off += round_up256(uint64_t(d.NCP) * 4u);
+  o.sal_idx = off;     off += round_up256(uint64_t(s.S > 1 ? s.S : 1) * 2u);
+  o.total = off;
+  return o;
+}
+
+// The 256-byte header at the start of a packed buffer (little-endian, all fields naturally aligned).
+struct Header {
+  uint32_t magic;
+  uint32_t version;
+  fluxbin_shape shape;   // 56 bytes
+  int64_t Npad, Sv, NC, NSC, Mp, Gr, Gs, NRP;
+  uint64_t off_signs, off_rscale, off_colscale, off_xidx, off_chunk_plane, off_sal_idx, total;
+  uint8_t pad[256 - 8 - sizeof(fluxbin_shape) - 8 * 8 - 7 * 8];
+};
+static_assert(sizeof(Header) == 256, "header must be 256 bytes");
+
+// ---- error reporting (thread-local message) ----
+fluxbin_status fail(fluxbin_status s, const char* fmt, ...);
+fluxbin_status hip_fail(int hip_error, const char* what);
+
+// ---- launch plan of the GEMV/GEMM kernels ----
+struct Plan {
+  int kernel;       // 0 = mu8 batch-1 super-chunk kernel, 1 = generic (any mu, any batch)
+  int nt;           // threads per block
+  int rpt;          // rows per thread
+  int rows;         // rows per tile (nt * rpt)
+  int64_t n_tiles;  // ceil(M / rows)
+  int64_t units;    // work units (tile x chunk step [x batch group])
+  int64_t blocks;   // grid size
+  int bg;           // batch rows per LUT group (generic kernel)
+  int n_groups;     // batch groups
+  int bpad;         // bg * n_groups
+  uint64_t ws_counters_off, ws_partials_off, ws_bytes;
+};
+
+fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p);
+
+// ---- launchers (fluxbin_pack.hip, fluxbin_gemv.hip) ----
+fluxbin_status launch_pack(const fluxbin_layer& L, const fluxbin_weights& dev_w, const int32_t* d_sal_idx,
+                           hipStream_t stream);
+fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const uint16_t* d_x, int64_t ldx,
+                           void* d_y, int64_t ldy, int y_fp32, void* d_ws, hipStream_t stream);
+fluxbin_status launch_fill_zero(void* d, size_t bytes, hipStream_t stream);
+fluxbin_status launch_debug_indices(const fluxbin_layer& L, uint8_t* d_p, hipStream_t stream);
+fluxbin_status launch_unpack(const fluxbin_layer& L, uint32_t* d_signs, uint32_t* d_dense, hipStream_t stream);
+
+int device_cu_count();  // CUs of the current device (cached per device), or -1 on a HIP error
+
+}  // namespace fluxbin

@@ -1,0 +1,223 @@
+"""Thin ctypes binding of libfluxbin (include/fluxbin.h): argument marshalling only.
+
+Every step of the hot path runs in the library's HIP kernels; PyTorch only provides device memory and the stream.
+The functions keep the C names. Tensors must be on the current CUDA (HIP) device unless stated otherwise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfluxbin.so")
+
+FLUXBIN_OK = 0
+FLUXBIN_ERR_INVALID_ARG = 1
+FLUXBIN_ERR_UNSUPPORTED = 2
+FLUXBIN_ERR_BUFFER_TOO_SMALL = 3
+FLUXBIN_ERR_HIP = 4
+FORMAT_VERSION = 1
+HEADER_BYTES = 256
+
+# Entry points declared in include/fluxbin.h.
+EXPORTS = (
+    "fluxbin_status_string", "fluxbin_last_error_message", "fluxbin_pack_query", "fluxbin_pack",
+    "fluxbin_layer_from_header", "fluxbin_workspace_query", "fluxbin_workspace_init", "fluxbin_lut_gemv",
+    "fluxbin_lut_gemm_smallbatch", "fluxbin_debug_indices", "fluxbin_unpack_canonical",
+)
+
+
+class FluxbinError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"fluxbin status {status}: {message}")
+        self.status = status
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("Kb", ctypes.c_int32), ("Ks", ctypes.c_int32),
+                ("mu", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("g_r", ctypes.c_int64),
+                ("S", ctypes.c_int64), ("g_s", ctypes.c_int64)]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [("signs", ctypes.c_void_p), ("alpha_r", ctypes.c_void_p), ("alpha_c", ctypes.c_void_p),
+                ("sal_idx", ctypes.c_void_p), ("sal_signs", ctypes.c_void_p), ("alpha_sr", ctypes.c_void_p),
+                ("alpha_sc", ctypes.c_void_p), ("inputs_on_device", ctypes.c_int32)]
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("shape", Shape), ("d_base", ctypes.c_void_p), ("bytes", ctypes.c_uint64),
+                ("format_version", ctypes.c_uint32), ("reserved1", ctypes.c_uint32),
+                ("Npad", ctypes.c_int64), ("Sv", ctypes.c_int64), ("NC", ctypes.c_int64), ("NSC", ctypes.c_int64),
+                ("Mp", ctypes.c_int64), ("Gr", ctypes.c_int64), ("Gs", ctypes.c_int64), ("NRP", ctypes.c_int64),
+                ("off_signs", ctypes.c_uint64), ("off_rscale", ctypes.c_uint64), ("off_colscale", ctypes.c_uint64),
+                ("off_xidx", ctypes.c_uint64), ("off_chunk_plane", ctypes.c_uint64), ("off_sal_idx", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libfluxbin.so (built by ``python -m paper_2608_15602_amd.build``). Raises if it is missing: there is no
+    fallback implementation."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise FluxbinError(-1, f"{LIB_PATH} is missing; build it with `python -m paper_2608_15602_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.fluxbin_status_string.restype = ctypes.c_char_p
+        L.fluxbin_status_string.argtypes = [ctypes.c_int]
+        L.fluxbin_last_error_message.restype = ctypes.c_char_p
+        L.fluxbin_last_error_message.argtypes = []
+        L.fluxbin_pack_query.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(sz)]
+        L.fluxbin_pack.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(Weights), vp, sz, ctypes.POINTER(Layer), vp]
+        L.fluxbin_layer_from_header.argtypes = [vp, vp, sz, ctypes.POINTER(Layer)]
+        L.fluxbin_workspace_query.argtypes = [ctypes.POINTER(Layer), i32, ctypes.POINTER(sz)]
+        L.fluxbin_workspace_init.argtypes = [vp, sz, vp]
+        L.fluxbin_lut_gemv.argtypes = [ctypes.POINTER(Layer), vp, vp, i32, vp, sz, vp]
+        L.fluxbin_lut_gemm_smallbatch.argtypes = [ctypes.POINTER(Layer), i32, vp, i64, vp, i64, i32, vp, sz, vp]
+        L.fluxbin_debug_indices.argtypes = [ctypes.POINTER(Layer), vp, vp]
+        L.fluxbin_unpack_canonical.argtypes = [ctypes.POINTER(Layer), vp, vp, vp]
+        for name in EXPORTS:
+            if name not in ("fluxbin_status_string", "fluxbin_last_error_message"):
+                getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != FLUXBIN_OK:
+        msg = lib().fluxbin_last_error_message().decode(errors="replace")
+        raise FluxbinError(status, msg or lib().fluxbin_status_string(status).decode())
+
+
+def make_shape(M, N, Kb, Ks, mu, g_r, S, g_s) -> Shape:
+    return Shape(int(M), int(N), int(Kb), int(Ks), int(mu), 0, int(g_r), int(S), int(g_s))
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return int(stream) if not hasattr(stream, "cuda_stream") else stream.cuda_stream
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if hasattr(t, "data_ptr"):
+        return t.data_ptr()
+    return t.ctypes.data  # numpy array (host inputs)
+
+
+def fluxbin_pack_query(shape: Shape) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().fluxbin_pack_query(ctypes.byref(shape), ctypes.byref(n)))
+    return n.value
+
+
+class PackedLayer:
+    """A packed device buffer (torch uint8 tensor) and its C descriptor."""
+
+    def __init__(self, buf, layer: Layer):
+        self.buf = buf
+        self.layer = layer
+
+    @property
+    def shape(self) -> Shape:
+        return self.layer.shape
+
+
+def fluxbin_pack(shape: Shape, weights: Dict[str, object], stream=None, device=None) -> PackedLayer:
+    """Pack canonical weights. ``weights`` maps the fluxbin_weights field names to torch tensors on the device (or to
+    numpy arrays in host memory, then all of them must be numpy)."""
+    import torch
+    nbytes = fluxbin_pack_query(shape)
+    on_dev = all(hasattr(v, "data_ptr") for v in weights.values() if v is not None)
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=device or "cuda")
+    keep = {k: (v.contiguous() if hasattr(v, "contiguous") else v) for k, v in weights.items()}
+    w = Weights(_ptr(keep.get("signs")), _ptr(keep.get("alpha_r")), _ptr(keep.get("alpha_c")),
+                _ptr(keep.get("sal_idx")), _ptr(keep.get("sal_signs")), _ptr(keep.get("alpha_sr")),
+                _ptr(keep.get("alpha_sc")), 1 if on_dev else 0)
+    out = Layer()
+    _check(lib().fluxbin_pack(ctypes.byref(shape), ctypes.byref(w), buf.data_ptr(), nbytes, ctypes.byref(out),
+                              _stream(stream)))
+    return PackedLayer(buf, out)
+
+
+def fluxbin_layer_from_header(header: bytes, buf) -> PackedLayer:
+    out = Layer()
+    hb = ctypes.create_string_buffer(bytes(header[:HEADER_BYTES]), HEADER_BYTES)
+    _check(lib().fluxbin_layer_from_header(hb, buf.data_ptr(), buf.numel(), ctypes.byref(out)))
+    return PackedLayer(buf, out)
+
+
+def fluxbin_workspace_query(layer: PackedLayer, B: int = 1) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().fluxbin_workspace_query(ctypes.byref(layer.layer), int(B), ctypes.byref(n)))
+    return n.value
+
+
+def fluxbin_workspace_init(ws, stream=None) -> None:
+    _check(lib().fluxbin_workspace_init(ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def make_workspace(layer: PackedLayer, B: int = 1, stream=None):
+    """Allocate (torch) and zero-fill (library kernel) a workspace for batch B."""
+    import torch
+    n = fluxbin_workspace_query(layer, B)
+    ws = torch.empty(max(256, (n + 255) // 256 * 256), dtype=torch.uint8, device=layer.buf.device)
+    fluxbin_workspace_init(ws, stream)
+    return ws
+
+
+def fluxbin_lut_gemv(layer: PackedLayer, x, y=None, out_fp32: bool = False, workspace=None, stream=None):
+    import torch
+    M = layer.shape.M
+    if y is None:
+        y = torch.empty(M, dtype=torch.float32 if out_fp32 else torch.float16, device=x.device)
+    if workspace is None:
+        workspace = make_workspace(layer, 1, stream)
+    _check(lib().fluxbin_lut_gemv(ctypes.byref(layer.layer), x.data_ptr(), y.data_ptr(), 1 if out_fp32 else 0,
+                                  workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+    return y
+
+
+def fluxbin_lut_gemm_smallbatch(layer: PackedLayer, x, y=None, out_fp32: bool = False, workspace=None, stream=None):
+    """x: fp16 [B, N] (row stride x.stride(0)); returns y [B, M]."""
+    import torch
+    B = x.shape[0]
+    M = layer.shape.M
+    if y is None:
+        y = torch.empty(B, M, dtype=torch.float32 if out_fp32 else torch.float16, device=x.device)
+    if workspace is None:
+        workspace = make_workspace(layer, B, stream)
+    _check(lib().fluxbin_lut_gemm_smallbatch(ctypes.byref(layer.layer), int(B), x.data_ptr(), int(x.stride(0)),
+                                             y.data_ptr(), int(y.stride(0)), 1 if out_fp32 else 0,
+                                             workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                             _stream(stream)))
+    return y
+
+
+def fluxbin_debug_indices(layer: PackedLayer, stream=None):
+    import torch
+    s = layer.shape
+    n = (2 * layer.layer.NSC) * s.M * (128 // s.mu)
+    out = torch.empty(n, dtype=torch.uint8, device=layer.buf.device)
+    _check(lib().fluxbin_debug_indices(ctypes.byref(layer.layer), out.data_ptr(), _stream(stream)))
+    return out.view(2 * layer.layer.NSC, s.M, 128 // s.mu)
+
+
+def fluxbin_unpack_canonical(layer: PackedLayer, stream=None) -> Tuple[object, object]:
+    import torch
+    s = layer.shape
+    W = (s.N + 31) // 32
+    signs = torch.empty(s.Kb * s.M * W, dtype=torch.int32, device=layer.buf.device)
+    dense = None
+    if s.S > 0 and s.Ks > 0:
+        dense = torch.empty(s.Ks * s.M * ((s.S + 31) // 32), dtype=torch.int32, device=layer.buf.device)
+    _check(lib().fluxbin_unpack_canonical(ctypes.byref(layer.layer), signs.data_ptr(),
+                                          dense.data_ptr() if dense is not None else None, _stream(stream)))
+    return signs.view(s.Kb, s.M, W), (dense.view(s.Ks, s.M, -1) if dense is not None else None)

@@ -86,12 +86,12 @@ def _f16_bits(a: np.ndarray) -> np.ndarray:
 def _random_sign_words(rng: np.random.Generator, planes: int, M: int, N: int) -> np.ndarray:
     nbytes = -(-N // 8)
     W = -(-N // 32)
-    raw = rng.integers(0, 256, size=(planes, M, nbytes), dtype=np.uint8)
+    raw = np.frombuffer(rng.bytes(planes * M * nbytes), dtype=np.uint8).reshape(planes, M, nbytes)
     buf = np.zeros((planes, M, W * 4), dtype=np.uint8)
     buf[:, :, :nbytes] = raw
     if N % 8:
         buf[:, :, nbytes - 1] &= np.uint8((1 << (N % 8)) - 1)
-    return buf.view("<u4").reshape(planes, M, W).astype(np.uint32)
+    return buf.view("<u4").reshape(planes, M, W).astype(np.uint32, copy=False)
 
 
 def make_layer(spec: LayerSpec) -> SyntheticLayer:

@@ -1,0 +1,258 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Bar: packing and LUT indices bit-exact; outputs within |y - y*| <= 2e-3 * max(|y*|, 1e-3 * max|y*| of the row)
+(fp32 accumulation; x * alpha_c exact in fp32; fp16 output rounding 2^-11 relative). Full-size layers are checked on
+sampled rows that the oracle computes one by one; the smaller ones on every row."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import format_oracle as fmt
+from synth import CONFIGS, LayerSpec, config_layers, make_activations, make_layer
+
+from conftest import gpu_available
+from gpu_util import log, pack_layer, run_gemm, sample_rows, x_tensor
+
+pytestmark = pytest.mark.gpu
+
+REL = 2e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not gpu_available():
+        pytest.skip("no GPU")
+    from paper_2608_15602_amd import fluxbin as fb
+    fb.lib()
+
+
+def _check(y, y_ref, what):
+    r = oracle.parity_check(y, y_ref, rel=REL)
+    log(f"  {what}: normwise={r['normwise']:.2e} max_rel(>floor)={r['max_rel_above_floor']:.2e} "
+        f"worst/bound={r['worst_bound_ratio']:.3f}")
+    assert r["ok"], (what, r)
+
+
+def _parity(spec, B, rows=None, out_fp32=False, packed=None, L=None):
+    log(f"case {spec.name} M={spec.M} N={spec.N} Kb={spec.Kb} Ks={spec.Ks} mu={spec.mu} S={spec.S} g_r={spec.g_r} "
+        f"g_s={spec.g_s} B={B} fp32={out_fp32}")
+    L = L or make_layer(spec)
+    packed = packed or pack_layer(L)
+    x = make_activations(L, B)
+    y = run_gemm(packed, x, out_fp32=out_fp32)
+    if rows is None:
+        y_ref = oracle.gemv_dense(L, x)
+        _check(y, y_ref, "all rows")
+    else:
+        y_ref = oracle.gemv_dense(L, x, rows=rows)
+        _check(y[:, rows], y_ref, f"{len(rows)} sampled rows")
+    return L, packed, x, y
+
+
+# ---------------------------------------------------------------------------------------------- packing, bit-exact
+
+SMALL_SPECS = [
+    LayerSpec("c1", M=512, N=256, Kb=2, Ks=1, mu=4, S=8, g_r=128, g_s=8, seed=0),
+    LayerSpec("mu8_ragged", M=333, N=300, Kb=3, Ks=2, mu=8, S=77, g_r=128, g_s=77, seed=5),
+    LayerSpec("mu4_ragged", M=100, N=200, Kb=1, Ks=1, mu=4, S=130, g_r=200, g_s=128, seed=6),
+    LayerSpec("no_salient", M=64, N=128, Kb=2, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=7),
+]
+
+
+@pytest.mark.parametrize("spec", SMALL_SPECS, ids=lambda s: s.name)
+def test_pack_sections_bit_exact(spec):
+    import torch
+    log(f"case pack {spec.name}")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    torch.cuda.synchronize()
+    buf = packed.buf.cpu().numpy()
+    pb = fmt.packed_bytes(spec)
+    d = fmt.derived(spec)
+
+    def sec(name, dtype, count):
+        off = pb["off_" + name]
+        return buf[off:off + count * np.dtype(dtype).itemsize].view(dtype)
+
+    dev = fmt.device_signs(L)
+    assert np.array_equal(sec("signs", np.uint8, dev.size), dev.reshape(-1))
+    assert np.array_equal(sec("rscale", np.uint16, d["NRP"] * d["Mp"]), fmt.device_rscale(L).reshape(-1))
+    vc = fmt.virtual_columns(L)
+    assert np.array_equal(sec("colscale", np.uint16, d["V"]), vc["colscale"])
+    assert np.array_equal(sec("xidx", np.uint16, d["V"]), vc["xidx"])
+    assert np.array_equal(sec("chunk_plane", np.int32, d["NCP"]), vc["chunk_plane"])
+    assert np.array_equal(sec("sal_idx", np.uint16, max(spec.S, 1)), fmt.device_sal_idx(L))
+    hdr = buf[:8].view(np.uint32)
+    assert hdr[0] == fmt.MAGIC and hdr[1] == fmt.VERSION
+
+
+@pytest.mark.parametrize("spec", SMALL_SPECS, ids=lambda s: s.name)
+def test_unpack_and_indices_bit_exact(spec):
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    log(f"case unpack/indices {spec.name}")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    signs, dense = fb.fluxbin_unpack_canonical(packed)
+    p = fb.fluxbin_debug_indices(packed)
+    torch.cuda.synchronize()
+    bits = oracle.sign_bits(L.signs, spec.N)
+    got = oracle.sign_bits(signs.cpu().numpy().view(np.uint32), spec.N)
+    assert np.array_equal(got, bits)
+    if dense is not None:
+        want = oracle.vcm_dense_bits(L)
+        assert np.array_equal(oracle.sign_bits(dense.cpu().numpy().view(np.uint32), spec.S), want)
+    # LUT indices of every (chunk, row, sub-vector) equal the oracle's patterns of the same columns
+    idx = oracle.lut_indices(L)
+    pc = p.cpu().numpy()
+    per = 128 // spec.mu
+    ncg = fmt.derived(spec)["ncg"]
+    for k in range(spec.Kb):
+        g = pc[k * ncg:(k + 1) * ncg].transpose(1, 0, 2).reshape(spec.M, -1)
+        n = idx["global"].shape[2]
+        assert np.array_equal(g[:, :n], idx["global"][k])
+        assert np.all(g[:, n:] == 0)
+    if spec.S > 0 and spec.Ks > 0:
+        ncs = fmt.derived(spec)["ncs"]
+        for k in range(spec.Ks):
+            c0 = spec.Kb * ncg + k * ncs
+            sblk = pc[c0:c0 + ncs].transpose(1, 0, 2).reshape(spec.M, -1)
+            n = idx["salient"].shape[2]
+            assert np.array_equal(sblk[:, :n], idx["salient"][k])
+    assert per * 2 * fmt.derived(spec)["NSC"] == pc.shape[0] * pc.shape[2]
+
+
+def test_layer_survives_a_round_trip_through_its_header():
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    spec = SMALL_SPECS[1]
+    log("case header round trip")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    x = make_activations(L, 1)
+    y1 = run_gemm(packed, x)
+    copy = packed.buf.clone()
+    again = fb.fluxbin_layer_from_header(packed.buf[:256].cpu().numpy().tobytes(), copy)
+    y2 = run_gemm(again, x)
+    assert np.array_equal(y1, y2)
+
+
+# ---------------------------------------------------------------------------------------------- outputs
+
+def test_config1_tiny_mu4():
+    for spec in config_layers("c1_tiny", "128") + config_layers("c1_tiny", "N"):
+        _parity(spec, 1)
+
+
+@pytest.mark.parametrize("g_r", ["128", "N"])
+def test_config2_attn7b(g_r):
+    _parity(config_layers("c2_attn7b", g_r)[0], 1)
+
+
+@pytest.mark.parametrize("g_r", ["128", "N"])
+def test_config3_mlp7b(g_r):
+    for spec in config_layers("c3_mlp7b", g_r):
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        for B in CONFIGS["c3_mlp7b"]["batches"]:
+            _parity(spec, B, rows=sample_rows(spec.M, 512), packed=packed, L=L)
+
+
+@pytest.mark.parametrize("g_r", ["128", "N"])
+def test_config4_mlp70b(g_r):
+    for spec in config_layers("c4_mlp70b", g_r):
+        _parity(spec, 1, rows=sample_rows(spec.M, 768))
+
+
+def test_config5_layer70b():
+    import torch
+    for spec in config_layers("c5_layer70b", "128"):
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        for B in CONFIGS["c5_layer70b"]["batches"]:
+            _parity(spec, B, rows=sample_rows(spec.M, 128, seed=B), packed=packed, L=L)
+        del packed
+        torch.cuda.empty_cache()
+
+
+EDGE_SPECS = [
+    LayerSpec("one_row", M=1, N=128, Kb=1, Ks=1, mu=8, S=1, g_r=128, g_s=1, seed=11),
+    LayerSpec("ragged_rows", M=1000, N=512, Kb=2, Ks=1, mu=8, S=33, g_r=256, g_s=33, seed=12),
+    LayerSpec("ragged_cols", M=300, N=300, Kb=2, Ks=1, mu=8, S=5, g_r=128, g_s=5, seed=13),
+    LayerSpec("all_salient", M=256, N=256, Kb=1, Ks=1, mu=8, S=256, g_r=256, g_s=128, seed=14),
+    LayerSpec("salient_groups", M=640, N=1024, Kb=2, Ks=2, mu=8, S=300, g_r=512, g_s=128, seed=15),
+    LayerSpec("four_bases", M=513, N=1024, Kb=4, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=16),
+    LayerSpec("mu4_ragged", M=777, N=260, Kb=2, Ks=1, mu=4, S=20, g_r=260, g_s=20, seed=17),
+    LayerSpec("tiny_N", M=70, N=7, Kb=2, Ks=1, mu=4, S=3, g_r=7, g_s=3, seed=18),
+]
+
+
+@pytest.mark.parametrize("spec", EDGE_SPECS, ids=lambda s: s.name)
+@pytest.mark.parametrize("B", [1, 3])
+def test_edge_shapes(spec, B):
+    _parity(spec, B)
+
+
+def test_fp32_output_and_generic_kernel_at_batch1():
+    spec = LayerSpec("gen", M=2000, N=1024, Kb=2, Ks=1, mu=8, S=40, g_r=128, g_s=40, seed=21)
+    L, packed, x, y = _parity(spec, 1, out_fp32=True)
+    os.environ["FLUXBIN_GENERIC"] = "1"
+    try:
+        y2 = run_gemm(packed, x, out_fp32=True)
+    finally:
+        del os.environ["FLUXBIN_GENERIC"]
+    _check(y2, oracle.gemv_dense(L, x), "generic kernel at batch 1")
+
+
+@pytest.mark.parametrize("B", [2, 5, 16])
+def test_batch_rows_equal_batch1(B):
+    """Each batch row of the small-batch path matches the oracle, and the batch path gives the rows the oracle gives
+    for the same activations at batch 1."""
+    spec = LayerSpec("bat", M=1536, N=2048, Kb=2, Ks=1, mu=8, S=61, g_r=128, g_s=61, seed=22)
+    _parity(spec, B, out_fp32=True)
+
+
+def test_strided_batch():
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    spec = LayerSpec("strided", M=700, N=512, Kb=2, Ks=1, mu=8, S=16, g_r=128, g_s=16, seed=23)
+    log("case strided batch")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    x = make_activations(L, 4)
+    xt = torch.zeros(4, 600, dtype=torch.float16, device="cuda")
+    xt[:, :512] = x_tensor(x)
+    y = torch.full((4, 800), float("nan"), dtype=torch.float32, device="cuda")
+    fb.fluxbin_lut_gemm_smallbatch(packed, xt[:, :512], y=y[:, :700], out_fp32=True)
+    torch.cuda.synchronize()
+    yc = y.cpu().numpy().astype(np.float64)
+    assert np.all(np.isnan(yc[:, 700:]))
+    _check(yc[:, :700], oracle.gemv_dense(L, x), "strided")
+
+
+def test_deterministic_and_exact_power_of_two_scaling():
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    spec = config_layers("c2_attn7b", "128")[0]
+    log("case determinism + y(2x) == 2 y(x)")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    x = make_activations(L, 1)
+    ws = fb.make_workspace(packed, 1)
+    y1 = run_gemm(packed, x, out_fp32=True, ws=ws)
+    y2 = run_gemm(packed, x, out_fp32=True, ws=ws)
+    assert np.array_equal(y1, y2)
+    x2 = (oracle.f16_to_f64(x) * 2).astype(np.float16).view(np.uint16)
+    y3 = run_gemm(packed, x2, out_fp32=True, ws=ws)
+    assert np.array_equal(y3, 2 * y1)
+
+
+def test_zero_activation_gives_zero():
+    spec = LayerSpec("zero", M=512, N=512, Kb=2, Ks=1, mu=8, S=10, g_r=128, g_s=10, seed=24)
+    log("case zero activations")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    y = run_gemm(packed, np.zeros((1, 512), np.uint16), out_fp32=True)
+    assert np.all(y == 0)
