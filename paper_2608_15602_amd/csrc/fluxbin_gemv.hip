@@ -32,12 +32,16 @@ struct GemmArgs {
   float* partials;
   uint32_t* counters;
   int64_t ldx, ldy;
-  int64_t units, blocks;
+  int32_t units, blocks;
+  int32_t uq, ur;    // units per workgroup: uq + 1 for the first ur workgroups, uq for the others
   int32_t M, Mp, NSC, NCP;
-  int32_t steps;   // units per tile
-  int32_t B;       // batch rows actually present
+  int32_t steps;     // units per tile
+  int32_t B;         // batch rows actually present
   int32_t y_fp32;
   int32_t n_tiles;
+  int32_t N;         // input columns
+  int32_t ncg;       // chunks per global base
+  int32_t ngc;       // global chunks (Kb * ncg); chunks >= ngc are salient or padding
 };
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -51,9 +55,13 @@ __device__ __forceinline__ uint4 load_stream16(const uint8_t* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// Workgroup that owns unit u when `units` units are split into `blocks` ranges [b*units/blocks, (b+1)*units/blocks).
-__device__ __forceinline__ int64_t owner_of(int64_t u, int64_t units, int64_t blocks) {
-  return ((u + 1) * blocks + units - 1) / units - 1;
+// Balanced split of the units: workgroup b owns [first_unit(b), first_unit(b + 1)), uq + 1 units for b < ur and uq
+// units otherwise (uq >= 1).
+__device__ __forceinline__ int first_unit(const GemmArgs& a, int b) { return b * a.uq + (b < a.ur ? b : a.ur); }
+
+__device__ __forceinline__ int owner_of(const GemmArgs& a, int u) {
+  const int big = a.ur * (a.uq + 1);
+  return u < big ? u / (a.uq + 1) : a.ur + (u - big) / a.uq;
 }
 
 __device__ __forceinline__ void store_y(const GemmArgs& a, int b, int64_t row, float v) {
@@ -63,68 +71,124 @@ __device__ __forceinline__ void store_y(const GemmArgs& a, int b, int64_t row, f
     static_cast<uint16_t*>(a.y)[b * a.ldy + row] = f2h(v);
 }
 
-// End of a tile's contribution from this workgroup: store y directly when the workgroup covers the whole tile,
-// otherwise publish the partial sums; the last contributor adds them in workgroup order and stores y.
-// acc is [RPT][BP] (row j of this thread, batch row b).
+// ---------------------------------------------------------------------------------------------------------------------
+// End of a tile's contribution from one workgroup.
+//
+// tile_end() (store_tile_y / store_partial): if the workgroup covers the whole tile it stores y directly; otherwise it stores its partial sums with
+// device-coherent (agent-scope) stores into its slot (0 for its first tile, 1 for its last one) and returns true:
+// the tile is then "pending". Nothing waits here, so the prefetched sign loads stay in flight.
+// publish(): called once per pending tile after the workgroup has waited for all its memory operations. Thread 0
+// bumps the tile's counter; the workgroup that brings it to the number of contributors adds the partial sums of all
+// contributors in workgroup order (a fixed order, so y is the same on every run), stores y and resets the counter.
+// ---------------------------------------------------------------------------------------------------------------------
+
+// Whether workgroups other than the tile's first owner contribute to tile T.
+__device__ __forceinline__ bool tile_is_shared(const GemmArgs& a, int tile) {
+  return owner_of(a, tile * a.steps) != owner_of(a, (tile + 1) * a.steps - 1);
+}
+
 template <int NT, int RPT, int BP>
-__device__ __forceinline__ void finish_tile(const GemmArgs& a, int64_t tile, int64_t first_tile, float (&acc)[RPT][BP],
-                                            int* s_flag) {
-  const int t = threadIdx.x;
+__device__ __forceinline__ void store_tile_y(const GemmArgs& a, int64_t tile, const float (&acc)[RPT][BP]) {
   const int64_t R = int64_t(NT) * RPT;
-  const int64_t b_self = blockIdx.x;
-  const int64_t b_first = owner_of(tile * a.steps, a.units, a.blocks);
-  const int64_t b_last = owner_of((tile + 1) * a.steps - 1, a.units, a.blocks);
-  if (b_first == b_last) {
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const int64_t row = tile * R + t + NT * j;
-      if (row < a.M) {
+  for (int j = 0; j < RPT; ++j) {
+    const int64_t row = tile * R + threadIdx.x + NT * j;
+    if (row < a.M) {
 #pragma unroll
-        for (int b = 0; b < BP; ++b)
-          if (b < a.B) store_y(a, b, row, acc[j][b]);
-      }
+      for (int b = 0; b < BP; ++b)
+        if (b < a.B) store_y(a, b, row, acc[j][b]);
     }
-    return;
   }
-  // partial slot of a workgroup for a tile: 0 for its first tile, 1 for its last one
-  const int slot = (tile == first_tile) ? 0 : 1;
-  float* mine = a.partials + ((b_self * 2 + slot) * BP) * R;
+}
+
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ void store_partial(const GemmArgs& a, int slot, const float (&acc)[RPT][BP]) {
+  const int64_t R = int64_t(NT) * RPT;
+  float* mine = a.partials + ((int64_t(blockIdx.x) * 2 + slot) * BP) * R;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
 #pragma unroll
-    for (int b = 0; b < BP; ++b) mine[b * R + t + NT * j] = acc[j][b];
+    for (int b = 0; b < BP; ++b)
+      __hip_atomic_store(mine + b * R + threadIdx.x + NT * j, acc[j][b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  __threadfence();
-  __syncthreads();
+}
+
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ bool tile_end(const GemmArgs& a, int64_t tile, int64_t first_tile, const float (&acc)[RPT][BP]) {
+  if (!tile_is_shared(a, int(tile))) {
+    store_tile_y<NT, RPT, BP>(a, tile, acc);
+    return false;
+  }
+  store_partial<NT, RPT, BP>(a, tile == first_tile ? 0 : 1, acc);
+  return true;
+}
+
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ void publish(const GemmArgs& a, int64_t tile, int* s_flag) {
+  const int t = threadIdx.x;
+  const int64_t R = int64_t(NT) * RPT;
+  const int b_first = owner_of(a, int(tile) * a.steps);
+  const int b_last = owner_of(a, int(tile + 1) * a.steps - 1);
   if (t == 0) {
-    const uint32_t prev = atomicAdd(a.counters + tile, 1u);
+    const uint32_t prev = __hip_atomic_fetch_add(a.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *s_flag = (prev == uint32_t(b_last - b_first)) ? 1 : 0;
   }
   __syncthreads();
-  if (*s_flag) {
-    __threadfence();
+  const int last = *s_flag;
+  __syncthreads();
+  if (!last) return;
+  // Contributors b_first..b_last. All but the first start inside this tile (slot 0); the first one used slot 1 unless
+  // its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
+  constexpr int CH = 16;
+  const int n_c = int(b_last - b_first + 1);
+  const bool first_in_slot1 = first_unit(a, b_first) < int(tile) * a.steps;
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const int64_t r = t + NT * j;
-      const int64_t row = tile * R + r;
-      float sum[BP];
+  for (int j = 0; j < RPT; ++j) {
+    const int64_t r = t + NT * j;
+    const int64_t row = tile * R + r;
+    float sum[BP];
 #pragma unroll
-      for (int b = 0; b < BP; ++b) sum[b] = 0.f;
-      for (int64_t bb = b_first; bb <= b_last; ++bb) {
-        const int64_t first_of_bb = (bb * a.units / a.blocks) / a.steps;
-        const int sl = (tile == first_of_bb) ? 0 : 1;
-        const float* src = a.partials + ((bb * 2 + sl) * BP) * R;
+    for (int b = 0; b < BP; ++b) sum[b] = 0.f;
+    for (int c0 = 0; c0 < n_c; c0 += CH) {
+      float v[CH][BP];
 #pragma unroll
-        for (int b = 0; b < BP; ++b) sum[b] += __builtin_nontemporal_load(src + b * R + r);
-      }
-      if (row < a.M) {
+      for (int k = 0; k < CH; ++k) {
+        const int c = c0 + k < n_c ? c0 + k : n_c - 1;
+        const int sl = (c == 0 && first_in_slot1) ? 1 : 0;
+        const float* src = a.partials + ((int64_t(b_first + c) * 2 + sl) * BP) * R;
 #pragma unroll
         for (int b = 0; b < BP; ++b)
-          if (b < a.B) store_y(a, b, row, sum[b]);
+          v[k][b] = __hip_atomic_load(src + b * R + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+#pragma unroll
+      for (int k = 0; k < CH; ++k)
+#pragma unroll
+        for (int b = 0; b < BP; ++b) sum[b] += (c0 + k < n_c) ? v[k][b] : 0.f;
     }
-    if (t == 0) __hip_atomic_store(a.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (row < a.M) {
+#pragma unroll
+      for (int b = 0; b < BP; ++b)
+        if (b < a.B) store_y(a, b, row, sum[b]);
+    }
   }
+  if (t == 0) __hip_atomic_store(a.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until every memory operation of the workgroup has completed, then publishes its pending tiles.
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0, int pending1, int n_pending,
+                                                int* s_flag) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (n_pending > 0) publish<NT, RPT, BP>(a, pending0, s_flag);
+  if (n_pending > 1) publish<NT, RPT, BP>(a, pending1, s_flag);
+}
+
+// Read-only table entry with a wave-uniform index, through the constant address space so that it is a scalar load
+// (its own counter): waiting for it never waits for the vector loads in flight.
+__device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
+  return ((const __attribute__((address_space(4))) int32_t*)p)[i];
 }
 
 // =====================================================================================================================
@@ -138,34 +202,87 @@ __device__ __forceinline__ void finish_tile(const GemmArgs& a, int64_t tile, int
 // i.e. 32 different LDS banks, whatever the patterns are.
 // The byte address of a lookup, (p << 8) | (slot << 6) | (s << 2), is formed by one v_perm_b32 from the sign word and
 // a per-lane constant; the buffer is an immediate offset.
+//
+// Pipeline per workgroup: the sign words and row scales of unit k+2 are requested while the tables of unit k+1 are
+// built (other LDS buffer) and unit k is looked up, so two units of sign data are always in flight. The folded
+// activations of all the workgroup's units (at most kXvUnits, guaranteed by the launch plan) are staged in LDS first.
 // =====================================================================================================================
 
-constexpr int kXvUnits = 12;  // units whose folded activations are staged in LDS at a time (1 KB each)
+constexpr int kXvUnits = kB1MaxUnits;  // units whose folded activations are staged in LDS (1 KB each)
 
 template <int NT, int RPT>
 struct B1 {
   static constexpr int R = NT * RPT;
-  static constexpr int NHI = NT / 32;                                   // p-ranges per (slot, s) in the build
-  static constexpr int LO = NHI == 8 ? 5 : (NHI == 16 ? 4 : (NHI == 4 ? 6 : 7));
+  static constexpr int NHI = NT / 32;                                   // pattern ranges per (slot, s) in the build
+  static constexpr int LO = NHI == 4 ? 6 : (NHI == 8 ? 5 : (NHI == 16 ? 4 : 3));
   static constexpr int E = 1 << LO;                                     // entries per thread per build
+  static constexpr int KPT = kXvUnits / (NT / 256);                     // staged units per thread
 };
 
-// Stage the folded activations xv = x[xidx] * colscale of the n units starting at super-chunk sc0 into
-// xs[k*256 + col] (super-chunks wrap around at the end of a tile).
+template <int RPT>
+struct Ring {
+  uint32_t w[RPT][8];   // sign words of the thread's rows: [0..3] first stored chunk, [4..7] second
+  uint32_t ra[RPT];     // 32-bit word holding the fp16 row scales of rows (i & ~1, i | 1) for chunk 2sc
+  uint32_t rb[RPT];     // same for chunk 2sc+1
+};
+
+// Stage the folded activations xv = x[j] * colscale of the n <= kXvUnits units starting at super-chunk sc0 into
+// xs[k*256 + col] (super-chunks wrap around at the end of a tile). Global chunks read x[j] directly (j follows from the
+// chunk index); salient chunks read their input column from the VCM index table first. stage_issue() only issues the
+// loads; stage_finish() waits for them and writes LDS, so the sign loads can be issued in between.
 template <int NT>
-__device__ __forceinline__ void stage_xv_b1(const GemmArgs& a, float* xs, int sc0, int n) {
+struct Staged {
+  uint32_t v[B1<NT, 1>::KPT];    // x bits (global column) or the index (salient column)
+  uint32_t cs[B1<NT, 1>::KPT];   // column scale bits
+  int32_t plane;                 // threads t < 2*kXvUnits: row-scale plane of chunk 2*sc(t/2) + (t&1)
+};
+
+template <int NT>
+__device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, int sc0) {
+  using P = B1<NT, 1>;
   const int t = threadIdx.x;
-  int sc = sc0;
-  for (int k = 0; k < n; ++k) {
-    for (int col = t; col < 256; col += NT) {
-      const int v = sc * 256 + col;
-      const uint16_t xi = a.xidx[v];
-      const uint16_t cs = a.colscale[v];
-      float val = 0.f;
-      if (xi != 0xFFFFu) val = h2f(a.x[xi]) * h2f(cs);
-      xs[k * 256 + col] = val;
+  const int col = t & 255;
+#pragma unroll
+  for (int m = 0; m < P::KPT; ++m) {   // unconditional, always in-bounds loads: all in flight at once
+    const int k = (t >> 8) + m * (NT / 256);
+    int sc = sc0 + k;
+    while (sc >= a.steps) sc -= a.steps;
+    const int v = sc * 256 + col;
+    const int c = v >> 7;
+    int j = 0;
+    bool direct = false;
+    if (c < a.ngc) {
+      j = (c - (c / a.ncg) * a.ncg) * 128 + (col & 127);
+      direct = j < a.N;
     }
-    if (++sc == a.steps) sc = 0;
+    sg.v[m] = c < a.ngc ? (direct ? uint32_t(a.x[j]) : 0u) : uint32_t(a.xidx[v]);
+    sg.cs[m] = a.colscale[v];
+  }
+  int scp = sc0 + (t >> 1) % kXvUnits;
+  while (scp >= a.steps) scp -= a.steps;
+  sg.plane = a.chunk_plane[2 * scp + (t & 1)];
+}
+
+template <int NT>
+__device__ __forceinline__ void stage_finish(const GemmArgs& a, const Staged<NT>& sg, float* xs, int* s_planes,
+                                             int sc0, int n) {
+  using P = B1<NT, 1>;
+  const int t = threadIdx.x;
+  const int col = t & 255;
+  if (t < 2 * kXvUnits) s_planes[t] = sg.plane;
+#pragma unroll
+  for (int m = 0; m < P::KPT; ++m) {
+    const int k = (t >> 8) + m * (NT / 256);
+    int sc = sc0 + k;
+    while (sc >= a.steps) sc -= a.steps;
+    const int c = (sc * 256 + col) >> 7;
+    uint32_t xb = sg.v[m];
+    bool zero = false;
+    if (c >= a.ngc) {   // salient or padding column: v holds the VCM index
+      zero = sg.v[m] == 0xFFFFu;
+      xb = zero ? 0u : uint32_t(a.x[sg.v[m]]);
+    }
+    if (k < n) xs[k * 256 + col] = zero ? 0.f : h2f(uint16_t(xb)) * h2f(uint16_t(sg.cs[m]));
   }
 }
 
@@ -203,34 +320,73 @@ __device__ __forceinline__ void build_b1(float* lut, const float* xv256) {
   }
 }
 
+// Request cursor: the unit (tile, sc) to request next, the uniform base of its sign slots, and the per-thread byte
+// offsets of the thread's rows in the sign and row-scale sections for that tile. Rows past the packed rows (only in
+// the last tile) read the last packed row: their sums are never stored.
 template <int NT, int RPT>
-__device__ __forceinline__ void load_unit_b1(const GemmArgs& a, int tile, int sc, uint32_t (&w)[RPT][8],
-                                             float (&rs)[RPT][2], uint32_t hb) {
-  using P = B1<NT, RPT>;
-  const int t = threadIdx.x;
-  const int32_t pa = a.chunk_plane[2 * sc];
-  const int32_t pb = a.chunk_plane[2 * sc + 1];
-  const int32_t p1 = hb ? pb : pa;
-  const int32_t p2 = hb ? pa : pb;
+struct Cursor {
+  int tile, sc;
+  const uint8_t* sbase;     // signs + 2*sc*Mp*16
+  uint32_t soff[RPT];       // row * 16
+  uint32_t roff[RPT];       // (row >> 1) * 4
+};
+
+template <int NT, int RPT>
+__device__ __forceinline__ void cursor_rows(const GemmArgs& a, Cursor<NT, RPT>& c) {
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
-    const int row = tile * P::R + t + NT * j;
-    const int wave_row = tile * P::R + (t & ~63) + NT * j;
-    if (wave_row < a.Mp) {
-      const uint8_t* e0 = a.signs + (int64_t(2 * sc) * a.Mp + row) * 16;
-      const uint8_t* e1 = a.signs + (int64_t(2 * sc + 1) * a.Mp + row) * 16;
-      const uint4 v0 = load_stream16(e0);
-      const uint4 v1 = load_stream16(e1);
-      w[j][0] = v0.x; w[j][1] = v0.y; w[j][2] = v0.z; w[j][3] = v0.w;
-      w[j][4] = v1.x; w[j][5] = v1.y; w[j][6] = v1.z; w[j][7] = v1.w;
-      rs[j][0] = h2f(a.rscale[int64_t(p1) * a.Mp + row]);
-      rs[j][1] = h2f(a.rscale[int64_t(p2) * a.Mp + row]);
-    } else {
+    const int row_raw = c.tile * (NT * RPT) + int(threadIdx.x) + NT * j;
+    const uint32_t row = uint32_t(row_raw < a.Mp ? row_raw : a.Mp - 1);
+    c.soff[j] = row * 16u;
+    c.roff[j] = (row >> 1) * 4u;
+  }
+}
+
+template <int NT, int RPT>
+__device__ __forceinline__ void cursor_init(const GemmArgs& a, Cursor<NT, RPT>& c, int tile, int sc) {
+  c.tile = tile;
+  c.sc = sc;
+  c.sbase = a.signs + int64_t(2 * sc) * a.Mp * 16;
+  cursor_rows<NT, RPT>(a, c);
+}
+
+template <int NT, int RPT>
+__device__ __forceinline__ void cursor_next(const GemmArgs& a, Cursor<NT, RPT>& c) {
+  if (++c.sc == a.steps) {
+    c.sc = 0;
+    ++c.tile;
+    c.sbase = a.signs;
+    cursor_rows<NT, RPT>(a, c);
+  } else {
+    c.sbase += int64_t(2) * a.Mp * 16;
+  }
+}
+
+// Issue the loads of the cursor's unit: sign words of both stored chunks (issue_signs) and the row-scale words of both
+// chunks for row-scale planes pa, pb (issue_rscale), with uniform bases and the per-thread row offsets. Nothing here
+// waits for them.
+template <int NT, int RPT>
+__device__ __forceinline__ void issue_signs(const GemmArgs& a, const Cursor<NT, RPT>& c, Ring<RPT>& rg) {
+  const uint8_t* e0 = c.sbase;
+  const uint8_t* e1 = c.sbase + int64_t(a.Mp) * 16;
 #pragma unroll
-      for (int m = 0; m < 8; ++m) w[j][m] = 0u;
-      rs[j][0] = 0.f;
-      rs[j][1] = 0.f;
-    }
+  for (int j = 0; j < RPT; ++j) {
+    const uint4 v0 = load_stream16(e0 + c.soff[j]);
+    const uint4 v1 = load_stream16(e1 + c.soff[j]);
+    rg.w[j][0] = v0.x; rg.w[j][1] = v0.y; rg.w[j][2] = v0.z; rg.w[j][3] = v0.w;
+    rg.w[j][4] = v1.x; rg.w[j][5] = v1.y; rg.w[j][6] = v1.z; rg.w[j][7] = v1.w;
+  }
+}
+
+template <int NT, int RPT>
+__device__ __forceinline__ void issue_rscale(const GemmArgs& a, const Cursor<NT, RPT>& c, int32_t pa, int32_t pb,
+                                             Ring<RPT>& rg) {
+  const uint8_t* ba = reinterpret_cast<const uint8_t*>(a.rscale) + int64_t(pa) * a.Mp * 2;
+  const uint8_t* bb = reinterpret_cast<const uint8_t*>(a.rscale) + int64_t(pb) * a.Mp * 2;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    rg.ra[j] = *reinterpret_cast<const uint32_t*>(ba + c.roff[j]);
+    rg.rb[j] = *reinterpret_cast<const uint32_t*>(bb + c.roff[j]);
   }
 }
 
@@ -240,8 +396,9 @@ __device__ __forceinline__ float lds_at(const float* lut, uint32_t byte_addr) {
 }
 
 template <int NT, int RPT, int BUF>
-__device__ __forceinline__ void lookup_b1(const float* lut, const uint32_t (&w)[RPT][8], const float (&rs)[RPT][2],
-                                          const uint32_t (&c1)[4], const uint32_t (&c2)[4], float (&acc)[RPT][1]) {
+__device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT>& rg, const uint32_t (&c1)[4],
+                                          const uint32_t (&c2)[4], bool hb, float (&acc)[RPT][1]) {
+  const uint32_t sh = (threadIdx.x & 1u) * 16u;   // the rows of a thread have the parity of threadIdx.x
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
     float s1 = 0.f, s2 = 0.f;
@@ -250,7 +407,7 @@ __device__ __forceinline__ void lookup_b1(const float* lut, const uint32_t (&w)[
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb) {
         const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
-        s1 += lds_at<BUF>(lut, __builtin_amdgcn_perm(w[j][m], c1[m], sel));
+        s1 += lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][m], c1[m], sel));
       }
     }
 #pragma unroll
@@ -258,27 +415,113 @@ __device__ __forceinline__ void lookup_b1(const float* lut, const uint32_t (&w)[
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb) {
         const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
-        s2 += lds_at<BUF>(lut, __builtin_amdgcn_perm(w[j][4 + m], c2[m], sel));
+        s2 += lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][4 + m], c2[m], sel));
       }
     }
-    acc[j][0] = __builtin_fmaf(s1, rs[j][0], acc[j][0]);
-    acc[j][0] = __builtin_fmaf(s2, rs[j][1], acc[j][0]);
+    // s1 belongs to chunk 2sc + hb, s2 to the other one
+    const float sa = hb ? s2 : s1;
+    const float sb = hb ? s1 : s2;
+    acc[j][0] = __builtin_fmaf(sa, h2f(uint16_t(rg.ra[j] >> sh)), acc[j][0]);
+    acc[j][0] = __builtin_fmaf(sb, h2f(uint16_t(rg.rb[j] >> sh)), acc[j][0]);
   }
 }
 
+// Row-scale plane of chunk 2*sc(k) + half of the workgroup's unit k (clamped to its last unit), from the table the
+// prologue staged in LDS (a broadcast read; no scalar load is waited for inside the pipeline).
+__device__ __forceinline__ int32_t plane_of(const int* s_planes, int k, int n, int half = 0) {
+  const int kk = k < n ? k : n - 1;
+  return __builtin_amdgcn_readfirstlane(s_planes[2 * kk + half]);
+}
+
+// Per-workgroup state of the batch-1 kernel.
 template <int NT, int RPT>
+struct B1State {
+  int n;                       // units of this workgroup
+  int tile, sc;                // of the unit being looked up
+  int first_tile, last_tile;   // tiles touched by this workgroup
+  bool first_shared, last_shared;   // whether other workgroups contribute to them
+  int n_pending;               // shared tiles whose partial sums await publication (first, then last)
+  float acc[RPT][1];
+};
+
+// Step K of the pipeline (K = unit index within the workgroup): request unit K+D into its ring slot, build unit
+// K+1 into LDS buffer (K+1) % 2, look up unit K (ring slot K % (D+1), buffer K % 2). The steps are unrolled at compile
+// time (a workgroup has at most kXvUnits units) so that the wait before each lookup covers exactly the loads of unit
+// K: past the last unit the request repeats the last unit (cache hits), which keeps the count of loads in flight the
+// same on every path.
+template <int NT, int RPT, int D, int K>
+__device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
+                                         Ring<RPT> (&ring)[D + 1], float* lut, float* xs, const uint32_t (&c1)[4],
+                                         const uint32_t (&c2)[4], bool hb, const int* s_planes) {
+  if constexpr (K < kXvUnits) {
+    if (K >= st.n) return;
+    constexpr int BUF = K & 1;
+    constexpr int KI = (K + D) < kXvUnits ? (K + D) : kXvUnits - 1;   // unit requested now (clamped past the end)
+    issue_signs<NT, RPT>(a, cur, ring[(K + D) % (D + 1)]);
+    issue_rscale<NT, RPT>(a, cur, plane_of(s_planes, KI, st.n), plane_of(s_planes, KI, st.n, 1), ring[(K + D) % (D + 1)]);
+    if (K + D + 1 < st.n) cursor_next<NT, RPT>(a, cur);
+    if (K + 1 < st.n) build_b1<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
+    lookup_b1<NT, RPT, BUF>(lut, ring[K % (D + 1)], c1, c2, hb, st.acc);
+    if (st.sc == a.steps - 1 || K + 1 == st.n) {
+      const bool shared = st.tile == st.first_tile ? st.first_shared : (st.tile == st.last_tile ? st.last_shared : false);
+      if (shared) {
+        store_partial<NT, RPT, 1>(a, st.tile == st.first_tile ? 0 : 1, st.acc);
+        ++st.n_pending;
+      } else {
+        store_tile_y<NT, RPT, 1>(a, st.tile, st.acc);
+      }
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) st.acc[j][0] = 0.f;
+    }
+    __syncthreads();
+    if (++st.sc == a.steps) {
+      st.sc = 0;
+      ++st.tile;
+    }
+    steps_b1<NT, RPT, D, K + 1>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes);
+  }
+}
+
+template <int NT, int RPT, int D>
 __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float lut[256 * 64];       // 64 KB, two buffers interleaved per pattern
   __shared__ __attribute__((aligned(16))) float xs[kXvUnits * 256];  // staged folded activations
+  __shared__ int s_planes[2 * kXvUnits];                               // row-scale planes of the staged units
   __shared__ int s_flag;
 
   const int t = threadIdx.x;
-  const int64_t u0 = int64_t(blockIdx.x) * a.units / a.blocks;
-  const int64_t u1 = (int64_t(blockIdx.x) + 1) * a.units / a.blocks;
-  const int64_t first_tile = u0 / a.steps;
+  const int u0 = first_unit(a, blockIdx.x);
+  const int u1 = first_unit(a, blockIdx.x + 1);
+
+  B1State<NT, RPT> st;
+  st.n = u1 - u0;
+  st.tile = u0 / a.steps;
+  st.sc = u0 - st.tile * a.steps;
+  st.first_tile = st.tile;
+  st.last_tile = (u1 - 1) / a.steps;
+  st.first_shared = tile_is_shared(a, st.first_tile);
+  st.last_shared = tile_is_shared(a, st.last_tile);
+  st.n_pending = 0;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) st.acc[j][0] = 0.f;
+
+  // Prologue: activation, column-scale and row-scale-plane loads first, then the sign loads of units 0..D-1, so that
+  // waiting for the former does not wait for the latter. The row scales of units 0..D-1 follow once the planes are
+  // staged in LDS.
+  const bool hb = ((t >> 4) & 1) != 0;
+  Staged<NT> sg;
+  stage_issue<NT>(a, sg, st.sc);
+  Cursor<NT, RPT> cur;
+  cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
+  Ring<RPT> ring[D + 1];
+  Cursor<NT, RPT> cur0 = cur;
+#pragma unroll
+  for (int k = 0; k < D; ++k) {   // units 0..D-1 (repeating the last unit past the end)
+    issue_signs<NT, RPT>(a, cur, ring[k]);
+    if (k + 1 < st.n) cursor_next<NT, RPT>(a, cur);
+  }
 
   // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32.
-  const uint32_t hb = (t >> 4) & 1u;
   uint32_t c1[4], c2[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
@@ -287,81 +530,23 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
       const uint32_t s = (uint32_t(4 * m + bb) + uint32_t(t)) & 15u;
-      c1[m] |= ((hb << 6) | (s << 2)) << (8 * bb);
-      c2[m] |= (((hb ^ 1u) << 6) | (s << 2)) << (8 * bb);
+      c1[m] |= ((uint32_t(hb) << 6) | (s << 2)) << (8 * bb);
+      c2[m] |= ((uint32_t(!hb) << 6) | (s << 2)) << (8 * bb);
     }
   }
 
-  float acc[RPT][1];
-#pragma unroll
-  for (int j = 0; j < RPT; ++j) acc[j][0] = 0.f;
-  uint32_t wA[RPT][8], wB[RPT][8];
-  float rA[RPT][2], rB[RPT][2];
-
-  // (tile, sc) of the current unit and of the next one, advanced without divisions
-  const int steps = a.steps;
-  int n_left = int(u1 - u0);           // units still to process, current one included
-  int tile = int(first_tile);
-  int sc = int(u0 - first_tile * steps);
-  int tile_n = tile, sc_n = sc;
-  auto advance = [&](int& tl, int& s) {
-    if (++s == steps) { s = 0; ++tl; }
-  };
-
-  load_unit_b1<NT, RPT>(a, tile, sc, wA, rA, hb);
-  int staged_left = n_left < kXvUnits ? n_left : kXvUnits;   // staged units not yet built, current one included
-  int xs_pos = 0;                                             // slot of the current unit in xs
-  stage_xv_b1<NT>(a, xs, sc, staged_left);
+  stage_finish<NT>(a, sg, xs, s_planes, st.sc, st.n);   // the launch plan keeps n <= kXvUnits
   __syncthreads();
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    issue_rscale<NT, RPT>(a, cur0, plane_of(s_planes, k, st.n), plane_of(s_planes, k, st.n, 1), ring[k]);
+    if (k + 1 < st.n) cursor_next<NT, RPT>(a, cur0);
+  }
   build_b1<NT, 0>(lut, xs);
   __syncthreads();
-
-  while (true) {
-    // ---- even step: current unit in buffer 0 / registers A ----
-    tile_n = tile; sc_n = sc;
-    advance(tile_n, sc_n);
-    if (n_left > 1) {
-      load_unit_b1<NT, RPT>(a, tile_n, sc_n, wB, rB, hb);
-      if (--staged_left == 0) {
-        staged_left = (n_left - 1) < kXvUnits ? (n_left - 1) : kXvUnits;
-        stage_xv_b1<NT>(a, xs, sc_n, staged_left);
-        xs_pos = -1;
-        __syncthreads();
-      }
-      build_b1<NT, 1>(lut, xs + (xs_pos + 1) * 256);
-    }
-    lookup_b1<NT, RPT, 0>(lut, wA, rA, c1, c2, acc);
-    if (sc == steps - 1 || n_left == 1) {
-      finish_tile<NT, RPT, 1>(a, tile, first_tile, acc, &s_flag);
-#pragma unroll
-      for (int j = 0; j < RPT; ++j) acc[j][0] = 0.f;
-    }
-    __syncthreads();
-    if (--n_left == 0) break;
-    tile = tile_n; sc = sc_n; ++xs_pos;
-    // ---- odd step: current unit in buffer 1 / registers B ----
-    tile_n = tile; sc_n = sc;
-    advance(tile_n, sc_n);
-    if (n_left > 1) {
-      load_unit_b1<NT, RPT>(a, tile_n, sc_n, wA, rA, hb);
-      if (--staged_left == 0) {
-        staged_left = (n_left - 1) < kXvUnits ? (n_left - 1) : kXvUnits;
-        stage_xv_b1<NT>(a, xs, sc_n, staged_left);
-        xs_pos = -1;
-        __syncthreads();
-      }
-      build_b1<NT, 0>(lut, xs + (xs_pos + 1) * 256);
-    }
-    lookup_b1<NT, RPT, 1>(lut, wB, rB, c1, c2, acc);
-    if (sc == steps - 1 || n_left == 1) {
-      finish_tile<NT, RPT, 1>(a, tile, first_tile, acc, &s_flag);
-#pragma unroll
-      for (int j = 0; j < RPT; ++j) acc[j][0] = 0.f;
-    }
-    __syncthreads();
-    if (--n_left == 0) break;
-    tile = tile_n; sc = sc_n; ++xs_pos;
-  }
+  steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes);
+  const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
+  publish_pending<NT, RPT, 1>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
 
 // =====================================================================================================================
@@ -402,25 +587,50 @@ __device__ __forceinline__ void read_vec<4>(const float* p, float (&f)[4]) {
   f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
 }
 
-// Stage the folded activations of n units starting at (c, g) into xs[k*XV + col*BG + b].
+// Stage the folded activations of n <= XU units starting at (c, g) into xs[k*XV + col*BG + b]. Thread t handles
+// column t % 128 of every staged unit; all index/scale loads are issued before the activation gathers.
 template <int MU, int BG, int NG, int NT, int RPT>
 __device__ __forceinline__ void stage_xv_gen(const GemmArgs& a, float* xs, int c, int g, int n) {
   using P = Gen<MU, BG, NG, NT, RPT>;
+  static_assert(NT % 128 == 0, "whole columns per thread group");
+  constexpr int KPT = (P::XU * 128 + NT - 1) / NT;   // (unit, column) pairs per thread
   const int t = threadIdx.x;
-  for (int k = 0; k < n; ++k) {
-    for (int e = t; e < P::XV; e += NT) {
-      const int col = e / BG;
-      const int b = e % BG;
-      const int bat = g * BG + b;
-      const int v = c * 128 + col;
-      const uint16_t xi = a.xidx[v];
-      float val = 0.f;
-      if (xi != 0xFFFFu && bat < a.B) val = h2f(a.x[int64_t(bat) * a.ldx + xi]) * h2f(a.colscale[v]);
-      xs[k * P::XV + e] = val;
+  const int col = t % 128;
+  uint16_t xi[KPT], cs[KPT];
+  int cu[KPT], gu[KPT];
+  // walk the units; thread t takes units k = t/128, t/128 + NT/128, ...
+  int cc = c, gg = g;
+#pragma unroll
+  for (int k = 0; k < P::XU; ++k) {
+    if ((k % (NT / 128)) == (t / 128) && k / (NT / 128) < KPT) {
+      const int m = k / (NT / 128);
+      cu[m] = cc;
+      gu[m] = gg;
+      xi[m] = a.xidx[cc * 128 + col];          // unconditional, always in-bounds: all loads in flight at once
+      cs[m] = a.colscale[cc * 128 + col];
     }
-    if (++g == NG) {
-      g = 0;
-      if (++c == a.NCP) c = 0;
+    if (++gg == NG) {
+      gg = 0;
+      if (++cc == a.NCP) cc = 0;
+    }
+  }
+  uint16_t xr[KPT][BG];
+#pragma unroll
+  for (int m = 0; m < KPT; ++m)
+#pragma unroll
+    for (int b = 0; b < BG; ++b) {
+      const int bat = gu[m] * BG + b;
+      xr[m][b] = a.x[int64_t(bat < a.B ? bat : 0) * a.ldx + (xi[m] == 0xFFFFu ? 0 : xi[m])];
+    }
+#pragma unroll
+  for (int m = 0; m < KPT; ++m) {
+    const int k = m * (NT / 128) + t / 128;
+    if (k < n) {
+#pragma unroll
+      for (int b = 0; b < BG; ++b) {
+        const int bat = gu[m] * BG + b;
+        xs[k * P::XV + col * BG + b] = (xi[m] != 0xFFFFu && bat < a.B) ? h2f(xr[m][b]) * h2f(cs[m]) : 0.f;
+      }
     }
   }
 }
@@ -458,28 +668,25 @@ __device__ __forceinline__ void build_gen(float* tbl, const float* xs) {
 
 template <int MU, int BG, int NG, int NT, int RPT>
 __device__ __forceinline__ void load_unit_gen(const GemmArgs& a, int tile, int c, uint32_t (&w)[RPT][4],
-                                              float (&rs)[RPT]) {
+                                              uint32_t (&rs)[RPT]) {
   using P = Gen<MU, BG, NG, NT, RPT>;
   const int t = threadIdx.x;
-  const int32_t plane = a.chunk_plane[c];
+  const int cu = __builtin_amdgcn_readfirstlane(c);
+  const int tl = __builtin_amdgcn_readfirstlane(tile);
+  const int32_t plane = load_uniform_i32(a.chunk_plane, cu);
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
-    const int row = tile * P::R + t + NT * j;
-    const int wave_row = tile * P::R + (t & ~63) + NT * j;
-    if (wave_row < a.Mp) {
-      const int h = (MU == 8) ? ((c & 1) ^ ((row & 31) >= 16 ? 1 : 0)) : (c & 1);
-      const uint4 v = load_stream16(a.signs + ((int64_t(c >> 1) * 2 + h) * a.Mp + row) * 16);
-      w[j][0] = v.x; w[j][1] = v.y; w[j][2] = v.z; w[j][3] = v.w;
-      rs[j] = h2f(a.rscale[int64_t(plane) * a.Mp + row]);
-    } else {
-      w[j][0] = w[j][1] = w[j][2] = w[j][3] = 0u;
-      rs[j] = 0.f;
-    }
+    const int row_raw = tl * P::R + t + NT * j;
+    const int row = row_raw < a.Mp ? row_raw : a.Mp - 1;   // rows past the packed ones are never stored
+    const int h = (MU == 8) ? ((cu & 1) ^ ((t & 31) >= 16 ? 1 : 0)) : (cu & 1);
+    const uint4 v = load_stream16(a.signs + ((int64_t(cu >> 1) * 2 + h) * a.Mp + row) * 16);
+    w[j][0] = v.x; w[j][1] = v.y; w[j][2] = v.z; w[j][3] = v.w;
+    rs[j] = a.rscale[int64_t(plane) * a.Mp + row];
   }
 }
 
 template <int MU, int BG, int NG, int NT, int RPT>
-__device__ __forceinline__ void lookup_gen(const float* tbl, const uint32_t (&w)[RPT][4], const float (&rs)[RPT], int g,
+__device__ __forceinline__ void lookup_gen(const float* tbl, const uint32_t (&w)[RPT][4], const uint32_t (&rs)[RPT], int g,
                                            float (&acc)[RPT][BG * NG]) {
   using P = Gen<MU, BG, NG, NT, RPT>;
   const uint32_t t = threadIdx.x;
@@ -501,7 +708,7 @@ __device__ __forceinline__ void lookup_gen(const float* tbl, const uint32_t (&w)
     for (int gg = 0; gg < NG; ++gg) {
 #pragma unroll
       for (int b = 0; b < BG; ++b) {
-        const float upd = __builtin_fmaf(sum[b], rs[j], acc[j][gg * BG + b]);
+        const float upd = __builtin_fmaf(sum[b], h2f(uint16_t(rs[j])), acc[j][gg * BG + b]);
         acc[j][gg * BG + b] = (gg == g) ? upd : acc[j][gg * BG + b];
       }
     }
@@ -515,8 +722,8 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float xs[P::XU * P::XV];
   __shared__ int s_flag;
 
-  const int64_t u0 = int64_t(blockIdx.x) * a.units / a.blocks;
-  const int64_t u1 = (int64_t(blockIdx.x) + 1) * a.units / a.blocks;
+  const int64_t u0 = first_unit(a, blockIdx.x);
+  const int64_t u1 = first_unit(a, blockIdx.x + 1);
   const int64_t first_tile = u0 / a.steps;
   const int rem0 = int(u0 - first_tile * a.steps);
 
@@ -526,10 +733,11 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
 #pragma unroll
     for (int b = 0; b < P::BP; ++b) acc[j][b] = 0.f;
   uint32_t w[RPT][4], wn[RPT][4];
-  float rs[RPT], rsn[RPT];
+  uint32_t rs[RPT], rsn[RPT];
 
   int n_left = int(u1 - u0);
   int tile = int(first_tile), c = rem0 / NG, g = rem0 % NG;
+  int pending0 = 0, pending1 = 0, n_pending = 0;
   load_unit_gen<MU, BG, NG, NT, RPT>(a, tile, c, w, rs);
   int staged_left = n_left < P::XU ? n_left : P::XU;
   int xs_pos = 0;
@@ -559,7 +767,10 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
     }
     lookup_gen<MU, BG, NG, NT, RPT>(tbl + buf * P::TBL, w, rs, g, acc);
     if ((c == a.NCP - 1 && g == NG - 1) || n_left == 1) {
-      finish_tile<NT, RPT, P::BP>(a, tile, first_tile, acc, &s_flag);
+      if (tile_end<NT, RPT, P::BP>(a, tile, first_tile, acc)) {
+        if (n_pending == 0) pending0 = tile; else pending1 = tile;
+        ++n_pending;
+      }
 #pragma unroll
       for (int j = 0; j < RPT; ++j)
 #pragma unroll
@@ -577,6 +788,7 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
     tile = tile_n; c = c_n; g = g_n; ++xs_pos;
     buf ^= 1;
   }
+  publish_pending<NT, RPT, P::BP>(a, pending0, pending1, n_pending, &s_flag);
 }
 
 // =====================================================================================================================
@@ -584,8 +796,13 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
 // =====================================================================================================================
 
 template <int NT, int RPT>
-static void launch_b1(const GemmArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a);
+static void launch_b1(const GemmArgs& a, int depth, hipStream_t stream) {
+  switch (depth) {
+    case 3: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 3>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 4>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
+    case 6: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 6>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
+    default: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 2>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
+  }
 }
 
 template <int MU, int BG, int NG>
@@ -628,8 +845,13 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   a.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(d_ws) + p.ws_partials_off);
   a.ldx = ldx;
   a.ldy = ldy;
-  a.units = p.units;
-  a.blocks = p.blocks;
+  a.units = int32_t(p.units);
+  a.blocks = int32_t(p.blocks);
+  a.uq = int32_t(p.units / p.blocks);
+  a.ur = int32_t(p.units % p.blocks);
+  a.N = int32_t(L.shape.N);
+  a.ncg = int32_t(L.Npad / kChunk);
+  a.ngc = int32_t(L.shape.Kb * (L.Npad / kChunk));
   a.M = int32_t(L.shape.M);
   a.Mp = int32_t(L.Mp);
   a.NSC = int32_t(L.NSC);
@@ -640,10 +862,15 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   a.n_tiles = int32_t(p.n_tiles);
   bool ok = true;
   if (p.kernel == 0) {
-    switch (p.rpt) {
-      case 1: launch_b1<256, 1>(a, stream); break;
-      case 2: launch_b1<256, 2>(a, stream); break;
-      case 4: launch_b1<256, 4>(a, stream); break;
+    const int key = p.nt * 10 + p.rpt;
+    switch (key) {
+      case 2561: launch_b1<256, 1>(a, p.depth, stream); break;
+      case 2562: launch_b1<256, 2>(a, p.depth, stream); break;
+      case 2564: launch_b1<256, 4>(a, p.depth, stream); break;
+      case 5121: launch_b1<512, 1>(a, p.depth, stream); break;
+      case 5122: launch_b1<512, 2>(a, p.depth, stream); break;
+      case 10241: launch_b1<1024, 1>(a, p.depth, stream); break;
+      case 10242: launch_b1<1024, 2>(a, p.depth, stream); break;
       default: ok = false;
     }
   } else if (L.shape.mu == 8) {

@@ -130,6 +130,10 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   p->nt = 256;
   if (L.shape.mu == 8 && B == 1 && !force_generic) {
     p->kernel = 0;
+    const int nt_env = env_int("FLUXBIN_NT", 512);
+    const int depth_env = env_int("FLUXBIN_DEPTH", 2);
+    p->depth = (depth_env == 3 || depth_env == 4 || depth_env == 6) ? depth_env : 2;
+    p->nt = (nt_env == 256 || nt_env == 1024) ? nt_env : 512;
     p->bg = 1;
     p->n_groups = 1;
   } else {
@@ -140,8 +144,10 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   }
   p->bpad = p->bg * p->n_groups;
   const int64_t steps = (p->kernel == 0) ? L.NSC : (2 * L.NSC) * p->n_groups;
-  // instantiated rows per thread: 4 only for the batch-1 kernel and the mu=8 generic kernel with <= 2 batch rows
-  const int rpt_max = (p->kernel == 0 || (L.shape.mu == 8 && p->bpad <= 2)) ? 4 : 2;
+  // instantiated rows per thread: batch-1 kernel 4/2/1 at 256 threads, 2/1 at 512 and 1024; the generic kernel 4
+  // only for mu = 8 with <= 2 batch rows
+  int rpt_max = (p->kernel == 0 || (L.shape.mu == 8 && p->bpad <= 2)) ? 4 : 2;
+  if (p->kernel == 0) rpt_max = p->nt == 256 ? 4 : 2;
   int chosen = 1;
   if (rpt_env == 1 || rpt_env == 2 || rpt_env == 4) {
     chosen = rpt_env > rpt_max ? rpt_max : rpt_env;
@@ -158,7 +164,11 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   p->rows = p->nt * p->rpt;
   p->n_tiles = ceil_div(L.shape.M, p->rows);
   p->units = p->n_tiles * steps;
+  if (p->units > (int64_t(1) << 30))
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "layer too large for one launch (%lld work units)", (long long)p->units);
   p->blocks = p->units < target ? p->units : target;
+  // the batch-1 kernel stages the folded activations of all its units at once: at most kB1MaxUnits per workgroup
+  if (p->kernel == 0 && ceil_div(p->units, p->blocks) > kB1MaxUnits) p->blocks = ceil_div(p->units, kB1MaxUnits);
   p->ws_counters_off = 0;
   p->ws_partials_off = round_up256(uint64_t(p->n_tiles) * 4u);
   p->ws_bytes = p->ws_partials_off + uint64_t(p->blocks) * 2u * uint64_t(p->rows) * uint64_t(p->bpad) * 4u;

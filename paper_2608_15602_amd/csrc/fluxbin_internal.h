@@ -11,6 +11,7 @@ namespace fluxbin {
 constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes of signs per row)
 constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
 constexpr int kMaxBatch = 16;
+constexpr int kB1MaxUnits = 12;         // units per workgroup of the batch-1 kernel (its LDS staging capacity)
 
 struct Derived {
   int64_t Npad, ncg, Sv, ncs, NC, NSC, NCP, V, Mp, Gr, Gs, NRP;
@@ -81,6 +82,7 @@ struct Plan {
   int bg;           // batch rows per LUT group (generic kernel)
   int n_groups;     // batch groups
   int bpad;         // bg * n_groups
+  int depth;        // batch-1 kernel: units of sign data requested ahead (2, 3, 4 or 6)
   uint64_t ws_counters_off, ws_partials_off, ws_bytes;
 };
 
