@@ -80,33 +80,60 @@ class Bench:
         else:
             self.fb.fluxbin_lut_gemm_smallbatch(p, it["x"], y=it["y"], workspace=it["ws"])
 
+    def graph(self, steps: int, start: int = 0, items=None):
+        """Capture `steps` steps (every layer once per step, rotating packed copies) in one HIP graph."""
+        import torch
+        items = self.items if items is None else items
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g, stream=side):
+                for s in range(steps):
+                    for it in items:
+                        self.launch(it, start + s)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        return g
+
+    @staticmethod
+    def time_graph(g, reps: int = 1):
+        import torch
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
     def run(self, steps: int, warmup: int):
+        """Warmup steps, then exactly `steps` steps replayed from one HIP graph between two events (synchronized on
+        both sides). Returns the total milliseconds and the wall-clock seconds of the timed region."""
         import torch
         for s in range(warmup):
             for it in self.items:
                 self.launch(it, s)
-        torch.cuda.synchronize()
-        evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-               for _ in self.items]
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
+        g = self.graph(steps, warmup)
+        g.replay()          # first replay outside the timed region (graph upload)
         torch.cuda.synchronize()
         wall0 = time.perf_counter()
-        t0.record()
-        for s in range(steps):
-            for li, it in enumerate(self.items):
-                evs[li][s][0].record()
-                self.launch(it, warmup + s)
-                evs[li][s][1].record()
-        t1.record()
-        torch.cuda.synchronize()
+        total_ms = self.time_graph(g)
         wall = time.perf_counter() - wall0
-        total_ms = t0.elapsed_time(t1)
-        per = []
-        for li, it in enumerate(self.items):
-            ms = [a.elapsed_time(b) for a, b in evs[li]]
-            per.append(sum(ms) / len(ms))
-        return total_ms, per, wall
+        return total_ms, wall
+
+    def per_launch_us(self, launches: int = 60, reps: int = 5):
+        """Average duration of each layer's launch: a graph of `launches` launches of that layer alone (rotating
+        copies), median of `reps` replays, divided by the launch count."""
+        out = []
+        for it in self.items:
+            g = self.graph(launches, 0, [it])
+            g.replay()
+            ts = sorted(self.time_graph(g) * 1000.0 / launches for _ in range(reps))
+            out.append(ts[len(ts) // 2])
+        return out
 
 
 def cpu_baseline(bench, budget_s: float):
@@ -140,36 +167,11 @@ def cpu_baseline(bench, budget_s: float):
             "sample": "; ".join(parts) + f" (fp64 reconstruct + matvec, {t_total:.1f} s)"}
 
 
-def small_layer_us(spec, steps=200):
-    """Per-call microseconds of a small layer (4096x4096), launches captured in a HIP graph to take the CPU launch
-    cost out; distinct packed copies rotate so the signs come from HBM."""
-    import torch
+def small_layer_us(spec, launches=200):
+    """Per-call microseconds of a small layer (4096x4096): a HIP graph of back-to-back launches rotating distinct
+    packed copies (so the signs come from HBM), median of 5 replays."""
     b = Bench([spec], 1, 512e6)
-    for s in range(5):
-        b.launch(b.items[0], s)
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    s = torch.cuda.Stream()
-    s.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(s):
-        with torch.cuda.graph(g, stream=s):
-            for k in range(steps):
-                b.launch(b.items[0], k)
-    torch.cuda.current_stream().wait_stream(s)
-    torch.cuda.synchronize()
-    g.replay()
-    torch.cuda.synchronize()
-    times = []
-    for _ in range(5):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        times.append(e0.elapsed_time(e1) * 1000.0 / steps)
-    times.sort()
-    us = times[len(times) // 2]
+    us = b.per_launch_us(launches, 5)[0]
     return us, b.items[0]["bytes"]
 
 
@@ -195,11 +197,11 @@ def main():
     bench = Bench(specs, 1, 600e6)
     print("# packed " + ", ".join(f"{it['spec'].name} x{len(it['packs'])}" for it in bench.items), file=sys.stderr,
           flush=True)
-    total_ms, per_ms, wall = bench.run(args.steps, args.warmup)
+    total_ms, wall = bench.run(args.steps, args.warmup)
+    kern_us = bench.per_launch_us()
     step_bytes = sum(it["bytes"] for it in bench.items)
     value = step_bytes * args.steps / (total_ms * 1e-3) / 1e9
-    kern_us = [m * 1000.0 for m in per_ms]
-    achieved = step_bytes / (sum(per_ms) * 1e-3) / 1e9
+    achieved = step_bytes / (sum(kern_us) * 1e-6) / 1e9
     per_layer = {}
     for it, us in zip(bench.items, kern_us):
         s = it["spec"]
@@ -218,7 +220,7 @@ def main():
         "config": {"workload": WORKLOAD, "global_batch": 1, "g_r": args.g_r, "layers": per_layer},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "k_gemv_mu8_b1 (per-launch HIP events on the launch stream)",
+                     "kernel": "k_gemv_mu8_b1 (HIP events around graph replays of back-to-back launches)",
                      "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}},
         "wall_s_timed": round(wall, 3),
     }

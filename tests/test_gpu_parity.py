@@ -256,3 +256,39 @@ def test_zero_activation_gives_zero():
     packed = pack_layer(L)
     y = run_gemm(packed, np.zeros((1, 512), np.uint16), out_fp32=True)
     assert np.all(y == 0)
+
+
+def test_graph_replays_match_eager():
+    """The kernels captured in a HIP graph give the eager result on every replay, with eager work in between."""
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    log("case graph replay")
+    outs = []
+    specs = [LayerSpec("g1", M=3000, N=2048, Kb=2, Ks=1, mu=8, S=70, g_r=128, g_s=70, seed=31),
+             LayerSpec("g2", M=700, N=512, Kb=2, Ks=1, mu=4, S=9, g_r=512, g_s=9, seed=32)]
+    for spec in specs:
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        for B in (1, 3):
+            x = x_tensor(make_activations(L, B))
+            ws = fb.make_workspace(packed, B)
+            y_eager = (fb.fluxbin_lut_gemv(packed, x[0], out_fp32=True, workspace=ws)[None] if B == 1 else
+                       fb.fluxbin_lut_gemm_smallbatch(packed, x, out_fp32=True, workspace=ws)).clone()
+            y = torch.empty_like(y_eager)
+            g = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                with torch.cuda.graph(g, stream=side):
+                    if B == 1:
+                        fb.fluxbin_lut_gemv(packed, x[0], y=y[0], out_fp32=True, workspace=ws)
+                    else:
+                        fb.fluxbin_lut_gemm_smallbatch(packed, x, y=y, out_fp32=True, workspace=ws)
+            torch.cuda.current_stream().wait_stream(side)
+            for r in range(4):
+                y.fill_(float("nan"))
+                g.replay()
+                torch.cuda.synchronize()
+                assert torch.equal(y, y_eager), (spec.name, B, r)
+                fb.fluxbin_lut_gemv(packed, x[0], out_fp32=True, workspace=ws)   # eager work between replays
+                torch.cuda.synchronize()
