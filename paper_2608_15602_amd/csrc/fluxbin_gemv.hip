@@ -77,8 +77,8 @@ __device__ __forceinline__ void store_y(const GemmArgs& a, int b, int64_t row, f
 // tile_end() (store_tile_y / store_partial): if the workgroup covers the whole tile it stores y directly; otherwise it stores its partial sums with
 // device-coherent (agent-scope) stores into its slot (0 for its first tile, 1 for its last one) and returns true:
 // the tile is then "pending". Nothing waits here, so the prefetched sign loads stay in flight.
-// publish(): called once per pending tile after the workgroup has waited for all its memory operations. Thread 0
-// bumps the tile's counter; the workgroup that brings it to the number of contributors adds the partial sums of all
+// publish_pending(): once the workgroup has waited for all its memory operations, thread 0 bumps the counters of its
+// pending tiles; the workgroup that brings a counter to the number of contributors adds the partial sums of all
 // contributors in workgroup order (a fixed order, so y is the same on every run), stores y and resets the counter.
 // ---------------------------------------------------------------------------------------------------------------------
 
@@ -123,23 +123,16 @@ __device__ __forceinline__ bool tile_end(const GemmArgs& a, int64_t tile, int64_
   return true;
 }
 
+// Adds the partial sums of all contributors of a tile whose counter this workgroup completed, in workgroup order, and
+// stores y. Contributors b_first..b_last: all but the first start inside the tile (slot 0); the first one used slot 1
+// unless its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
 template <int NT, int RPT, int BP>
-__device__ __forceinline__ void publish(const GemmArgs& a, int64_t tile, int* s_flag) {
+__device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
+  constexpr int CH = (RPT * BP == 1) ? 32 : 16;
   const int t = threadIdx.x;
   const int64_t R = int64_t(NT) * RPT;
   const int b_first = owner_of(a, int(tile) * a.steps);
   const int b_last = owner_of(a, int(tile + 1) * a.steps - 1);
-  if (t == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(a.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *s_flag = (prev == uint32_t(b_last - b_first)) ? 1 : 0;
-  }
-  __syncthreads();
-  const int last = *s_flag;
-  __syncthreads();
-  if (!last) return;
-  // Contributors b_first..b_last. All but the first start inside this tile (slot 0); the first one used slot 1 unless
-  // its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
-  constexpr int CH = 16;
   const int n_c = int(b_last - b_first + 1);
   const bool first_in_slot1 = first_unit(a, b_first) < int(tile) * a.steps;
 #pragma unroll
@@ -174,15 +167,38 @@ __device__ __forceinline__ void publish(const GemmArgs& a, int64_t tile, int* s_
   if (t == 0) __hip_atomic_store(a.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Waits until every memory operation of the workgroup has completed, then publishes its pending tiles.
+// Waits until every memory operation of the workgroup has completed, then publishes its pending tiles (at most two:
+// its first and its last tile). Thread 0 bumps both counters back to back, so the two round trips overlap; a counter
+// that reaches the number of contributors makes this workgroup the one that reduces that tile.
 template <int NT, int RPT, int BP>
 __device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0, int pending1, int n_pending,
                                                 int* s_flag) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (n_pending > 0) publish<NT, RPT, BP>(a, pending0, s_flag);
-  if (n_pending > 1) publish<NT, RPT, BP>(a, pending1, s_flag);
+  if (n_pending == 0) return;
+  if (threadIdx.x == 0) {
+    const int tiles[2] = {pending0, pending1};
+    uint32_t prev[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      if (i < n_pending)
+        prev[i] = __hip_atomic_fetch_add(a.counters + tiles[i], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int flags = 0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (i < n_pending) {
+        const int bf = owner_of(a, tiles[i] * a.steps);
+        const int bl = owner_of(a, (tiles[i] + 1) * a.steps - 1);
+        if (prev[i] == uint32_t(bl - bf)) flags |= 1 << i;
+      }
+    }
+    *s_flag = flags;
+  }
+  __syncthreads();
+  const int flags = *s_flag;
+  if (flags & 1) reduce_tile<NT, RPT, BP>(a, pending0);
+  if (flags & 2) reduce_tile<NT, RPT, BP>(a, pending1);
 }
 
 // Read-only table entry with a wave-uniform index, through the constant address space so that it is a scalar load
@@ -203,8 +219,9 @@ __device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
 // The byte address of a lookup, (p << 8) | (slot << 6) | (s << 2), is formed by one v_perm_b32 from the sign word and
 // a per-lane constant; the buffer is an immediate offset.
 //
-// Pipeline per workgroup: the sign words and row scales of unit k+2 are requested while the tables of unit k+1 are
-// built (other LDS buffer) and unit k is looked up, so two units of sign data are always in flight. The folded
+// Pipeline per workgroup: a register ring of D+1 units of sign words and row scales; unit k+D is requested while the
+// tables of unit k+1 are built (other LDS buffer) and unit k is looked up, so D+1 units of sign data are in flight at
+// every wait. The folded
 // activations of all the workgroup's units (at most kXvUnits, guaranteed by the launch plan) are staged in LDS first.
 // =====================================================================================================================
 
@@ -350,6 +367,23 @@ __device__ __forceinline__ void cursor_init(const GemmArgs& a, Cursor<NT, RPT>& 
   cursor_rows<NT, RPT>(a, c);
 }
 
+// Past the workgroup's last unit the pipeline keeps requesting (so that the number of loads in flight, which the
+// waits count, is the same on every path): those requests read a 1 KB region at the start of the sign section and
+// the first row-scale word, which stay cached.
+template <int NT, int RPT>
+__device__ __forceinline__ void cursor_dummy(const GemmArgs& a, Cursor<NT, RPT>& c) {
+  c.sbase = a.signs;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    c.soff[j] = (threadIdx.x & 63u) * 16u;
+    c.roff[j] = 0u;
+  }
+}
+
+// Advances the cursor to the next unit, or to the dummy region when that unit is past the workgroup's range.
+template <int NT, int RPT>
+__device__ __forceinline__ void cursor_advance(const GemmArgs& a, Cursor<NT, RPT>& c, bool has_next);
+
 template <int NT, int RPT>
 __device__ __forceinline__ void cursor_next(const GemmArgs& a, Cursor<NT, RPT>& c) {
   if (++c.sc == a.steps) {
@@ -360,6 +394,14 @@ __device__ __forceinline__ void cursor_next(const GemmArgs& a, Cursor<NT, RPT>& 
   } else {
     c.sbase += int64_t(2) * a.Mp * 16;
   }
+}
+
+template <int NT, int RPT>
+__device__ __forceinline__ void cursor_advance(const GemmArgs& a, Cursor<NT, RPT>& c, bool has_next) {
+  if (has_next)
+    cursor_next<NT, RPT>(a, c);
+  else
+    cursor_dummy<NT, RPT>(a, c);
 }
 
 // Issue the loads of the cursor's unit: sign words of both stored chunks (issue_signs) and the row-scale words of both
@@ -444,11 +486,11 @@ struct B1State {
   float acc[RPT][1];
 };
 
-// Step K of the pipeline (K = unit index within the workgroup): request unit K+D into its ring slot, build unit
-// K+1 into LDS buffer (K+1) % 2, look up unit K (ring slot K % (D+1), buffer K % 2). The steps are unrolled at compile
-// time (a workgroup has at most kXvUnits units) so that the wait before each lookup covers exactly the loads of unit
-// K: past the last unit the request repeats the last unit (cache hits), which keeps the count of loads in flight the
-// same on every path.
+// Step K of the pipeline (K = unit index within the workgroup): request unit K+D into ring slot (K+D) % (D+1) (the
+// slot of unit K-1, looked up in the previous step), build unit K+1 into LDS buffer (K+1) % 2, look up unit K (slot
+// K % (D+1), buffer K % 2). The prologue requests units 0..D-1, so D+1 units are in flight at every wait. The steps
+// are unrolled at compile time (a workgroup has at most kXvUnits units) so that the wait before each lookup covers
+// exactly the loads of unit K.
 template <int NT, int RPT, int D, int K>
 __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
                                          Ring<RPT> (&ring)[D + 1], float* lut, float* xs, const uint32_t (&c1)[4],
@@ -456,10 +498,11 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
   if constexpr (K < kXvUnits) {
     if (K >= st.n) return;
     constexpr int BUF = K & 1;
-    constexpr int KI = (K + D) < kXvUnits ? (K + D) : kXvUnits - 1;   // unit requested now (clamped past the end)
+    constexpr int KI = (K + D) < kXvUnits ? (K + D) : kXvUnits - 1;   // unit requested (clamped)
     issue_signs<NT, RPT>(a, cur, ring[(K + D) % (D + 1)]);
-    issue_rscale<NT, RPT>(a, cur, plane_of(s_planes, KI, st.n), plane_of(s_planes, KI, st.n, 1), ring[(K + D) % (D + 1)]);
-    if (K + D + 1 < st.n) cursor_next<NT, RPT>(a, cur);
+    issue_rscale<NT, RPT>(a, cur, plane_of(s_planes, KI, st.n), plane_of(s_planes, KI, st.n, 1),
+                          ring[(K + D) % (D + 1)]);
+    cursor_advance<NT, RPT>(a, cur, K + D + 1 < st.n);
     if (K + 1 < st.n) build_b1<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
     lookup_b1<NT, RPT, BUF>(lut, ring[K % (D + 1)], c1, c2, hb, st.acc);
     if (st.sc == a.steps - 1 || K + 1 == st.n) {
@@ -505,10 +548,18 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
 #pragma unroll
   for (int j = 0; j < RPT; ++j) st.acc[j][0] = 0.f;
 
-  // Prologue: activation, column-scale and row-scale-plane loads first, then the sign loads of units 0..D-1, so that
-  // waiting for the former does not wait for the latter. The row scales of units 0..D-1 follow once the planes are
-  // staged in LDS.
+  // Prologue: the row-scale planes of units 0..D-1 as scalar loads (their own counter), the activation, column-scale
+  // and plane-table loads, then the sign loads of units 0..D-1 and their row-scale loads, so that waiting for the
+  // staged activations never waits for the sign data and the first lookup does not wait for a late row-scale request.
   const bool hb = ((t >> 4) & 1) != 0;
+  int32_t pl[D][2];
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    int sck = st.sc + (k < st.n ? k : st.n - 1);
+    while (sck >= a.steps) sck -= a.steps;
+    pl[k][0] = load_uniform_i32(a.chunk_plane, 2 * sck);
+    pl[k][1] = load_uniform_i32(a.chunk_plane, 2 * sck + 1);
+  }
   Staged<NT> sg;
   stage_issue<NT>(a, sg, st.sc);
   Cursor<NT, RPT> cur;
@@ -516,9 +567,14 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   Ring<RPT> ring[D + 1];
   Cursor<NT, RPT> cur0 = cur;
 #pragma unroll
-  for (int k = 0; k < D; ++k) {   // units 0..D-1 (repeating the last unit past the end)
+  for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
     issue_signs<NT, RPT>(a, cur, ring[k]);
-    if (k + 1 < st.n) cursor_next<NT, RPT>(a, cur);
+    cursor_advance<NT, RPT>(a, cur, k + 1 < st.n);
+  }
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    issue_rscale<NT, RPT>(a, cur0, pl[k][0], pl[k][1], ring[k]);
+    cursor_advance<NT, RPT>(a, cur0, k + 1 < st.n);
   }
 
   // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32.
@@ -537,11 +593,6 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
 
   stage_finish<NT>(a, sg, xs, s_planes, st.sc, st.n);   // the launch plan keeps n <= kXvUnits
   __syncthreads();
-#pragma unroll
-  for (int k = 0; k < D; ++k) {
-    issue_rscale<NT, RPT>(a, cur0, plane_of(s_planes, k, st.n), plane_of(s_planes, k, st.n, 1), ring[k]);
-    if (k + 1 < st.n) cursor_next<NT, RPT>(a, cur0);
-  }
   build_b1<NT, 0>(lut, xs);
   __syncthreads();
   steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes);

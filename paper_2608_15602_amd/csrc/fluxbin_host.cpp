@@ -123,17 +123,24 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int cus = device_cu_count();
   if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
   std::memset(p, 0, sizeof(*p));
-  const int per_cu = env_int("FLUXBIN_BLOCKS_PER_CU", 2);
-  const int64_t target = int64_t(cus) * (per_cu >= 1 && per_cu <= 8 ? per_cu : 2);
   const int force_generic = env_int("FLUXBIN_GENERIC", 0);
   const int rpt_env = env_int("FLUXBIN_RPT", 0);
+  int per_cu = env_int("FLUXBIN_BLOCKS_PER_CU", 0);
   p->nt = 256;
   if (L.shape.mu == 8 && B == 1 && !force_generic) {
     p->kernel = 0;
-    const int nt_env = env_int("FLUXBIN_NT", 512);
+    const int nt_env = env_int("FLUXBIN_NT", 0);
     const int depth_env = env_int("FLUXBIN_DEPTH", 2);
     p->depth = (depth_env == 3 || depth_env == 4 || depth_env == 6) ? depth_env : 2;
-    p->nt = (nt_env == 256 || nt_env == 1024) ? nt_env : 512;
+    // 1024-thread workgroups, one per CU, amortize each table over the most rows and keep the fewest, longest
+    // pipelines; layers with fewer than one 1024-row unit per CU use smaller workgroups (more, shorter units).
+    if (nt_env == 256 || nt_env == 512 || nt_env == 1024) {
+      p->nt = nt_env;
+    } else {
+      p->nt = 1024;
+      while (p->nt > 256 && ceil_div(L.shape.M, p->nt) * L.NSC < cus) p->nt /= 2;
+    }
+    if (per_cu < 1 || per_cu > 8) per_cu = 1024 / p->nt;
     p->bg = 1;
     p->n_groups = 1;
   } else {
@@ -141,16 +148,21 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     p->bg = B == 1 ? 1 : (B == 2 ? 2 : 4);
     p->n_groups = int((B + p->bg - 1) / p->bg);
     if (p->n_groups == 3) p->n_groups = 4;  // instantiated batch paddings: 1, 2, 4, 8, 16
+    if (per_cu < 1 || per_cu > 8) per_cu = 2;
   }
+  const int64_t target = int64_t(cus) * per_cu;
   p->bpad = p->bg * p->n_groups;
   const int64_t steps = (p->kernel == 0) ? L.NSC : (2 * L.NSC) * p->n_groups;
-  // instantiated rows per thread: batch-1 kernel 4/2/1 at 256 threads, 2/1 at 512 and 1024; the generic kernel 4
-  // only for mu = 8 with <= 2 batch rows
+  // instantiated rows per thread: batch-1 kernel 4/2/1 at 256 threads, 2/1 at 512 and 1024 (default 1: one row per
+  // thread gives the most units to balance and the lightest registers); the generic kernel 4 only for mu = 8 with
+  // <= 2 batch rows
   int rpt_max = (p->kernel == 0 || (L.shape.mu == 8 && p->bpad <= 2)) ? 4 : 2;
   if (p->kernel == 0) rpt_max = p->nt == 256 ? 4 : 2;
   int chosen = 1;
   if (rpt_env == 1 || rpt_env == 2 || rpt_env == 4) {
     chosen = rpt_env > rpt_max ? rpt_max : rpt_env;
+  } else if (p->kernel == 0) {
+    chosen = 1;
   } else {
     for (int rpt = rpt_max; rpt >= 1; rpt /= 2) {
       const int64_t tiles = ceil_div(L.shape.M, int64_t(p->nt) * rpt);
