@@ -136,6 +136,36 @@ class Bench:
         return out
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_gemv_mu8_b1_mlp70b_hbm_traffic.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_15602_amd", "csrc", f) for f in ("fluxbin_gemv.hip", "fluxbin_host.cpp")]
+
+
+def measured_traffic():
+    """HBM bytes per launch of each layer from the committed counter summary (FETCH_SIZE and WRITE_SIZE passes scaled
+    by a plain copy of known size), or None when the kernel or launch-plan sources changed since it was taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    sha = None
+    per = {}
+    for line in text.splitlines():
+        if line.startswith("kernel_source_sha256:"):
+            sha = line.split()[1]
+        if line.startswith("traffic_bytes_per_launch:"):
+            for kv in line.split(":", 1)[1].split():
+                k, v = kv.split("=")
+                per[k] = int(v)
+    if sha != h.hexdigest() or not per:
+        return None
+    return per
+
+
 def cpu_baseline(bench, budget_s: float):
     """The fp64 oracle (explicit reconstruction + matvec, untuned) on a bounded contiguous row sample of each layer;
     throughput scaled to the same algorithmic bytes per row as the GPU figure."""
@@ -184,6 +214,11 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 per-call figure")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="before anything else, run a plain device-to-device copy of this many MiB three times "
+                         "(the reference dispatch for HBM byte counters)")
+    ap.add_argument("--eager-launches", type=int, default=0,
+                    help="counter-collection mode: launch each layer this many times without graphs, then exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is design-only (DESIGN.md)",
@@ -193,15 +228,34 @@ def main():
     from synth import config_layers
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     print(f"# device {torch.cuda.get_device_name(0)}", file=sys.stderr, flush=True)
+    if args.copy_calib_mib > 0:
+        n = args.copy_calib_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        print(f"# copy calibration: 3 x {n} bytes device-to-device", file=sys.stderr, flush=True)
     specs = config_layers("c4_mlp70b", args.g_r)
     bench = Bench(specs, 1, 600e6)
     print("# packed " + ", ".join(f"{it['spec'].name} x{len(it['packs'])}" for it in bench.items), file=sys.stderr,
           flush=True)
+    if args.eager_launches > 0:
+        for it in bench.items:
+            for s in range(args.eager_launches):
+                bench.launch(it, s)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "eager launches for counter collection", "launches_per_layer": args.eager_launches,
+                          "layers": [it["spec"].name for it in bench.items],
+                          "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}}), flush=True)
+        return
     total_ms, wall = bench.run(args.steps, args.warmup)
     kern_us = bench.per_launch_us()
     step_bytes = sum(it["bytes"] for it in bench.items)
     value = step_bytes * args.steps / (total_ms * 1e-3) / 1e9
     achieved = step_bytes / (sum(kern_us) * 1e-6) / 1e9
+    traffic = measured_traffic()
     per_layer = {}
     for it, us in zip(bench.items, kern_us):
         s = it["spec"]
@@ -219,7 +273,9 @@ def main():
         "data": "synthetic (seeded Llama-70B-shaped MLP layers; no trained weights)",
         "config": {"workload": WORKLOAD, "global_batch": 1, "g_r": args.g_r, "layers": per_layer},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": (sum(traffic[it["spec"].name] for it in bench.items) if traffic else None),
+                     "traffic_per_launch": traffic,
                      "kernel": "k_gemv_mu8_b1 (HIP events around graph replays of back-to-back launches)",
                      "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}},
         "wall_s_timed": round(wall, 3),

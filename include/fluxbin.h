@@ -52,7 +52,7 @@ const char* fluxbin_last_error_message(void);
 
 /*
  * Logical shape of one layer (paper notation, Sec. 3.1 and App. C.2).
- *   M    output channels (rows of W), 1 <= M <= 2^31 - 1.
+ *   M    output channels (rows of W), 1 <= M <= 2^27 (the kernels address a row of a sign plane with 32-bit offsets).
  *   N    input channels (columns of W), 1 <= N <= 65535 (salient and activation indices are stored in 16 bits, as in
  *        App. C.2).
  *   Kb   global bases, 1..4.            Ks   salient bases, 0..4 (the paper uses Ks = Kb; the hybrid configs here 1).

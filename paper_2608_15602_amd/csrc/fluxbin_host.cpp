@@ -44,8 +44,9 @@ int device_cu_count() {
 
 static fluxbin_status check_shape(const fluxbin_shape* s) {
   if (!s) return fail(FLUXBIN_ERR_INVALID_ARG, "shape is NULL");
-  if (s->M < 1 || s->M > (int64_t(1) << 30))
-    return fail(FLUXBIN_ERR_INVALID_ARG, "M = %lld out of range [1, 2^30]", (long long)s->M);
+  // M <= 2^27 keeps every byte offset of a row inside the two sign planes of a super-chunk below 2^32
+  if (s->M < 1 || s->M > (int64_t(1) << 27))
+    return fail(FLUXBIN_ERR_INVALID_ARG, "M = %lld out of range [1, 2^27]", (long long)s->M);
   if (s->N < 1) return fail(FLUXBIN_ERR_INVALID_ARG, "N = %lld must be >= 1", (long long)s->N);
   if (s->N > 65535)
     return fail(FLUXBIN_ERR_UNSUPPORTED, "N = %lld exceeds 65535 (16-bit column indices)", (long long)s->N);

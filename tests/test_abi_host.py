@@ -65,6 +65,7 @@ def test_pack_query_matches_format(L, kw):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(M=0), fb.FLUXBIN_ERR_INVALID_ARG),
+    (dict(M=(1 << 27) + 1), fb.FLUXBIN_ERR_INVALID_ARG),
     (dict(N=0), fb.FLUXBIN_ERR_INVALID_ARG),
     (dict(N=70000, g_r=70000), fb.FLUXBIN_ERR_UNSUPPORTED),
     (dict(Kb=0), fb.FLUXBIN_ERR_INVALID_ARG),
