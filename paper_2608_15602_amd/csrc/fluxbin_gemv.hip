@@ -128,16 +128,17 @@ __device__ __forceinline__ bool tile_end(const GemmArgs& a, int64_t tile, int64_
 // unless its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
 template <int NT, int RPT, int BP>
 __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
-  constexpr int CH = (RPT * BP == 1) ? 32 : 16;
+  constexpr int CH = (RPT * BP == 1) ? 48 : 16;
   const int t = threadIdx.x;
   const int64_t R = int64_t(NT) * RPT;
   const int b_first = owner_of(a, int(tile) * a.steps);
   const int b_last = owner_of(a, int(tile + 1) * a.steps - 1);
   const int n_c = int(b_last - b_first + 1);
   const bool first_in_slot1 = first_unit(a, b_first) < int(tile) * a.steps;
+  const char* pbase = reinterpret_cast<const char*>(a.partials);
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
-    const int64_t r = t + NT * j;
+    const int r = t + NT * j;
     const int64_t row = tile * R + r;
     float sum[BP];
 #pragma unroll
@@ -146,17 +147,20 @@ __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
       float v[CH][BP];
 #pragma unroll
       for (int k = 0; k < CH; ++k) {
-        const int c = c0 + k < n_c ? c0 + k : n_c - 1;
-        const int sl = (c == 0 && first_in_slot1) ? 1 : 0;
-        const float* src = a.partials + ((int64_t(b_first + c) * 2 + sl) * BP) * R;
+        const int c = c0 + k;
+        // slot of contributor c (wave-uniform); contributors past n_c are not read
+        const int slot = (b_first + c) * 2 + ((c == 0 && first_in_slot1) ? 1 : 0);
+        const char* src = pbase + int64_t(slot) * (BP * R * 4);
 #pragma unroll
         for (int b = 0; b < BP; ++b)
-          v[k][b] = __hip_atomic_load(src + b * R + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          v[k][b] = c < n_c ? __hip_atomic_load(reinterpret_cast<const float*>(src + uint32_t((b * R + r) * 4)),
+                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                            : 0.f;
       }
 #pragma unroll
       for (int k = 0; k < CH; ++k)
 #pragma unroll
-        for (int b = 0; b < BP; ++b) sum[b] += (c0 + k < n_c) ? v[k][b] : 0.f;
+        for (int b = 0; b < BP; ++b) sum[b] += v[k][b];
     }
     if (row < a.M) {
 #pragma unroll
@@ -245,12 +249,16 @@ struct Ring {
 
 // Stage the folded activations xv = x[j] * colscale of the n <= kXvUnits units starting at super-chunk sc0 into
 // xs[k*256 + col] (super-chunks wrap around at the end of a tile). Global chunks read x[j] directly (j follows from the
-// chunk index); salient chunks read their input column from the VCM index table first. stage_issue() only issues the
-// loads; stage_finish() waits for them and writes LDS, so the sign loads can be issued in between.
+// chunk index); salient chunks read their input column from the VCM index table first (Eq. 13), then gather it.
+// stage_issue() issues the loads. stage_write_global() waits for them (nothing else is in flight yet, so this is one
+// short round trip), writes the global and padding columns and issues the salient gathers; the sign loads follow, and
+// stage_write_salient() writes the gathered columns of a range of units when they are needed (waiting for the gathers
+// never waits for sign data, which was requested after them).
 template <int NT>
 struct Staged {
   uint32_t v[B1<NT, 1>::KPT];    // x bits (global column) or the index (salient column)
   uint32_t cs[B1<NT, 1>::KPT];   // column scale bits
+  uint32_t g[B1<NT, 1>::KPT];    // gathered x bits of salient columns
   int32_t plane;                 // threads t < 2*kXvUnits: row-scale plane of chunk 2*sc(t/2) + (t&1)
 };
 
@@ -281,8 +289,15 @@ __device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, i
 }
 
 template <int NT>
-__device__ __forceinline__ void stage_finish(const GemmArgs& a, const Staged<NT>& sg, float* xs, int* s_planes,
-                                             int sc0, int n) {
+__device__ __forceinline__ bool staged_salient(const GemmArgs& a, int sc0, int k, int col) {
+  int sc = sc0 + k;
+  while (sc >= a.steps) sc -= a.steps;
+  return ((sc * 256 + col) >> 7) >= a.ngc;
+}
+
+template <int NT>
+__device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT>& sg, float* xs, int* s_planes,
+                                                   int sc0, int n) {
   using P = B1<NT, 1>;
   const int t = threadIdx.x;
   const int col = t & 255;
@@ -290,16 +305,24 @@ __device__ __forceinline__ void stage_finish(const GemmArgs& a, const Staged<NT>
 #pragma unroll
   for (int m = 0; m < P::KPT; ++m) {
     const int k = (t >> 8) + m * (NT / 256);
-    int sc = sc0 + k;
-    while (sc >= a.steps) sc -= a.steps;
-    const int c = (sc * 256 + col) >> 7;
-    uint32_t xb = sg.v[m];
-    bool zero = false;
-    if (c >= a.ngc) {   // salient or padding column: v holds the VCM index
-      zero = sg.v[m] == 0xFFFFu;
-      xb = zero ? 0u : uint32_t(a.x[sg.v[m]]);
-    }
-    if (k < n) xs[k * 256 + col] = zero ? 0.f : h2f(uint16_t(xb)) * h2f(uint16_t(sg.cs[m]));
+    const bool sal = staged_salient<NT>(a, sc0, k, col);
+    // unconditional, always in-bounds gather (x[0] for the other columns)
+    sg.g[m] = a.x[(sal && sg.v[m] != 0xFFFFu) ? sg.v[m] : 0u];
+    if (k < n && !sal) xs[k * 256 + col] = h2f(uint16_t(sg.v[m])) * h2f(uint16_t(sg.cs[m]));
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void stage_write_salient(const GemmArgs& a, const Staged<NT>& sg, float* xs, int sc0,
+                                                    int n, int k_begin, int k_end) {
+  using P = B1<NT, 1>;
+  const int t = threadIdx.x;
+  const int col = t & 255;
+#pragma unroll
+  for (int m = 0; m < P::KPT; ++m) {
+    const int k = (t >> 8) + m * (NT / 256);
+    if (k >= k_begin && k < k_end && k < n && staged_salient<NT>(a, sc0, k, col))
+      xs[k * 256 + col] = sg.v[m] == 0xFFFFu ? 0.f : h2f(uint16_t(sg.g[m])) * h2f(uint16_t(sg.cs[m]));
   }
 }
 
@@ -494,7 +517,8 @@ struct B1State {
 template <int NT, int RPT, int D, int K>
 __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
                                          Ring<RPT> (&ring)[D + 1], float* lut, float* xs, const uint32_t (&c1)[4],
-                                         const uint32_t (&c2)[4], bool hb, const int* s_planes) {
+                                         const uint32_t (&c2)[4], bool hb, const int* s_planes,
+                                         const Staged<NT>& sg, int sc0) {
   if constexpr (K < kXvUnits) {
     if (K >= st.n) return;
     constexpr int BUF = K & 1;
@@ -504,6 +528,7 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
                           ring[(K + D) % (D + 1)]);
     cursor_advance<NT, RPT>(a, cur, K + D + 1 < st.n);
     if (K + 1 < st.n) build_b1<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
+    if constexpr (K == 0) stage_write_salient<NT>(a, sg, xs, sc0, st.n, 2, kXvUnits);   // built from step 1 on
     lookup_b1<NT, RPT, BUF>(lut, ring[K % (D + 1)], c1, c2, hb, st.acc);
     if (st.sc == a.steps - 1 || K + 1 == st.n) {
       const bool shared = st.tile == st.first_tile ? st.first_shared : (st.tile == st.last_tile ? st.last_shared : false);
@@ -521,7 +546,7 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
       st.sc = 0;
       ++st.tile;
     }
-    steps_b1<NT, RPT, D, K + 1>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes);
+    steps_b1<NT, RPT, D, K + 1>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes, sg, sc0);
   }
 }
 
@@ -548,9 +573,10 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
 #pragma unroll
   for (int j = 0; j < RPT; ++j) st.acc[j][0] = 0.f;
 
-  // Prologue: the row-scale planes of units 0..D-1 as scalar loads (their own counter), the activation, column-scale
-  // and plane-table loads, then the sign loads of units 0..D-1 and their row-scale loads, so that waiting for the
-  // staged activations never waits for the sign data and the first lookup does not wait for a late row-scale request.
+  // Prologue: the row-scale planes of units 0..D-1 as scalar loads (their own counter) and the activation,
+  // column-scale and plane-table loads; once they are in (a short round trip: nothing else is in flight yet) the
+  // global columns are staged and the salient gathers, the sign loads of units 0..D-1 and their row-scale loads are
+  // issued. The tables of unit 0 are built right after, so the pipeline starts while the first sign data streams in.
   const bool hb = ((t >> 4) & 1) != 0;
   int32_t pl[D][2];
 #pragma unroll
@@ -561,11 +587,13 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
     pl[k][1] = load_uniform_i32(a.chunk_plane, 2 * sck + 1);
   }
   Staged<NT> sg;
-  stage_issue<NT>(a, sg, st.sc);
+  const int sc0 = st.sc;
+  stage_issue<NT>(a, sg, sc0);
   Cursor<NT, RPT> cur;
   cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
   Ring<RPT> ring[D + 1];
   Cursor<NT, RPT> cur0 = cur;
+  stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);   // the launch plan keeps n <= kXvUnits
 #pragma unroll
   for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
     issue_signs<NT, RPT>(a, cur, ring[k]);
@@ -591,11 +619,11 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
     }
   }
 
-  stage_finish<NT>(a, sg, xs, s_planes, st.sc, st.n);   // the launch plan keeps n <= kXvUnits
+  stage_write_salient<NT>(a, sg, xs, sc0, st.n, 0, 2);
   __syncthreads();
   build_b1<NT, 0>(lut, xs);
   __syncthreads();
-  steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes);
+  steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes, sg, sc0);
   const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
   publish_pending<NT, RPT, 1>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
@@ -852,7 +880,8 @@ static void launch_b1(const GemmArgs& a, int depth, hipStream_t stream) {
     case 3: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 3>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
     case 4: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 4>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
     case 6: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 6>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
-    default: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 2>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 2>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
+    default: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 1>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
   }
 }
 

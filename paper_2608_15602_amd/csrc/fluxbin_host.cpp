@@ -131,8 +131,10 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   if (L.shape.mu == 8 && B == 1 && !force_generic) {
     p->kernel = 0;
     const int nt_env = env_int("FLUXBIN_NT", 0);
-    const int depth_env = env_int("FLUXBIN_DEPTH", 2);
-    p->depth = (depth_env == 3 || depth_env == 4 || depth_env == 6) ? depth_env : 2;
+    // units of sign data requested ahead of the one being looked up: one (two units, 64 KB per CU, in flight) already
+    // keeps HBM saturated; deeper rings only add queueing and prologue latency
+    const int depth_env = env_int("FLUXBIN_DEPTH", 1);
+    p->depth = (depth_env == 2 || depth_env == 3 || depth_env == 4 || depth_env == 6) ? depth_env : 1;
     // 1024-thread workgroups, one per CU, amortize each table over the most rows and keep the fewest, longest
     // pipelines; layers with fewer than one 1024-row unit per CU use smaller workgroups (more, shorter units).
     if (nt_env == 256 || nt_env == 512 || nt_env == 1024) {

@@ -82,7 +82,7 @@ struct Plan {
   int bg;           // batch rows per LUT group (generic kernel)
   int n_groups;     // batch groups
   int bpad;         // bg * n_groups
-  int depth;        // batch-1 kernel: units of sign data requested ahead (2, 3, 4 or 6)
+  int depth;        // batch-1 kernel: units of sign data requested ahead (1, 2, 3, 4 or 6)
   uint64_t ws_counters_off, ws_partials_off, ws_bytes;
 };
 
