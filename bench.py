@@ -197,6 +197,22 @@ def cpu_baseline(bench, budget_s: float):
             "sample": "; ".join(parts) + f" (fp64 reconstruct + matvec, {t_total:.1f} s)"}
 
 
+def small_batch_us(specs, batches, launches=40):
+    """Per-call microseconds of the small-batch LUT-GEMM (batch-interleaved tables, each sign word read once for all
+    batch rows) on the same layers, graph-timed like the batch-1 figure."""
+    import torch
+    out = {}
+    for B in batches:
+        b = Bench(specs, B, 600e6)
+        for it, us in zip(b.items, b.per_launch_us(launches, 3)):
+            s = it["spec"]
+            out[f"{s.name}_B{B}"] = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
+                                     "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2)}
+        del b
+        torch.cuda.empty_cache()
+    return out
+
+
 def small_layer_us(spec, launches=200):
     """Per-call microseconds of a small layer (4096x4096): a HIP graph of back-to-back launches rotating distinct
     packed copies (so the signs come from HBM), median of 5 replays."""
@@ -213,7 +229,7 @@ def main():
     ap.add_argument("--g-r", choices=["128", "N"], default="128")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 per-call figure")
+    ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 and small-batch per-call figures")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before anything else, run a plain device-to-device copy of this many MiB three times "
                          "(the reference dispatch for HBM byte counters)")
@@ -285,6 +301,7 @@ def main():
         us, b2 = small_layer_us(spec2)
         out["config"]["attn_4096x4096_us_per_gemv"] = round(us, 3)
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
+        out["config"]["small_batch"] = small_batch_us(specs, (4, 16))
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
     print(json.dumps(out), flush=True)

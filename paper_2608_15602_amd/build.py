@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfluxbin.so")
 
-SOURCES = ["fluxbin_host.cpp", "fluxbin_pack.hip", "fluxbin_gemv.hip"]
+SOURCES = ["fluxbin_host.cpp", "fluxbin_pack.hip", "fluxbin_gemv.hip", "fluxbin_gemm_batch.hip"]
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are kept out of the generated code (plain float code only).
@@ -47,7 +47,7 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(jobs: int = 3, verbose: bool = True) -> str:
+def build(jobs: int = 4, verbose: bool = True) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
         objs = list(ex.map(_compile, SOURCES))

@@ -1,0 +1,205 @@
+// Device-side pieces shared by the LUT-GEMV/GEMM kernels of libfluxbin: kernel arguments, the balanced split of
+// the work units over workgroups, and the deterministic split-tile reduction (tile counters + partial sums).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "fluxbin_internal.h"
+
+namespace fluxbin {
+
+struct GemmArgs {
+  const uint8_t* signs;
+  const uint16_t* rscale;
+  const uint16_t* colscale;
+  const uint16_t* xidx;
+  const int32_t* chunk_plane;
+  const uint16_t* x;
+  void* y;
+  float* partials;
+  uint32_t* counters;
+  int64_t ldx, ldy;
+  int32_t units, blocks;
+  int32_t uq, ur;    // units per workgroup: uq + 1 for the first ur workgroups, uq for the others
+  int32_t M, Mp, NSC, NCP;
+  int32_t steps;     // units per tile
+  int32_t B;         // batch rows actually present
+  int32_t y_fp32;
+  int32_t n_tiles;
+  int32_t N;         // input columns
+  int32_t ncg;       // chunks per global base
+  int32_t ngc;       // global chunks (Kb * ncg); chunks >= ngc are salient or padding
+};
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float h2f(uint16_t u) { return static_cast<float>(__builtin_bit_cast(_Float16, u)); }
+
+__device__ __forceinline__ uint16_t f2h(float f) { return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f)); }
+
+__device__ __forceinline__ uint4 load_stream16(const uint8_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Balanced split of the units: workgroup b owns [first_unit(b), first_unit(b + 1)), uq + 1 units for b < ur and uq
+// units otherwise (uq >= 1).
+__device__ __forceinline__ int first_unit(const GemmArgs& a, int b) { return b * a.uq + (b < a.ur ? b : a.ur); }
+
+__device__ __forceinline__ int owner_of(const GemmArgs& a, int u) {
+  const int big = a.ur * (a.uq + 1);
+  return u < big ? u / (a.uq + 1) : a.ur + (u - big) / a.uq;
+}
+
+__device__ __forceinline__ void store_y(const GemmArgs& a, int b, int64_t row, float v) {
+  if (a.y_fp32)
+    static_cast<float*>(a.y)[b * a.ldy + row] = v;
+  else
+    static_cast<uint16_t*>(a.y)[b * a.ldy + row] = f2h(v);
+}
+
+// ---------------------------------------------------------------------------------------------------------------------
+// End of a tile's contribution from one workgroup.
+//
+// tile_end() (store_tile_y / store_partial): if the workgroup covers the whole tile it stores y directly; otherwise it stores its partial sums with
+// device-coherent (agent-scope) stores into its slot (0 for its first tile, 1 for its last one) and returns true:
+// the tile is then "pending". Nothing waits here, so the prefetched sign loads stay in flight.
+// publish_pending(): once the workgroup has waited for all its memory operations, thread 0 bumps the counters of its
+// pending tiles; the workgroup that brings a counter to the number of contributors adds the partial sums of all
+// contributors in workgroup order (a fixed order, so y is the same on every run), stores y and resets the counter.
+// ---------------------------------------------------------------------------------------------------------------------
+
+// Whether workgroups other than the tile's first owner contribute to tile T.
+__device__ __forceinline__ bool tile_is_shared(const GemmArgs& a, int tile) {
+  return owner_of(a, tile * a.steps) != owner_of(a, (tile + 1) * a.steps - 1);
+}
+
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ void store_tile_y(const GemmArgs& a, int64_t tile, const float (&acc)[RPT][BP]) {
+  const int64_t R = int64_t(NT) * RPT;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    const int64_t row = tile * R + threadIdx.x + NT * j;
+    if (row < a.M) {
+#pragma unroll
+      for (int b = 0; b < BP; ++b)
+        if (b < a.B) store_y(a, b, row, acc[j][b]);
+    }
+  }
+}
+
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ void store_partial(const GemmArgs& a, int slot, const float (&acc)[RPT][BP]) {
+  const int64_t R = int64_t(NT) * RPT;
+  float* mine = a.partials + ((int64_t(blockIdx.x) * 2 + slot) * BP) * R;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+#pragma unroll
+    for (int b = 0; b < BP; ++b)
+      __hip_atomic_store(mine + b * R + threadIdx.x + NT * j, acc[j][b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ bool tile_end(const GemmArgs& a, int64_t tile, int64_t first_tile, const float (&acc)[RPT][BP]) {
+  if (!tile_is_shared(a, int(tile))) {
+    store_tile_y<NT, RPT, BP>(a, tile, acc);
+    return false;
+  }
+  store_partial<NT, RPT, BP>(a, tile == first_tile ? 0 : 1, acc);
+  return true;
+}
+
+// Adds the partial sums of all contributors of a tile whose counter this workgroup completed, in workgroup order, and
+// stores y. Contributors b_first..b_last: all but the first start inside the tile (slot 0); the first one used slot 1
+// unless its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
+  constexpr int CH = (RPT * BP == 1) ? 48 : 16;
+  const int t = threadIdx.x;
+  const int64_t R = int64_t(NT) * RPT;
+  const int b_first = owner_of(a, int(tile) * a.steps);
+  const int b_last = owner_of(a, int(tile + 1) * a.steps - 1);
+  const int n_c = int(b_last - b_first + 1);
+  const bool first_in_slot1 = first_unit(a, b_first) < int(tile) * a.steps;
+  const char* pbase = reinterpret_cast<const char*>(a.partials);
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    const int r = t + NT * j;
+    const int64_t row = tile * R + r;
+    float sum[BP];
+#pragma unroll
+    for (int b = 0; b < BP; ++b) sum[b] = 0.f;
+    for (int c0 = 0; c0 < n_c; c0 += CH) {
+      float v[CH][BP];
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        const int c = c0 + k;
+        // slot of contributor c (wave-uniform); contributors past n_c are not read
+        const int slot = (b_first + c) * 2 + ((c == 0 && first_in_slot1) ? 1 : 0);
+        const char* src = pbase + int64_t(slot) * (BP * R * 4);
+#pragma unroll
+        for (int b = 0; b < BP; ++b)
+          v[k][b] = c < n_c ? __hip_atomic_load(reinterpret_cast<const float*>(src + uint32_t((b * R + r) * 4)),
+                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                            : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < CH; ++k)
+#pragma unroll
+        for (int b = 0; b < BP; ++b) sum[b] += v[k][b];
+    }
+    if (row < a.M) {
+#pragma unroll
+      for (int b = 0; b < BP; ++b)
+        if (b < a.B) store_y(a, b, row, sum[b]);
+    }
+  }
+  if (t == 0) __hip_atomic_store(a.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until every memory operation of the workgroup has completed, then publishes its pending tiles (at most two:
+// its first and its last tile). Thread 0 bumps both counters back to back, so the two round trips overlap; a counter
+// that reaches the number of contributors makes this workgroup the one that reduces that tile.
+template <int NT, int RPT, int BP>
+__device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0, int pending1, int n_pending,
+                                                int* s_flag) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (n_pending == 0) return;
+  if (threadIdx.x == 0) {
+    const int tiles[2] = {pending0, pending1};
+    uint32_t prev[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      if (i < n_pending)
+        prev[i] = __hip_atomic_fetch_add(a.counters + tiles[i], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int flags = 0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (i < n_pending) {
+        const int bf = owner_of(a, tiles[i] * a.steps);
+        const int bl = owner_of(a, (tiles[i] + 1) * a.steps - 1);
+        if (prev[i] == uint32_t(bl - bf)) flags |= 1 << i;
+      }
+    }
+    *s_flag = flags;
+  }
+  __syncthreads();
+  const int flags = *s_flag;
+  if (flags & 1) reduce_tile<NT, RPT, BP>(a, pending0);
+  if (flags & 2) reduce_tile<NT, RPT, BP>(a, pending1);
+}
+
+// Read-only table entry with a wave-uniform index, through the constant address space so that it is a scalar load
+// (its own counter): waiting for it never waits for the vector loads in flight.
+__device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
+  return ((const __attribute__((address_space(4))) int32_t*)p)[i];
+}
+
+// Small-batch mu = 8 kernel (fluxbin_gemm_batch.hip): launches k_gemm_mu8_batch with n_groups groups of four batch
+// rows; false if no instance exists.
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, hipStream_t stream);
+
+}  // namespace fluxbin

@@ -146,6 +146,14 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (per_cu < 1 || per_cu > 8) per_cu = 1024 / p->nt;
     p->bg = 1;
     p->n_groups = 1;
+  } else if (L.shape.mu == 8 && B >= 2 && !force_generic) {
+    // small batch: 1024-row tiles, one 128-column chunk per unit, batch in groups of four rows
+    p->kernel = 2;
+    p->nt = 1024;
+    p->depth = 1;
+    p->bg = 4;
+    p->n_groups = B <= 4 ? 1 : (B <= 8 ? 2 : 4);
+    if (per_cu < 1 || per_cu > 8) per_cu = 1;
   } else {
     p->kernel = 1;
     p->bg = B == 1 ? 1 : (B == 2 ? 2 : 4);
@@ -155,14 +163,16 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   }
   const int64_t target = int64_t(cus) * per_cu;
   p->bpad = p->bg * p->n_groups;
-  const int64_t steps = (p->kernel == 0) ? L.NSC : (2 * L.NSC) * p->n_groups;
+  const int64_t steps = p->kernel == 0 ? L.NSC : (p->kernel == 2 ? 2 * L.NSC : (2 * L.NSC) * p->n_groups);
   // instantiated rows per thread: batch-1 kernel 4/2/1 at 256 threads, 2/1 at 512 and 1024 (default 1: one row per
   // thread gives the most units to balance and the lightest registers); the generic kernel 4 only for mu = 8 with
   // <= 2 batch rows
   int rpt_max = (p->kernel == 0 || (L.shape.mu == 8 && p->bpad <= 2)) ? 4 : 2;
   if (p->kernel == 0) rpt_max = p->nt == 256 ? 4 : 2;
   int chosen = 1;
-  if (rpt_env == 1 || rpt_env == 2 || rpt_env == 4) {
+  if (p->kernel != 1) {
+    chosen = 1;   // the batch-1 and small-batch kernels: one row per thread
+  } else if (rpt_env == 1 || rpt_env == 2 || rpt_env == 4) {
     chosen = rpt_env > rpt_max ? rpt_max : rpt_env;
   } else if (p->kernel == 0) {
     chosen = 1;
@@ -184,8 +194,11 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   p->blocks = p->units < target ? p->units : target;
   // the batch-1 kernel stages the folded activations of all its units at once: at most kB1MaxUnits per workgroup
   if (p->kernel == 0 && ceil_div(p->units, p->blocks) > kB1MaxUnits) p->blocks = ceil_div(p->units, kB1MaxUnits);
+  if (p->kernel == 2 && ceil_div(p->units, p->blocks) > kBatMaxUnits) p->blocks = ceil_div(p->units, kBatMaxUnits);
   p->ws_counters_off = 0;
-  p->ws_partials_off = round_up256(uint64_t(p->n_tiles) * 4u);
+  // the small-batch kernel runs one row of workgroups per group of four batch rows, each with its own counters
+  const uint64_t counter_sets = p->kernel == 2 ? uint64_t(p->n_groups) : 1u;
+  p->ws_partials_off = counter_sets * round_up256(uint64_t(p->n_tiles) * 4u);
   p->ws_bytes = p->ws_partials_off + uint64_t(p->blocks) * 2u * uint64_t(p->rows) * uint64_t(p->bpad) * 4u;
   return FLUXBIN_OK;
 }

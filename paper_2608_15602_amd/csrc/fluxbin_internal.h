@@ -12,6 +12,7 @@ constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes o
 constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
 constexpr int kMaxBatch = 16;
 constexpr int kB1MaxUnits = 12;         // units per workgroup of the batch-1 kernel (its LDS staging capacity)
+constexpr int kBatMaxUnits = 24;        // units per workgroup of the small-batch mu = 8 kernel (its LDS index table)
 
 struct Derived {
   int64_t Npad, ncg, Sv, ncs, NC, NSC, NCP, V, Mp, Gr, Gs, NRP;
@@ -72,14 +73,14 @@ fluxbin_status hip_fail(int hip_error, const char* what);
 
 // ---- launch plan of the GEMV/GEMM kernels ----
 struct Plan {
-  int kernel;       // 0 = mu8 batch-1 super-chunk kernel, 1 = generic (any mu, any batch)
+  int kernel;       // 0 = mu8 batch-1 super-chunk kernel, 1 = generic (any mu, any batch), 2 = mu8 batch 2..16
   int nt;           // threads per block
   int rpt;          // rows per thread
   int rows;         // rows per tile (nt * rpt)
   int64_t n_tiles;  // ceil(M / rows)
   int64_t units;    // work units (tile x chunk step [x batch group])
   int64_t blocks;   // grid size
-  int bg;           // batch rows per LUT group (generic kernel)
+  int bg;           // batch rows per LUT group (generic and small-batch kernels)
   int n_groups;     // batch groups
   int bpad;         // bg * n_groups
   int depth;        // batch-1 kernel: units of sign data requested ahead (1, 2, 3, 4 or 6)

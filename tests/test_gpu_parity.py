@@ -206,12 +206,18 @@ def test_fp32_output_and_generic_kernel_at_batch1():
     _check(y2, oracle.gemv_dense(L, x), "generic kernel at batch 1")
 
 
+@pytest.mark.parametrize("generic", [False, True], ids=["mu8_batch_kernel", "generic_kernel"])
 @pytest.mark.parametrize("B", [2, 5, 16])
-def test_batch_rows_equal_batch1(B):
-    """Each batch row of the small-batch path matches the oracle, and the batch path gives the rows the oracle gives
-    for the same activations at batch 1."""
+def test_batch_rows_equal_batch1(B, generic):
+    """Each batch row of the small-batch path matches the oracle (mu = 8 batch kernel: groups of four rows on
+    workgroup rows; and the generic kernel)."""
     spec = LayerSpec("bat", M=1536, N=2048, Kb=2, Ks=1, mu=8, S=61, g_r=128, g_s=61, seed=22)
-    _parity(spec, B, out_fp32=True)
+    if generic:
+        os.environ["FLUXBIN_GENERIC"] = "1"
+    try:
+        _parity(spec, B, out_fp32=True)
+    finally:
+        os.environ.pop("FLUXBIN_GENERIC", None)
 
 
 def test_strided_batch():
