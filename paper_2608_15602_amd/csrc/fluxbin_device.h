@@ -199,7 +199,7 @@ __device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
 }
 
 // Small-batch mu = 8 kernel (fluxbin_gemm_batch.hip): launches k_gemm_mu8_batch with n_groups groups of four batch
-// rows; false if no instance exists.
-bool launch_gemm_batch(const GemmArgs& a, int n_groups, hipStream_t stream);
+// rows and depth units of sign data requested ahead; false if no instance exists.
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, hipStream_t stream);
 
 }  // namespace fluxbin

@@ -5,20 +5,22 @@
 //   LUT_{b,c,s}[p] = sum_n xv[b, 128c + 8s + n] (2 bit_n(p) - 1),   xv = x[xidx] * colscale.
 // Each sign word is read from HBM once and used for every batch row (the tables are what grows with B).
 //
-// Work decomposition. A tile is 1024 rows (one row per thread of a 1024-thread workgroup); a unit is one tile times
-// one 128-column chunk. Units are numbered tile-major and split into equal contiguous ranges, one per workgroup, as in
-// the batch-1 kernel, and split tiles are reduced by the same counter protocol (fluxbin_device.h).
+// Work decomposition, as in the batch-1 kernel: a tile is 1024 rows (one row per thread of a 1024-thread workgroup);
+// a unit is one tile times one super-chunk (two 128-column chunks, i.e. both stored sign slots of a row); units are
+// numbered tile-major and split into equal contiguous ranges, one per workgroup; split tiles are reduced by the
+// counter protocol of fluxbin_device.h. So the sign stream has the batch-1 kernel's access pattern.
 //
 // A workgroup handles one group of (up to) four batch rows, blockIdx.y; larger batches launch one row of workgroups
 // per group. The groups read the same sign data at nearly the same time, so HBM streams it about once (the 256 MB
 // last-level cache serves the repeats), while the table work, which grows with B and bounds this kernel, spreads over
-// all CUs. LDS holds two table buffers of 256 patterns x 16 sub-vectors x 4 batch rows (64 KB each): entry (p, s, b)
-// at (p*16 + s)*4 + b, so one ds_read_b128 returns the four batch values of a lookup. By the packed format a lane of
-// row i reads sub-vector (q + i) mod 16 at byte q, so any 16 consecutive lanes read 16 different sub-vectors, i.e. all
-// 64 LDS banks once: the lookups are conflict-free. Step k builds the tables of unit k+1 in the other buffer and looks
-// up unit k. The folded activations of a unit (128 columns x 4 batch rows, fp32) are staged through a two-slot LDS
-// ring: they are requested two units ahead into registers and written one unit ahead, so neither wait stalls the sign
-// stream.
+// all CUs. A unit is processed in two sub-steps, one per chunk. LDS holds two table buffers of 256 patterns x 16
+// sub-vectors x 4 batch rows (64 KB each; buffer h holds chunk h of a unit): entry (p, s, b) at (p*16 + s)*4 + b, so
+// one ds_read_b128 returns the four batch values of a lookup. By the packed format a lane of row i reads sub-vector
+// (q + i) mod 16 at byte q, so any 16 consecutive lanes read 16 different sub-vectors, i.e. all 64 LDS banks once:
+// the lookups are conflict-free. Each sub-step builds the tables of the next chunk in the other buffer and looks up
+// the current one. The folded activations of a unit (256 columns x 4 batch rows, fp32) are staged through a two-slot
+// LDS ring: they are requested four units ahead into registers and written two units ahead, so neither wait stalls
+// the sign stream.
 #include <hip/hip_runtime.h>
 
 #include "fluxbin_device.h"
@@ -27,116 +29,164 @@ namespace fluxbin {
 
 struct Bat {
   static constexpr int NT = 1024;
-  static constexpr int BPN = 4;              // batch rows per workgroup
-  static constexpr int TBL = 256 * 16 * 4;  // floats per table buffer (64 KB)
-  static constexpr int XSS = 12;            // floats per (batch row, sub-vector) in the staging layout (8 + pad)
-  static constexpr int XS = BPN * 16 * XSS;  // floats per staged unit
+  static constexpr int BPN = 4;               // batch rows per workgroup
+  static constexpr int TBL = 256 * 16 * 4;   // floats per table buffer (64 KB)
+  static constexpr int XSS = 12;             // floats per (chunk, batch row, sub-vector) in the staging layout
+  static constexpr int XC = BPN * 16 * XSS;  // floats per staged chunk
+  static constexpr int XS = 2 * XC;          // floats per staged unit
 };
 
-// Unit cursor: tile and chunk of the unit to request next, and the thread's byte offsets for that unit.
-struct BatCursor {
-  const uint8_t* sbase;  // signs + (c >> 1) * 2 * Mp * 16
-  uint32_t soff;         // (h * Mp + row) * 16, h = stored slot of chunk c for this row (below 2^32 since M <= 2^27)
-  uint32_t roff;         // (row >> 1) * 4
-  int tile, c;
+// Per-thread constants of the current tile: byte offsets of the thread's row in the two stored sign slots of a
+// super-chunk, and in a row-scale plane.
+struct BatRow {
+  uint32_t soff0, soff1;   // row * 16 and (Mp + row) * 16 (below 2^32: M <= 2^27)
+  uint32_t roff;           // (row >> 1) * 4
 };
 
-__device__ __forceinline__ void bat_cursor_set(const GemmArgs& a, BatCursor& cu, int tile, int c) {
-  const int t = threadIdx.x;
-  cu.tile = tile;
-  cu.c = c;
-  const int row_raw = tile * 1024 + t;
+__device__ __forceinline__ void bat_row_set(const GemmArgs& a, BatRow& rw, int tile) {
+  const int row_raw = tile * 1024 + int(threadIdx.x);
   const uint32_t row = uint32_t(row_raw < a.Mp ? row_raw : a.Mp - 1);   // rows past M are never stored
-  const uint32_t h = uint32_t(c & 1) ^ uint32_t((t >> 4) & 1);           // slot swap of rows with i mod 32 >= 16
-  cu.sbase = a.signs + int64_t((c >> 1) * 2) * a.Mp * 16;
-  cu.soff = (h * uint32_t(a.Mp) + row) * 16u;
-  cu.roff = (row >> 1) * 4u;
+  rw.soff0 = row * 16u;
+  rw.soff1 = (uint32_t(a.Mp) + row) * 16u;
+  rw.roff = (row >> 1) * 4u;
 }
 
-// Next unit, or a small cached region past the workgroup's range (the requests continue so that the number of loads
-// in flight, which the waits count, is the same on every path).
+// Request cursor (wave-uniform): the unit (tile, super-chunk sc) requested next. Past the workgroup's range the
+// requests continue (so that the number of loads in flight, which the waits count, is the same on every path) from a
+// 1 KB region at the start of the sign section and the first row-scale word.
+struct BatCursor {
+  int tile, sc;
+  const uint8_t* sbase;   // signs + sc * 2 * Mp * 16
+  bool dummy;
+  BatRow rw;
+};
+
+__device__ __forceinline__ void bat_cursor_init(const GemmArgs& a, BatCursor& cu, int tile, int sc) {
+  cu.tile = tile;
+  cu.sc = sc;
+  cu.dummy = false;
+  cu.sbase = a.signs + int64_t(sc) * 2 * a.Mp * 16;
+  bat_row_set(a, cu.rw, tile);
+}
+
 __device__ __forceinline__ void bat_cursor_advance(const GemmArgs& a, BatCursor& cu, bool has_next) {
-  if (has_next) {
-    int c = cu.c + 1, tile = cu.tile;
-    if (c == a.NCP) {
-      c = 0;
-      ++tile;
-    }
-    bat_cursor_set(a, cu, tile, c);
-  } else {
+  if (!has_next) {
+    cu.dummy = true;
+    return;
+  }
+  if (++cu.sc == a.steps) {
+    cu.sc = 0;
+    ++cu.tile;
     cu.sbase = a.signs;
-    cu.soff = (threadIdx.x & 63u) * 16u;
-    cu.roff = 0u;
+    bat_row_set(a, cu.rw, cu.tile);
+  } else {
+    cu.sbase += int64_t(2) * a.Mp * 16;
   }
 }
 
 struct BatRing {
-  uint32_t w[4];  // the row's 16-byte sign entry of the unit's chunk
-  uint32_t r;     // 32-bit word with the fp16 row scales of rows (i & ~1, i | 1) in the chunk's plane
+  uint32_t w[8];   // the row's two 16-byte sign entries of the super-chunk (stored slots 0 and 1)
+  uint32_t r[2];   // 32-bit words with the fp16 row scales of rows (i & ~1, i | 1) for chunks 2sc and 2sc+1
 };
 
-__device__ __forceinline__ void bat_issue(const GemmArgs& a, const BatCursor& cu, int32_t plane, BatRing& rg) {
-  const uint4 v = load_stream16(cu.sbase + cu.soff);
-  rg.w[0] = v.x; rg.w[1] = v.y; rg.w[2] = v.z; rg.w[3] = v.w;
-  const uint8_t* rb = reinterpret_cast<const uint8_t*>(a.rscale) + int64_t(plane) * a.Mp * 2;
-  rg.r = *reinterpret_cast<const uint32_t*>(rb + cu.roff);
+// Loads of the cursor's unit (wave-uniform bases, 32-bit per-lane offsets): both sign entries, and the row-scale
+// words of its two chunks from planes pa and pb.
+__device__ __forceinline__ void bat_issue_signs(const GemmArgs& a, const BatCursor& cu, BatRing& rg) {
+  const uint8_t* sb = cu.dummy ? a.signs : cu.sbase;
+  const uint32_t o0 = cu.dummy ? (threadIdx.x & 63u) * 16u : cu.rw.soff0;
+  const uint32_t o1 = cu.dummy ? (threadIdx.x & 63u) * 16u : cu.rw.soff1;
+  const uint4 v0 = load_stream16(sb + o0);
+  const uint4 v1 = load_stream16(sb + o1);
+  rg.w[0] = v0.x; rg.w[1] = v0.y; rg.w[2] = v0.z; rg.w[3] = v0.w;
+  rg.w[4] = v1.x; rg.w[5] = v1.y; rg.w[6] = v1.z; rg.w[7] = v1.w;
 }
 
-// Staging registers of one unit: thread t holds column t & 127 of batch row t >> 7 (rows 4..7 of the mapping idle).
+__device__ __forceinline__ void bat_issue_rscale(const GemmArgs& a, const BatCursor& cu, int32_t pa, int32_t pb,
+                                                 BatRing& rg) {
+  const uint32_t ro = cu.dummy ? 0u : cu.rw.roff;
+  const uint8_t* ra = reinterpret_cast<const uint8_t*>(a.rscale) + int64_t(pa) * a.Mp * 2;
+  const uint8_t* rb = reinterpret_cast<const uint8_t*>(a.rscale) + int64_t(pb) * a.Mp * 2;
+  rg.r[0] = *reinterpret_cast<const uint32_t*>(ra + ro);
+  rg.r[1] = *reinterpret_cast<const uint32_t*>(rb + ro);
+}
+
+// Staging cursor (wave-uniform): unit requested for staging next: its index in the workgroup, super-chunk sc, and
+// (2sc) mod ncg for the global-chunk column arithmetic.
+struct BatStageCursor {
+  int k, sc, cm;
+};
+
+__device__ __forceinline__ void bat_stage_cursor_next(const GemmArgs& a, BatStageCursor& s) {
+  ++s.k;
+  if (++s.sc == a.steps) {
+    s.sc = 0;
+    s.cm = 0;
+  } else {
+    s.cm += 2;
+    if (s.cm >= a.ncg) s.cm -= a.ncg;
+  }
+}
+
+// Staging registers of one unit: thread t holds column t & 255 of the unit (chunk 2sc + ((t >> 7) & 1)) for batch
+// row t >> 8.
 struct BatStage {
   uint32_t xb;   // x bits
   uint32_t cs;   // column scale bits
   bool ok;       // a real activation (else the staged value is 0)
 };
 
-// Request the activations of unit (chunk c, index k in the workgroup). Global chunks read x[b][j] with j following
-// from the chunk; salient chunks take j from the VCM index table staged in LDS (0xFFFF: padding column). Every load is
-// unconditional and in bounds.
-__device__ __forceinline__ void bat_stage_load(const GemmArgs& a, const uint16_t* s_xidx, int k, int c, bool real,
-                                               BatStage& r) {
+// Request the activations of the staging cursor's unit. Global chunks read x[b][(c mod ncg) * 128 + col]; salient
+// chunks take the column from the VCM index table staged in LDS (0xFFFF: padding column). xrow is the thread's byte
+// offset of its batch row in x. Every load is unconditional and in bounds.
+__device__ __forceinline__ void bat_stage_load(const GemmArgs& a, const uint16_t* s_xidx, const BatStageCursor& s,
+                                               int n, uint32_t xrow, BatStage& r) {
   const int t = threadIdx.x;
-  const int col = t & 127;
-  const int b = t >> 7;
-  int j = 0;
-  bool valid = false;
-  if (real) {
-    if (c < a.ngc) {
-      j = (c - (c / a.ncg) * a.ncg) * 128 + col;
-      valid = j < a.N;
-    } else {
-      const uint32_t idx = s_xidx[k * 128 + col];
-      valid = idx != 0xFFFFu;
-      j = valid ? int(idx) : 0;
-    }
+  const int col = t & 255;
+  const int half = col >> 7;
+  const bool real = s.k < n;
+  const int c = 2 * s.sc + half;
+  uint32_t j;
+  bool valid;
+  if (c < a.ngc) {
+    int cm = s.cm + half;
+    if (cm == a.ncg) cm = 0;
+    j = uint32_t(cm * 128 + (col & 127));
+    valid = j < uint32_t(a.N);
+  } else {
+    const uint32_t idx = real ? uint32_t(s_xidx[s.k * 256 + col]) : 0xFFFFu;
+    valid = idx != 0xFFFFu;
+    j = idx;
   }
-  if (!valid) j = 0;
-  r.cs = real ? a.colscale[c * 128 + col] : a.colscale[0];
-  const int bl = b < a.B ? b : a.B - 1;
-  r.xb = a.x[int64_t(bl) * a.ldx + j];
-  r.ok = valid && b < a.B;
+  valid = valid && real;
+  j = valid ? j : 0u;
+  const int cs_unit = real ? s.sc : 0;
+  r.cs = *reinterpret_cast<const uint16_t*>(reinterpret_cast<const uint8_t*>(a.colscale) + cs_unit * 512 +
+                                            uint32_t(col) * 2u);
+  r.xb = *reinterpret_cast<const uint16_t*>(reinterpret_cast<const uint8_t*>(a.x) + xrow + j * 2u);
+  r.ok = valid && (t >> 8) < a.B;
 }
 
-// Staged layout: batch row b, column 8s + n at (b*16 + s)*12 + n, so a build thread reads the 8 columns of its
-// sub-vector with two 16-byte reads and the 16 sub-vectors of one batch row lie in 16 different groups of four LDS
-// banks (the stride of 12 floats spreads them).
+// Staged layout: chunk h of the unit, batch row b, column 8s + n at h*XC + (b*16 + s)*12 + n, so a build thread reads
+// the 8 columns of its sub-vector with two 16-byte reads and the 16 sub-vectors of one batch row lie in 16 different
+// groups of four LDS banks (the stride of 12 floats spreads them).
 __device__ __forceinline__ void bat_stage_write(float* xs_slot, const BatStage& r) {
   const int t = threadIdx.x;
-  const int b = t >> 7;
-  const int col = t & 127;
-  if (b < Bat::BPN)
-    xs_slot[(b * 16 + (col >> 3)) * Bat::XSS + (col & 7)] = r.ok ? h2f(uint16_t(r.xb)) * h2f(uint16_t(r.cs)) : 0.f;
+  const int b = t >> 8;
+  const int col = t & 255;
+  xs_slot[(col >> 7) * Bat::XC + (b * 16 + ((col & 127) >> 3)) * Bat::XSS + (col & 7)] =
+      r.ok ? h2f(uint16_t(r.xb)) * h2f(uint16_t(r.cs)) : 0.f;
 }
 
-// Build the 16 tables (256 patterns x 4 batch rows) of a staged unit. Thread t owns sub-vector s = t & 15, batch row
-// b = (t >> 4) & 3 and the 16 patterns whose top four bits are t >> 6, enumerated in Gray order (each entry is the
+// Build the 16 tables (256 patterns x 4 batch rows) of one staged chunk. Thread t owns sub-vector s = t & 15, batch
+// row b = (t >> 4) & 3 and the 16 patterns whose top four bits are t >> 6, enumerated in Gray order (each entry is the
 // previous one plus or minus 2*xv[n]). A wavefront writes 64 consecutive floats per entry step.
-__device__ __forceinline__ void bat_build(float* tbl, const float* xs_slot) {
+__device__ __forceinline__ void bat_build(float* tbl, const float* xs_chunk) {
   const int t = threadIdx.x;
   const int s = t & 15;
   const int b = (t >> 4) & 3;
   const int hi = t >> 6;
-  const float4 lo4 = *reinterpret_cast<const float4*>(xs_slot + (b * 16 + s) * Bat::XSS);
-  const float4 hi4 = *reinterpret_cast<const float4*>(xs_slot + (b * 16 + s) * Bat::XSS + 4);
+  const float4 lo4 = *reinterpret_cast<const float4*>(xs_chunk + (b * 16 + s) * Bat::XSS);
+  const float4 hi4 = *reinterpret_cast<const float4*>(xs_chunk + (b * 16 + s) * Bat::XSS + 4);
   const float xv[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
   float v = 0.f;
 #pragma unroll
@@ -159,22 +209,26 @@ __device__ __forceinline__ void bat_build(float* tbl, const float* xs_slot) {
   }
 }
 
-// 16 lookups of four batch values, times the row scale, into acc.
-__device__ __forceinline__ void bat_lookup(const float* tbl, const BatRing& rg, const uint32_t (&cq)[4],
+// Chunk J of the unit: the thread's sign words of that chunk are in stored slot J XOR [row mod 32 >= 16]; 16 lookups
+// of four batch values, times the chunk's row scale, into acc.
+template <int J>
+__device__ __forceinline__ void bat_lookup(const float* tbl, const BatRing& rg, const uint32_t (&cq)[4], bool swap,
                                            float (&acc)[1][Bat::BPN]) {
   const uint32_t sh = (threadIdx.x & 1u) * 16u;
+  const bool upper = (J == 1) != swap;
   float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
+    const uint32_t w = upper ? rg.w[4 + m] : rg.w[m];
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
       const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
-      const uint32_t addr = __builtin_amdgcn_perm(rg.w[m], cq[m], sel);   // (p << 8) | (s << 4)
+      const uint32_t addr = __builtin_amdgcn_perm(w, cq[m], sel);   // (p << 8) | (s << 4)
       const float4 e = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(tbl) + addr);
       s4.x += e.x; s4.y += e.y; s4.z += e.z; s4.w += e.w;
     }
   }
-  const float rs = h2f(uint16_t(rg.r >> sh));
+  const float rs = h2f(uint16_t(rg.r[J] >> sh));
   acc[0][0] = __builtin_fmaf(s4.x, rs, acc[0][0]);
   acc[0][1] = __builtin_fmaf(s4.y, rs, acc[0][1]);
   acc[0][2] = __builtin_fmaf(s4.z, rs, acc[0][2]);
@@ -183,56 +237,71 @@ __device__ __forceinline__ void bat_lookup(const float* tbl, const BatRing& rg, 
 
 struct BatState {
   int n;                      // units of this workgroup
-  int tile, c;                // unit being looked up
-  int first_tile;
-  int pending0, pending1, n_pending;
+  int tile, sc;               // unit being looked up
+  int first_tile, last_tile;
+  bool first_shared, last_shared;
+  int n_pending;
   float acc[1][Bat::BPN];
 };
 
-__device__ __forceinline__ int bat_plane(const int* s_planes, int k, int n) {
-  const int kk = k < n ? k : n - 1;
-  return __builtin_amdgcn_readfirstlane(s_planes[kk]);
+// Row-scale plane of chunk 2*sc(k) + half of unit k (clamped), from the table staged in LDS.
+__device__ __forceinline__ int32_t bat_plane(const int* s_planes, int k, int half) {
+  return __builtin_amdgcn_readfirstlane(s_planes[2 * (k < kBatMaxUnits ? k : kBatMaxUnits - 1) + half]);
 }
 
-// Step K of the workgroup (compile-time K, at most kBatMaxUnits units): request unit K+1 into the ring slot unit K-1
-// used, build unit K+1's tables in the other buffer, look up unit K, then write unit K+2's activations (requested
-// during step K-1) into the staging slot unit K no longer needs and request unit K+3's.
-template <int K>
-__device__ __forceinline__ void bat_steps(const GemmArgs& a, BatState& st, BatCursor& cur, BatRing (&ring)[2],
-                                          BatStage& sr, float* tbl, float* xs, const uint16_t* s_xidx,
-                                          const int* s_planes, const uint32_t (&cq)[4]) {
+// Unit K of the workgroup (compile-time K, at most kBatMaxUnits units), in two sub-steps.
+// Sub-step 0: request unit K+4's activations into a free set of staging registers and unit K+D's signs into the ring
+// slot unit K-1 used (D+1 units of sign data in flight at every wait); build chunk 1's tables into buffer 1; look up
+// chunk 0 (buffer 0).
+// Sub-step 1: write unit K+2's activations (requested two units earlier) into the staging slot unit K no longer
+// needs; build unit K+1's chunk 0 into buffer 0; look up chunk 1. Each wait covers loads that the step needs anyway:
+// the staging loads waited for were issued before the sign loads of unit K+D-2.
+template <int D, int K>
+__device__ __forceinline__ void bat_units(const GemmArgs& a, BatState& st, BatCursor& cur, BatRing (&ring)[D + 1],
+                                          BatStageCursor& scur, BatStage (&sr)[3], uint32_t xrow, float* tbl,
+                                          float* xs, const uint16_t* s_xidx, const int* s_planes,
+                                          const uint32_t (&cq)[4], bool swap) {
   if constexpr (K < kBatMaxUnits) {
     if (K >= st.n) return;
-    bat_issue(a, cur, bat_plane(s_planes, K + 1, st.n), ring[(K + 1) & 1]);
-    bat_cursor_advance(a, cur, K + 2 < st.n);
-    if (K + 1 < st.n) bat_build(tbl + ((K + 1) & 1) * Bat::TBL, xs + ((K + 1) & 1) * Bat::XS);
-    bat_lookup(tbl + (K & 1) * Bat::TBL, ring[K & 1], cq, st.acc);
-    if (K + 2 < st.n) bat_stage_write(xs + (K & 1) * Bat::XS, sr);
-    int c3 = st.c + 3;
-    while (c3 >= a.NCP) c3 -= a.NCP;
-    bat_stage_load(a, s_xidx, K + 3, c3, K + 3 < st.n, sr);
-    if (st.c == a.NCP - 1 || K + 1 == st.n) {
-      if (tile_end<1024, 1, Bat::BPN>(a, st.tile, st.first_tile, st.acc)) {
-        if (st.n_pending == 0) st.pending0 = st.tile; else st.pending1 = st.tile;
+    // sub-step 0
+    bat_stage_load(a, s_xidx, scur, st.n, xrow, sr[(K + 4) % 3]);   // unit K+4
+    bat_stage_cursor_next(a, scur);
+    bat_issue_signs(a, cur, ring[(K + D) % (D + 1)]);
+    bat_issue_rscale(a, cur, bat_plane(s_planes, K + D, 0), bat_plane(s_planes, K + D, 1), ring[(K + D) % (D + 1)]);
+    bat_cursor_advance(a, cur, K + D + 1 < st.n);
+    bat_build(tbl + Bat::TBL, xs + (K & 1) * Bat::XS + Bat::XC);
+    bat_lookup<0>(tbl, ring[K % (D + 1)], cq, swap, st.acc);
+    __syncthreads();
+    // sub-step 1
+    if (K + 2 < st.n) bat_stage_write(xs + (K & 1) * Bat::XS, sr[(K + 2) % 3]);
+    if (K + 1 < st.n) bat_build(tbl, xs + ((K + 1) & 1) * Bat::XS);
+    bat_lookup<1>(tbl + Bat::TBL, ring[K % (D + 1)], cq, swap, st.acc);
+    if (st.sc == a.steps - 1 || K + 1 == st.n) {
+      const bool shared = st.tile == st.first_tile ? st.first_shared : (st.tile == st.last_tile && st.last_shared);
+      if (shared) {
+        store_partial<1024, 1, Bat::BPN>(a, st.tile == st.first_tile ? 0 : 1, st.acc);
         ++st.n_pending;
+      } else {
+        store_tile_y<1024, 1, Bat::BPN>(a, st.tile, st.acc);
       }
 #pragma unroll
       for (int b = 0; b < Bat::BPN; ++b) st.acc[0][b] = 0.f;
     }
     __syncthreads();
-    if (++st.c == a.NCP) {
-      st.c = 0;
+    if (++st.sc == a.steps) {
+      st.sc = 0;
       ++st.tile;
     }
-    bat_steps<K + 1>(a, st, cur, ring, sr, tbl, xs, s_xidx, s_planes, cq);
+    bat_units<D, K + 1>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
   }
 }
 
+template <int D>
 __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
-  __shared__ __attribute__((aligned(16))) float tbl[2 * Bat::TBL];   // 128 KB
+  __shared__ __attribute__((aligned(16))) float tbl[2 * Bat::TBL];   // 128 KB: buffer 0 chunk 0, buffer 1 chunk 1
   __shared__ __attribute__((aligned(16))) float xs[2 * Bat::XS];      // staged activations, two units
-  __shared__ uint16_t s_xidx[kBatMaxUnits * 128];                      // VCM indices of the workgroup's units
-  __shared__ int s_planes[kBatMaxUnits];
+  __shared__ uint16_t s_xidx[kBatMaxUnits * 256];                      // VCM indices of the workgroup's units
+  __shared__ int s_planes[2 * kBatMaxUnits];                           // row-scale planes of their chunks
   __shared__ int s_flag;
 
   // This workgroup's group of batch rows, with its own slice of the workspace (counters, then partial sums).
@@ -249,61 +318,84 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   const int u1 = first_unit(a, blockIdx.x + 1);
   BatState st;
   st.n = u1 - u0;
-  st.tile = u0 / a.NCP;
-  st.c = u0 - st.tile * a.NCP;
+  st.tile = u0 / a.steps;
+  st.sc = u0 - st.tile * a.steps;
   st.first_tile = st.tile;
-  st.pending0 = st.pending1 = st.n_pending = 0;
+  st.last_tile = (u1 - 1) / a.steps;
+  st.first_shared = tile_is_shared(a, st.first_tile);
+  st.last_shared = tile_is_shared(a, st.last_tile);
+  st.n_pending = 0;
 #pragma unroll
   for (int b = 0; b < Bat::BPN; ++b) st.acc[0][b] = 0.f;
+  const bool swap = ((t >> 4) & 1) != 0;   // rows with i mod 32 >= 16 hold the super-chunk's chunks swapped
+  // byte offset of the thread's batch row in x (rows past B read row B-1; their values are masked)
+  const uint32_t xrow = uint32_t(((t >> 8) < a.B ? (t >> 8) : a.B - 1) * a.ldx * 2);
 
-  // Row-scale planes and VCM indices of the workgroup's units (the launch plan keeps n <= kBatMaxUnits).
-  if (t < kBatMaxUnits) {
-    int c = st.c + t;
-    while (c >= a.NCP) c -= a.NCP;
-    s_planes[t] = a.chunk_plane[c];
-  }
+  // VCM indices of the workgroup's units into LDS, if one of them has a salient chunk.
   bool has_sal = false;
-  for (int k = 0, c = st.c; k < st.n; ++k) {
-    has_sal |= c >= a.ngc;
-    if (++c == a.NCP) c = 0;
+  for (int k = 0, sc = st.sc; k < st.n; ++k) {
+    has_sal |= 2 * sc + 1 >= a.ngc;
+    if (++sc == a.steps) sc = 0;
   }
   if (has_sal) {
-    constexpr int PER = kBatMaxUnits * 128 / 1024;
+    constexpr int PER = kBatMaxUnits * 256 / 1024;
     uint16_t xi[PER];
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
-      const int k = (t >> 7) + 8 * m;
-      int c = st.c + k;
-      while (c >= a.NCP) c -= a.NCP;
-      xi[m] = a.xidx[c * 128 + (t & 127)];
+      const int k = (t >> 8) + 4 * m;
+      int sc = st.sc + k;
+      while (sc >= a.steps) sc -= a.steps;
+      xi[m] = a.xidx[sc * 256 + (t & 255)];
     }
 #pragma unroll
-    for (int m = 0; m < PER; ++m) s_xidx[((t >> 7) + 8 * m) * 128 + (t & 127)] = xi[m];
+    for (int m = 0; m < PER; ++m) s_xidx[((t >> 8) + 4 * m) * 256 + (t & 255)] = xi[m];
+    __syncthreads();
   }
-  __syncthreads();
 
-  // Sign data of unit 0, then the activations of units 0 and 1 (their wait follows the sign request, which unit 0
-  // needs right after anyway), then unit 2's activations into the staging registers.
+  // Prologue order: the row-scale planes of the workgroup's chunks (lane 2k+h of a register loads unit k's chunk
+  // 2sc+h; units past the range repeat valid chunks; the launch plan keeps n <= kBatMaxUnits), the activations of
+  // units 0 and 1, the sign data of units 0..D-1, then (each wait covering only older loads) their row scales once the
+  // planes are in, the staging of units 0 and 1, and units 2 and 3's activations into the staging registers. The
+  // planes reach LDS for the steps through the barrier before the first table build.
+  int32_t planes;
+  {
+    const int lane = t & 63;
+    int sc = st.sc + (lane >> 1) % kBatMaxUnits;
+    while (sc >= a.steps) sc -= a.steps;
+    planes = a.chunk_plane[2 * sc + (lane & 1)];
+  }
+  BatStageCursor scur;
+  scur.k = 0;
+  scur.sc = st.sc;
+  scur.cm = (2 * st.sc) % a.ncg;
+  BatStage r0, r1;
+  bat_stage_load(a, s_xidx, scur, st.n, xrow, r0);
+  bat_stage_cursor_next(a, scur);
+  bat_stage_load(a, s_xidx, scur, st.n, xrow, r1);
+  bat_stage_cursor_next(a, scur);
   BatCursor cur;
-  bat_cursor_set(a, cur, st.tile, st.c);
-  BatRing ring[2];
-  bat_issue(a, cur, bat_plane(s_planes, 0, st.n), ring[0]);
-  bat_cursor_advance(a, cur, 1 < st.n);
-  {
-    BatStage r0, r1;
-    int c1 = st.c + 1;
-    if (c1 == a.NCP) c1 = 0;
-    bat_stage_load(a, s_xidx, 0, st.c, true, r0);
-    bat_stage_load(a, s_xidx, 1, c1, 1 < st.n, r1);
-    bat_stage_write(xs, r0);
-    bat_stage_write(xs + Bat::XS, r1);
+  bat_cursor_init(a, cur, st.tile, st.sc);
+  BatCursor cur0 = cur;
+  BatRing ring[D + 1];
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    bat_issue_signs(a, cur, ring[k]);
+    bat_cursor_advance(a, cur, k + 1 < st.n);
   }
-  BatStage sr;
-  {
-    int c2 = st.c + 2;
-    while (c2 >= a.NCP) c2 -= a.NCP;
-    bat_stage_load(a, s_xidx, 2, c2, 2 < st.n, sr);
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    bat_issue_rscale(a, cur0, __builtin_amdgcn_readlane(planes, 2 * k), __builtin_amdgcn_readlane(planes, 2 * k + 1),
+                     ring[k]);
+    bat_cursor_advance(a, cur0, k + 1 < st.n);
   }
+  if (t < 2 * kBatMaxUnits) s_planes[t] = planes;
+  bat_stage_write(xs, r0);
+  bat_stage_write(xs + Bat::XS, r1);
+  BatStage sr[3];
+  bat_stage_load(a, s_xidx, scur, st.n, xrow, sr[2]);   // unit 2
+  bat_stage_cursor_next(a, scur);
+  bat_stage_load(a, s_xidx, scur, st.n, xrow, sr[0]);   // unit 3
+  bat_stage_cursor_next(a, scur);
   // Per-lane byte offsets of the table columns read at step q: sub-vector (q + t) mod 16 (rows are t mod 16).
   uint32_t cq[4];
 #pragma unroll
@@ -313,16 +405,22 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
     for (int bb = 0; bb < 4; ++bb) cq[m] |= (((uint32_t(4 * m + bb) + uint32_t(t)) & 15u) << 4) << (8 * bb);
   }
   __syncthreads();
-  bat_build(tbl, xs);
+  bat_build(tbl, xs);   // unit 0, chunk 0
   __syncthreads();
-  bat_steps<0>(a, st, cur, ring, sr, tbl, xs, s_xidx, s_planes, cq);
-  publish_pending<1024, 1, Bat::BPN>(a, st.pending0, st.pending1, st.n_pending, &s_flag);
+  bat_units<D, 0>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
+  const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
+  publish_pending<1024, 1, Bat::BPN>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
 
-bool launch_gemm_batch(const GemmArgs& a, int n_groups, hipStream_t stream) {
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, hipStream_t stream) {
   if (n_groups < 1 || n_groups > 4) return false;
-  hipLaunchKernelGGL(k_gemm_mu8_batch, dim3(unsigned(a.blocks), unsigned(n_groups)), dim3(1024), 0, stream, a);
-  return true;
+  const dim3 grid(unsigned(a.blocks), unsigned(n_groups));
+  switch (depth) {
+    case 1: hipLaunchKernelGGL((k_gemm_mu8_batch<1>), grid, dim3(1024), 0, stream, a); return true;
+    case 2: hipLaunchKernelGGL((k_gemm_mu8_batch<2>), grid, dim3(1024), 0, stream, a); return true;
+    case 3: hipLaunchKernelGGL((k_gemm_mu8_batch<3>), grid, dim3(1024), 0, stream, a); return true;
+  }
+  return false;
 }
 
 }  // namespace fluxbin

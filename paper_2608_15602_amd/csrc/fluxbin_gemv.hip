@@ -764,7 +764,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
       default: ok = false;
     }
   } else if (p.kernel == 2) {
-    ok = launch_gemm_batch(a, p.n_groups, stream);
+    ok = launch_gemm_batch(a, p.n_groups, p.depth, stream);
   } else if (L.shape.mu == 8) {
     ok = launch_gen_mu<8>(a, p, stream);
   } else {

@@ -147,10 +147,11 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     p->bg = 1;
     p->n_groups = 1;
   } else if (L.shape.mu == 8 && B >= 2 && !force_generic) {
-    // small batch: 1024-row tiles, one 128-column chunk per unit, batch in groups of four rows
+    // small batch: 1024-row tiles, one super-chunk per unit (the batch-1 sign stream), batch in groups of four rows
     p->kernel = 2;
     p->nt = 1024;
-    p->depth = 1;
+    const int depth_env = env_int("FLUXBIN_DEPTH", 1);
+    p->depth = (depth_env == 2 || depth_env == 3) ? depth_env : 1;
     p->bg = 4;
     p->n_groups = B <= 4 ? 1 : (B <= 8 ? 2 : 4);
     if (per_cu < 1 || per_cu > 8) per_cu = 1;
@@ -163,7 +164,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   }
   const int64_t target = int64_t(cus) * per_cu;
   p->bpad = p->bg * p->n_groups;
-  const int64_t steps = p->kernel == 0 ? L.NSC : (p->kernel == 2 ? 2 * L.NSC : (2 * L.NSC) * p->n_groups);
+  const int64_t steps = p->kernel == 1 ? (2 * L.NSC) * p->n_groups : L.NSC;
   // instantiated rows per thread: batch-1 kernel 4/2/1 at 256 threads, 2/1 at 512 and 1024 (default 1: one row per
   // thread gives the most units to balance and the lightest registers); the generic kernel 4 only for mu = 8 with
   // <= 2 batch rows

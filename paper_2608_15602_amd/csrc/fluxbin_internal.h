@@ -12,7 +12,7 @@ constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes o
 constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
 constexpr int kMaxBatch = 16;
 constexpr int kB1MaxUnits = 12;         // units per workgroup of the batch-1 kernel (its LDS staging capacity)
-constexpr int kBatMaxUnits = 24;        // units per workgroup of the small-batch mu = 8 kernel (its LDS index table)
+constexpr int kBatMaxUnits = 12;        // units per workgroup of the small-batch mu = 8 kernel (its LDS index table)
 
 struct Derived {
   int64_t Npad, ncg, Sv, ncs, NC, NSC, NCP, V, Mp, Gr, Gs, NRP;
