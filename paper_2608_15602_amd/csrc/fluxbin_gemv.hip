@@ -360,7 +360,7 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
   }
 }
 
-template <int NT, int RPT, int D>
+template <int NT, int RPT, int D, bool EARLY>
 __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float lut[256 * 64];       // 64 KB, two buffers interleaved per pattern
   __shared__ __attribute__((aligned(16))) float xs[kXvUnits * 256];  // staged folded activations
@@ -384,9 +384,11 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   for (int j = 0; j < RPT; ++j) st.acc[j][0] = 0.f;
 
   // Prologue: the row-scale planes of units 0..D-1 as scalar loads (their own counter) and the activation,
-  // column-scale and plane-table loads; once they are in (a short round trip: nothing else is in flight yet) the
-  // global columns are staged and the salient gathers, the sign loads of units 0..D-1 and their row-scale loads are
-  // issued. The tables of unit 0 are built right after, so the pipeline starts while the first sign data streams in.
+  // column-scale and plane-table loads. Large layers (not EARLY) stage the activations before requesting any sign
+  // data: with every CU starting its sign stream at once, activation loads queued with it would return only after the
+  // first burst; so the global columns are staged after one short round trip, then the salient gathers, the sign
+  // loads of units 0..D-1 and their row scales are issued. Small layers (EARLY) request the sign data right after the
+  // activation loads, so the two round trips overlap. The tables of unit 0 are built right after.
   const bool hb = ((t >> 4) & 1) != 0;
   int32_t pl[D][2];
 #pragma unroll
@@ -403,12 +405,13 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
   Ring<RPT> ring[D + 1];
   Cursor<NT, RPT> cur0 = cur;
-  stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);   // the launch plan keeps n <= kXvUnits
+  if constexpr (!EARLY) stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);   // n <= kXvUnits (launch plan)
 #pragma unroll
   for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
     issue_signs<NT, RPT>(a, cur, ring[k]);
     cursor_advance<NT, RPT>(a, cur, k + 1 < st.n);
   }
+  if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     issue_rscale<NT, RPT>(a, cur0, pl[k][0], pl[k][1], ring[k]);
@@ -684,15 +687,22 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
 // Launch
 // =====================================================================================================================
 
-template <int NT, int RPT>
-static void launch_b1(const GemmArgs& a, int depth, hipStream_t stream) {
+template <int NT, int RPT, bool EARLY>
+static void launch_b1_d(const GemmArgs& a, int depth, hipStream_t stream) {
+  const dim3 grid(unsigned(a.blocks));
   switch (depth) {
-    case 3: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 3>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 4>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
-    case 6: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 6>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 2>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
-    default: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 1>), dim3(unsigned(a.blocks)), dim3(NT), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 2, EARLY>), grid, dim3(NT), 0, stream, a); break;
+    case 3: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 3, EARLY>), grid, dim3(NT), 0, stream, a); break;
+    default: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 1, EARLY>), grid, dim3(NT), 0, stream, a); break;
   }
+}
+
+template <int NT, int RPT>
+static void launch_b1(const GemmArgs& a, int depth, bool early, hipStream_t stream) {
+  if (early)
+    launch_b1_d<NT, RPT, true>(a, depth, stream);
+  else
+    launch_b1_d<NT, RPT, false>(a, depth, stream);
 }
 
 template <int MU, int BG, int NG>
@@ -752,15 +762,10 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   a.n_tiles = int32_t(p.n_tiles);
   bool ok = true;
   if (p.kernel == 0) {
-    const int key = p.nt * 10 + p.rpt;
-    switch (key) {
-      case 2561: launch_b1<256, 1>(a, p.depth, stream); break;
-      case 2562: launch_b1<256, 2>(a, p.depth, stream); break;
-      case 2564: launch_b1<256, 4>(a, p.depth, stream); break;
-      case 5121: launch_b1<512, 1>(a, p.depth, stream); break;
-      case 5122: launch_b1<512, 2>(a, p.depth, stream); break;
-      case 10241: launch_b1<1024, 1>(a, p.depth, stream); break;
-      case 10242: launch_b1<1024, 2>(a, p.depth, stream); break;
+    switch (p.nt) {   // one row per thread (the launch plan's only choice for this kernel)
+      case 256: launch_b1<256, 1>(a, p.depth, p.early, stream); break;
+      case 512: launch_b1<512, 1>(a, p.depth, p.early, stream); break;
+      case 1024: launch_b1<1024, 1>(a, p.depth, p.early, stream); break;
       default: ok = false;
     }
   } else if (p.kernel == 2) {

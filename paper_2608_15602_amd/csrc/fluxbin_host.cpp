@@ -134,7 +134,11 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     // units of sign data requested ahead of the one being looked up: one (two units, 64 KB per CU, in flight) already
     // keeps HBM saturated; deeper rings only add queueing and prologue latency
     const int depth_env = env_int("FLUXBIN_DEPTH", 1);
-    p->depth = (depth_env == 2 || depth_env == 3 || depth_env == 4 || depth_env == 6) ? depth_env : 1;
+    p->depth = (depth_env == 2 || depth_env == 3) ? depth_env : 1;
+    // layers whose sign stream is small for the chip overlap the activation and sign round trips (see the kernel)
+    const int early_env = env_int("FLUXBIN_EARLY", -1);
+    const int64_t sign_bytes = int64_t(L.NSC) * 2 * L.Mp * 16;
+    p->early = early_env >= 0 ? early_env != 0 : sign_bytes <= (int64_t(32) << 20);
     // 1024-thread workgroups, one per CU, amortize each table over the most rows and keep the fewest, longest
     // pipelines; layers with fewer than one 1024-row unit per CU use smaller workgroups (more, shorter units).
     if (nt_env == 256 || nt_env == 512 || nt_env == 1024) {
@@ -162,7 +166,8 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (p->n_groups == 3) p->n_groups = 4;  // instantiated batch paddings: 1, 2, 4, 8, 16
     if (per_cu < 1 || per_cu > 8) per_cu = 2;
   }
-  const int64_t target = int64_t(cus) * per_cu;
+  const int blocks_env = env_int("FLUXBIN_BLOCKS", 0);   // tuning override: grid size target
+  const int64_t target = blocks_env > 0 ? blocks_env : int64_t(cus) * per_cu;
   p->bpad = p->bg * p->n_groups;
   const int64_t steps = p->kernel == 1 ? (2 * L.NSC) * p->n_groups : L.NSC;
   // instantiated rows per thread: batch-1 kernel 4/2/1 at 256 threads, 2/1 at 512 and 1024 (default 1: one row per
@@ -193,6 +198,11 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   if (p->units > (int64_t(1) << 30))
     return fail(FLUXBIN_ERR_UNSUPPORTED, "layer too large for one launch (%lld work units)", (long long)p->units);
   p->blocks = p->units < target ? p->units : target;
+  // small layers: give every workgroup at least a few units, so that its fixed start-up cost is amortized and a split
+  // tile has fewer contributors to reduce
+  const int min_units = env_int("FLUXBIN_MIN_UNITS", 3);
+  if (min_units > 1 && p->kernel == 0 && p->blocks > 1 && ceil_div(p->units, p->blocks) < min_units)
+    p->blocks = ceil_div(p->units, int64_t(min_units)) > 0 ? ceil_div(p->units, int64_t(min_units)) : 1;
   // the batch-1 kernel stages the folded activations of all its units at once: at most kB1MaxUnits per workgroup
   if (p->kernel == 0 && ceil_div(p->units, p->blocks) > kB1MaxUnits) p->blocks = ceil_div(p->units, kB1MaxUnits);
   if (p->kernel == 2 && ceil_div(p->units, p->blocks) > kBatMaxUnits) p->blocks = ceil_div(p->units, kBatMaxUnits);

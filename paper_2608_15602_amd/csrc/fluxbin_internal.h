@@ -83,7 +83,8 @@ struct Plan {
   int bg;           // batch rows per LUT group (generic and small-batch kernels)
   int n_groups;     // batch groups
   int bpad;         // bg * n_groups
-  int depth;        // batch-1 kernel: units of sign data requested ahead (1, 2, 3, 4 or 6)
+  int depth;        // units of sign data requested ahead of the one looked up
+  bool early;       // batch-1 kernel: request sign data before staging the activations (small layers)
   uint64_t ws_counters_off, ws_partials_off, ws_bytes;
 };
 
