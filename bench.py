@@ -135,6 +135,27 @@ class Bench:
             out.append(ts[len(ts) // 2])
         return out
 
+    def stream_probe_us(self, launches: int = 60, reps: int = 5):
+        """Average duration of the stream probe on each layer (the batch-1 kernel's weight requests, same launch plan,
+        without the table work), timed like per_launch_us: the bandwidth this access pattern reaches on the device."""
+        import torch
+        sink = torch.zeros(256, dtype=torch.int32, device="cuda")
+        out = []
+        for it in self.items:
+            g = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                with torch.cuda.graph(g, stream=side):
+                    for s in range(launches):
+                        self.fb.fluxbin_stream_probe(it["packs"][s % len(it["packs"])], sink)
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            g.replay()
+            ts = sorted(self.time_graph(g) * 1000.0 / launches for _ in range(reps))
+            out.append(ts[len(ts) // 2])
+        return out
+
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_gemv_mu8_b1_mlp70b_hbm_traffic.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_15602_amd", "csrc", f) for f in ("fluxbin_gemv.hip", "fluxbin_host.cpp")]
@@ -268,12 +289,13 @@ def main():
         return
     total_ms, wall = bench.run(args.steps, args.warmup)
     kern_us = bench.per_launch_us()
+    probe_us = bench.stream_probe_us()
     step_bytes = sum(it["bytes"] for it in bench.items)
     value = step_bytes * args.steps / (total_ms * 1e-3) / 1e9
     achieved = step_bytes / (sum(kern_us) * 1e-6) / 1e9
     traffic = measured_traffic()
     per_layer = {}
-    for it, us in zip(bench.items, kern_us):
+    for it, us, pus in zip(bench.items, kern_us, probe_us):
         s = it["spec"]
         per_layer[s.name] = {
             "shape_out_x_in": f"{s.M}x{s.N}", "us_per_gemv": round(us, 3),
@@ -281,6 +303,7 @@ def main():
             "pct_of_8TBps": round(100 * it["bytes"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 1),
             "tflop_eq": round(2.0 * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
             "bytes": it["bytes"], "lookups": it["lookups"],
+            "stream_probe_us": round(pus, 3), "frac_of_stream_probe": round(pus / us, 4),
         }
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -293,7 +316,8 @@ def main():
                      "traffic": (sum(traffic[it["spec"].name] for it in bench.items) if traffic else None),
                      "traffic_per_launch": traffic,
                      "kernel": "k_gemv_mu8_b1 (HIP events around graph replays of back-to-back launches)",
-                     "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}},
+                     "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items},
+                     "frac_of_stream_probe": round(sum(probe_us) / sum(kern_us), 4)},
         "wall_s_timed": round(wall, 3),
     }
     if not args.no_small:

@@ -441,4 +441,18 @@ fluxbin_status fluxbin_unpack_canonical(const fluxbin_layer* layer, uint32_t* d_
   return launch_unpack(*layer, d_signs_out, d_dense_out, stream);
 }
 
+fluxbin_status fluxbin_stream_probe(const fluxbin_layer* layer, uint32_t* d_sink, size_t sink_bytes,
+                                    hipStream_t stream) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_layer(layer);
+  if (st != FLUXBIN_OK) return st;
+  if (layer->shape.mu != 8) return fail(FLUXBIN_ERR_UNSUPPORTED, "the stream probe follows the mu = 8 batch-1 kernel");
+  if (!d_sink) return fail(FLUXBIN_ERR_INVALID_ARG, "d_sink is NULL");
+  if (sink_bytes < 1024) return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "sink of %zu bytes < 1024", sink_bytes);
+  Plan p;
+  st = make_plan(*layer, 1, &p);
+  if (st != FLUXBIN_OK) return st;
+  return launch_stream_probe(*layer, p, d_sink, stream);
+}
+
 }  // extern "C"

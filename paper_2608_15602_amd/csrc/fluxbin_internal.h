@@ -96,6 +96,7 @@ fluxbin_status launch_pack(const fluxbin_layer& L, const fluxbin_weights& dev_w,
 fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const uint16_t* d_x, int64_t ldx,
                            void* d_y, int64_t ldy, int y_fp32, void* d_ws, hipStream_t stream);
 fluxbin_status launch_fill_zero(void* d, size_t bytes, hipStream_t stream);
+fluxbin_status launch_stream_probe(const fluxbin_layer& L, const Plan& p, uint32_t* d_sink, hipStream_t stream);
 fluxbin_status launch_debug_indices(const fluxbin_layer& L, uint8_t* d_p, hipStream_t stream);
 fluxbin_status launch_unpack(const fluxbin_layer& L, uint32_t* d_signs, uint32_t* d_dense, hipStream_t stream);
 

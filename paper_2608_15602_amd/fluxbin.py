@@ -24,7 +24,7 @@ HEADER_BYTES = 256
 EXPORTS = (
     "fluxbin_status_string", "fluxbin_last_error_message", "fluxbin_pack_query", "fluxbin_pack",
     "fluxbin_layer_from_header", "fluxbin_workspace_query", "fluxbin_workspace_init", "fluxbin_lut_gemv",
-    "fluxbin_lut_gemm_smallbatch", "fluxbin_debug_indices", "fluxbin_unpack_canonical",
+    "fluxbin_lut_gemm_smallbatch", "fluxbin_debug_indices", "fluxbin_unpack_canonical", "fluxbin_stream_probe",
 )
 
 
@@ -80,6 +80,7 @@ def lib() -> ctypes.CDLL:
         L.fluxbin_lut_gemm_smallbatch.argtypes = [ctypes.POINTER(Layer), i32, vp, i64, vp, i64, i32, vp, sz, vp]
         L.fluxbin_debug_indices.argtypes = [ctypes.POINTER(Layer), vp, vp]
         L.fluxbin_unpack_canonical.argtypes = [ctypes.POINTER(Layer), vp, vp, vp]
+        L.fluxbin_stream_probe.argtypes = [ctypes.POINTER(Layer), vp, sz, vp]
         for name in EXPORTS:
             if name not in ("fluxbin_status_string", "fluxbin_last_error_message"):
                 getattr(L, name).restype = ctypes.c_int
@@ -221,3 +222,10 @@ def fluxbin_unpack_canonical(layer: PackedLayer, stream=None) -> Tuple[object, o
     _check(lib().fluxbin_unpack_canonical(ctypes.byref(layer.layer), signs.data_ptr(),
                                           dense.data_ptr() if dense is not None else None, _stream(stream)))
     return signs.view(s.Kb, s.M, W), (dense.view(s.Ks, s.M, -1) if dense is not None else None)
+
+
+def fluxbin_stream_probe(layer: PackedLayer, sink, stream=None) -> None:
+    """Launch the measurement-only stream probe (the batch-1 kernel's weight requests without the table work) on
+    ``sink``, a device buffer of at least 1024 bytes."""
+    _check(lib().fluxbin_stream_probe(ctypes.byref(layer.layer), sink.data_ptr(), sink.numel() * sink.element_size(),
+                                      _stream(stream)))

@@ -193,6 +193,7 @@ def test_gemv_rejects_bad_arguments(L):
     assert gb(ctypes.byref(lay), 17, X, 300, Y, 1000, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert gb(ctypes.byref(lay), 2, X, 299, Y, 1000, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert gb(ctypes.byref(lay), 2, X, 300, Y, 999, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
+    assert L.fluxbin_stream_probe(ctypes.byref(lay), X, 1000, None) == fb.FLUXBIN_ERR_BUFFER_TOO_SMALL
     # a descriptor edited by hand no longer matches its shape
     lay.off_signs += 256
     assert g(ctypes.byref(lay), X, Y, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
@@ -200,3 +201,4 @@ def test_gemv_rejects_bad_arguments(L):
     assert L.fluxbin_workspace_init(WS, 6, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert L.fluxbin_debug_indices(None, X, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert L.fluxbin_unpack_canonical(None, X, None, None) == fb.FLUXBIN_ERR_INVALID_ARG
+    assert L.fluxbin_stream_probe(None, X, 1024, None) == fb.FLUXBIN_ERR_INVALID_ARG

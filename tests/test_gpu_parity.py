@@ -264,6 +264,27 @@ def test_zero_activation_gives_zero():
     assert np.all(y == 0)
 
 
+def test_stream_probe_runs_and_leaves_results_alone():
+    """The measurement-only probe launches on every batch-1 plan shape (small and large layers) and writes nothing
+    the GEMV reads: a GEMV after it gives the same result as before."""
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    log("case stream probe")
+    sink = torch.zeros(256, dtype=torch.int32, device="cuda")
+    for spec in (LayerSpec("p1", M=700, N=512, Kb=2, Ks=1, mu=8, S=9, g_r=128, g_s=9, seed=41),
+                 LayerSpec("p2", M=4096, N=4096, Kb=2, Ks=1, mu=8, S=41, g_r=128, g_s=41, seed=42)):
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        xb = make_activations(L, 1)
+        y0 = run_gemm(packed, xb, out_fp32=True)
+        fb.fluxbin_stream_probe(packed, sink)
+        torch.cuda.synchronize()
+        assert np.array_equal(run_gemm(packed, xb, out_fp32=True), y0)
+    L = make_layer(LayerSpec("p3", M=300, N=256, Kb=2, Ks=0, mu=4, S=0, g_r=128, g_s=1, seed=43))
+    with pytest.raises(fb.FluxbinError):
+        fb.fluxbin_stream_probe(pack_layer(L), sink)
+
+
 def test_graph_replays_match_eager():
     """The kernels captured in a HIP graph give the eager result on every replay, with eager work in between."""
     import torch
