@@ -387,8 +387,11 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   // column-scale and plane-table loads. Large layers (not EARLY) stage the activations before requesting any sign
   // data: with every CU starting its sign stream at once, activation loads queued with it would return only after the
   // first burst; so the global columns are staged after one short round trip, then the salient gathers, the sign
-  // loads of units 0..D-1 and their row scales are issued. Small layers (EARLY) request the sign data right after the
-  // activation loads, so the two round trips overlap. The tables of unit 0 are built right after.
+  // loads of units 0..D-1 and their row scales are issued. Small layers (EARLY) request the sign data and row scales
+  // of units 0..D-1 right after the activation loads, so the round trips overlap; the salient gathers follow them
+  // (loads complete in issue order, so a gather issued before the row scales would hold the first lookups back until
+  // the activations arrived and the row scales made a round trip of their own). The tables of unit 0 are built right
+  // after.
   const bool hb = ((t >> 4) & 1) != 0;
   int32_t pl[D][2];
 #pragma unroll
@@ -411,12 +414,12 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
     issue_signs<NT, RPT>(a, cur, ring[k]);
     cursor_advance<NT, RPT>(a, cur, k + 1 < st.n);
   }
-  if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     issue_rscale<NT, RPT>(a, cur0, pl[k][0], pl[k][1], ring[k]);
     cursor_advance<NT, RPT>(a, cur0, k + 1 < st.n);
   }
+  if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);
 
   // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32.
   uint32_t c1[4], c2[4];
