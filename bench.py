@@ -44,7 +44,7 @@ def lookups(spec, B: int = 1) -> int:
 
 
 class Bench:
-    def __init__(self, layer_specs, B: int, copies_target_bytes: float):
+    def __init__(self, layer_specs, B: int, copies_target_bytes: float, min_copies: int = 1):
         import numpy as np
         import torch
         from paper_2608_15602_amd import fluxbin as fb
@@ -63,7 +63,7 @@ class Bench:
                 dev[name] = torch.from_numpy(np.ascontiguousarray(a).view(dt)).cuda()
             shape = fb.make_shape(spec.M, spec.N, spec.Kb, spec.Ks, spec.mu, spec.g_r, spec.S, spec.g_s)
             one = fb.fluxbin_pack_query(shape)
-            n_copies = max(1, math.ceil(copies_target_bytes / (one * len(layer_specs))))
+            n_copies = max(min_copies, math.ceil(copies_target_bytes / (one * len(layer_specs))))
             packs = [fb.fluxbin_pack(shape, dev) for _ in range(n_copies)]
             del dev
             x = torch.from_numpy(make_activations(L, B).view(np.float16)).cuda()
@@ -156,6 +156,41 @@ class Bench:
             out.append(ts[len(ts) // 2])
         return out
 
+    def set_batch(self, B: int):
+        """Rebind activations, outputs and workspaces for batch B (the packed copies stay)."""
+        import numpy as np
+        import torch
+        from synth import make_activations
+        self.B = B
+        for it in self.items:
+            it["x"] = torch.from_numpy(make_activations(it["L"], B).view(np.float16)).cuda()
+            it["y"] = torch.empty(B, it["spec"].M, dtype=torch.float16, device="cuda")
+            it["ws"] = self.fb.make_workspace(it["packs"][0], B)
+            it["bytes"] = algorithmic_bytes(it["spec"], B)
+            it["lookups"] = lookups(it["spec"], B)
+        torch.cuda.synchronize()
+
+    def cold_launch_us(self, trials: int = 5):
+        """Single eager launches, each event-timed on its own: the caches hold none of the packed copy it reads (the
+        copies rotate and together exceed the 256 MB last-level cache), and the launch overhead is included. Median
+        over `trials` per layer."""
+        import torch
+        out = []
+        for it in self.items:
+            ts = []
+            for k in range(trials):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                e0.record()
+                self.launch(it, 1 + k)
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1000.0)
+            ts.sort()
+            out.append(ts[len(ts) // 2])
+        return out
+
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_gemv_mu8_b1_mlp70b_hbm_traffic.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_15602_amd", "csrc", f) for f in ("fluxbin_gemv.hip", "fluxbin_host.cpp")]
@@ -214,8 +249,45 @@ def cpu_baseline(bench, budget_s: float):
         t_total += dt
         done_bytes += it["bytes"] * rows / spec.M
         parts.append(f"{spec.name}: rows 0..{rows - 1} of {spec.M}")
-    return {"value": round(done_bytes / t_total / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
-            "sample": "; ".join(parts) + f" (fp64 reconstruct + matvec, {t_total:.1f} s)"}
+    res = {"value": round(done_bytes / t_total / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+           "sample": "; ".join(parts) + f" (fp64 reconstruct + matvec, {t_total:.1f} s)"}
+    it = bench.items[0]
+    spec = it["spec"]
+    x = it["x"].cpu().numpy().view(np.uint16)
+    # the same oracle on one core (BLAS limited to one thread), on a smaller sample of the first layer
+    try:
+        from threadpoolctl import threadpool_limits
+        rows = 512
+        with threadpool_limits(limits=1):
+            t = time.perf_counter()
+            oracle.gemv_dense(it["L"], x, row_range=(0, rows))
+            dt = time.perf_counter() - t
+        res["one_core"] = {"value": round(it["bytes"] * rows / spec.M / dt / 1e9, 4), "unit": "GB/s",
+                           "sample": f"{spec.name}: rows 0..{rows - 1} ({dt:.1f} s)"}
+    except Exception as e:   # threadpoolctl missing: report why
+        res["one_core"] = {"value": None, "error": str(e)}
+    # matvec only, on an already reconstructed fp64 block of W-hat (the reconstruction is not timed); 8192 rows of the
+    # first layer are 0.5 GB, more than the host's last-level cache, so the matvecs stream it from memory
+    rows = min(spec.M, 8192)
+    W = oracle.reconstruct_rows(it["L"], 0, rows)
+    xv = oracle.f16_to_f64(x)[0]
+    reps = 0
+    t = time.perf_counter()
+    while time.perf_counter() - t < 2.0 or reps < 3:
+        W @ xv
+        reps += 1
+    dt = (time.perf_counter() - t) / reps
+    res["matvec_only"] = {"value": round(it["bytes"] * rows / spec.M / dt / 1e9, 4), "unit": "GB/s",
+                          "sample": f"{spec.name}: fp64 rows 0..{rows - 1} reconstructed beforehand, {reps} matvecs",
+                          "fp64_bytes_read_GBps": round(W.nbytes / dt / 1e9, 2)}
+    del W
+    try:
+        with open("/proc/cpuinfo") as f:
+            res["cpu_model"] = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:
+        pass
+    res["logical_cpus"] = os.cpu_count()
+    return res
 
 
 def small_batch_us(specs, batches, launches=40):
@@ -229,6 +301,31 @@ def small_batch_us(specs, batches, launches=40):
             s = it["spec"]
             out[f"{s.name}_B{B}"] = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
                                      "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2)}
+        del b
+        torch.cuda.empty_cache()
+    return out
+
+
+def decoder_layer_us(g_r: str, batches=(1, 4, 16), steps: int = 40):
+    """A synthetic 70B decoder layer's seven linears (q, k, v, o, gate, up, down) in one HIP graph per step, for both
+    hybrid variants (2 bases + 1% salient, 3 bases + 5% salient), at least three rotated copies of every layer;
+    end-to-end microseconds per decoder layer (all seven calls) and the whole layer's bytes per microsecond."""
+    import torch
+    from synth import config_layers
+    out = {}
+    allspecs = config_layers("c5_layer70b", g_r)
+    for variant in ("2b1pct", "3b5pct"):
+        specs = [sp for sp in allspecs if sp.name.startswith(variant)]
+        b = Bench(specs, 1, 1.6e9, min_copies=3)
+        for B in batches:
+            if B != b.B:
+                b.set_batch(B)
+            b.run(2, 2)   # warm up graph capture for this batch
+            total_ms, _ = b.run(steps, 2)
+            us = total_ms * 1000.0 / steps
+            step_bytes = sum(it["bytes"] for it in b.items)
+            out[f"{variant}_B{B}"] = {"us_per_layer": round(us, 2), "GBps": round(step_bytes / (us * 1e-6) / 1e9, 1),
+                                      "calls": len(b.items), "copies_min": min(len(it["packs"]) for it in b.items)}
         del b
         torch.cuda.empty_cache()
     return out
@@ -251,6 +348,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 and small-batch per-call figures")
+    ap.add_argument("--no-decoder", action="store_true", help="skip the 70B decoder-layer graph figures")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before anything else, run a plain device-to-device copy of this many MiB three times "
                          "(the reference dispatch for HBM byte counters)")
@@ -290,12 +388,13 @@ def main():
     total_ms, wall = bench.run(args.steps, args.warmup)
     kern_us = bench.per_launch_us()
     probe_us = bench.stream_probe_us()
+    cold_us = bench.cold_launch_us()
     step_bytes = sum(it["bytes"] for it in bench.items)
     value = step_bytes * args.steps / (total_ms * 1e-3) / 1e9
     achieved = step_bytes / (sum(kern_us) * 1e-6) / 1e9
     traffic = measured_traffic()
     per_layer = {}
-    for it, us, pus in zip(bench.items, kern_us, probe_us):
+    for it, us, pus, cus in zip(bench.items, kern_us, probe_us, cold_us):
         s = it["spec"]
         per_layer[s.name] = {
             "shape_out_x_in": f"{s.M}x{s.N}", "us_per_gemv": round(us, 3),
@@ -304,6 +403,7 @@ def main():
             "tflop_eq": round(2.0 * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
             "bytes": it["bytes"], "lookups": it["lookups"],
             "stream_probe_us": round(pus, 3), "frac_of_stream_probe": round(pus / us, 4),
+            "cold_single_launch_us": round(cus, 2),
         }
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -326,6 +426,8 @@ def main():
         out["config"]["attn_4096x4096_us_per_gemv"] = round(us, 3)
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
         out["config"]["small_batch"] = small_batch_us(specs, (4, 16))
+    if not args.no_decoder:
+        out["config"]["decoder_layer_70b"] = decoder_layer_us(args.g_r)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -115,7 +115,7 @@ __device__ __forceinline__ bool tile_end(const GemmArgs& a, int64_t tile, int64_
 // unless its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
 template <int NT, int RPT, int BP>
 __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
-  constexpr int CH = (RPT * BP == 1) ? 48 : 16;
+  constexpr int CH = 16;   // loads in flight per thread; larger unrolls lengthen this rarely run (cold) code
   const int t = threadIdx.x;
   const int64_t R = int64_t(NT) * RPT;
   const int b_first = owner_of(a, int(tile) * a.steps);
