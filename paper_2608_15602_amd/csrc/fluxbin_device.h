@@ -159,8 +159,9 @@ __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
 }
 
 // Waits until every memory operation of the workgroup has completed, then publishes its pending tiles (at most two:
-// its first and its last tile). Thread 0 bumps both counters back to back, so the two round trips overlap; a counter
-// that reaches the number of contributors makes this workgroup the one that reduces that tile.
+// its first and its last tile). Lanes 0 and 1 of the first wave bump the two counters with one instruction, so the two
+// round trips are one; a counter that reaches the number of contributors makes this workgroup the one that reduces
+// that tile.
 template <int NT, int RPT, int BP>
 __device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0, int pending1, int n_pending,
                                                 int* s_flag) {
@@ -168,23 +169,18 @@ __device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0,
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (n_pending == 0) return;
-  if (threadIdx.x == 0) {
-    const int tiles[2] = {pending0, pending1};
-    uint32_t prev[2] = {0u, 0u};
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      if (i < n_pending)
-        prev[i] = __hip_atomic_fetch_add(a.counters + tiles[i], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    int flags = 0;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      if (i < n_pending) {
-        const int bf = owner_of(a, tiles[i] * a.steps);
-        const int bl = owner_of(a, (tiles[i] + 1) * a.steps - 1);
-        if (prev[i] == uint32_t(bl - bf)) flags |= 1 << i;
-      }
+  if (threadIdx.x < 64) {
+    const int lane = int(threadIdx.x);
+    const int tile = lane == 0 ? pending0 : pending1;
+    bool last = false;
+    if (lane < n_pending) {
+      const uint32_t prev = __hip_atomic_fetch_add(a.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int bf = owner_of(a, tile * a.steps);
+      const int bl = owner_of(a, (tile + 1) * a.steps - 1);
+      last = prev == uint32_t(bl - bf);
     }
-    *s_flag = flags;
+    const uint64_t m = __ballot(last);
+    if (lane == 0) *s_flag = int(m & 3u);
   }
   __syncthreads();
   const int flags = *s_flag;
