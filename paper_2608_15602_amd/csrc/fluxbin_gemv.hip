@@ -57,6 +57,14 @@ struct Ring {
   uint32_t rb[RPT];     // same for chunk 2sc+1
 };
 
+// Super-chunk index sc0 + k of a workgroup's unit k, wrapped at the end of the tile: v < steps + kXvUnits, so one
+// subtraction suffices unless the layer has fewer than kXvUnits super-chunks (then the remainder).
+__device__ __forceinline__ int wrap_sc(int v, int steps) {
+  if (v >= steps) v -= steps;
+  if (v >= steps) v %= steps;
+  return v;
+}
+
 // Stage the folded activations xv = x[j] * colscale of the n <= kXvUnits units starting at super-chunk sc0 into
 // xs[k*256 + col] (super-chunks wrap around at the end of a tile). Global chunks read x[j] directly (j follows from the
 // chunk index); salient chunks read their input column from the VCM index table first (Eq. 13), then gather it.
@@ -64,45 +72,55 @@ struct Ring {
 // short round trip), writes the global and padding columns and issues the salient gathers; the sign loads follow, and
 // stage_write_salient() writes the gathered columns of a range of units when they are needed (waiting for the gathers
 // never waits for sign data, which was requested after them).
+// Every wavefront covers 64 columns of one half (one chunk) of each of its units, so the unit, its super-chunk, the
+// chunk and whether it is salient are wavefront-uniform (scalar) values; only the column within the chunk is per lane.
+// All 16 wavefronts of a workgroup run this prologue at once, so it is kept free of divisions and loops: its scalar
+// instructions, issued for every wavefront, delay the first sign requests of the last wavefronts.
 template <int NT>
 struct Staged {
   uint32_t v[B1<NT, 1>::KPT];    // x bits (global column) or the index (salient column)
   uint32_t cs[B1<NT, 1>::KPT];   // column scale bits
   uint32_t g[B1<NT, 1>::KPT];    // gathered x bits of salient columns
+  uint32_t sal;                  // bit m: the wavefront's chunk of its m-th staged unit is salient (or padding)
+  uint32_t pad;                  // bit m: this lane's column of a global chunk is past the N input columns
   int32_t plane;                 // threads t < 2*kXvUnits: row-scale plane of chunk 2*sc(t/2) + (t&1)
 };
+
+// k-th staged unit of this thread's wavefront (wavefront-uniform).
+template <int NT>
+__device__ __forceinline__ int staged_unit(int m) {
+  return (__builtin_amdgcn_readfirstlane(int(threadIdx.x)) >> 8) + m * (NT / 256);
+}
 
 template <int NT>
 __device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, int sc0) {
   using P = B1<NT, 1>;
   const int t = threadIdx.x;
   const int col = t & 255;
+  const int half = (__builtin_amdgcn_readfirstlane(t) >> 7) & 1;   // chunk of the super-chunk this wavefront covers
+  sg.sal = 0u;
+  sg.pad = 0u;
 #pragma unroll
   for (int m = 0; m < P::KPT; ++m) {   // unconditional, always in-bounds loads: all in flight at once
-    const int k = (t >> 8) + m * (NT / 256);
-    int sc = sc0 + k;
-    while (sc >= a.steps) sc -= a.steps;
+    const int k = staged_unit<NT>(m);
+    const int sc = wrap_sc(sc0 + k, a.steps);
+    const int c = 2 * sc + half;       // chunk (scalar)
     const int v = sc * 256 + col;
-    const int c = v >> 7;
-    int j = 0;
-    bool direct = false;
-    if (c < a.ngc) {
-      j = (c - (c / a.ncg) * a.ncg) * 128 + (col & 127);
-      direct = j < a.N;
-    }
-    sg.v[m] = c < a.ngc ? (direct ? uint32_t(a.x[j]) : 0u) : uint32_t(a.xidx[v]);
+    const bool sal = c >= a.ngc;
+    int cm = c;                        // global chunk: its column block within its base, c mod ncg (Kb <= 4)
+    if (cm >= a.ncg) cm -= a.ncg;
+    if (cm >= a.ncg) cm -= a.ncg;
+    if (cm >= a.ncg) cm -= a.ncg;
+    const int j = cm * 128 + (col & 127);
+    const bool pad = !sal && j >= a.N;
+    // one unconditional load per unit (a select of addresses, not of loads, so that no load waits for another)
+    sg.v[m] = uint32_t(*(sal ? a.xidx + v : a.x + (pad ? 0 : j)));
     sg.cs[m] = a.colscale[v];
+    sg.sal |= uint32_t(sal) << m;
+    sg.pad |= uint32_t(pad) << m;
   }
-  int scp = sc0 + (t >> 1) % kXvUnits;
-  while (scp >= a.steps) scp -= a.steps;
-  sg.plane = a.chunk_plane[2 * scp + (t & 1)];
-}
-
-template <int NT>
-__device__ __forceinline__ bool staged_salient(const GemmArgs& a, int sc0, int k, int col) {
-  int sc = sc0 + k;
-  while (sc >= a.steps) sc -= a.steps;
-  return ((sc * 256 + col) >> 7) >= a.ngc;
+  sg.plane = 0;
+  if (t < 2 * kXvUnits) sg.plane = a.chunk_plane[2 * wrap_sc(sc0 + (t >> 1), a.steps) + (t & 1)];
 }
 
 template <int NT>
@@ -114,11 +132,11 @@ __device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT>
   if (t < 2 * kXvUnits) s_planes[t] = sg.plane;
 #pragma unroll
   for (int m = 0; m < P::KPT; ++m) {
-    const int k = (t >> 8) + m * (NT / 256);
-    const bool sal = staged_salient<NT>(a, sc0, k, col);
+    const int k = staged_unit<NT>(m);
+    const bool sal = (sg.sal >> m) & 1u;
     // unconditional, always in-bounds gather (x[0] for the other columns)
     sg.g[m] = a.x[(sal && sg.v[m] != 0xFFFFu) ? sg.v[m] : 0u];
-    if (k < n && !sal) xs[k * 256 + col] = h2f(uint16_t(sg.v[m])) * h2f(uint16_t(sg.cs[m]));
+    if (k < n && !sal) xs[k * 256 + col] = ((sg.pad >> m) & 1u) ? 0.f : h2f(uint16_t(sg.v[m])) * h2f(uint16_t(sg.cs[m]));
   }
 }
 
@@ -130,8 +148,8 @@ __device__ __forceinline__ void stage_write_salient(const GemmArgs& a, const Sta
   const int col = t & 255;
 #pragma unroll
   for (int m = 0; m < P::KPT; ++m) {
-    const int k = (t >> 8) + m * (NT / 256);
-    if (k >= k_begin && k < k_end && k < n && staged_salient<NT>(a, sc0, k, col))
+    const int k = staged_unit<NT>(m);
+    if (k >= k_begin && k < k_end && k < n && ((sg.sal >> m) & 1u))
       xs[k * 256 + col] = sg.v[m] == 0xFFFFu ? 0.f : h2f(uint16_t(sg.g[m])) * h2f(uint16_t(sg.cs[m]));
   }
 }
@@ -376,9 +394,18 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   st.tile = u0 / a.steps;
   st.sc = u0 - st.tile * a.steps;
   st.first_tile = st.tile;
-  st.last_tile = (u1 - 1) / a.steps;
-  st.first_shared = tile_is_shared(a, st.first_tile);
-  st.last_shared = tile_is_shared(a, st.last_tile);
+  {   // the last unit's tile without a division: st.sc + n - 1 < steps + kXvUnits
+    int r = st.sc + st.n - 1;
+    st.last_tile = st.tile;
+    if (r >= a.steps) {
+      r -= a.steps;
+      ++st.last_tile;
+      if (r >= a.steps) st.last_tile += r / a.steps;
+    }
+  }
+  // a tile is shared unless this workgroup covers all of it (its units are one contiguous range)
+  st.first_shared = u0 != st.first_tile * a.steps || u1 < (st.first_tile + 1) * a.steps;
+  st.last_shared = u1 != (st.last_tile + 1) * a.steps || u0 > st.last_tile * a.steps;
   st.n_pending = 0;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) st.acc[j][0] = 0.f;
@@ -396,8 +423,7 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   int32_t pl[D][2];
 #pragma unroll
   for (int k = 0; k < D; ++k) {
-    int sck = st.sc + (k < st.n ? k : st.n - 1);
-    while (sck >= a.steps) sck -= a.steps;
+    const int sck = wrap_sc(st.sc + (k < st.n ? k : st.n - 1), a.steps);
     pl[k][0] = load_uniform_i32(a.chunk_plane, 2 * sck);
     pl[k][1] = load_uniform_i32(a.chunk_plane, 2 * sck + 1);
   }
@@ -421,18 +447,14 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   }
   if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);
 
-  // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32.
+  // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32. Byte bb of c1[m] is
+  // (hb << 6) | (s << 2) with s = (t + 4m + bb) mod 16 (the four bytes at once: no byte exceeds 18 before the mask).
   uint32_t c1[4], c2[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
-    c1[m] = 0u;
-    c2[m] = 0u;
-#pragma unroll
-    for (int bb = 0; bb < 4; ++bb) {
-      const uint32_t s = (uint32_t(4 * m + bb) + uint32_t(t)) & 15u;
-      c1[m] |= ((uint32_t(hb) << 6) | (s << 2)) << (8 * bb);
-      c2[m] |= ((uint32_t(!hb) << 6) | (s << 2)) << (8 * bb);
-    }
+    const uint32_t sb = ((((uint32_t(t) + 4u * m) & 15u) * 0x01010101u + 0x03020100u) & 0x0F0F0F0Fu) << 2;
+    c1[m] = sb | (hb ? 0x40404040u : 0u);
+    c2[m] = sb | (hb ? 0u : 0x40404040u);
   }
 
   stage_write_salient<NT>(a, sg, xs, sc0, st.n, 0, 2);
