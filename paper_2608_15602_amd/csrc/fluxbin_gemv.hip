@@ -124,12 +124,12 @@ __device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, i
 }
 
 template <int NT>
-__device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT>& sg, float* xs, int* s_planes,
+__device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT>& sg, float* xs, int64_t* s_roff,
                                                    int sc0, int n) {
   using P = B1<NT, 1>;
   const int t = threadIdx.x;
   const int col = t & 255;
-  if (t < 2 * kXvUnits) s_planes[t] = sg.plane;
+  if (t < 2 * kXvUnits) s_roff[t] = int64_t(sg.plane) * a.Mp * 2;
 #pragma unroll
   for (int m = 0; m < P::KPT; ++m) {
     const int k = staged_unit<NT>(m);
@@ -272,10 +272,10 @@ __device__ __forceinline__ void issue_signs(const GemmArgs& a, const Cursor<NT, 
 }
 
 template <int NT, int RPT>
-__device__ __forceinline__ void issue_rscale(const GemmArgs& a, const Cursor<NT, RPT>& c, int32_t pa, int32_t pb,
+__device__ __forceinline__ void issue_rscale(const GemmArgs& a, const Cursor<NT, RPT>& c, int64_t oa, int64_t ob,
                                              Ring<RPT>& rg) {
-  const uint8_t* ba = reinterpret_cast<const uint8_t*>(a.rscale) + int64_t(pa) * a.Mp * 2;
-  const uint8_t* bb = reinterpret_cast<const uint8_t*>(a.rscale) + int64_t(pb) * a.Mp * 2;
+  const uint8_t* ba = reinterpret_cast<const uint8_t*>(a.rscale) + oa;
+  const uint8_t* bb = reinterpret_cast<const uint8_t*>(a.rscale) + ob;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
     rg.ra[j] = *reinterpret_cast<const uint32_t*>(ba + c.roff[j]);
@@ -288,19 +288,29 @@ __device__ __forceinline__ float lds_at(const float* lut, uint32_t byte_addr) {
   return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(lut) + byte_addr + BUF * 128);
 }
 
+// Sum of 16 lookups as a balanced tree: the reads are all issued before the first add, and the adds wait for pairs of
+// results instead of one result each.
+__device__ __forceinline__ float tree16(float (&v)[16]) {
+#pragma unroll
+  for (int w = 1; w < 16; w *= 2)
+#pragma unroll
+    for (int i = 0; i < 16; i += 2 * w) v[i] += v[i + w];
+  return v[0];
+}
+
 template <int NT, int RPT, int BUF>
 __device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT>& rg, const uint32_t (&c1)[4],
                                           const uint32_t (&c2)[4], bool hb, float (&acc)[RPT][1]) {
   const uint32_t sh = (threadIdx.x & 1u) * 16u;   // the rows of a thread have the parity of threadIdx.x
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
-    float s1 = 0.f, s2 = 0.f;
+    float v1[16], v2[16];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb) {
         const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
-        s1 += lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][m], c1[m], sel));
+        v1[4 * m + bb] = lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][m], c1[m], sel));
       }
     }
 #pragma unroll
@@ -308,9 +318,11 @@ __device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT>& rg,
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb) {
         const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
-        s2 += lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][4 + m], c2[m], sel));
+        v2[4 * m + bb] = lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][4 + m], c2[m], sel));
       }
     }
+    const float s1 = tree16(v1);
+    const float s2 = tree16(v2);
     // s1 belongs to chunk 2sc + hb, s2 to the other one
     const float sa = hb ? s2 : s1;
     const float sb = hb ? s1 : s2;
@@ -319,11 +331,16 @@ __device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT>& rg,
   }
 }
 
-// Row-scale plane of chunk 2*sc(k) + half of the workgroup's unit k (clamped to its last unit), from the table the
-// prologue staged in LDS (a broadcast read; no scalar load is waited for inside the pipeline).
-__device__ __forceinline__ int32_t plane_of(const int* s_planes, int k, int n, int half = 0) {
+// Byte offsets in the row-scale section of the planes of chunks 2*sc(k) and 2*sc(k)+1 of the workgroup's unit k
+// (clamped to its last unit), from the table the prologue staged in LDS (one broadcast read; no scalar load is waited
+// for inside the pipeline).
+__device__ __forceinline__ void roff_of(const int64_t* s_roff, int k, int n, int64_t& oa, int64_t& ob) {
   const int kk = k < n ? k : n - 1;
-  return __builtin_amdgcn_readfirstlane(s_planes[2 * kk + half]);
+  const int4 v = *reinterpret_cast<const int4*>(s_roff + 2 * kk);
+  oa = int64_t((uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(v.y))) << 32) |
+               uint32_t(__builtin_amdgcn_readfirstlane(v.x)));
+  ob = int64_t((uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(v.w))) << 32) |
+               uint32_t(__builtin_amdgcn_readfirstlane(v.z)));
 }
 
 // Per-workgroup state of the batch-1 kernel.
@@ -345,15 +362,16 @@ struct B1State {
 template <int NT, int RPT, int D, int K>
 __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
                                          Ring<RPT> (&ring)[D + 1], float* lut, float* xs, const uint32_t (&c1)[4],
-                                         const uint32_t (&c2)[4], bool hb, const int* s_planes,
+                                         const uint32_t (&c2)[4], bool hb, const int64_t* s_roff,
                                          const Staged<NT>& sg, int sc0) {
   if constexpr (K < kXvUnits) {
     if (K >= st.n) return;
     constexpr int BUF = K & 1;
     constexpr int KI = (K + D) < kXvUnits ? (K + D) : kXvUnits - 1;   // unit requested (clamped)
     issue_signs<NT, RPT>(a, cur, ring[(K + D) % (D + 1)]);
-    issue_rscale<NT, RPT>(a, cur, plane_of(s_planes, KI, st.n), plane_of(s_planes, KI, st.n, 1),
-                          ring[(K + D) % (D + 1)]);
+    int64_t oa, ob;
+    roff_of(s_roff, KI, st.n, oa, ob);
+    issue_rscale<NT, RPT>(a, cur, oa, ob, ring[(K + D) % (D + 1)]);
     cursor_advance<NT, RPT>(a, cur, K + D + 1 < st.n);
     if (K + 1 < st.n) build_b1<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
     if constexpr (K == 0) stage_write_salient<NT>(a, sg, xs, sc0, st.n, 2, kXvUnits);   // built from step 1 on
@@ -374,7 +392,7 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
       st.sc = 0;
       ++st.tile;
     }
-    steps_b1<NT, RPT, D, K + 1>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes, sg, sc0);
+    steps_b1<NT, RPT, D, K + 1>(a, st, cur, ring, lut, xs, c1, c2, hb, s_roff, sg, sc0);
   }
 }
 
@@ -382,7 +400,7 @@ template <int NT, int RPT, int D, bool EARLY>
 __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float lut[256 * 64];       // 64 KB, two buffers interleaved per pattern
   __shared__ __attribute__((aligned(16))) float xs[kXvUnits * 256];  // staged folded activations
-  __shared__ int s_planes[2 * kXvUnits];                               // row-scale planes of the staged units
+  __shared__ __attribute__((aligned(16))) int64_t s_roff[2 * kXvUnits];   // row-scale plane byte offsets, staged units
   __shared__ int s_flag;
 
   const int t = threadIdx.x;
@@ -420,12 +438,12 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   // the activations arrived and the row scales made a round trip of their own). The tables of unit 0 are built right
   // after.
   const bool hb = ((t >> 4) & 1) != 0;
-  int32_t pl[D][2];
+  int64_t pl[D][2];   // byte offsets of the row-scale planes of units 0..D-1
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int sck = wrap_sc(st.sc + (k < st.n ? k : st.n - 1), a.steps);
-    pl[k][0] = load_uniform_i32(a.chunk_plane, 2 * sck);
-    pl[k][1] = load_uniform_i32(a.chunk_plane, 2 * sck + 1);
+    pl[k][0] = int64_t(load_uniform_i32(a.chunk_plane, 2 * sck)) * a.Mp * 2;
+    pl[k][1] = int64_t(load_uniform_i32(a.chunk_plane, 2 * sck + 1)) * a.Mp * 2;
   }
   Staged<NT> sg;
   const int sc0 = st.sc;
@@ -434,7 +452,7 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
   Ring<RPT> ring[D + 1];
   Cursor<NT, RPT> cur0 = cur;
-  if constexpr (!EARLY) stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);   // n <= kXvUnits (launch plan)
+  if constexpr (!EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);   // n <= kXvUnits (launch plan)
 #pragma unroll
   for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
     issue_signs<NT, RPT>(a, cur, ring[k]);
@@ -445,7 +463,7 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
     issue_rscale<NT, RPT>(a, cur0, pl[k][0], pl[k][1], ring[k]);
     cursor_advance<NT, RPT>(a, cur0, k + 1 < st.n);
   }
-  if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_planes, sc0, st.n);
+  if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);
 
   // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32. Byte bb of c1[m] is
   // (hb << 6) | (s << 2) with s = (t + 4m + bb) mod 16 (the four bytes at once: no byte exceeds 18 before the mask).
@@ -461,7 +479,7 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   __syncthreads();
   build_b1<NT, 0>(lut, xs);
   __syncthreads();
-  steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_planes, sg, sc0);
+  steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_roff, sg, sc0);
   const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
   publish_pending<NT, RPT, 1>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
@@ -484,7 +502,8 @@ __global__ void __launch_bounds__(NT) k_stream_probe(GemmArgs a, uint32_t* sink)
   for (int k = 0; k < D; ++k) {
     issue_signs<NT, 1>(a, cur, ring[k]);
     const int32_t p0 = load_uniform_i32(a.chunk_plane, 2 * sck);
-    issue_rscale<NT, 1>(a, cur, p0, load_uniform_i32(a.chunk_plane, 2 * sck + 1), ring[k]);
+    issue_rscale<NT, 1>(a, cur, int64_t(p0) * a.Mp * 2, int64_t(load_uniform_i32(a.chunk_plane, 2 * sck + 1)) * a.Mp * 2,
+                        ring[k]);
     cursor_advance<NT, 1>(a, cur, k + 1 < n);
     if (++sck == a.steps) sck = 0;
   }
@@ -493,8 +512,8 @@ __global__ void __launch_bounds__(NT) k_stream_probe(GemmArgs a, uint32_t* sink)
     if (k < n) {
       Ring<1>& nx = ring[(k + D) % (D + 1)];
       issue_signs<NT, 1>(a, cur, nx);
-      issue_rscale<NT, 1>(a, cur, load_uniform_i32(a.chunk_plane, 2 * sck),
-                          load_uniform_i32(a.chunk_plane, 2 * sck + 1), nx);
+      issue_rscale<NT, 1>(a, cur, int64_t(load_uniform_i32(a.chunk_plane, 2 * sck)) * a.Mp * 2,
+                          int64_t(load_uniform_i32(a.chunk_plane, 2 * sck + 1)) * a.Mp * 2, nx);
       cursor_advance<NT, 1>(a, cur, k + D + 1 < n);
       if (++sck == a.steps) sck = 0;
       const Ring<1>& r = ring[k % (D + 1)];
