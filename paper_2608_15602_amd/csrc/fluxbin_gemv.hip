@@ -93,7 +93,7 @@ __device__ __forceinline__ int staged_unit(int m) {
 }
 
 template <int NT>
-__device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, int sc0) {
+__device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, const int2* s_unit) {
   using P = B1<NT, 1>;
   const int t = threadIdx.x;
   const int col = t & 255;
@@ -103,15 +103,12 @@ __device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, i
 #pragma unroll
   for (int m = 0; m < P::KPT; ++m) {   // unconditional, always in-bounds loads: all in flight at once
     const int k = staged_unit<NT>(m);
-    const int sc = wrap_sc(sc0 + k, a.steps);
-    const int c = 2 * sc + half;       // chunk (scalar)
-    const int v = sc * 256 + col;
-    const bool sal = c >= a.ngc;
-    int cm = c;                        // global chunk: its column block within its base, c mod ncg (Kb <= 4)
-    if (cm >= a.ncg) cm -= a.ncg;
-    if (cm >= a.ncg) cm -= a.ncg;
-    if (cm >= a.ncg) cm -= a.ncg;
-    const int j = cm * 128 + (col & 127);
+    const int2 u = s_unit[2 * k + half];
+    const int jb = __builtin_amdgcn_readfirstlane(u.x);   // column base within the input, or -1: salient chunk
+    const int c = __builtin_amdgcn_readfirstlane(u.y);    // chunk
+    const int v = c * 128 + (col & 127);                   // virtual column
+    const bool sal = jb < 0;
+    const int j = jb + (col & 127);
     const bool pad = !sal && j >= a.N;
     // one unconditional load per unit (a select of addresses, not of loads, so that no load waits for another)
     sg.v[m] = uint32_t(*(sal ? a.xidx + v : a.x + (pad ? 0 : j)));
@@ -120,7 +117,7 @@ __device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, i
     sg.pad |= uint32_t(pad) << m;
   }
   sg.plane = 0;
-  if (t < 2 * kXvUnits) sg.plane = a.chunk_plane[2 * wrap_sc(sc0 + (t >> 1), a.steps) + (t & 1)];
+  if (t < 2 * kXvUnits) sg.plane = a.chunk_plane[s_unit[t].y];
 }
 
 template <int NT>
@@ -403,51 +400,70 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) int64_t s_roff[2 * kXvUnits];   // row-scale plane byte offsets, staged units
   __shared__ int s_flag;
 
+  __shared__ int s_hdr[4];                                  // tile, sc, last tile, sharing flags
+  __shared__ __attribute__((aligned(8))) int2 s_unit[2 * kXvUnits];   // per staged chunk: column base, chunk index
+
   const int t = threadIdx.x;
   const int u0 = first_unit(a, blockIdx.x);
   const int u1 = first_unit(a, blockIdx.x + 1);
 
-  B1State<NT, RPT> st;
-  st.n = u1 - u0;
-  st.tile = u0 / a.steps;
-  st.sc = u0 - st.tile * a.steps;
-  st.first_tile = st.tile;
-  {   // the last unit's tile without a division: st.sc + n - 1 < steps + kXvUnits
-    int r = st.sc + st.n - 1;
-    st.last_tile = st.tile;
+  // Values that are the same for the whole workgroup are computed once, by the first wavefront, and read back by all
+  // (16 wavefronts computing them each would spend their scalar issue slots on it while the first ones wait).
+  if (t < 64) {
+    const int n = u1 - u0;
+    const int tile = u0 / a.steps;
+    const int sc = u0 - tile * a.steps;
+    int last_tile = tile;   // the last unit's tile without a division: sc + n - 1 < steps + kXvUnits
+    int r = sc + n - 1;
     if (r >= a.steps) {
       r -= a.steps;
-      ++st.last_tile;
-      if (r >= a.steps) st.last_tile += r / a.steps;
+      ++last_tile;
+      if (r >= a.steps) last_tile += r / a.steps;
+    }
+    if (t < 2 * kXvUnits) {   // staged chunk t: unit t/2 (wrapped at the end of the tile), half t&1
+      const int c = 2 * wrap_sc(sc + (t >> 1), a.steps) + (t & 1);
+      int cm = c;             // global chunk: its column block within its base, c mod ncg (Kb <= 4)
+      if (cm >= a.ncg) cm -= a.ncg;
+      if (cm >= a.ncg) cm -= a.ncg;
+      if (cm >= a.ncg) cm -= a.ncg;
+      s_unit[t] = make_int2(c < a.ngc ? cm * 128 : -1, c);
+    }
+    if (t == 0) {
+      // a tile is shared unless this workgroup covers all of it (its units are one contiguous range)
+      const bool fs = u0 != tile * a.steps || u1 < (tile + 1) * a.steps;
+      const bool ls = u1 != (last_tile + 1) * a.steps || u0 > last_tile * a.steps;
+      s_hdr[0] = tile;
+      s_hdr[1] = sc;
+      s_hdr[2] = last_tile;
+      s_hdr[3] = int(fs) | (int(ls) << 1);
     }
   }
-  // a tile is shared unless this workgroup covers all of it (its units are one contiguous range)
-  st.first_shared = u0 != st.first_tile * a.steps || u1 < (st.first_tile + 1) * a.steps;
-  st.last_shared = u1 != (st.last_tile + 1) * a.steps || u0 > st.last_tile * a.steps;
+  __syncthreads();
+
+  B1State<NT, RPT> st;
+  st.n = u1 - u0;
+  st.tile = __builtin_amdgcn_readfirstlane(s_hdr[0]);
+  st.sc = __builtin_amdgcn_readfirstlane(s_hdr[1]);
+  st.first_tile = st.tile;
+  st.last_tile = __builtin_amdgcn_readfirstlane(s_hdr[2]);
+  const int sh_flags = __builtin_amdgcn_readfirstlane(s_hdr[3]);
+  st.first_shared = (sh_flags & 1) != 0;
+  st.last_shared = (sh_flags & 2) != 0;
   st.n_pending = 0;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) st.acc[j][0] = 0.f;
 
-  // Prologue: the row-scale planes of units 0..D-1 as scalar loads (their own counter) and the activation,
-  // column-scale and plane-table loads. Large layers (not EARLY) stage the activations before requesting any sign
-  // data: with every CU starting its sign stream at once, activation loads queued with it would return only after the
-  // first burst; so the global columns are staged after one short round trip, then the salient gathers, the sign
-  // loads of units 0..D-1 and their row scales are issued. Small layers (EARLY) request the sign data and row scales
-  // of units 0..D-1 right after the activation loads, so the round trips overlap; the salient gathers follow them
-  // (loads complete in issue order, so a gather issued before the row scales would hold the first lookups back until
-  // the activations arrived and the row scales made a round trip of their own). The tables of unit 0 are built right
-  // after.
+  // Prologue: the activation, column-scale and plane-table loads. Large layers (not EARLY) stage the activations
+  // before requesting any sign data: with every CU starting its sign stream at once, activation loads queued with it
+  // would return only after the first burst; so the global columns are staged after one short round trip, then the
+  // salient gathers and the sign loads of units 0..D-1 are issued. Small layers (EARLY) request the sign data of units
+  // 0..D-1 right after the activation loads, so the round trips overlap; the salient gathers follow them. The row
+  // scales of units 0..D-1 are requested after the first barrier, from the plane offsets staged in LDS (a unit's row
+  // scales are used last, after all its lookups), and the tables of unit 0 are built right after.
   const bool hb = ((t >> 4) & 1) != 0;
-  int64_t pl[D][2];   // byte offsets of the row-scale planes of units 0..D-1
-#pragma unroll
-  for (int k = 0; k < D; ++k) {
-    const int sck = wrap_sc(st.sc + (k < st.n ? k : st.n - 1), a.steps);
-    pl[k][0] = int64_t(load_uniform_i32(a.chunk_plane, 2 * sck)) * a.Mp * 2;
-    pl[k][1] = int64_t(load_uniform_i32(a.chunk_plane, 2 * sck + 1)) * a.Mp * 2;
-  }
   Staged<NT> sg;
   const int sc0 = st.sc;
-  stage_issue<NT>(a, sg, sc0);
+  stage_issue<NT>(a, sg, s_unit);
   Cursor<NT, RPT> cur;
   cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
   Ring<RPT> ring[D + 1];
@@ -457,11 +473,6 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
     issue_signs<NT, RPT>(a, cur, ring[k]);
     cursor_advance<NT, RPT>(a, cur, k + 1 < st.n);
-  }
-#pragma unroll
-  for (int k = 0; k < D; ++k) {
-    issue_rscale<NT, RPT>(a, cur0, pl[k][0], pl[k][1], ring[k]);
-    cursor_advance<NT, RPT>(a, cur0, k + 1 < st.n);
   }
   if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);
 
@@ -477,6 +488,14 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
 
   stage_write_salient<NT>(a, sg, xs, sc0, st.n, 0, 2);
   __syncthreads();
+  // the row scales of units 0..D-1, from the plane offsets just staged (they are used last in a unit's lookups)
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    int64_t oa, ob;
+    roff_of(s_roff, k, st.n, oa, ob);
+    issue_rscale<NT, RPT>(a, cur0, oa, ob, ring[k]);
+    cursor_advance<NT, RPT>(a, cur0, k + 1 < st.n);
+  }
   build_b1<NT, 0>(lut, xs);
   __syncthreads();
   steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_roff, sg, sc0);
