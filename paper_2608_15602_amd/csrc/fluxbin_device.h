@@ -155,7 +155,7 @@ __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
         if (b < a.B) store_y(a, b, row, sum[b]);
     }
   }
-  if (t == 0) __hip_atomic_store(a.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (t == 0) __hip_atomic_store(a.counters + tile * kCounterStride, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Waits until every memory operation of the workgroup has completed, then publishes its pending tiles (at most two:
@@ -174,7 +174,8 @@ __device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0,
     const int tile = lane == 0 ? pending0 : pending1;
     bool last = false;
     if (lane < n_pending) {
-      const uint32_t prev = __hip_atomic_fetch_add(a.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t prev = __hip_atomic_fetch_add(a.counters + int64_t(tile) * kCounterStride, 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
       const int bf = owner_of(a, tile * a.steps);
       const int bl = owner_of(a, (tile + 1) * a.steps - 1);
       last = prev == uint32_t(bl - bf);

@@ -310,7 +310,7 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   a.B = args.B - 4 * grp < 4 ? args.B - 4 * grp : 4;
   a.x = args.x + int64_t(4 * grp) * args.ldx;
   a.y = static_cast<char*>(args.y) + int64_t(4 * grp) * args.ldy * (args.y_fp32 ? 4 : 2);
-  a.counters = args.counters + int64_t(grp) * (((args.n_tiles * 4 + 255) & ~255) / 4);
+  a.counters = args.counters + int64_t(grp) * (((int64_t(args.n_tiles) * kCounterStride * 4 + 255) & ~255) / 4);
   a.partials = args.partials + int64_t(grp) * args.blocks * 2 * 1024 * Bat::BPN;
 
   const int t = threadIdx.x;

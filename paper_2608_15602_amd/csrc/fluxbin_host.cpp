@@ -209,7 +209,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   p->ws_counters_off = 0;
   // the small-batch kernel runs one row of workgroups per group of four batch rows, each with its own counters
   const uint64_t counter_sets = p->kernel == 2 ? uint64_t(p->n_groups) : 1u;
-  p->ws_partials_off = counter_sets * round_up256(uint64_t(p->n_tiles) * 4u);
+  p->ws_partials_off = counter_sets * round_up256(uint64_t(p->n_tiles) * uint64_t(kCounterStride) * 4u);
   p->ws_bytes = p->ws_partials_off + uint64_t(p->blocks) * 2u * uint64_t(p->rows) * uint64_t(p->bpad) * 4u;
   return FLUXBIN_OK;
 }
