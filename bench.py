@@ -193,7 +193,7 @@ class Bench:
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_gemv_mu8_b1_mlp70b_hbm_traffic.md")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_15602_amd", "csrc", f) for f in ("fluxbin_gemv.hip", "fluxbin_host.cpp")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_15602_amd", "csrc", f) for f in ("fluxbin_gemv.hip", "fluxbin_host.cpp", "fluxbin_device.h", "fluxbin_internal.h")]
 
 
 def measured_traffic():
