@@ -43,6 +43,11 @@ def lookups(spec, B: int = 1) -> int:
     return B * spec.M * (spec.Kb * -(-spec.N // spec.mu) + spec.Ks * -(-spec.S // spec.mu))
 
 
+# Every layer's launches rotate over distinct packed copies totalling at least this many bytes (over twice the 256 MB
+# last-level cache), so that each launch reads its weights from HBM.
+COPIES_BYTES_PER_LAYER = 600e6
+
+
 class Bench:
     def __init__(self, layer_specs, B: int, copies_target_bytes: float, min_copies: int = 1):
         import numpy as np
@@ -296,7 +301,7 @@ def small_batch_us(specs, batches, launches=40):
     import torch
     out = {}
     for B in batches:
-        b = Bench(specs, B, 600e6)
+        b = Bench(specs, B, COPIES_BYTES_PER_LAYER * len(specs))
         for it, us in zip(b.items, b.per_launch_us(launches, 3)):
             s = it["spec"]
             out[f"{s.name}_B{B}"] = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
@@ -331,10 +336,27 @@ def decoder_layer_us(g_r: str, batches=(1, 4, 16), steps: int = 40):
     return out
 
 
+def kernel_variants_us(g_r: str, launches: int = 40):
+    """The 28672 x 8192 layer in the kernel variants the paper ablates (mu = 8 vs 4, pure global 3 and 4 bases, 2 bases
+    + 1% salient), batch 1, graph-timed like the headline figure; the mu = 4 variant runs the generic kernel."""
+    import torch
+    from synth import kernel_variant_layers
+    out = {}
+    for spec in kernel_variant_layers(g_r):
+        b = Bench([spec], 1, COPIES_BYTES_PER_LAYER)
+        us = b.per_launch_us(launches, 3)[0]
+        it = b.items[0]
+        out[spec.name] = {"Kb": spec.Kb, "Ks": spec.Ks, "S": spec.S, "mu": spec.mu, "us_per_call": round(us, 3),
+                          "bytes": it["bytes"], "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1)}
+        del b
+        torch.cuda.empty_cache()
+    return out
+
+
 def small_layer_us(spec, launches=200):
     """Per-call microseconds of a small layer (4096x4096): a HIP graph of back-to-back launches rotating distinct
     packed copies (so the signs come from HBM), median of 5 replays."""
-    b = Bench([spec], 1, 512e6)
+    b = Bench([spec], 1, COPIES_BYTES_PER_LAYER)
     us = b.per_launch_us(launches, 5)[0]
     return us, b.items[0]["bytes"]
 
@@ -349,6 +371,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 and small-batch per-call figures")
     ap.add_argument("--no-decoder", action="store_true", help="skip the 70B decoder-layer graph figures")
+    ap.add_argument("--no-variants", action="store_true", help="skip the kernel-variant figures (mu 4, pure global)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before anything else, run a plain device-to-device copy of this many MiB three times "
                          "(the reference dispatch for HBM byte counters)")
@@ -373,7 +396,7 @@ def main():
         del src, dst
         print(f"# copy calibration: 3 x {n} bytes device-to-device", file=sys.stderr, flush=True)
     specs = config_layers("c4_mlp70b", args.g_r)
-    bench = Bench(specs, 1, 600e6)
+    bench = Bench(specs, 1, COPIES_BYTES_PER_LAYER * len(specs))
     print("# packed " + ", ".join(f"{it['spec'].name} x{len(it['packs'])}" for it in bench.items), file=sys.stderr,
           flush=True)
     if args.eager_launches > 0:
@@ -428,6 +451,8 @@ def main():
         out["config"]["small_batch"] = small_batch_us(specs, (4, 16))
     if not args.no_decoder:
         out["config"]["decoder_layer_70b"] = decoder_layer_us(args.g_r)
+    if not args.no_variants:
+        out["config"]["kernel_variants_28672x8192"] = kernel_variants_us(args.g_r)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -11,4 +11,5 @@ from .layers import (  # noqa: F401
     make_layer,
     make_activations,
     salient_count,
+    kernel_variant_layers,
 )

@@ -137,6 +137,21 @@ def config_layers(cfg: str, g_r: str = "128") -> List[LayerSpec]:
     return out
 
 
+def kernel_variant_layers(g_r: str = "128") -> List[LayerSpec]:
+    """The 70B MLP up shape (28672 x 8192, out x in) in the kernel variants the paper ablates: mu = 8 and mu = 4 with
+    3 bases + 1 salient base on 5% of the columns, pure global bases (3 and 4, no salient part), and 2 bases + 1 on 1%
+    of the columns. Used for timing and for sampled-row parity at full size."""
+    M, N = 28672, 8192
+    out = [_attn_mlp("hyb3b5_mu8", M, N, 3, 0.05, seed=3, layer_id=10, outlier_frac=0.001),
+           _attn_mlp("hyb3b5_mu4", M, N, 3, 0.05, seed=3, layer_id=11, mu=4, outlier_frac=0.001),
+           LayerSpec("glob3b_mu8", M=M, N=N, Kb=3, Ks=0, mu=8, S=0, g_r=128, g_s=1, outlier_frac=0.001, seed=3,
+                     layer_id=12),
+           LayerSpec("glob4b_mu8", M=M, N=N, Kb=4, Ks=0, mu=8, S=0, g_r=128, g_s=1, outlier_frac=0.001, seed=3,
+                     layer_id=13),
+           _attn_mlp("hyb2b1_mu8", M, N, 2, 0.01, seed=3, layer_id=14, outlier_frac=0.001)]
+    return [s.with_(g_r=s.N) if g_r == "N" else s for s in out]
+
+
 def _build_configs() -> Dict[str, dict]:
     c = {}
     c["c1_tiny"] = dict(

@@ -177,6 +177,16 @@ def test_config5_layer70b():
         torch.cuda.empty_cache()
 
 
+def test_kernel_variants_full_size():
+    """The 28672 x 8192 layer in the kernel variants the benchmark times (mu 4, pure global bases, 2b + 1%), sampled
+    rows at full size in the launch configuration the benchmark uses."""
+    import torch
+    from synth import kernel_variant_layers
+    for spec in kernel_variant_layers("128"):
+        _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=5))
+        torch.cuda.empty_cache()
+
+
 EDGE_SPECS = [
     LayerSpec("one_row", M=1, N=128, Kb=1, Ks=1, mu=8, S=1, g_r=128, g_s=1, seed=11),
     LayerSpec("ragged_rows", M=1000, N=512, Kb=2, Ks=1, mu=8, S=33, g_r=256, g_s=33, seed=12),
