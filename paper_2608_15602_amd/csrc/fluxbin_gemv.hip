@@ -36,10 +36,9 @@ namespace fluxbin {
 // Pipeline per workgroup: a register ring of D+1 units of sign words and row scales; unit k+D is requested while the
 // tables of unit k+1 are built (other LDS buffer) and unit k is looked up, so D+1 units of sign data are in flight at
 // every wait. The folded
-// activations of all the workgroup's units (at most kXvUnits, guaranteed by the launch plan) are staged in LDS first.
+// activations of all the workgroup's units (at most XV = b1_max_units(NT), guaranteed by the launch plan) are staged in LDS first.
 // =====================================================================================================================
 
-constexpr int kXvUnits = kB1MaxUnits;  // units whose folded activations are staged in LDS (1 KB each)
 
 template <int NT, int RPT>
 struct B1 {
@@ -47,7 +46,8 @@ struct B1 {
   static constexpr int NHI = NT / 32;                                   // pattern ranges per (slot, s) in the build
   static constexpr int LO = NHI == 4 ? 6 : (NHI == 8 ? 5 : (NHI == 16 ? 4 : 3));
   static constexpr int E = 1 << LO;                                     // entries per thread per build
-  static constexpr int KPT = kXvUnits / (NT / 256);                     // staged units per thread
+  static constexpr int XV = b1_max_units(NT);                            // units staged in LDS (1 KB each)
+  static constexpr int KPT = XV / (NT / 256);                           // staged units per thread
 };
 
 template <int RPT>
@@ -57,15 +57,15 @@ struct Ring {
   uint32_t rb[RPT];     // same for chunk 2sc+1
 };
 
-// Super-chunk index sc0 + k of a workgroup's unit k, wrapped at the end of the tile: v < steps + kXvUnits, so one
-// subtraction suffices unless the layer has fewer than kXvUnits super-chunks (then the remainder).
+// Super-chunk index sc0 + k of a workgroup's unit k, wrapped at the end of the tile: v < steps + XV, so one
+// subtraction suffices unless the layer has fewer than XV super-chunks (then the remainder).
 __device__ __forceinline__ int wrap_sc(int v, int steps) {
   if (v >= steps) v -= steps;
   if (v >= steps) v %= steps;
   return v;
 }
 
-// Stage the folded activations xv = x[j] * colscale of the n <= kXvUnits units starting at super-chunk sc0 into
+// Stage the folded activations xv = x[j] * colscale of the n <= XV units starting at super-chunk sc0 into
 // xs[k*256 + col] (super-chunks wrap around at the end of a tile). Global chunks read x[j] directly (j follows from the
 // chunk index); salient chunks read their input column from the VCM index table first (Eq. 13), then gather it.
 // stage_issue() issues the loads. stage_write_global() waits for them (nothing else is in flight yet, so this is one
@@ -83,7 +83,7 @@ struct Staged {
   uint32_t g[B1<NT, 1>::KPT];    // gathered x bits of salient columns
   uint32_t sal;                  // bit m: the wavefront's chunk of its m-th staged unit is salient (or padding)
   uint32_t pad;                  // bit m: this lane's column of a global chunk is past the N input columns
-  int32_t plane;                 // threads t < 2*kXvUnits: row-scale plane of chunk 2*sc(t/2) + (t&1)
+  int32_t plane;                 // threads t < 2*XV: row-scale plane of chunk 2*sc(t/2) + (t&1)
 };
 
 // k-th staged unit of this thread's wavefront (wavefront-uniform).
@@ -117,7 +117,7 @@ __device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, c
     sg.pad |= uint32_t(pad) << m;
   }
   sg.plane = 0;
-  if (t < 2 * kXvUnits) sg.plane = a.chunk_plane[s_unit[t].y];
+  if (t < 2 * P::XV) sg.plane = a.chunk_plane[s_unit[t].y];
 }
 
 template <int NT>
@@ -126,7 +126,7 @@ __device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT>
   using P = B1<NT, 1>;
   const int t = threadIdx.x;
   const int col = t & 255;
-  if (t < 2 * kXvUnits) s_roff[t] = int64_t(sg.plane) * a.Mp * 2;
+  if (t < 2 * P::XV) s_roff[t] = int64_t(sg.plane) * a.Mp * 2;
 #pragma unroll
   for (int m = 0; m < P::KPT; ++m) {
     const int k = staged_unit<NT>(m);
@@ -354,24 +354,25 @@ struct B1State {
 // Step K of the pipeline (K = unit index within the workgroup): request unit K+D into ring slot (K+D) % (D+1) (the
 // slot of unit K-1, looked up in the previous step), build unit K+1 into LDS buffer (K+1) % 2, look up unit K (slot
 // K % (D+1), buffer K % 2). The prologue requests units 0..D-1, so D+1 units are in flight at every wait. The steps
-// are unrolled at compile time (a workgroup has at most kXvUnits units) so that the wait before each lookup covers
+// are unrolled at compile time (a workgroup has at most XV units) so that the wait before each lookup covers
 // exactly the loads of unit K.
 template <int NT, int RPT, int D, int K>
 __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
                                          Ring<RPT> (&ring)[D + 1], float* lut, float* xs, const uint32_t (&c1)[4],
                                          const uint32_t (&c2)[4], bool hb, const int64_t* s_roff,
                                          const Staged<NT>& sg, int sc0) {
-  if constexpr (K < kXvUnits) {
+  constexpr int XV = B1<NT, 1>::XV;
+  if constexpr (K < XV) {
     if (K >= st.n) return;
     constexpr int BUF = K & 1;
-    constexpr int KI = (K + D) < kXvUnits ? (K + D) : kXvUnits - 1;   // unit requested (clamped)
+    constexpr int KI = (K + D) < XV ? (K + D) : XV - 1;   // unit requested (clamped)
     issue_signs<NT, RPT>(a, cur, ring[(K + D) % (D + 1)]);
     int64_t oa, ob;
     roff_of(s_roff, KI, st.n, oa, ob);
     issue_rscale<NT, RPT>(a, cur, oa, ob, ring[(K + D) % (D + 1)]);
     cursor_advance<NT, RPT>(a, cur, K + D + 1 < st.n);
     if (K + 1 < st.n) build_b1<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
-    if constexpr (K == 0) stage_write_salient<NT>(a, sg, xs, sc0, st.n, 2, kXvUnits);   // built from step 1 on
+    if constexpr (K == 0) stage_write_salient<NT>(a, sg, xs, sc0, st.n, 2, XV);   // built from step 1 on
     lookup_b1<NT, RPT, BUF>(lut, ring[K % (D + 1)], c1, c2, hb, st.acc);
     if (st.sc == a.steps - 1 || K + 1 == st.n) {
       const bool shared = st.tile == st.first_tile ? st.first_shared : (st.tile == st.last_tile ? st.last_shared : false);
@@ -396,12 +397,13 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
 template <int NT, int RPT, int D, bool EARLY>
 __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float lut[256 * 64];       // 64 KB, two buffers interleaved per pattern
-  __shared__ __attribute__((aligned(16))) float xs[kXvUnits * 256];  // staged folded activations
-  __shared__ __attribute__((aligned(16))) int64_t s_roff[2 * kXvUnits];   // row-scale plane byte offsets, staged units
+  constexpr int XV = B1<NT, 1>::XV;
+  __shared__ __attribute__((aligned(16))) float xs[XV * 256];  // staged folded activations
+  __shared__ __attribute__((aligned(16))) int64_t s_roff[2 * XV];   // row-scale plane byte offsets, staged units
   __shared__ int s_flag;
 
   __shared__ int s_hdr[4];                                  // tile, sc, last tile, sharing flags
-  __shared__ __attribute__((aligned(8))) int2 s_unit[2 * kXvUnits];   // per staged chunk: column base, chunk index
+  __shared__ __attribute__((aligned(8))) int2 s_unit[2 * XV];   // per staged chunk: column base, chunk index
 
   const int t = threadIdx.x;
   const int u0 = first_unit(a, blockIdx.x);
@@ -413,14 +415,14 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
     const int n = u1 - u0;
     const int tile = u0 / a.steps;
     const int sc = u0 - tile * a.steps;
-    int last_tile = tile;   // the last unit's tile without a division: sc + n - 1 < steps + kXvUnits
+    int last_tile = tile;   // the last unit's tile without a division: sc + n - 1 < steps + XV
     int r = sc + n - 1;
     if (r >= a.steps) {
       r -= a.steps;
       ++last_tile;
       if (r >= a.steps) last_tile += r / a.steps;
     }
-    if (t < 2 * kXvUnits) {   // staged chunk t: unit t/2 (wrapped at the end of the tile), half t&1
+    if (t < 2 * XV) {   // staged chunk t: unit t/2 (wrapped at the end of the tile), half t&1
       const int c = 2 * wrap_sc(sc + (t >> 1), a.steps) + (t & 1);
       int cm = c;             // global chunk: its column block within its base, c mod ncg (Kb <= 4)
       if (cm >= a.ncg) cm -= a.ncg;
@@ -468,7 +470,7 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
   cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
   Ring<RPT> ring[D + 1];
   Cursor<NT, RPT> cur0 = cur;
-  if constexpr (!EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);   // n <= kXvUnits (launch plan)
+  if constexpr (!EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);   // n <= XV (launch plan)
 #pragma unroll
   for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
     issue_signs<NT, RPT>(a, cur, ring[k]);
@@ -527,7 +529,7 @@ __global__ void __launch_bounds__(NT) k_stream_probe(GemmArgs a, uint32_t* sink)
     if (++sck == a.steps) sck = 0;
   }
 #pragma unroll
-  for (int k = 0; k < kB1MaxUnits; ++k) {   // n <= kB1MaxUnits (launch plan); unrolled so the ring stays in registers
+  for (int k = 0; k < B1<NT, 1>::XV; ++k) {   // n <= XV (launch plan); unrolled so the ring stays in registers
     if (k < n) {
       Ring<1>& nx = ring[(k + D) % (D + 1)];
       issue_signs<NT, 1>(a, cur, nx);

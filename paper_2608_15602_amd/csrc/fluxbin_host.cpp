@@ -203,8 +203,9 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int min_units = env_int("FLUXBIN_MIN_UNITS", 3);
   if (min_units > 1 && p->kernel == 0 && p->blocks > 1 && ceil_div(p->units, p->blocks) < min_units)
     p->blocks = ceil_div(p->units, int64_t(min_units)) > 0 ? ceil_div(p->units, int64_t(min_units)) : 1;
-  // the batch-1 kernel stages the folded activations of all its units at once: at most kB1MaxUnits per workgroup
-  if (p->kernel == 0 && ceil_div(p->units, p->blocks) > kB1MaxUnits) p->blocks = ceil_div(p->units, kB1MaxUnits);
+  // the batch-1 kernel stages the folded activations of all its units at once: at most b1_max_units(nt) per workgroup
+  if (p->kernel == 0 && ceil_div(p->units, p->blocks) > b1_max_units(p->nt))
+    p->blocks = ceil_div(p->units, int64_t(b1_max_units(p->nt)));
   if (p->kernel == 2 && ceil_div(p->units, p->blocks) > kBatMaxUnits) p->blocks = ceil_div(p->units, kBatMaxUnits);
   p->ws_counters_off = 0;
   // the small-batch kernel runs one row of workgroups per group of four batch rows, each with its own counters

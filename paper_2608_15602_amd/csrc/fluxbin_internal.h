@@ -11,7 +11,9 @@ namespace fluxbin {
 constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes of signs per row)
 constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
 constexpr int kMaxBatch = 16;
-constexpr int kB1MaxUnits = 12;         // units per workgroup of the batch-1 kernel (its LDS staging capacity)
+// Units per workgroup of the batch-1 kernel (its LDS staging capacity): 16 for 1024-thread workgroups (one per CU),
+// 12 for the smaller ones (two or more share a CU's LDS).
+constexpr int b1_max_units(int nt) { return nt == 1024 ? 16 : 12; }
 constexpr int kBatMaxUnits = 12;        // units per workgroup of the small-batch mu = 8 kernel (its LDS index table)
 // Tile counters of the split-tile reduction sit kCounterStride 32-bit words (256 bytes) apart: every workgroup
 // publishes at the end of a launch, and device-scope atomics on one memory line are serialized (densely packed
