@@ -49,7 +49,7 @@ COPIES_BYTES_PER_LAYER = 600e6
 
 
 class Bench:
-    def __init__(self, layer_specs, B: int, copies_target_bytes: float, min_copies: int = 1):
+    def __init__(self, layer_specs, B: int, copies_target_bytes: float, min_copies: int = 1, layers=None):
         import numpy as np
         import torch
         from paper_2608_15602_amd import fluxbin as fb
@@ -58,8 +58,8 @@ class Bench:
         self.specs = layer_specs
         self.B = B
         self.items = []
-        for spec in layer_specs:
-            L = make_layer(spec)
+        for li, spec in enumerate(layer_specs):
+            L = layers[li] if layers is not None else make_layer(spec)
             dev = {}
             for name in ("signs", "alpha_r", "alpha_c", "sal_idx", "sal_signs", "alpha_sr", "alpha_sc"):
                 a = getattr(L, name)
@@ -353,6 +353,29 @@ def kernel_variants_us(g_r: str, launches: int = 40):
     return out
 
 
+def vcm_ablation_us(g_r: str, launches: int = 40):
+    """The paper's VCM ablation on the 70B MLP layers: each layer as packed (salient columns repacked densely, VCM on)
+    and as the same weights with the salient bases kept full width (VCM off: Ks more global bases with a column scale
+    that is zero off the salient set), batch 1, graph-timed."""
+    import torch
+    from synth import config_layers, make_layer, vcm_off_equivalent
+    out = {}
+    for spec in config_layers("c4_mlp70b", g_r):
+        L = make_layer(spec)
+        for name, lay in (("vcm_on", L), ("vcm_off", vcm_off_equivalent(L))):
+            b = Bench([lay.spec], 1, COPIES_BYTES_PER_LAYER, layers=[lay])
+            us = b.per_launch_us(launches, 3)[0]
+            it = b.items[0]
+            out[f"{spec.name}_{name}"] = {"us_per_call": round(us, 3), "bytes": it["bytes"],
+                                          "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1)}
+            del b
+            torch.cuda.empty_cache()
+    for nm in ("up", "down"):
+        on, off = out[f"{nm}_vcm_on"]["us_per_call"], out[f"{nm}_vcm_off"]["us_per_call"]
+        out[f"{nm}_latency_change_with_vcm"] = round(on / off - 1.0, 4)
+    return out
+
+
 def small_layer_us(spec, launches=200):
     """Per-call microseconds of a small layer (4096x4096): a HIP graph of back-to-back launches rotating distinct
     packed copies (so the signs come from HBM), median of 5 replays."""
@@ -453,6 +476,7 @@ def main():
         out["config"]["decoder_layer_70b"] = decoder_layer_us(args.g_r)
     if not args.no_variants:
         out["config"]["kernel_variants_28672x8192"] = kernel_variants_us(args.g_r)
+        out["config"]["vcm_ablation"] = vcm_ablation_us(args.g_r)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -12,4 +12,5 @@ from .layers import (  # noqa: F401
     make_activations,
     salient_count,
     kernel_variant_layers,
+    vcm_off_equivalent,
 )

@@ -111,6 +111,32 @@ def make_layer(spec: LayerSpec) -> SyntheticLayer:
     return SyntheticLayer(spec, signs, alpha_r, alpha_c, sal_idx, sal_signs, alpha_sr, alpha_sc, outliers)
 
 
+def vcm_off_equivalent(layer: SyntheticLayer) -> SyntheticLayer:
+    """The same weights without the dense salient repack (the paper's VCM ablation): the Ks salient bases become Ks
+    more global bases over all N columns, with their full-width sign planes as stored, a column scale that is zero off
+    the salient set, and the one salient row scale of each row repeated over the row-scale groups. Only valid when a
+    row has one salient row scale per base (g_s >= S, as in every workload here). Same activations (same seed, layer
+    id and outlier channels); same exact result."""
+    sp = layer.spec
+    if sp.S > 0 and sp.g_s < sp.S:
+        raise ValueError("vcm_off_equivalent needs one salient row scale per row and base (g_s >= S)")
+    ks = sp.Ks if sp.S > 0 else 0
+    spec = sp.with_(name=sp.name + "_vcmoff", Kb=sp.Kb + ks, Ks=0, S=0, g_s=1)
+    G = spec.G_r
+    signs = np.concatenate([layer.signs, layer.sal_signs[:ks]], axis=0)
+    ar_sal = (np.repeat(layer.alpha_sr[:ks, :, :1], G, axis=2) if ks
+              else np.zeros((0, sp.M, G), dtype=layer.alpha_r.dtype))
+    alpha_r = np.concatenate([layer.alpha_r, ar_sal], axis=0)
+    ac_sal = np.zeros((ks, sp.N), dtype=np.uint16)
+    if ks:
+        ac_sal[:, layer.sal_idx] = layer.alpha_sc[:ks, layer.sal_idx]
+    alpha_c = np.concatenate([layer.alpha_c, ac_sal], axis=0)
+    W = -(-sp.N // 32)
+    return SyntheticLayer(spec, np.ascontiguousarray(signs), np.ascontiguousarray(alpha_r),
+                          np.ascontiguousarray(alpha_c), np.zeros(0, np.int32), np.zeros((0, sp.M, W), np.uint32),
+                          np.zeros((0, sp.M, 1), np.uint16), np.zeros((0, sp.N), np.uint16), layer.outliers)
+
+
 def make_activations(layer: SyntheticLayer, B: int, draw: int = 0) -> np.ndarray:
     """fp16 activations [B, N] (as uint16 bits); outlier channels scaled by 20 before rounding."""
     spec = layer.spec

@@ -187,6 +187,23 @@ def test_kernel_variants_full_size():
         torch.cuda.empty_cache()
 
 
+def test_vcm_off_equivalent_full_size():
+    """The VCM ablation's layer (salient bases kept full width as extra global bases) gives the oracle's result of
+    the original hybrid layer, on sampled rows of the 70B MLP up layer."""
+    import torch
+    from synth import vcm_off_equivalent
+    spec = config_layers("c4_mlp70b", "128")[0]
+    L = make_layer(spec)
+    V = vcm_off_equivalent(L)
+    packed = pack_layer(V)
+    x = make_activations(L, 1)
+    y = run_gemm(packed, x)
+    rows = sample_rows(spec.M, 256, seed=6)
+    _check(y[:, rows], oracle.gemv_dense(L, x, rows=rows), "VCM-off layer vs hybrid oracle")
+    del packed
+    torch.cuda.empty_cache()
+
+
 EDGE_SPECS = [
     LayerSpec("one_row", M=1, N=128, Kb=1, Ks=1, mu=8, S=1, g_r=128, g_s=1, seed=11),
     LayerSpec("ragged_rows", M=1000, N=512, Kb=2, Ks=1, mu=8, S=33, g_r=256, g_s=33, seed=12),
