@@ -353,6 +353,25 @@ def kernel_variants_us(g_r: str, launches: int = 40):
     return out
 
 
+def mu_profile_us(g_r: str, launches: int = 40):
+    """mu = 8 against mu = 4 (same weights' shapes and seeds) on the 7B attention and MLP layers, batch 1; mu = 4 runs
+    the generic kernel (one chunk per unit, tables of 16 entries)."""
+    import torch
+    from synth import config_layers
+    out = {}
+    for cfg in ("c2_attn7b", "c3_mlp7b"):
+        for spec in config_layers(cfg, g_r):
+            for mu in (8, 4):
+                sp = spec.with_(mu=mu, name=f"{spec.name}_mu{mu}")
+                b = Bench([sp], 1, COPIES_BYTES_PER_LAYER)
+                us = b.per_launch_us(launches, 3)[0]
+                out[f"{cfg}_{sp.name}"] = {"shape_out_x_in": f"{sp.M}x{sp.N}", "us_per_call": round(us, 3),
+                                           "GBps": round(b.items[0]["bytes"] / (us * 1e-6) / 1e9, 1)}
+                del b
+                torch.cuda.empty_cache()
+    return out
+
+
 def vcm_ablation_us(g_r: str, launches: int = 40):
     """The paper's VCM ablation on the 70B MLP layers: each layer as packed (salient columns repacked densely, VCM on)
     and as the same weights with the salient bases kept full width (VCM off: Ks more global bases with a column scale
@@ -477,6 +496,7 @@ def main():
     if not args.no_variants:
         out["config"]["kernel_variants_28672x8192"] = kernel_variants_us(args.g_r)
         out["config"]["vcm_ablation"] = vcm_ablation_us(args.g_r)
+        out["config"]["mu_profile"] = mu_profile_us(args.g_r)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
     print(json.dumps(out), flush=True)

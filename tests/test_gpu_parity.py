@@ -187,6 +187,13 @@ def test_kernel_variants_full_size():
         torch.cuda.empty_cache()
 
 
+def test_mu4_profile_layers_full_size():
+    """The 7B attention and MLP layers at mu = 4 (the benchmark's mu profile), sampled rows at full size."""
+    for cfg in ("c2_attn7b", "c3_mlp7b"):
+        for spec in config_layers(cfg, "128"):
+            _parity(spec.with_(mu=4, name=spec.name + "_mu4"), 1, rows=sample_rows(spec.M, 256, seed=7))
+
+
 def test_vcm_off_equivalent_full_size():
     """The VCM ablation's layer (salient bases kept full width as extra global bases) gives the oracle's result of
     the original hybrid layer, on sampled rows of the 70B MLP up layer."""
