@@ -197,7 +197,7 @@ class Bench:
         return out
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_gemv_mu8_b1_mlp70b_hbm_traffic.md")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_gemv_b1_mlp70b_hbm_traffic.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_15602_amd", "csrc", f) for f in ("fluxbin_gemv.hip", "fluxbin_host.cpp", "fluxbin_device.h", "fluxbin_internal.h")]
 
 
@@ -480,7 +480,7 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": (sum(traffic[it["spec"].name] for it in bench.items) if traffic else None),
                      "traffic_per_launch": traffic,
-                     "kernel": "k_gemv_mu8_b1 (HIP events around graph replays of back-to-back launches)",
+                     "kernel": "k_gemv_b1<8,...> (HIP events around graph replays of back-to-back launches)",
                      "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items},
                      "frac_of_stream_probe": round(sum(probe_us) / sum(kern_us), 4)},
         "wall_s_timed": round(wall, 3),

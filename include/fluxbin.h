@@ -207,7 +207,7 @@ fluxbin_status fluxbin_unpack_canonical(const fluxbin_layer* layer, uint32_t* d_
  * layer exactly as the batch-1 GEMV does (same launch plan, units, per-thread addresses and request depth) but does no
  * table work, giving the bandwidth this access pattern can reach on the device; the benchmark reports the GEMV's
  * bandwidth against it. d_sink (device, at least 1024 bytes) receives meaningless checksums. Same validation and
- * stream semantics as fluxbin_lut_gemv; mu must be 8.
+ * stream semantics as fluxbin_lut_gemv.
  */
 fluxbin_status fluxbin_stream_probe(const fluxbin_layer* layer, uint32_t* d_sink, size_t sink_bytes,
                                     hipStream_t stream);

@@ -185,6 +185,25 @@ __device__ __forceinline__ void build_b1(float* lut, const float* xv256) {
   }
 }
 
+// mu = 4: the 2 x 32 tables (16 entries each) of one super-chunk into buffer BUF. Layout (floats): buffer BUF at
+// BUF*2048, chunk h at h*1024, entry (p, u) at p*64 + u and again at p*64 + u + 32, so that a lookup of sub-vector
+// (base + j) mod 32 is the address p*64 + base + j with no wrap (j < 8 an immediate). Entry e of the 1024 is
+// (h, p, u) = (e >> 9, (e >> 5) & 15, e & 31): the sum of the sub-vector's four folded activations with the signs of p.
+template <int NT, int BUF>
+__device__ __forceinline__ void build_b1_mu4(float* lut, const float* xv256) {
+#pragma unroll
+  for (int e0 = 0; e0 < 1024; e0 += NT) {
+    const int e = e0 + int(threadIdx.x);
+    const int h = e >> 9, p = (e >> 5) & 15, u = e & 31;
+    const float4 x4 = *reinterpret_cast<const float4*>(xv256 + h * 128 + 4 * u);
+    const float v = ((p & 1) ? x4.x : -x4.x) + ((p & 2) ? x4.y : -x4.y) + ((p & 4) ? x4.z : -x4.z) +
+                    ((p & 8) ? x4.w : -x4.w);
+    float* dst = lut + BUF * 2048 + h * 1024 + p * 64 + u;
+    dst[0] = v;
+    dst[32] = v;
+  }
+}
+
 // Request cursor: the unit (tile, sc) to request next, the uniform base of its sign slots, and the per-thread byte
 // offsets of the thread's rows in the sign and row-scale sections for that tile. Rows past the packed rows (only in
 // the last tile) read the last packed row: their sums are never stored.
@@ -328,6 +347,38 @@ __device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT>& rg,
   }
 }
 
+// mu = 4: chunk h of the unit is in stored slot h; nibble q of its 16 bytes (word q/8, bits 4(q%8)..) is sub-vector
+// (q + i) mod 32 of row i. bm[m] = ((8m + t) mod 32) * 4 is the lane's byte column for word m, and nibble j of the word
+// adds 4j (an immediate offset). Eight lookups per word, summed as a tree.
+template <int NT, int RPT, int BUF>
+__device__ __forceinline__ void lookup_b1_mu4(const float* lut, const Ring<RPT>& rg, const uint32_t (&bm)[4],
+                                              float (&acc)[RPT][1]) {
+  const uint32_t sh = (threadIdx.x & 1u) * 16u;
+  const char* base = reinterpret_cast<const char*>(lut) + BUF * 8192;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    float sum[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float part[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const uint32_t w = rg.w[j][4 * h + m];
+        float v[8];
+#pragma unroll
+        for (int n = 0; n < 8; ++n) {
+          const uint32_t addr = (__builtin_amdgcn_ubfe(w, 4 * n, 4) << 8) | bm[m];
+          v[n] = *reinterpret_cast<const float*>(base + h * 4096 + 4 * n + addr);
+        }
+        part[m] = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+      }
+      sum[h] = (part[0] + part[1]) + (part[2] + part[3]);
+    }
+    acc[j][0] = __builtin_fmaf(sum[0], h2f(uint16_t(rg.ra[j] >> sh)), acc[j][0]);
+    acc[j][0] = __builtin_fmaf(sum[1], h2f(uint16_t(rg.rb[j] >> sh)), acc[j][0]);
+  }
+}
+
 // Byte offsets in the row-scale section of the planes of chunks 2*sc(k) and 2*sc(k)+1 of the workgroup's unit k
 // (clamped to its last unit), from the table the prologue staged in LDS (one broadcast read; no scalar load is waited
 // for inside the pipeline).
@@ -356,7 +407,7 @@ struct B1State {
 // K % (D+1), buffer K % 2). The prologue requests units 0..D-1, so D+1 units are in flight at every wait. The steps
 // are unrolled at compile time (a workgroup has at most XV units) so that the wait before each lookup covers
 // exactly the loads of unit K.
-template <int NT, int RPT, int D, int K>
+template <int MU, int NT, int RPT, int D, int K>
 __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
                                          Ring<RPT> (&ring)[D + 1], float* lut, float* xs, const uint32_t (&c1)[4],
                                          const uint32_t (&c2)[4], bool hb, const int64_t* s_roff,
@@ -371,9 +422,17 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
     roff_of(s_roff, KI, st.n, oa, ob);
     issue_rscale<NT, RPT>(a, cur, oa, ob, ring[(K + D) % (D + 1)]);
     cursor_advance<NT, RPT>(a, cur, K + D + 1 < st.n);
-    if (K + 1 < st.n) build_b1<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
+    if (K + 1 < st.n) {
+      if constexpr (MU == 8)
+        build_b1<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
+      else
+        build_b1_mu4<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
+    }
     if constexpr (K == 0) stage_write_salient<NT>(a, sg, xs, sc0, st.n, 2, XV);   // built from step 1 on
-    lookup_b1<NT, RPT, BUF>(lut, ring[K % (D + 1)], c1, c2, hb, st.acc);
+    if constexpr (MU == 8)
+      lookup_b1<NT, RPT, BUF>(lut, ring[K % (D + 1)], c1, c2, hb, st.acc);
+    else
+      lookup_b1_mu4<NT, RPT, BUF>(lut, ring[K % (D + 1)], c1, st.acc);
     if (st.sc == a.steps - 1 || K + 1 == st.n) {
       const bool shared = st.tile == st.first_tile ? st.first_shared : (st.tile == st.last_tile ? st.last_shared : false);
       if (shared) {
@@ -390,13 +449,14 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
       st.sc = 0;
       ++st.tile;
     }
-    steps_b1<NT, RPT, D, K + 1>(a, st, cur, ring, lut, xs, c1, c2, hb, s_roff, sg, sc0);
+    steps_b1<MU, NT, RPT, D, K + 1>(a, st, cur, ring, lut, xs, c1, c2, hb, s_roff, sg, sc0);
   }
 }
 
-template <int NT, int RPT, int D, bool EARLY>
-__global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) float lut[256 * 64];       // 64 KB, two buffers interleaved per pattern
+template <int MU, int NT, int RPT, int D, bool EARLY>
+__global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
+  // mu = 8: 64 KB, two buffers interleaved per pattern; mu = 4: two buffers of 8 KB
+  __shared__ __attribute__((aligned(16))) float lut[MU == 8 ? 256 * 64 : 2 * 2048];
   constexpr int XV = B1<NT, 1>::XV;
   __shared__ __attribute__((aligned(16))) float xs[XV * 256];  // staged folded activations
   __shared__ __attribute__((aligned(16))) int64_t s_roff[2 * XV];   // row-scale plane byte offsets, staged units
@@ -480,12 +540,18 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
 
   // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32. Byte bb of c1[m] is
   // (hb << 6) | (s << 2) with s = (t + 4m + bb) mod 16 (the four bytes at once: no byte exceeds 18 before the mask).
+  // (mu = 4: c1[m] is the lane's byte column of word m, ((8m + t) mod 32) * 4; c2 and hb are not used.)
   uint32_t c1[4], c2[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
-    const uint32_t sb = ((((uint32_t(t) + 4u * m) & 15u) * 0x01010101u + 0x03020100u) & 0x0F0F0F0Fu) << 2;
-    c1[m] = sb | (hb ? 0x40404040u : 0u);
-    c2[m] = sb | (hb ? 0u : 0x40404040u);
+    if constexpr (MU == 8) {
+      const uint32_t sb = ((((uint32_t(t) + 4u * m) & 15u) * 0x01010101u + 0x03020100u) & 0x0F0F0F0Fu) << 2;
+      c1[m] = sb | (hb ? 0x40404040u : 0u);
+      c2[m] = sb | (hb ? 0u : 0x40404040u);
+    } else {
+      c1[m] = ((uint32_t(t) + 8u * m) & 31u) * 4u;
+      c2[m] = 0u;
+    }
   }
 
   stage_write_salient<NT>(a, sg, xs, sc0, st.n, 0, 2);
@@ -498,9 +564,12 @@ __global__ void __launch_bounds__(NT) k_gemv_mu8_b1(GemmArgs a) {
     issue_rscale<NT, RPT>(a, cur0, oa, ob, ring[k]);
     cursor_advance<NT, RPT>(a, cur0, k + 1 < st.n);
   }
-  build_b1<NT, 0>(lut, xs);
+  if constexpr (MU == 8)
+    build_b1<NT, 0>(lut, xs);
+  else
+    build_b1_mu4<NT, 0>(lut, xs);
   __syncthreads();
-  steps_b1<NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_roff, sg, sc0);
+  steps_b1<MU, NT, RPT, D, 0>(a, st, cur, ring, lut, xs, c1, c2, hb, s_roff, sg, sc0);
   const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
   publish_pending<NT, RPT, 1>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
@@ -793,22 +862,25 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
 // Launch
 // =====================================================================================================================
 
-template <int NT, int RPT, bool EARLY>
+template <int MU, int NT, int RPT, bool EARLY>
 static void launch_b1_d(const GemmArgs& a, int depth, hipStream_t stream) {
   const dim3 grid(unsigned(a.blocks));
-  switch (depth) {
-    case 2: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 2, EARLY>), grid, dim3(NT), 0, stream, a); break;
-    case 3: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 3, EARLY>), grid, dim3(NT), 0, stream, a); break;
-    default: hipLaunchKernelGGL((k_gemv_mu8_b1<NT, RPT, 1, EARLY>), grid, dim3(NT), 0, stream, a); break;
+  if constexpr (MU == 8) {
+    switch (depth) {
+      case 2: hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 2, EARLY>), grid, dim3(NT), 0, stream, a); return;
+      case 3: hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 3, EARLY>), grid, dim3(NT), 0, stream, a); return;
+      default: break;
+    }
   }
+  hipLaunchKernelGGL((k_gemv_b1<MU, NT, RPT, 1, EARLY>), grid, dim3(NT), 0, stream, a);   // mu = 4: depth 1 only
 }
 
-template <int NT, int RPT>
+template <int MU, int NT, int RPT>
 static void launch_b1(const GemmArgs& a, int depth, bool early, hipStream_t stream) {
   if (early)
-    launch_b1_d<NT, RPT, true>(a, depth, stream);
+    launch_b1_d<MU, NT, RPT, true>(a, depth, stream);
   else
-    launch_b1_d<NT, RPT, false>(a, depth, stream);
+    launch_b1_d<MU, NT, RPT, false>(a, depth, stream);
 }
 
 template <int MU, int BG, int NG>
@@ -905,9 +977,12 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   bool ok = true;
   if (p.kernel == 0) {
     switch (p.nt) {   // one row per thread (the launch plan's only choice for this kernel)
-      case 256: launch_b1<256, 1>(a, p.depth, p.early, stream); break;
-      case 512: launch_b1<512, 1>(a, p.depth, p.early, stream); break;
-      case 1024: launch_b1<1024, 1>(a, p.depth, p.early, stream); break;
+      case 256: L.shape.mu == 8 ? launch_b1<8, 256, 1>(a, p.depth, p.early, stream)
+                                : launch_b1<4, 256, 1>(a, p.depth, p.early, stream); break;
+      case 512: L.shape.mu == 8 ? launch_b1<8, 512, 1>(a, p.depth, p.early, stream)
+                                : launch_b1<4, 512, 1>(a, p.depth, p.early, stream); break;
+      case 1024: L.shape.mu == 8 ? launch_b1<8, 1024, 1>(a, p.depth, p.early, stream)
+                                 : launch_b1<4, 1024, 1>(a, p.depth, p.early, stream); break;
       default: ok = false;
     }
   } else if (p.kernel == 2) {

@@ -128,7 +128,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int rpt_env = env_int("FLUXBIN_RPT", 0);
   int per_cu = env_int("FLUXBIN_BLOCKS_PER_CU", 0);
   p->nt = 256;
-  if (L.shape.mu == 8 && B == 1 && !force_generic) {
+  if (B == 1 && !force_generic) {   // batch-1 kernel (mu = 8 or 4)
     p->kernel = 0;
     const int nt_env = env_int("FLUXBIN_NT", 0);
     // units of sign data requested ahead of the one being looked up: one (two units, 64 KB per CU, in flight) already
@@ -447,7 +447,6 @@ fluxbin_status fluxbin_stream_probe(const fluxbin_layer* layer, uint32_t* d_sink
   g_msg[0] = 0;
   fluxbin_status st = check_layer(layer);
   if (st != FLUXBIN_OK) return st;
-  if (layer->shape.mu != 8) return fail(FLUXBIN_ERR_UNSUPPORTED, "the stream probe follows the mu = 8 batch-1 kernel");
   if (!d_sink) return fail(FLUXBIN_ERR_INVALID_ARG, "d_sink is NULL");
   if (sink_bytes < 1024) return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "sink of %zu bytes < 1024", sink_bytes);
   Plan p;

@@ -82,7 +82,7 @@ fluxbin_status hip_fail(int hip_error, const char* what);
 
 // ---- launch plan of the GEMV/GEMM kernels ----
 struct Plan {
-  int kernel;       // 0 = mu8 batch-1 super-chunk kernel, 1 = generic (any mu, any batch), 2 = mu8 batch 2..16
+  int kernel;       // 0 = batch-1 super-chunk kernel (mu 8 or 4), 1 = generic (any mu, any batch), 2 = mu8 batch 2..16
   int nt;           // threads per block
   int rpt;          // rows per thread
   int rows;         // rows per tile (nt * rpt)

@@ -229,6 +229,23 @@ def test_edge_shapes(spec, B):
     _parity(spec, B)
 
 
+@pytest.mark.parametrize("spec", [
+    LayerSpec("mu4_b1_a", M=3000, N=2048, Kb=2, Ks=1, mu=4, S=70, g_r=128, g_s=70, seed=51),
+    LayerSpec("mu4_b1_b", M=1500, N=777, Kb=3, Ks=2, mu=4, S=300, g_r=256, g_s=128, seed=52),
+    LayerSpec("mu4_b1_c", M=64, N=300, Kb=1, Ks=0, mu=4, S=0, g_r=300, g_s=1, seed=53),
+], ids=lambda s: s.name)
+def test_mu4_batch1_kernel_matches_oracle_and_generic(spec):
+    """mu = 4 at batch 1 runs the batch-1 kernel (16-entry tables); it matches the oracle on every row and the
+    generic kernel's result within the tolerance."""
+    L, packed, x, y = _parity(spec, 1, out_fp32=True)
+    os.environ["FLUXBIN_GENERIC"] = "1"
+    try:
+        y_gen = run_gemm(packed, x, out_fp32=True)
+    finally:
+        del os.environ["FLUXBIN_GENERIC"]
+    _check(y, y_gen, "batch-1 kernel vs generic kernel")
+
+
 def test_fp32_output_and_generic_kernel_at_batch1():
     spec = LayerSpec("gen", M=2000, N=1024, Kb=2, Ks=1, mu=8, S=40, g_r=128, g_s=40, seed=21)
     L, packed, x, y = _parity(spec, 1, out_fp32=True)
@@ -306,7 +323,8 @@ def test_stream_probe_runs_and_leaves_results_alone():
     log("case stream probe")
     sink = torch.zeros(256, dtype=torch.int32, device="cuda")
     for spec in (LayerSpec("p1", M=700, N=512, Kb=2, Ks=1, mu=8, S=9, g_r=128, g_s=9, seed=41),
-                 LayerSpec("p2", M=4096, N=4096, Kb=2, Ks=1, mu=8, S=41, g_r=128, g_s=41, seed=42)):
+                 LayerSpec("p2", M=4096, N=4096, Kb=2, Ks=1, mu=8, S=41, g_r=128, g_s=41, seed=42),
+                 LayerSpec("p3", M=3000, N=1024, Kb=2, Ks=1, mu=4, S=20, g_r=128, g_s=20, seed=43)):
         L = make_layer(spec)
         packed = pack_layer(L)
         xb = make_activations(L, 1)
@@ -314,9 +332,8 @@ def test_stream_probe_runs_and_leaves_results_alone():
         fb.fluxbin_stream_probe(packed, sink)
         torch.cuda.synchronize()
         assert np.array_equal(run_gemm(packed, xb, out_fp32=True), y0)
-    L = make_layer(LayerSpec("p3", M=300, N=256, Kb=2, Ks=0, mu=4, S=0, g_r=128, g_s=1, seed=43))
-    with pytest.raises(fb.FluxbinError):
-        fb.fluxbin_stream_probe(pack_layer(L), sink)
+    with pytest.raises(fb.FluxbinError):   # sink below 1024 bytes
+        fb.fluxbin_stream_probe(packed, sink[:100])
 
 
 def test_graph_replays_match_eager():
