@@ -296,16 +296,30 @@ def cpu_baseline(bench, budget_s: float):
 
 
 def small_batch_us(specs, batches, launches=40):
-    """Per-call microseconds of the small-batch LUT-GEMM (batch-interleaved tables, each sign word read once for all
-    batch rows) on the same layers, graph-timed like the batch-1 figure."""
+    """Per-call microseconds of the small-batch product on the same layers, graph-timed like the batch-1 figure, for
+    the default kernel (matrix cores: the sign decode per bit is shared by all batch rows) and, on the same packed
+    copies, the LUT batch kernel (batch-interleaved tables, each sign word read once for all batch rows)."""
     import torch
     out = {}
     for B in batches:
         b = Bench(specs, B, COPIES_BYTES_PER_LAYER * len(specs))
-        for it, us in zip(b.items, b.per_launch_us(launches, 3)):
+        us_k = {}
+        for kern, flag in (("mfma", "1"), ("lut", "0")):
+            os.environ["FLUXBIN_MFMA"] = flag
+            try:
+                for it in b.items:
+                    it["ws"] = b.fb.make_workspace(it["packs"][0], B)
+                us_k[kern] = b.per_launch_us(launches, 3)
+            finally:
+                os.environ.pop("FLUXBIN_MFMA", None)
+        for i, it in enumerate(b.items):
             s = it["spec"]
+            um, ul = us_k["mfma"][i], us_k["lut"][i]
+            us = um if B > 4 else ul   # the launch plan's choice for mu = 8
             out[f"{s.name}_B{B}"] = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
-                                     "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2)}
+                                     "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
+                                     "matrix_core_kernel_us": round(um, 3), "lut_batch_kernel_us": round(ul, 3),
+                                     "default_kernel": "matrix cores" if B > 4 else "LUT batch"}
         del b
         torch.cuda.empty_cache()
     return out
@@ -490,7 +504,7 @@ def main():
         us, b2 = small_layer_us(spec2)
         out["config"]["attn_4096x4096_us_per_gemv"] = round(us, 3)
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
-        out["config"]["small_batch"] = small_batch_us(specs, (4, 16))
+        out["config"]["small_batch"] = small_batch_us(specs, (2, 4, 8, 16))
     if not args.no_decoder:
         out["config"]["decoder_layer_70b"] = decoder_layer_us(args.g_r)
     if not args.no_variants:

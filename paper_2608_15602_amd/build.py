@@ -19,7 +19,8 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfluxbin.so")
 
-SOURCES = ["fluxbin_host.cpp", "fluxbin_pack.hip", "fluxbin_gemv.hip", "fluxbin_gemm_batch.hip"]
+SOURCES = ["fluxbin_host.cpp", "fluxbin_pack.hip", "fluxbin_gemv.hip", "fluxbin_gemm_batch.hip",
+           "fluxbin_gemm_mfma.hip"]
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are kept out of the generated code (plain float code only).

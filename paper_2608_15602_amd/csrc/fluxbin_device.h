@@ -115,7 +115,9 @@ __device__ __forceinline__ bool tile_end(const GemmArgs& a, int64_t tile, int64_
 // unless its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
 template <int NT, int RPT, int BP>
 __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
-  constexpr int CH = 16;   // loads in flight per thread; larger unrolls lengthen this rarely run (cold) code
+  // loads in flight per thread: 16 contributors, at most 64 values (larger unrolls lengthen this rarely run, cold code;
+  // the contributors are added in the same order whatever CH is)
+  constexpr int CH = BP <= 4 ? 16 : 64 / BP;
   const int t = threadIdx.x;
   const int64_t R = int64_t(NT) * RPT;
   const int b_first = owner_of(a, int(tile) * a.steps);
@@ -198,5 +200,9 @@ __device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
 // Small-batch mu = 8 kernel (fluxbin_gemm_batch.hip): launches k_gemm_mu8_batch with n_groups groups of four batch
 // rows and depth units of sign data requested ahead; false if no instance exists.
 bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, hipStream_t stream);
+
+// Matrix-core small-batch kernel (fluxbin_gemm_mfma.hip): 256-row tiles, partial sums padded to bpad (4, 8 or 16)
+// batch rows, data requested depth (2 or 3) units ahead; false if no instance exists.
+bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, hipStream_t stream);
 
 }  // namespace fluxbin

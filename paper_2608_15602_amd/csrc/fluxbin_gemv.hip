@@ -987,6 +987,8 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
     }
   } else if (p.kernel == 2) {
     ok = launch_gemm_batch(a, p.n_groups, p.depth, stream);
+  } else if (p.kernel == 3) {
+    ok = launch_gemm_mfma(a, p.bpad, int(L.shape.mu), p.depth, stream);
   } else if (L.shape.mu == 8) {
     ok = launch_gen_mu<8>(a, p, stream);
   } else {

@@ -120,6 +120,17 @@ static int env_int(const char* name, int dflt) {
   return std::atoi(v);
 }
 
+// Small-batch kernel choice. The matrix-core kernel's cost per sign bit (decode) is the same for every B <= 16; the mu = 8
+// LUT batch kernel's table work grows with B. Measured on the 70B MLP layers (us per call, matrix cores / LUT):
+// B = 2: 54 / 44-49, B = 4: 55 / 45-50, B = 8: 58-68 / 83-91, B = 16: 73-96 / 162-172. So mu = 8 uses the LUT kernel up
+// to B = 4 and the matrix cores above; mu = 4 (whose LUT path for B >= 2 is the generic kernel) always the matrix cores.
+// FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
+static bool use_mfma(const fluxbin_layer& L, int B) {
+  const int forced = env_int("FLUXBIN_MFMA", -1);
+  if (forced == 0 || forced == 1) return forced == 1;
+  return L.shape.mu == 4 || B > 4;
+}
+
 fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int cus = device_cu_count();
   if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
@@ -153,6 +164,17 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (per_cu < 1 || per_cu > 8) per_cu = 1024 / p->nt;
     p->bg = 1;
     p->n_groups = 1;
+  } else if (B >= 2 && !force_generic && use_mfma(L, B)) {
+    // small batch on the matrix cores: the sign decode per bit is shared by all batch rows (B <= 16 fit one MFMA tile)
+    p->kernel = 3;
+    p->nt = 256;
+    p->rpt = 1;   // four 16-row blocks per wavefront: 256-row tiles
+    // units of data requested ahead: two (measured 2-8 us faster than three on the 70B MLP layers at B = 2..16)
+    const int depth_env = env_int("FLUXBIN_MFMA_DEPTH", 2);
+    p->depth = depth_env == 3 ? 3 : 2;
+    p->bg = B <= 4 ? 4 : (B <= 8 ? 8 : 16);
+    p->n_groups = 1;
+    if (per_cu < 1 || per_cu > 8) per_cu = 3;   // three 256-thread workgroups per CU (the kernel's occupancy)
   } else if (L.shape.mu == 8 && B >= 2 && !force_generic) {
     // small batch: 1024-row tiles, one super-chunk per unit (the batch-1 sign stream), batch in groups of four rows
     p->kernel = 2;
@@ -179,7 +201,9 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   int rpt_max = (p->kernel == 0 || (L.shape.mu == 8 && p->bpad <= 2)) ? 4 : 2;
   if (p->kernel == 0) rpt_max = p->nt == 256 ? 4 : 2;
   int chosen = 1;
-  if (p->kernel != 1) {
+  if (p->kernel == 3) {
+    chosen = p->rpt;
+  } else if (p->kernel != 1) {
     chosen = 1;   // the batch-1 and small-batch kernels: one row per thread
   } else if (rpt_env == 1 || rpt_env == 2 || rpt_env == 4) {
     chosen = rpt_env > rpt_max ? rpt_max : rpt_env;
@@ -210,6 +234,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   if (p->kernel == 0 && ceil_div(p->units, p->blocks) > b1_max_units(p->nt))
     p->blocks = ceil_div(p->units, int64_t(b1_max_units(p->nt)));
   if (p->kernel == 2 && ceil_div(p->units, p->blocks) > kBatMaxUnits) p->blocks = ceil_div(p->units, kBatMaxUnits);
+  if (p->kernel == 3 && ceil_div(p->units, p->blocks) > kMfMaxUnits) p->blocks = ceil_div(p->units, kMfMaxUnits);
   p->ws_counters_off = 0;
   // the small-batch kernel runs one row of workgroups per group of four batch rows, each with its own counters
   const uint64_t counter_sets = p->kernel == 2 ? uint64_t(p->n_groups) : 1u;

@@ -15,6 +15,7 @@ constexpr int kMaxBatch = 16;
 // 12 for the smaller ones (two or more share a CU's LDS).
 constexpr int b1_max_units(int nt) { return nt == 1024 ? 16 : 12; }
 constexpr int kBatMaxUnits = 12;        // units per workgroup of the small-batch mu = 8 kernel (its LDS index table)
+constexpr int kMfMaxUnits = 16;         // units per workgroup of the matrix-core small-batch kernel (unrolled steps)
 // Tile counters of the split-tile reduction sit kCounterStride 32-bit words (256 bytes) apart: every workgroup
 // publishes at the end of a launch, and device-scope atomics on one memory line are serialized (densely packed
 // counters cost the batch-1 GEMV on 8192 x 28672 layers 0.3-0.5 us).
@@ -82,7 +83,8 @@ fluxbin_status hip_fail(int hip_error, const char* what);
 
 // ---- launch plan of the GEMV/GEMM kernels ----
 struct Plan {
-  int kernel;       // 0 = batch-1 super-chunk kernel (mu 8 or 4), 1 = generic (any mu, any batch), 2 = mu8 batch 2..16
+  int kernel;       // 0 = batch-1 super-chunk kernel (mu 8 or 4), 1 = generic (any mu, any batch), 2 = mu8 batch 2..16,
+                    // 3 = matrix-core small batch (mu 8 or 4, batch 2..16)
   int nt;           // threads per block
   int rpt;          // rows per thread
   int rows;         // rows per tile (nt * rpt)

@@ -257,18 +257,48 @@ def test_fp32_output_and_generic_kernel_at_batch1():
     _check(y2, oracle.gemv_dense(L, x), "generic kernel at batch 1")
 
 
-@pytest.mark.parametrize("generic", [False, True], ids=["mu8_batch_kernel", "generic_kernel"])
-@pytest.mark.parametrize("B", [2, 5, 16])
-def test_batch_rows_equal_batch1(B, generic):
-    """Each batch row of the small-batch path matches the oracle (mu = 8 batch kernel: groups of four rows on
-    workgroup rows; and the generic kernel)."""
-    spec = LayerSpec("bat", M=1536, N=2048, Kb=2, Ks=1, mu=8, S=61, g_r=128, g_s=61, seed=22)
-    if generic:
-        os.environ["FLUXBIN_GENERIC"] = "1"
+# Small-batch kernels: the matrix-core kernel (FLUXBIN_MFMA=1; the default for mu = 4 and for B > 4), the mu = 8 LUT
+# batch kernel (FLUXBIN_MFMA=0; the default for mu = 8 up to B = 4) and the generic LUT kernel (FLUXBIN_GENERIC=1; with
+# FLUXBIN_MFMA=0 also the mu = 4 small-batch path).
+SMALL_BATCH_KERNELS = {"mfma": {"FLUXBIN_MFMA": "1"}, "lut_batch": {"FLUXBIN_MFMA": "0"},
+                       "generic": {"FLUXBIN_GENERIC": "1"}}
+
+
+def _with_env(env, fn):
+    for k, v in env.items():
+        os.environ[k] = v
     try:
-        _parity(spec, B, out_fp32=True)
+        return fn()
     finally:
-        os.environ.pop("FLUXBIN_GENERIC", None)
+        for k in env:
+            os.environ.pop(k, None)
+
+
+@pytest.mark.parametrize("kernel", list(SMALL_BATCH_KERNELS))
+@pytest.mark.parametrize("mu", [8, 4])
+@pytest.mark.parametrize("B", [2, 5, 16])
+def test_batch_rows_equal_batch1(B, mu, kernel):
+    """Each batch row of every small-batch kernel matches the oracle (rows of several split tiles, a ragged last
+    tile, B not a multiple of four)."""
+    spec = LayerSpec("bat", M=1536, N=2048, Kb=2, Ks=1, mu=mu, S=61, g_r=128, g_s=61, seed=22)
+    _with_env(SMALL_BATCH_KERNELS[kernel], lambda: _parity(spec, B, out_fp32=True))
+
+
+@pytest.mark.parametrize("B", [4, 16])
+def test_mfma_small_batch_mlp70b_full_size(B):
+    """The matrix-core kernel on both 70B MLP layers at full size, in the launch configuration the benchmark times:
+    sampled rows against the oracle, bitwise repeatable, and close to the LUT batch kernel's result."""
+    import torch
+    for spec in config_layers("c4_mlp70b", "128"):
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        rows = sample_rows(spec.M, 256, seed=B)
+        _, _, x, y = _with_env(SMALL_BATCH_KERNELS["mfma"], lambda: _parity(spec, B, rows=rows, packed=packed, L=L))
+        assert np.array_equal(_with_env(SMALL_BATCH_KERNELS["mfma"], lambda: run_gemm(packed, x)), y), "repeat differs"
+        y_lut = _with_env(SMALL_BATCH_KERNELS["lut_batch"], lambda: run_gemm(packed, x))
+        _check(y, y_lut, "matrix-core vs LUT batch kernel")
+        del packed
+        torch.cuda.empty_cache()
 
 
 def test_strided_batch():
