@@ -431,6 +431,8 @@ def main():
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before anything else, run a plain device-to-device copy of this many MiB three times "
                          "(the reference dispatch for HBM byte counters)")
+    ap.add_argument("--eager-batch", type=int, default=1,
+                    help="batch rows of the counter-collection launches (2..16: the small-batch product)")
     ap.add_argument("--eager-launches", type=int, default=0,
                     help="counter-collection mode: launch each layer this many times without graphs, then exit")
     args = ap.parse_args()
@@ -456,11 +458,14 @@ def main():
     print("# packed " + ", ".join(f"{it['spec'].name} x{len(it['packs'])}" for it in bench.items), file=sys.stderr,
           flush=True)
     if args.eager_launches > 0:
+        if args.eager_batch != 1:
+            bench.set_batch(args.eager_batch)
         for it in bench.items:
             for s in range(args.eager_launches):
                 bench.launch(it, s)
         torch.cuda.synchronize()
         print(json.dumps({"mode": "eager launches for counter collection", "launches_per_layer": args.eager_launches,
+                          "batch": args.eager_batch,
                           "layers": [it["spec"].name for it in bench.items],
                           "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}}), flush=True)
         return
