@@ -115,9 +115,9 @@ __device__ __forceinline__ bool tile_end(const GemmArgs& a, int64_t tile, int64_
 // unless its range starts exactly at the tile. Loads are issued CH at a time so that they are in flight together.
 template <int NT, int RPT, int BP>
 __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
-  // loads in flight per thread: 16 contributors, at most 128 values (larger unrolls lengthen this rarely run, cold code,
+  // loads in flight per thread: 16 contributors, at most 64 values (larger unrolls lengthen this rarely run, cold code,
   // and its registers count against the kernel's; the contributors are added in the same order whatever CH is)
-  constexpr int CH = BP <= 8 ? 16 : 128 / BP;
+  constexpr int CH = BP <= 4 ? 16 : 64 / BP;
   const int t = threadIdx.x;
   const int64_t R = int64_t(NT) * RPT;
   const int b_first = owner_of(a, int(tile) * a.steps);

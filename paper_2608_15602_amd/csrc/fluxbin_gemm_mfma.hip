@@ -52,6 +52,9 @@ constexpr int kMfXStride = 68;                      // dwords per (chunk, column
 constexpr int kMfXUnit = 2 * 4 * 4 * kMfXStride;    // dwords of staged activation pairs per unit
 constexpr int kMfAUnit = 2 * 4 * 16;                // dwords of column-scale pairs per unit
 constexpr int kMfScr = 64 * 8;                      // dwords of a wavefront's sign scratch: 64 rows x 32 bytes
+constexpr int kMfTStride = 68;                      // dwords per batch row of a wavefront's tile-end transpose
+constexpr int kMfScrWave = 16 * kMfTStride;         // dwords of a wavefront's scratch (>= kMfScr + 64 row scales)
+static_assert(kMfScrWave >= kMfScr + 64, "scratch too small");
 
 // Requested data of one unit: the lane's row entries of both chunks (lane l: row 16 (l >> 4) + (l & 15) of the
 // wavefront's 64 rows), one word of row scales (lane l: rows 2 (l & 31) and 2 (l & 31) + 1 of chunk l >> 5), and the
@@ -186,27 +189,31 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
 
 // End of a tile's contribution: y for a tile only this workgroup covers, else its partial sums (slot 0 for the
 // workgroup's first tile, 1 for its last), in the layout reduce_tile reads: element (b, row in tile) at b * R + row.
-// Lane (b = r16, g) holds rows 16 rb + 4 g + v of the wavefront's 64.
+// Lane (b = r16, g) holds rows 16 rb + 4 g + v of the wavefront's 64; the wavefront first transposes them through its
+// LDS scratch (row block rb of batch row b at b * kMfTStride + 16 rb), so that every store instruction writes 64
+// consecutive rows of one batch row (whole memory lines: scattered 4-byte stores wrote each line several times).
 template <int BP>
-__device__ __forceinline__ void mf_tile_end(const GemmArgs& a, int tile, bool shared, int slot, int wave, int r16,
-                                            int g, const float (&acc)[4][4]) {
-  if (r16 >= BP) return;
+__device__ __forceinline__ void mf_tile_end(const GemmArgs& a, int tile, bool shared, int slot, int wave, int lane,
+                                            int r16, int g, const float (&acc)[4][4], uint32_t* scr) {
+  float* t = reinterpret_cast<float*>(scr);
+  if (r16 < BP) {
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+      *reinterpret_cast<mf_float4*>(t + r16 * kMfTStride + 16 * rb + 4 * g) =
+          mf_float4{acc[rb][0], acc[rb][1], acc[rb][2], acc[rb][3]};
+  }
   if (shared) {
-    float* mine = a.partials + ((int64_t(blockIdx.x) * 2 + slot) * BP) * kMfR + int64_t(r16) * kMfR;
+    float* mine = a.partials + ((int64_t(blockIdx.x) * 2 + slot) * BP) * kMfR + wave * 64 + lane;
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int b = 0; b < BP; ++b)
+      __hip_atomic_store(mine + b * kMfR, t[b * kMfTStride + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  } else {
+    const int64_t row = int64_t(tile) * kMfR + wave * 64 + lane;
+    if (row < a.M) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        __hip_atomic_store(mine + wave * 64 + 16 * rb + 4 * g + v, acc[rb][v], __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-  } else if (r16 < a.B) {
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t row = int64_t(tile) * kMfR + wave * 64 + 16 * rb + 4 * g + v;
-        if (row < a.M) store_y(a, r16, row, acc[rb][v]);
-      }
+      for (int b = 0; b < BP; ++b)
+        if (b < a.B) store_y(a, b, row, t[b * kMfTStride + lane]);
+    }
   }
 }
 
@@ -258,7 +265,7 @@ struct MfKernel {
       if (s.cur.sc == a.steps - 1 || K + 1 == s.n) {
         const int tile = s.cur.tile;
         const bool shared = tile == s.first_tile ? s.first_shared : (tile == s.last_tile && s.last_shared);
-        mf_tile_end<BP>(a, tile, shared, tile == s.first_tile ? 0 : 1, ln.wave, ln.r16, ln.g, s.acc);
+        mf_tile_end<BP>(a, tile, shared, tile == s.first_tile ? 0 : 1, ln.wave, ln.lane, ln.r16, ln.g, s.acc, scr);
         if (shared) ++s.n_pending;
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb)
@@ -277,7 +284,7 @@ __global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
   using K = MfKernel<BP, MU, D>;
   __shared__ __attribute__((aligned(16))) uint32_t sx[2 * kMfXUnit];
   __shared__ __attribute__((aligned(16))) uint32_t sa[2 * kMfAUnit];
-  __shared__ __attribute__((aligned(16))) uint32_t scr_all[4 * (kMfScr + 64)];
+  __shared__ __attribute__((aligned(16))) uint32_t scr_all[4 * kMfScrWave];
   __shared__ int s_planes[2 * kMfMaxUnits];
   __shared__ int s_flag;
 
@@ -296,7 +303,7 @@ __global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
       ln.aw[par] = uint32_t(((32 * ln.g - rot0 - (MU == 4 ? 64 * par : 0)) & 127) >> 5);
     ln.sh = uint32_t((32 * ln.g - rot0) & 31);
   }
-  uint32_t* scr = scr_all + ln.wave * (kMfScr + 64);
+  uint32_t* scr = scr_all + ln.wave * kMfScrWave;
 
   const int u0 = first_unit(a, blockIdx.x);
   const int u1 = first_unit(a, blockIdx.x + 1);
