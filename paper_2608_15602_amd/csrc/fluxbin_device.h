@@ -137,14 +137,31 @@ __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
 #pragma unroll
       for (int k = 0; k < CH; ++k) {
         const int c = c0 + k;
-        // slot of contributor c (wave-uniform); contributors past n_c are not read
-        const int slot = (b_first + c) * 2 + ((c == 0 && first_in_slot1) ? 1 : 0);
-        const char* src = pbase + int64_t(slot) * (BP * R * 4);
-#pragma unroll
-        for (int b = 0; b < BP; ++b)
-          v[k][b] = c < n_c ? __hip_atomic_load(reinterpret_cast<const float*>(src + uint32_t((b * R + r) * 4)),
+        if constexpr (BP == 1) {
+          // one batch row: contributors past n_c are not read (fewer loads in the launch's last microseconds)
+          const int slot = (b_first + c) * 2 + ((c == 0 && first_in_slot1) ? 1 : 0);
+          const char* src = pbase + int64_t(slot) * (R * 4);
+          v[k][0] = c < n_c ? __hip_atomic_load(reinterpret_cast<const float*>(src + uint32_t(r * 4)),
                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
                             : 0.f;
+        } else {
+          // several batch rows: past n_c the last contributor's slot is read again and its values are replaced by
+          // zeros, so that the loads are unconditional and issued together (conditional loads become branches)
+          const int cc = c < n_c ? c : n_c - 1;
+          const int slot = (b_first + cc) * 2 + ((cc == 0 && first_in_slot1) ? 1 : 0);
+          const char* src = pbase + int64_t(slot) * (BP * R * 4);
+#pragma unroll
+          for (int b = 0; b < BP; ++b)
+            v[k][b] = __hip_atomic_load(reinterpret_cast<const float*>(src + uint32_t((b * R + r) * 4)),
+                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+      if constexpr (BP > 1) {
+#pragma unroll
+        for (int k = 0; k < CH; ++k)
+#pragma unroll
+          for (int b = 0; b < BP; ++b)
+            if (c0 + k >= n_c) v[k][b] = 0.f;
       }
 #pragma unroll
       for (int k = 0; k < CH; ++k)
