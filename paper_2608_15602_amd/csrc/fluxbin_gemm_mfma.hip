@@ -64,7 +64,7 @@ struct MfUnitRegs {
   mf_u32x4 e[2];
   uint32_t r;
   uint32_t meta;        // xidx | colscale << 16 (thread t owns virtual column t of the unit)
-  uint32_t xv[BP];      // x bits of batch rows 0..BP-1, one register each (rows >= B are masked when staged)
+  uint32_t xv[BP];      // x bits of batch rows 0..BP-1, one register each (rows >= B read row B-1)
 };
 
 struct MfCursor {
@@ -119,8 +119,10 @@ __device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, i
                                            (int64_t(plane) * a.Mp + rrow) * 2);
 }
 
-// Writes a staged unit: the activation pairs (sign of the column scale folded in; 0 for padding columns and batch rows
-// >= B) and the column-scale pairs (magnitudes) in the order the MFMA operands read them.
+// Writes a staged unit: the activation pairs (sign of the column scale folded in; 0 for padding columns, so that x is
+// never multiplied there, not even by a zero) and the column-scale pairs (magnitudes) in the order the MFMA operands
+// read them. Batch rows b >= B hold row B-1's values: MFMA output column b depends on activation column b only, and
+// columns >= B are never stored.
 template <int BP>
 __device__ __forceinline__ void mf_stage_write(const GemmArgs& a, const MfUnitRegs<BP>& u, uint32_t* sx, uint32_t* sa,
                                                int t) {
@@ -129,13 +131,11 @@ __device__ __forceinline__ void mf_stage_write(const GemmArgs& a, const MfUnitRe
   const uint32_t xi = u.meta & 0xFFFFu;
   const uint16_t cs = uint16_t(u.meta >> 16);
   const uint16_t flip = cs & 0x8000u;
+  const uint16_t keep = xi != 0xFFFFu ? uint16_t(0xFFFFu) : uint16_t(0);
   uint16_t* sx16 = reinterpret_cast<uint16_t*>(sx);
   const int base = ((h * 4 + g) * 4 + q) * kMfXStride + k;
 #pragma unroll
-  for (int b = 0; b < BP; ++b) {
-    const uint16_t v = (b < a.B && xi != 0xFFFFu) ? uint16_t(u.xv[b] ^ flip) : uint16_t(0);
-    sx16[(base + 4 * b) * 2 + hf] = v;
-  }
+  for (int b = 0; b < BP; ++b) sx16[(base + 4 * b) * 2 + hf] = uint16_t((uint16_t(u.xv[b]) ^ flip) & keep);
   reinterpret_cast<uint16_t*>(sa)[((h * 4 + g) * 16 + j) * 2 + hf] = uint16_t(cs & 0x7FFFu);
 }
 
