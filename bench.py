@@ -326,27 +326,32 @@ def small_batch_us(specs, batches, launches=40):
 
 
 def decoder_layer_us(g_r: str, batches=(1, 4, 16), steps: int = 40):
-    """A synthetic 70B decoder layer's seven linears (q, k, v, o, gate, up, down) in one HIP graph per step, for both
-    hybrid variants (2 bases + 1% salient, 3 bases + 5% salient), at least three rotated copies of every layer;
-    end-to-end microseconds per decoder layer (all seven calls) and the whole layer's bytes per microsecond."""
+    """A synthetic 70B decoder layer's linears in one HIP graph per step, for both hybrid variants (2 bases + 1%
+    salient, 3 bases + 5% salient), at least three rotated copies of every layer; end-to-end microseconds per decoder
+    layer and the whole layer's bytes per microsecond. Two launch sets: the seven linears (q, k, v, o, gate, up, down)
+    and four fused launches (q|k|v stacked as one 10240-row layer, gate|up as one 57344-row layer, o, down)."""
     import torch
-    from synth import config_layers
+    from synth import config_layers, fused_decoder_layers
     out = {}
     allspecs = config_layers("c5_layer70b", g_r)
+    fused = fused_decoder_layers(g_r)
     for variant in ("2b1pct", "3b5pct"):
-        specs = [sp for sp in allspecs if sp.name.startswith(variant)]
-        b = Bench(specs, 1, 1.6e9, min_copies=3)
-        for B in batches:
-            if B != b.B:
-                b.set_batch(B)
-            b.run(2, 2)   # warm up graph capture for this batch
-            total_ms, _ = b.run(steps, 2)
-            us = total_ms * 1000.0 / steps
-            step_bytes = sum(it["bytes"] for it in b.items)
-            out[f"{variant}_B{B}"] = {"us_per_layer": round(us, 2), "GBps": round(step_bytes / (us * 1e-6) / 1e9, 1),
-                                      "calls": len(b.items), "copies_min": min(len(it["packs"]) for it in b.items)}
-        del b
-        torch.cuda.empty_cache()
+        for kind, pool in (("", allspecs), ("_fused", fused)):
+            specs = [sp for sp in pool if sp.name.startswith(variant)]
+            b = Bench(specs, 1, 1.6e9, min_copies=3)
+            for B in batches:
+                if B != b.B:
+                    b.set_batch(B)
+                b.run(2, 2)   # warm up graph capture for this batch
+                total_ms, _ = b.run(steps, 2)
+                us = total_ms * 1000.0 / steps
+                step_bytes = sum(it["bytes"] for it in b.items)
+                out[f"{variant}{kind}_B{B}"] = {"us_per_layer": round(us, 2),
+                                                "GBps": round(step_bytes / (us * 1e-6) / 1e9, 1),
+                                                "calls": len(b.items),
+                                                "copies_min": min(len(it["packs"]) for it in b.items)}
+            del b
+            torch.cuda.empty_cache()
     return out
 
 

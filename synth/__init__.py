@@ -12,5 +12,6 @@ from .layers import (  # noqa: F401
     make_activations,
     salient_count,
     kernel_variant_layers,
+    fused_decoder_layers,
     vcm_off_equivalent,
 )

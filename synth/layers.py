@@ -178,6 +178,19 @@ def kernel_variant_layers(g_r: str = "128") -> List[LayerSpec]:
     return [s.with_(g_r=s.N) if g_r == "N" else s for s in out]
 
 
+def fused_decoder_layers(g_r: str = "128") -> List[LayerSpec]:
+    """The 70B decoder layer's linears with the launches that share an input fused by stacking output rows: q, k and v
+    as one 10240 x 8192 layer, gate and up as one 57344 x 8192 layer, then o and down. A fused layer has one salient
+    column set (the stacked rows read the same input columns), drawn like any other layer. Both hybrid variants."""
+    out = []
+    lid = 100
+    for variant, Kb, frac in (("2b1pct", 2, 0.01), ("3b5pct", 3, 0.05)):
+        for nm, M, N in (("qkv", 10240, 8192), ("o", 8192, 8192), ("gate_up", 57344, 8192), ("down", 8192, 28672)):
+            out.append(_attn_mlp(f"{variant}_{nm}", M, N, Kb, frac, seed=4, layer_id=lid, outlier_frac=0.001))
+            lid += 1
+    return [s.with_(g_r=s.N) if g_r == "N" else s for s in out]
+
+
 def _build_configs() -> Dict[str, dict]:
     c = {}
     c["c1_tiny"] = dict(

@@ -177,6 +177,22 @@ def test_config5_layer70b():
         torch.cuda.empty_cache()
 
 
+def test_fused_decoder_layers_full_size():
+    """The fused launches of the decoder layer (q|k|v as 10240 x 8192, gate|up as 57344 x 8192) at batch 1, 4 and 16,
+    sampled rows at full size, in the launch configuration the benchmark times."""
+    import torch
+    from synth import fused_decoder_layers
+    for spec in fused_decoder_layers("128"):
+        if not spec.name.endswith(("qkv", "gate_up")):
+            continue
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        for B in (1, 4, 16):
+            _parity(spec, B, rows=sample_rows(spec.M, 128, seed=B), packed=packed, L=L)
+        del packed
+        torch.cuda.empty_cache()
+
+
 def test_kernel_variants_full_size():
     """The 28672 x 8192 layer in the kernel variants the benchmark times (mu 4, pure global bases, 2b + 1%), sampled
     rows at full size in the launch configuration the benchmark uses."""
