@@ -25,3 +25,4 @@ from .fluxbin_oracle import (  # noqa: F401
     vcm_gather,
 )
 from . import format_oracle  # noqa: F401
+from . import rc_oracle  # noqa: F401

@@ -232,3 +232,18 @@ def _build_configs() -> Dict[str, dict]:
 
 
 CONFIGS = _build_configs()
+
+
+def make_weight_matrix(M: int, N: int, seed: int, outlier_frac: float = 0.01, outlier_scale: float = 10.0):
+    """A dense fp32 weight matrix [M, N] for the decomposition: N(0, 0.02) entries, with round_half_up(frac * N)
+    uniformly chosen outlier columns scaled by outlier_scale (the column-clustered outliers the saliency search is
+    for), and a synthetic diagonal inverse Hessian [N] drawn uniform(0.5, 2.0). Draw order: entries, outlier columns,
+    Hessian diagonal, from numpy.random.default_rng([seed, 9000])."""
+    rng = np.random.default_rng([seed, 9000])
+    W = rng.normal(0.0, 0.02, size=(M, N))
+    n_out = salient_count(N, outlier_frac)
+    cols = rng.choice(N, size=n_out, replace=False) if n_out > 0 else np.zeros(0, dtype=np.int64)
+    W[:, cols] *= outlier_scale
+    hinv = rng.uniform(0.5, 2.0, size=N)
+    return W.astype(np.float32), hinv
+
