@@ -216,6 +216,43 @@ fluxbin_status fluxbin_unpack_canonical(const fluxbin_layer* layer, uint32_t* d_
 fluxbin_status fluxbin_stream_probe(const fluxbin_layer* layer, uint32_t* d_sink, size_t sink_bytes,
                                     hipStream_t stream);
 
+/*
+ * Weight decomposition (the step that produces the hybrid bases; FluxBin Sec. 3.1), fp64 on the device.
+ *
+ * fluxbin_rc_decompose: RC_Decomp (App. algorithm "FluxBin Sub-routines"; Def. RC decomposition, Props. 3.2 and
+ * 3.3) of X * mask, independently per block of g consecutive columns, into K binary bases
+ * W^(k) = (alpha_r^(k) alpha_c^(k)^T) * B^(k) with one row scale per (row, block) and one column scale per column:
+ * greedy residual initialization of every base (signs of the residual, column scale 1, one row-scale and one
+ * column-scale least-squares update), then T rounds of (least-squares row and column scales of each base against
+ * X * mask minus the other bases, Prop. 3.2; joint exhaustive sign search over the 2^K combinations per element,
+ * first minimum in the order c = 0..2^K-1 with bit k of c set meaning +1, Prop. 3.3; signs times the mask).
+ *   d_X        fp32 [M][N] row-major, device.        d_mask  uint8 [N] device (nonzero: column included), or NULL.
+ *   K 1..4, T >= 0 rounds, g >= 1, eps >= 0 (the stability constant of Prop. 3.2).
+ *   d_signs    uint32 [K][M][ceil(N/32)] device, canonical planes (bit t of word w: B[k][i][32w+t] == +1; columns
+ *              off the mask have sign 0 and their bit clear).
+ *   d_alpha_r  fp64 [K][M][ceil(N/g)] device.        d_alpha_c  fp64 [K][N] device (0 off the mask).
+ *   d_ws       device workspace of fluxbin_rc_workspace_query bytes (the int8 signs during the rounds).
+ *   Prior bases (optional, d_prior_signs NULL for none): X is replaced by X minus the approximation of Kp earlier bases
+ *   (canonical ±1 bit planes [Kp][M][ceil(N/32)], row scales fp64 [Kp][M][ceil(N/gp)], column scales fp64 [Kp][N],
+ *   all device), computed in fp64: the residual on which FluxBin-Hybrid decomposes the salient bases.
+ * Asynchronous on `stream`; deterministic (fixed reduction orders, no atomics). Up to 2^36 elements.
+ *
+ * fluxbin_structural_search: Hessian-based column saliency (Def. in Sec. 3.1) with a diagonal inverse Hessian,
+ * S_j = sum_i W_ij^2 / hinv_j^2 into d_scores (fp64 [N], device), and per block of g columns (g <= 1024, s <= g) the
+ * s columns of largest saliency (equal scores: the smaller index first) into d_sal_idx (int32, device, increasing),
+ * sum over blocks of min(s, block size) entries; if d_mask is not NULL also the column mask (uint8 [N], device: 1 for
+ * a selected column).
+ */
+fluxbin_status fluxbin_rc_workspace_query(int64_t M, int64_t N, int32_t K, size_t* bytes);
+fluxbin_status fluxbin_rc_decompose(const float* d_X, const uint8_t* d_mask, const uint32_t* d_prior_signs,
+                                    const double* d_prior_alpha_r, const double* d_prior_alpha_c, int32_t Kp,
+                                    int64_t gp, int64_t M, int64_t N, int32_t K, int32_t T, int64_t g, double eps,
+                                    uint32_t* d_signs, double* d_alpha_r, double* d_alpha_c, void* d_ws,
+                                    size_t ws_bytes, hipStream_t stream);
+fluxbin_status fluxbin_structural_search(const float* d_W, const double* d_hinv_diag, int64_t M, int64_t N,
+                                         int64_t g, int64_t s, double* d_scores, int32_t* d_sal_idx, uint8_t* d_mask,
+                                         hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

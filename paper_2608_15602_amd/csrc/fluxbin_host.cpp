@@ -15,6 +15,8 @@ namespace fluxbin {
 
 static thread_local char g_msg[512] = "";
 
+void clear_error() { g_msg[0] = 0; }
+
 fluxbin_status fail(fluxbin_status s, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);

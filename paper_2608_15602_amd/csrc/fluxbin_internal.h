@@ -79,6 +79,7 @@ static_assert(sizeof(Header) == 256, "header must be 256 bytes");
 
 // ---- error reporting (thread-local message) ----
 fluxbin_status fail(fluxbin_status s, const char* fmt, ...);
+void clear_error();  // every entry point starts with it: the message describes the last failed call only
 fluxbin_status hip_fail(int hip_error, const char* what);
 
 // ---- launch plan of the GEMV/GEMM kernels ----

@@ -25,6 +25,7 @@ EXPORTS = (
     "fluxbin_status_string", "fluxbin_last_error_message", "fluxbin_pack_query", "fluxbin_pack",
     "fluxbin_layer_from_header", "fluxbin_workspace_query", "fluxbin_workspace_init", "fluxbin_lut_gemv",
     "fluxbin_lut_gemm_smallbatch", "fluxbin_debug_indices", "fluxbin_unpack_canonical", "fluxbin_stream_probe",
+    "fluxbin_rc_workspace_query", "fluxbin_rc_decompose", "fluxbin_structural_search",
 )
 
 
@@ -81,6 +82,10 @@ def lib() -> ctypes.CDLL:
         L.fluxbin_debug_indices.argtypes = [ctypes.POINTER(Layer), vp, vp]
         L.fluxbin_unpack_canonical.argtypes = [ctypes.POINTER(Layer), vp, vp, vp]
         L.fluxbin_stream_probe.argtypes = [ctypes.POINTER(Layer), vp, sz, vp]
+        L.fluxbin_rc_workspace_query.argtypes = [i64, i64, i32, ctypes.POINTER(sz)]
+        L.fluxbin_rc_decompose.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, i32, i32, i64, ctypes.c_double,
+                                           vp, vp, vp, vp, sz, vp]
+        L.fluxbin_structural_search.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp]
         for name in EXPORTS:
             if name not in ("fluxbin_status_string", "fluxbin_last_error_message"):
                 getattr(L, name).restype = ctypes.c_int
@@ -229,3 +234,40 @@ def fluxbin_stream_probe(layer: PackedLayer, sink, stream=None) -> None:
     ``sink``, a device buffer of at least 1024 bytes."""
     _check(lib().fluxbin_stream_probe(ctypes.byref(layer.layer), sink.data_ptr(), sink.numel() * sink.element_size(),
                                       _stream(stream)))
+
+
+def fluxbin_rc_decompose(X, K: int, T: int, g: int, mask=None, prior=None, eps: float = 1e-12, stream=None):
+    """RC_Decomp of X * mask (X: float32 [M, N] device tensor; mask: uint8 [N] device tensor or None) into K bases
+    with one row scale per (row, block of g columns). prior: None, or (signs, alpha_r, alpha_c, gp) of earlier bases
+    (as returned here) whose approximation is subtracted from X first. Returns (signs int32 [K, M, ceil(N/32)]
+    canonical bit planes, alpha_r float64 [K, M, ceil(N/g)], alpha_c float64 [K, N])."""
+    import torch
+    M, N = X.shape
+    ws_n = ctypes.c_size_t(0)
+    _check(lib().fluxbin_rc_workspace_query(int(M), int(N), int(K), ctypes.byref(ws_n)))
+    ws = torch.empty(ws_n.value, dtype=torch.uint8, device=X.device)
+    signs = torch.empty(K, M, (N + 31) // 32, dtype=torch.int32, device=X.device)
+    ar = torch.empty(K, M, -(-N // g), dtype=torch.float64, device=X.device)
+    ac = torch.empty(K, N, dtype=torch.float64, device=X.device)
+    ps, par, pac, gp = prior if prior is not None else (None, None, None, 1)
+    kp = int(ps.shape[0]) if ps is not None else 0
+    _check(lib().fluxbin_rc_decompose(X.data_ptr(), _ptr(mask), _ptr(ps), _ptr(par), _ptr(pac), kp, int(gp), int(M),
+                                      int(N), int(K), int(T), int(g), float(eps), signs.data_ptr(), ar.data_ptr(),
+                                      ac.data_ptr(), ws.data_ptr(), ws_n.value, _stream(stream)))
+    return signs, ar, ac
+
+
+def fluxbin_structural_search(W, hinv_diag, g: int, s: int, stream=None):
+    """Column saliency with a diagonal inverse Hessian and the s most salient columns of every block of g columns.
+    W: float32 [M, N] device tensor, hinv_diag: float64 [N] device tensor. Returns (scores float64 [N], indices int32,
+    column mask uint8 [N])."""
+    import torch
+    M, N = W.shape
+    n_sal = sum(min(s, N - b0) for b0 in range(0, N, g))
+    scores = torch.empty(N, dtype=torch.float64, device=W.device)
+    idx = torch.empty(n_sal, dtype=torch.int32, device=W.device)
+    mask = torch.empty(N, dtype=torch.uint8, device=W.device)
+    _check(lib().fluxbin_structural_search(W.data_ptr(), hinv_diag.data_ptr(), int(M), int(N), int(g), int(s),
+                                           scores.data_ptr(), idx.data_ptr(), mask.data_ptr(), _stream(stream)))
+    return scores, idx, mask
+
