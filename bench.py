@@ -414,6 +414,47 @@ def vcm_ablation_us(g_r: str, launches: int = 40):
     return out
 
 
+def decomposition_ms(M: int = 8192, N: int = 8192, g: int = 128, s: int = 8, Kb: int = 2, Ks: int = 1, T: int = 10,
+                     oracle_rows: int = 512):
+    """The weight decomposition (FluxBin-Hybrid with a diagonal inverse Hessian: saliency search, Kb global bases per
+    g-column block, Ks salient bases on s columns per block, T alternating rounds) of a synthetic M x N fp32 matrix on
+    the GPU (HIP events around the three library calls, median of 3), and the fp64 oracle on an oracle_rows x N
+    slice of it on the host (one run), reported per million weights."""
+    import numpy as np
+    import torch
+    from oracle import rc_oracle as rc
+    from paper_2608_15602_amd import fluxbin as fb
+    from synth import make_weight_matrix
+    W, hinv = make_weight_matrix(M, N, seed=50, outlier_frac=0.01)
+    Wt = torch.from_numpy(W).cuda()
+    ht = torch.from_numpy(hinv).cuda()
+
+    def run():
+        _, _, mask = fb.fluxbin_structural_search(Wt, ht, g, s)
+        gs, gar, gac = fb.fluxbin_rc_decompose(Wt, Kb, T, g)
+        fb.fluxbin_rc_decompose(Wt, Ks, T, N, mask=mask, prior=(gs, gar, gac, g))
+
+    run()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(3):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    gpu_ms = sorted(ts)[1]
+    t0 = time.perf_counter()
+    rc.hybrid_quantize(W[:oracle_rows].astype(np.float64), hinv, g=g, s=s, Kb=Kb, Ks=Ks, T=T)
+    cpu_s = time.perf_counter() - t0
+    return {"shape_out_x_in": f"{M}x{N}", "Kb": Kb, "Ks": Ks, "g": g, "s_per_group": s, "rounds": T,
+            "gpu_ms": round(gpu_ms, 2), "gpu_ms_per_Mweight": round(gpu_ms / (M * N / 1e6), 4),
+            "oracle_s_per_Mweight": round(cpu_s / (oracle_rows * N / 1e6), 4),
+            "oracle_sample": f"rows 0..{oracle_rows - 1} (fp64 NumPy, {cpu_s:.1f} s)"}
+
+
 def small_layer_us(spec, launches=200):
     """Per-call microseconds of a small layer (4096x4096): a HIP graph of back-to-back launches rotating distinct
     packed copies (so the signs come from HBM), median of 5 replays."""
@@ -521,6 +562,8 @@ def main():
         out["config"]["kernel_variants_28672x8192"] = kernel_variants_us(args.g_r)
         out["config"]["vcm_ablation"] = vcm_ablation_us(args.g_r)
         out["config"]["mu_profile"] = mu_profile_us(args.g_r)
+    if not args.no_variants:
+        out["config"]["decomposition"] = decomposition_ms()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -113,28 +113,42 @@ __global__ void __launch_bounds__(256) k_rc_row(RcArgs a, int k, int init) {
   if (lane == 0) a.ar[(int64_t(k) * a.M + i) * a.G + blk] = num / (den + a.eps);
 }
 
-// Column scales of base k (Prop. 3.2): a workgroup per 64 columns, four row slices combined in a fixed order.
-__global__ void __launch_bounds__(256) k_rc_col(RcArgs a, int k, int init) {
+// Column scales of base k (Prop. 3.2), first stage: workgroup (tile of 64 columns, row slice r of RS) sums its rows
+// in four interleaved sub-slices combined in a fixed order, into part[r][2][N] (numerator, denominator).
+__global__ void __launch_bounds__(256) k_rc_col(RcArgs a, int k, int init, int64_t rows_per_slice, double* part) {
   __shared__ double s_num[4][64], s_den[4][64];
-  const int c = threadIdx.x & 63, slice = threadIdx.x >> 6;
+  const int c = threadIdx.x & 63, sub = threadIdx.x >> 6;
   const int64_t j = int64_t(blockIdx.x) * 64 + c;
+  const int64_t r = blockIdx.y;
+  const int64_t i0 = r * rows_per_slice, i1 = i0 + rows_per_slice < a.M ? i0 + rows_per_slice : a.M;
   double num = 0.0, den = 0.0;
   if (j < a.N) {
     const int64_t blk = j / a.g;
-    for (int64_t i = slice; i < a.M; i += 4) {
+    for (int64_t i = i0 + sub; i < i1; i += 4) {
       const double rb = a.ar[(int64_t(k) * a.M + i) * a.G + blk] * double(a.B[(int64_t(k) * a.M + i) * a.N + j]);
       num += rb * rc_target(a, k, init, i, j);
       den += rb * rb;
     }
   }
-  s_num[slice][c] = num;
-  s_den[slice][c] = den;
+  s_num[sub][c] = num;
+  s_den[sub][c] = den;
   __syncthreads();
-  if (slice == 0 && j < a.N) {
-    const double n = ((s_num[0][c] + s_num[1][c]) + s_num[2][c]) + s_num[3][c];
-    const double d = ((s_den[0][c] + s_den[1][c]) + s_den[2][c]) + s_den[3][c];
-    a.ac[int64_t(k) * a.N + j] = n / (d + a.eps);
+  if (sub == 0 && j < a.N) {
+    part[(r * 2 + 0) * a.N + j] = ((s_num[0][c] + s_num[1][c]) + s_num[2][c]) + s_num[3][c];
+    part[(r * 2 + 1) * a.N + j] = ((s_den[0][c] + s_den[1][c]) + s_den[2][c]) + s_den[3][c];
   }
+}
+
+// Second stage: the slices' sums added in slice order, then the least-squares quotient.
+__global__ void k_rc_col_fin(RcArgs a, int k, int64_t slices, const double* part) {
+  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= a.N) return;
+  double n = 0.0, d = 0.0;
+  for (int64_t r = 0; r < slices; ++r) {
+    n += part[(r * 2 + 0) * a.N + j];
+    d += part[(r * 2 + 1) * a.N + j];
+  }
+  a.ac[int64_t(k) * a.N + j] = n / (d + a.eps);
 }
 
 // Joint sign search (Prop. 3.3) for every element: the first of the 2^K combinations with the smallest |x - approx|.
@@ -227,6 +241,12 @@ __global__ void __launch_bounds__(1024) k_topk(const double* S, int64_t N, int64
 
 unsigned grid_for(int64_t n, int per) { return unsigned((n + per - 1) / per); }
 
+// Row slices of the column-scale sums: at least 256 rows each, at most 64 slices.
+int64_t col_slices(int64_t M) {
+  const int64_t s = M / 256;
+  return s < 1 ? 1 : (s > 64 ? 64 : s);
+}
+
 }  // namespace
 
 }  // namespace fluxbin
@@ -239,7 +259,8 @@ fluxbin_status fluxbin_rc_workspace_query(int64_t M, int64_t N, int32_t K, size_
   clear_error();
   if (!bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "bytes is NULL");
   if (M < 1 || N < 1 || K < 1 || K > 4) return fail(FLUXBIN_ERR_INVALID_ARG, "M, N >= 1 and K in 1..4 required");
-  *bytes = size_t(K) * size_t(M) * size_t(N);
+  // int8 signs [K][M][N], then (256-byte aligned) the column-scale partial sums [slices][2][N] fp64
+  *bytes = ((size_t(K) * size_t(M) * size_t(N) + 255) & ~size_t(255)) + size_t(col_slices(M)) * 2 * size_t(N) * 8;
   return FLUXBIN_OK;
 }
 
@@ -280,16 +301,23 @@ fluxbin_status fluxbin_rc_decompose(const float* d_X, const uint8_t* d_mask, con
   a.pG = (N + a.pg - 1) / a.pg;
   a.pW = (N + 31) / 32;
   const int64_t elems = M * N;
+  const int64_t slices = col_slices(M);
+  const int64_t rows_per_slice = (M + slices - 1) / slices;
+  double* part = reinterpret_cast<double*>(static_cast<char*>(d_ws) +
+                                           ((size_t(K) * size_t(M) * size_t(N) + 255) & ~size_t(255)));
+  const dim3 col_grid(grid_for(N, 64), unsigned(slices));
   for (int k = 0; k < K; ++k) {
     hipLaunchKernelGGL(k_rc_fill, dim3(grid_for(N, 256)), dim3(256), 0, stream, d_alpha_c + int64_t(k) * N, N, 1.0);
     hipLaunchKernelGGL(k_rc_init_sign, dim3(grid_for(elems, 256)), dim3(256), 0, stream, a, k);
     hipLaunchKernelGGL(k_rc_row, dim3(grid_for(M * a.G, 4)), dim3(256), 0, stream, a, k, 1);
-    hipLaunchKernelGGL(k_rc_col, dim3(grid_for(N, 64)), dim3(256), 0, stream, a, k, 1);
+    hipLaunchKernelGGL(k_rc_col, col_grid, dim3(256), 0, stream, a, k, 1, rows_per_slice, part);
+    hipLaunchKernelGGL(k_rc_col_fin, dim3(grid_for(N, 256)), dim3(256), 0, stream, a, k, slices, part);
   }
   for (int t = 0; t < T; ++t) {
     for (int k = 0; k < K; ++k) {
       hipLaunchKernelGGL(k_rc_row, dim3(grid_for(M * a.G, 4)), dim3(256), 0, stream, a, k, 0);
-      hipLaunchKernelGGL(k_rc_col, dim3(grid_for(N, 64)), dim3(256), 0, stream, a, k, 0);
+      hipLaunchKernelGGL(k_rc_col, col_grid, dim3(256), 0, stream, a, k, 0, rows_per_slice, part);
+      hipLaunchKernelGGL(k_rc_col_fin, dim3(grid_for(N, 256)), dim3(256), 0, stream, a, k, slices, part);
     }
     switch (K) {
       case 1: hipLaunchKernelGGL(k_rc_sign<1>, dim3(grid_for(elems, 256)), dim3(256), 0, stream, a); break;
