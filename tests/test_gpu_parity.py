@@ -240,8 +240,9 @@ EDGE_SPECS = [
 
 
 @pytest.mark.parametrize("spec", EDGE_SPECS, ids=lambda s: s.name)
-@pytest.mark.parametrize("B", [1, 3])
+@pytest.mark.parametrize("B", [1, 3, 9])
 def test_edge_shapes(spec, B):
+    """B = 1: batch-1 kernels; B = 3: LUT batch kernel (mu = 8) or matrix cores (mu = 4); B = 9: matrix cores."""
     _parity(spec, B)
 
 
