@@ -18,9 +18,10 @@
 // R(i) bits (mu = 8: R = 8 (i mod 16); mu = 4: R = 4 (i mod 32)). Lane (r, g) of a 16-row MFMA block needs canonical
 // bits 32g .. 32g+31 of its row r: two 32-bit words of the entry and one funnel shift give them, whatever the
 // rotation. The K dimension of the contraction is ordered so that element pair k of K step q holds canonical columns
-// (32g + 4q + k, 32g + 4q + k + 16): a right rotation of the 32 bits by (4q + k + 17) puts both sign bits at bit
+// (32g + 4q + k, 32g + 4q + k + 16): a left shift of the 32 bits by 15 - (4q + k) puts both sign bits at bit
 // positions 15 and 31, the fp16 sign bits of the pair, so one and-or with the column-scale pair forms the operand
-// (a set bit gives -|colscale|, so the matrix core sums -s; the row scale is applied negated).
+// (a set bit gives -|colscale|, so the matrix core sums -s; the row scale is applied negated). The words of two row
+// blocks are shifted together as one 64-bit value.
 //
 // Work decomposition (as in the LUT kernels): a tile is 256 rows, 64 per wavefront of a 256-thread workgroup (four
 // 16-row MFMA blocks); a unit is a tile times a super-chunk (256 virtual columns, both stored chunk slots); units are
@@ -139,9 +140,20 @@ __device__ __forceinline__ void mf_stage_write(const GemmArgs& a, const MfUnitRe
   reinterpret_cast<uint16_t*>(sa)[((h * 4 + g) * 16 + j) * 2 + hf] = uint16_t(cs & 0x7FFFu);
 }
 
+// 64-bit left shift by a constant, as one v_lshlrev_b64: it shifts two 32-bit words in the time a 32-bit shift takes
+// one (measured on gfx950). Written as an instruction because the compiler, seeing that only bits 15 and 31 of each
+// half are used, would split it back into two 32-bit shifts. For {w_hi : w_lo} << s (s <= 15), bits 15 and 31 of each
+// half are bits 15 - s and 31 - s of its own word: the bits the low word pushes into the high half land below bit 15.
+__device__ __forceinline__ uint64_t mf_shl64(uint64_t v, uint32_t s) {
+  uint64_t r;
+  asm("v_lshlrev_b64 %0, %1, %2" : "=v"(r) : "s"(s), "v"(v));
+  return r;
+}
+
 // Multiplies one staged unit into the accumulators. xs/as: the unit's staged activation and column-scale pairs;
 // scr: the wavefront's sign scratch (32 bytes per row: the 16-byte entry, then its first 8 bytes again, so that the two
 // words a lane reads never wrap), followed by 64 words of row scales.
+template <bool SHL64>
 __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, const mf_u32x4 (&e)[2], uint32_t r,
                                         uint32_t* scr, int lane, int r16, int g, const uint32_t (&aw)[2], uint32_t sh,
                                         float (&acc)[4][4]) {
@@ -159,22 +171,38 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
       w[rb] = __builtin_amdgcn_alignbit(ent[1], ent[0], sh);
       rs[rb] = *reinterpret_cast<const uint2*>(srs + h * 32 + 8 * rb + 2 * g);
     }
+    // the words of row blocks 2rp and 2rp + 1 as one 64-bit value (high: 2rp + 1), shifted together below
+    uint64_t w2[2] = {0, 0};
+    if constexpr (SHL64) {
+      w2[0] = (uint64_t(w[1]) << 32) | w[0];
+      w2[1] = (uint64_t(w[3]) << 32) | w[2];
+    }
     mf_float4 tmp[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const mf_u32x4 bx = *reinterpret_cast<const mf_u32x4*>(xs + ((h * 4 + g) * 4 + q) * kMfXStride + 4 * r16);
       const mf_u32x4 ac = *reinterpret_cast<const mf_u32x4*>(as + (h * 4 + g) * 16 + 4 * q);
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        mf_u32x4 av;
+      for (int rp = 0; rp < 2; ++rp) {
+        mf_u32x4 av0, av1;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const uint32_t rot = __builtin_amdgcn_alignbit(w[rb], w[rb], uint32_t((4 * q + k + 17) & 31));
-          av[k] = (rot & 0x80008000u) | ac[k];
+          const uint32_t s = uint32_t(15 - (4 * q + k));
+          if constexpr (SHL64) {
+            const uint64_t sft = mf_shl64(w2[rp], s);
+            av0[k] = (uint32_t(sft) & 0x80008000u) | ac[k];
+            av1[k] = (uint32_t(sft >> 32) & 0x80008000u) | ac[k];
+          } else {
+            av0[k] = ((w[2 * rp] << s) & 0x80008000u) | ac[k];
+            av1[k] = ((w[2 * rp + 1] << s) & 0x80008000u) | ac[k];
+          }
         }
-        const mf_float4 c0 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[rb];
-        tmp[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av),
-                                                         __builtin_bit_cast(mf_half8, bx), c0, 0, 0, 0);
+        const mf_float4 c0 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[2 * rp];
+        const mf_float4 c1 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[2 * rp + 1];
+        tmp[2 * rp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av0),
+                                                             __builtin_bit_cast(mf_half8, bx), c0, 0, 0, 0);
+        tmp[2 * rp + 1] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av1),
+                                                                 __builtin_bit_cast(mf_half8, bx), c1, 0, 0, 0);
       }
     }
 #pragma unroll
@@ -258,7 +286,8 @@ struct MfKernel {
         if (K + D + 2 < s.n && ++s.stg_sc == a.steps) s.stg_sc = 0;
       }
       __builtin_amdgcn_sched_barrier(0);
-      mf_unit(sx + (K & 1) * kMfXUnit, sa + (K & 1) * kMfAUnit, ur[P].e, ur[P].r, scr, ln.lane, ln.r16, ln.g, ln.aw,
+      // 64-bit shifts free VALU issue slots; with 16 batch rows their register pairs would spill
+      mf_unit<(BP <= 8)>(sx + (K & 1) * kMfXUnit, sa + (K & 1) * kMfAUnit, ur[P].e, ur[P].r, scr, ln.lane, ln.r16, ln.g, ln.aw,
               ln.sh, s.acc);
       if (K + 1 < s.n)
         mf_stage_write<BP>(a, ur[PS], sx + ((K + 1) & 1) * kMfXUnit, sa + ((K + 1) & 1) * kMfAUnit, ln.t);
