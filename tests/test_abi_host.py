@@ -202,3 +202,41 @@ def test_gemv_rejects_bad_arguments(L):
     assert L.fluxbin_debug_indices(None, X, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert L.fluxbin_unpack_canonical(None, X, None, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert L.fluxbin_stream_probe(None, X, 1024, None) == fb.FLUXBIN_ERR_INVALID_ARG
+
+
+def test_decomposition_sizes_and_bad_arguments(L):
+    """Workspace of the decomposition (int8 signs, then the column-scale partial sums of up to 64 row slices of at
+    least 256 rows) and argument checks that fail before any launch."""
+    n = ctypes.c_size_t(0)
+    assert L.fluxbin_rc_workspace_query(1000, 300, 3, ctypes.byref(n)) == fb.FLUXBIN_OK
+    signs = 3 * 1000 * 300
+    assert n.value == ((signs + 255) // 256) * 256 + 3 * 2 * 300 * 8   # 1000 // 256 = 3 slices
+    assert L.fluxbin_rc_workspace_query(100, 300, 1, ctypes.byref(n)) == fb.FLUXBIN_OK
+    assert n.value == ((100 * 300 + 255) // 256) * 256 + 1 * 2 * 300 * 8
+    assert L.fluxbin_rc_workspace_query(100000, 10, 1, ctypes.byref(n)) == fb.FLUXBIN_OK
+    assert n.value == ((100000 * 10 + 255) // 256) * 256 + 64 * 2 * 10 * 8
+    assert L.fluxbin_rc_workspace_query(0, 300, 1, ctypes.byref(n)) == fb.FLUXBIN_ERR_INVALID_ARG
+    assert L.fluxbin_rc_workspace_query(10, 300, 5, ctypes.byref(n)) == fb.FLUXBIN_ERR_INVALID_ARG
+    assert L.fluxbin_rc_workspace_query(10, 300, 1, None) == fb.FLUXBIN_ERR_INVALID_ARG
+    X, S, A, C, WS = 0x7F0000100000, 0x7F0000200000, 0x7F0000300000, 0x7F0000400000, 0x7F0000500000
+    d = L.fluxbin_rc_decompose
+    ok_ws = 1 << 30
+    assert d(None, None, None, None, None, 0, 1, 64, 256, 2, 3, 128, 1e-12, S, A, C, WS, ok_ws, None) == \
+        fb.FLUXBIN_ERR_INVALID_ARG
+    assert d(X, None, None, None, None, 0, 1, 64, 256, 2, -1, 128, 1e-12, S, A, C, WS, ok_ws, None) == \
+        fb.FLUXBIN_ERR_INVALID_ARG
+    assert d(X, None, None, None, None, 0, 1, 64, 256, 2, 3, 0, 1e-12, S, A, C, WS, ok_ws, None) == \
+        fb.FLUXBIN_ERR_INVALID_ARG
+    assert d(X, None, None, None, None, 0, 1, 64, 256, 2, 3, 128, float("nan"), S, A, C, WS, ok_ws, None) == \
+        fb.FLUXBIN_ERR_INVALID_ARG
+    assert d(X, None, None, None, None, 0, 1, 64, 256, 2, 3, 128, -1.0, S, A, C, WS, ok_ws, None) == \
+        fb.FLUXBIN_ERR_INVALID_ARG
+    assert d(X, None, None, None, None, 0, 1, 64, 256, 2, 3, 128, 1e-12, S, A, C, WS, 100, None) == \
+        fb.FLUXBIN_ERR_BUFFER_TOO_SMALL
+    assert d(X, None, S, None, C, 2, 128, 64, 256, 2, 3, 128, 1e-12, S, A, C, WS, ok_ws, None) == \
+        fb.FLUXBIN_ERR_INVALID_ARG   # prior signs without their row scales
+    ss = L.fluxbin_structural_search
+    assert ss(None, A, 64, 256, 128, 8, C, S, None, None) == fb.FLUXBIN_ERR_INVALID_ARG
+    assert ss(X, A, 64, 256, 2048, 8, C, S, None, None) == fb.FLUXBIN_ERR_UNSUPPORTED   # group > 1024
+    assert ss(X, A, 64, 256, 128, 200, C, S, None, None) == fb.FLUXBIN_ERR_INVALID_ARG  # s > g
+    assert ss(X, A, 64, 256, 128, 0, C, S, None, None) == fb.FLUXBIN_ERR_INVALID_ARG

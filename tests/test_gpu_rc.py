@@ -2,7 +2,9 @@
 against the fp64 oracle (oracle/rc_oracle.py), and the decomposed layer through fluxbin_pack and the GEMV.
 
 Bar: signs and selected columns bit-exact (both sides decide in fp64); row and column scales within 1e-9 relative
-(fp64 sums in different orders); the GEMV of the decomposed layer within the hot path's 2e-3 rule."""
+(fp64 sums in different orders), or within 1e-10 of the largest scale of the decomposition for the small scales of
+later bases (their least-squares quotients divide residuals that cancel, which magnifies the fp64 rounding of the
+residual relative to the scale itself); the GEMV of the decomposed layer within the hot path's 2e-3 rule."""
 import numpy as np
 import pytest
 
@@ -37,11 +39,12 @@ def _bits(B):
 def _close(got, ref, what, rtol=1e-9):
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
-    floor = 1e-12 * max(np.abs(ref).max(), 1e-300)
+    atol = 1e-10 * max(np.abs(ref).max(), 1e-300)
     err = np.abs(got - ref)
-    worst = float((err / np.maximum(np.abs(ref), floor)).max()) if ref.size else 0.0
-    log(f"  {what}: max rel {worst:.2e}")
-    assert np.all(err <= rtol * np.maximum(np.abs(ref), floor)), what
+    bound = np.maximum(rtol * np.abs(ref), atol)
+    worst = float((err / bound).max()) if ref.size else 0.0
+    log(f"  {what}: max err / bound {worst:.2e}")
+    assert np.all(err <= bound), what
 
 
 def _gpu_rc(W, K, T, g, mask=None, prior=None):
@@ -140,3 +143,18 @@ def test_decomposed_layer_through_pack_and_gemv():
     Wg = rc.reconstruct(ref["glob"]["B"], ref["glob"]["alpha_r"], ref["glob"]["alpha_c"], g)
     Wh = Wg + rc.reconstruct(ref["sal"]["B"], ref["sal"]["alpha_r"], ref["sal"]["alpha_c"], N)
     assert ((W - Wh) ** 2).sum() < ((W - Wg) ** 2).sum()
+
+
+@pytest.mark.parametrize("M,N,K,g,masked", [(1, 40, 2, 16, False), (33, 70, 4, 32, False), (50, 45, 3, 100, True),
+                                            (300, 33, 1, 7, True)], ids=["one_row", "K4_ragged", "g_gt_N", "g7"])
+def test_rc_decompose_edge_shapes(M, N, K, g, masked):
+    """One row, N not a multiple of 32 (tail bits of the planes), four bases, a group wider than the matrix, a group of
+    7 columns, masks; bit-exact signs and 1e-9 scales against the oracle."""
+    W, _ = make_weight_matrix(M, N, seed=60 + M)
+    mask = (np.random.default_rng(61).random(N) < 0.4) if masked else np.ones(N, bool)
+    ref = rc.rc_decomp(W.astype(np.float64), mask, K=K, T=3, g=g)
+    signs, ar, ac = _gpu_rc(W, K, 3, g, mask=mask if masked else None)
+    log(f"case rc edge M={M} N={N} K={K} g={g} masked={masked}")
+    assert np.array_equal(signs.cpu().numpy().view(np.uint32), _bits(ref["B"])), "signs differ"
+    _close(ar.cpu().numpy(), ref["alpha_r"], "alpha_r")
+    _close(ac.cpu().numpy(), ref["alpha_c"], "alpha_c")
