@@ -214,9 +214,9 @@ __device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
   return ((const __attribute__((address_space(4))) int32_t*)p)[i];
 }
 
-// Small-batch mu = 8 kernel (fluxbin_gemm_batch.hip): launches k_gemm_mu8_batch with n_groups groups of four batch
-// rows and depth units of sign data requested ahead; false if no instance exists.
-bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, hipStream_t stream);
+// Small-batch mu = 8 kernel (fluxbin_gemm_batch.hip): launches k_gemm_mu8_batch with n_groups groups of nb (2 or 4)
+// batch rows and depth units of sign data requested ahead; false if no instance exists.
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, hipStream_t stream);
 
 // Matrix-core small-batch kernel (fluxbin_gemm_mfma.hip): 256-row tiles, partial sums padded to bpad (4, 8 or 16)
 // batch rows, data requested depth (2 or 3) units ahead; false if no instance exists.

@@ -29,7 +29,7 @@ namespace fluxbin {
 
 struct Bat {
   static constexpr int NT = 1024;
-  static constexpr int BPN = 4;               // batch rows per workgroup
+  static constexpr int BPN = 4;               // batch rows staged per workgroup (NB <= BPN of them are computed)
   static constexpr int TBL = 256 * 16 * 4;   // floats per table buffer (64 KB)
   static constexpr int XSS = 12;             // floats per (chunk, batch row, sub-vector) in the staging layout
   static constexpr int XC = BPN * 16 * XSS;  // floats per staged chunk
@@ -177,31 +177,35 @@ __device__ __forceinline__ void bat_stage_write(float* xs_slot, const BatStage& 
       r.ok ? h2f(uint16_t(r.xb)) * h2f(uint16_t(r.cs)) : 0.f;
 }
 
-// Build the 16 tables (256 patterns x 4 batch rows) of one staged chunk. Thread t owns sub-vector s = t & 15, batch
-// row b = (t >> 4) & 3 and the 16 patterns whose top four bits are t >> 6, enumerated in Gray order (each entry is the
-// previous one plus or minus 2*xv[n]). A wavefront writes 64 consecutive floats per entry step.
+// Build the 16 tables (256 patterns x NB batch rows) of one staged chunk; entry (p, s, b) at (p*16 + s)*4 + b whatever
+// NB is, so the lookups' addresses do not depend on it. NB = 4: thread t owns sub-vector s = t & 15, batch row
+// b = (t >> 4) & 3 and the 16 patterns whose top four bits are t >> 6; NB = 2: b = (t >> 4) & 1 and the 8 patterns
+// whose top five bits are t >> 5. Patterns are enumerated in Gray order (each entry is the previous one plus or minus
+// 2*xv[n]).
+template <int NB>
 __device__ __forceinline__ void bat_build(float* tbl, const float* xs_chunk) {
+  constexpr int LOW = NB == 4 ? 4 : 3;   // low pattern bits enumerated by one thread
   const int t = threadIdx.x;
   const int s = t & 15;
-  const int b = (t >> 4) & 3;
-  const int hi = t >> 6;
+  const int b = (t >> 4) & (NB - 1);
+  const int hi = t >> (NB == 4 ? 6 : 5);
   const float4 lo4 = *reinterpret_cast<const float4*>(xs_chunk + (b * 16 + s) * Bat::XSS);
   const float4 hi4 = *reinterpret_cast<const float4*>(xs_chunk + (b * 16 + s) * Bat::XSS + 4);
   const float xv[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
   float v = 0.f;
 #pragma unroll
   for (int n = 0; n < 8; ++n) {
-    const bool plus = n >= 4 && ((hi >> (n - 4)) & 1);
+    const bool plus = n >= LOW && ((hi >> (n - LOW)) & 1);
     v += plus ? xv[n] : -xv[n];
   }
-  float d[4];
+  float d[LOW];
 #pragma unroll
-  for (int n = 0; n < 4; ++n) d[n] = 2.f * xv[n];
+  for (int n = 0; n < LOW; ++n) d[n] = 2.f * xv[n];
   float* col = tbl + s * 4 + b;
-  const int pbase = hi << 4;
+  const int pbase = hi << LOW;
   col[pbase * 64] = v;
 #pragma unroll
-  for (int k = 1; k < 16; ++k) {
+  for (int k = 1; k < (1 << LOW); ++k) {
     const int n = __builtin_ctz(k);
     const int gk = k ^ (k >> 1);
     v += ((gk >> n) & 1) ? d[n] : -d[n];
@@ -210,13 +214,15 @@ __device__ __forceinline__ void bat_build(float* tbl, const float* xs_chunk) {
 }
 
 // Chunk J of the unit: the thread's sign words of that chunk are in stored slot J XOR [row mod 32 >= 16]; 16 lookups
-// of four batch values, times the chunk's row scale, into acc.
-template <int J>
+// of NB batch values (one 16- or 8-byte LDS read each), times the chunk's row scale, into acc.
+template <int J, int NB>
 __device__ __forceinline__ void bat_lookup(const float* tbl, const BatRing& rg, const uint32_t (&cq)[4], bool swap,
-                                           float (&acc)[1][Bat::BPN]) {
+                                           float (&acc)[1][NB]) {
   const uint32_t sh = (threadIdx.x & 1u) * 16u;
   const bool upper = (J == 1) != swap;
-  float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  float sum[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) sum[b] = 0.f;
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     const uint32_t w = upper ? rg.w[4 + m] : rg.w[m];
@@ -224,24 +230,28 @@ __device__ __forceinline__ void bat_lookup(const float* tbl, const BatRing& rg, 
     for (int bb = 0; bb < 4; ++bb) {
       const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
       const uint32_t addr = __builtin_amdgcn_perm(w, cq[m], sel);   // (p << 8) | (s << 4)
-      const float4 e = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(tbl) + addr);
-      s4.x += e.x; s4.y += e.y; s4.z += e.z; s4.w += e.w;
+      if constexpr (NB == 4) {
+        const float4 e = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(tbl) + addr);
+        sum[0] += e.x; sum[1] += e.y; sum[2] += e.z; sum[3] += e.w;
+      } else {
+        const float2 e = *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(tbl) + addr);
+        sum[0] += e.x; sum[1] += e.y;
+      }
     }
   }
   const float rs = h2f(uint16_t(rg.r[J] >> sh));
-  acc[0][0] = __builtin_fmaf(s4.x, rs, acc[0][0]);
-  acc[0][1] = __builtin_fmaf(s4.y, rs, acc[0][1]);
-  acc[0][2] = __builtin_fmaf(s4.z, rs, acc[0][2]);
-  acc[0][3] = __builtin_fmaf(s4.w, rs, acc[0][3]);
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[0][b] = __builtin_fmaf(sum[b], rs, acc[0][b]);
 }
 
+template <int NB>
 struct BatState {
   int n;                      // units of this workgroup
   int tile, sc;               // unit being looked up
   int first_tile, last_tile;
   bool first_shared, last_shared;
   int n_pending;
-  float acc[1][Bat::BPN];
+  float acc[1][NB];
 };
 
 // Row-scale plane of chunk 2*sc(k) + half of unit k (clamped), from the table staged in LDS.
@@ -256,8 +266,8 @@ __device__ __forceinline__ int32_t bat_plane(const int* s_planes, int k, int hal
 // Sub-step 1: write unit K+2's activations (requested two units earlier) into the staging slot unit K no longer
 // needs; build unit K+1's chunk 0 into buffer 0; look up chunk 1. Each wait covers loads that the step needs anyway:
 // the staging loads waited for were issued before the sign loads of unit K+D-2.
-template <int D, int K>
-__device__ __forceinline__ void bat_units(const GemmArgs& a, BatState& st, BatCursor& cur, BatRing (&ring)[D + 1],
+template <int D, int K, int NB>
+__device__ __forceinline__ void bat_units(const GemmArgs& a, BatState<NB>& st, BatCursor& cur, BatRing (&ring)[D + 1],
                                           BatStageCursor& scur, BatStage (&sr)[3], uint32_t xrow, float* tbl,
                                           float* xs, const uint16_t* s_xidx, const int* s_planes,
                                           const uint32_t (&cq)[4], bool swap) {
@@ -269,34 +279,34 @@ __device__ __forceinline__ void bat_units(const GemmArgs& a, BatState& st, BatCu
     bat_issue_signs(a, cur, ring[(K + D) % (D + 1)]);
     bat_issue_rscale(a, cur, bat_plane(s_planes, K + D, 0), bat_plane(s_planes, K + D, 1), ring[(K + D) % (D + 1)]);
     bat_cursor_advance(a, cur, K + D + 1 < st.n);
-    bat_build(tbl + Bat::TBL, xs + (K & 1) * Bat::XS + Bat::XC);
-    bat_lookup<0>(tbl, ring[K % (D + 1)], cq, swap, st.acc);
+    bat_build<NB>(tbl + Bat::TBL, xs + (K & 1) * Bat::XS + Bat::XC);
+    bat_lookup<0, NB>(tbl, ring[K % (D + 1)], cq, swap, st.acc);
     __syncthreads();
     // sub-step 1
     if (K + 2 < st.n) bat_stage_write(xs + (K & 1) * Bat::XS, sr[(K + 2) % 3]);
-    if (K + 1 < st.n) bat_build(tbl, xs + ((K + 1) & 1) * Bat::XS);
-    bat_lookup<1>(tbl + Bat::TBL, ring[K % (D + 1)], cq, swap, st.acc);
+    if (K + 1 < st.n) bat_build<NB>(tbl, xs + ((K + 1) & 1) * Bat::XS);
+    bat_lookup<1, NB>(tbl + Bat::TBL, ring[K % (D + 1)], cq, swap, st.acc);
     if (st.sc == a.steps - 1 || K + 1 == st.n) {
       const bool shared = st.tile == st.first_tile ? st.first_shared : (st.tile == st.last_tile && st.last_shared);
       if (shared) {
-        store_partial<1024, 1, Bat::BPN>(a, st.tile == st.first_tile ? 0 : 1, st.acc);
+        store_partial<1024, 1, NB>(a, st.tile == st.first_tile ? 0 : 1, st.acc);
         ++st.n_pending;
       } else {
-        store_tile_y<1024, 1, Bat::BPN>(a, st.tile, st.acc);
+        store_tile_y<1024, 1, NB>(a, st.tile, st.acc);
       }
 #pragma unroll
-      for (int b = 0; b < Bat::BPN; ++b) st.acc[0][b] = 0.f;
+      for (int b = 0; b < NB; ++b) st.acc[0][b] = 0.f;
     }
     __syncthreads();
     if (++st.sc == a.steps) {
       st.sc = 0;
       ++st.tile;
     }
-    bat_units<D, K + 1>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
+    bat_units<D, K + 1, NB>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
   }
 }
 
-template <int D>
+template <int D, int NB>
 __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   __shared__ __attribute__((aligned(16))) float tbl[2 * Bat::TBL];   // 128 KB: buffer 0 chunk 0, buffer 1 chunk 1
   __shared__ __attribute__((aligned(16))) float xs[2 * Bat::XS];      // staged activations, two units
@@ -304,19 +314,19 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   __shared__ int s_planes[2 * kBatMaxUnits];                           // row-scale planes of their chunks
   __shared__ int s_flag;
 
-  // This workgroup's group of batch rows, with its own slice of the workspace (counters, then partial sums).
+  // This workgroup's group of NB batch rows, with its own slice of the workspace (counters, then partial sums).
   GemmArgs a = args;
   const int grp = blockIdx.y;
-  a.B = args.B - 4 * grp < 4 ? args.B - 4 * grp : 4;
-  a.x = args.x + int64_t(4 * grp) * args.ldx;
-  a.y = static_cast<char*>(args.y) + int64_t(4 * grp) * args.ldy * (args.y_fp32 ? 4 : 2);
+  a.B = args.B - NB * grp < NB ? args.B - NB * grp : NB;
+  a.x = args.x + int64_t(NB * grp) * args.ldx;
+  a.y = static_cast<char*>(args.y) + int64_t(NB * grp) * args.ldy * (args.y_fp32 ? 4 : 2);
   a.counters = args.counters + int64_t(grp) * (((int64_t(args.n_tiles) * kCounterStride * 4 + 255) & ~255) / 4);
-  a.partials = args.partials + int64_t(grp) * args.blocks * 2 * 1024 * Bat::BPN;
+  a.partials = args.partials + int64_t(grp) * args.blocks * 2 * 1024 * NB;
 
   const int t = threadIdx.x;
   const int u0 = first_unit(a, blockIdx.x);
   const int u1 = first_unit(a, blockIdx.x + 1);
-  BatState st;
+  BatState<NB> st;
   st.n = u1 - u0;
   st.tile = u0 / a.steps;
   st.sc = u0 - st.tile * a.steps;
@@ -326,7 +336,7 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   st.last_shared = tile_is_shared(a, st.last_tile);
   st.n_pending = 0;
 #pragma unroll
-  for (int b = 0; b < Bat::BPN; ++b) st.acc[0][b] = 0.f;
+  for (int b = 0; b < NB; ++b) st.acc[0][b] = 0.f;
   const bool swap = ((t >> 4) & 1) != 0;   // rows with i mod 32 >= 16 hold the super-chunk's chunks swapped
   // byte offset of the thread's batch row in x (rows past B read row B-1; their values are masked)
   const uint32_t xrow = uint32_t(((t >> 8) < a.B ? (t >> 8) : a.B - 1) * a.ldx * 2);
@@ -405,21 +415,28 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
     for (int bb = 0; bb < 4; ++bb) cq[m] |= (((uint32_t(4 * m + bb) + uint32_t(t)) & 15u) << 4) << (8 * bb);
   }
   __syncthreads();
-  bat_build(tbl, xs);   // unit 0, chunk 0
+  bat_build<NB>(tbl, xs);   // unit 0, chunk 0
   __syncthreads();
-  bat_units<D, 0>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
+  bat_units<D, 0, NB>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
   const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
-  publish_pending<1024, 1, Bat::BPN>(a, pend0, st.last_tile, st.n_pending, &s_flag);
+  publish_pending<1024, 1, NB>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
 
-bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, hipStream_t stream) {
-  if (n_groups < 1 || n_groups > 4) return false;
+template <int NB>
+static bool launch_batch_nb(const GemmArgs& a, int n_groups, int depth, hipStream_t stream) {
   const dim3 grid(unsigned(a.blocks), unsigned(n_groups));
   switch (depth) {
-    case 1: hipLaunchKernelGGL((k_gemm_mu8_batch<1>), grid, dim3(1024), 0, stream, a); return true;
-    case 2: hipLaunchKernelGGL((k_gemm_mu8_batch<2>), grid, dim3(1024), 0, stream, a); return true;
-    case 3: hipLaunchKernelGGL((k_gemm_mu8_batch<3>), grid, dim3(1024), 0, stream, a); return true;
+    case 1: hipLaunchKernelGGL((k_gemm_mu8_batch<1, NB>), grid, dim3(1024), 0, stream, a); return true;
+    case 2: hipLaunchKernelGGL((k_gemm_mu8_batch<2, NB>), grid, dim3(1024), 0, stream, a); return true;
+    case 3: hipLaunchKernelGGL((k_gemm_mu8_batch<3, NB>), grid, dim3(1024), 0, stream, a); return true;
   }
+  return false;
+}
+
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, hipStream_t stream) {
+  if (n_groups < 1 || n_groups > 4) return false;
+  if (nb == 2) return n_groups == 1 && launch_batch_nb<2>(a, n_groups, depth, stream);
+  if (nb == 4) return launch_batch_nb<4>(a, n_groups, depth, stream);
   return false;
 }
 

@@ -179,11 +179,12 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (per_cu < 1 || per_cu > 8) per_cu = 3;   // three 256-thread workgroups per CU (the kernel's occupancy)
   } else if (L.shape.mu == 8 && B >= 2 && !force_generic) {
     // small batch: 1024-row tiles, one super-chunk per unit (the batch-1 sign stream), batch in groups of four rows
+    // (two for B = 2: half the table entries and lookup additions of a padded group of four)
     p->kernel = 2;
     p->nt = 1024;
     const int depth_env = env_int("FLUXBIN_DEPTH", 1);
     p->depth = (depth_env == 2 || depth_env == 3) ? depth_env : 1;
-    p->bg = 4;
+    p->bg = B == 2 ? 2 : 4;
     p->n_groups = B <= 4 ? 1 : (B <= 8 ? 2 : 4);
     if (per_cu < 1 || per_cu > 8) per_cu = 1;
   } else {
