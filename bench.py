@@ -483,7 +483,7 @@ def main():
                     help="counter-collection mode: launch each layer this many times without graphs, then exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is design-only (DESIGN.md)",
+        print(json.dumps({"error": "the library runs on one GPU; sharding the path over several GPUs is not implemented",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch

@@ -13,7 +13,7 @@ Paper: FluxBin (arXiv 2608.15602). Equation numbers are the paper's:
   (14) LUT-BSF: LUT[p] = sum_n (x_sub[n] alpha_c,sub[n]) (2 b_n(p) - 1) (Sec. 3.2, Def. LUT-BSF);
   (15) LUT reading with row scales, for the global and the VCM salient term (Sec. 3.2).
 
-Readings where the paper is silent or ambiguous (each is also listed in the design doc):
+Readings where the paper is silent or ambiguous:
   * bit n of a pattern p (n = 0..mu-1) belongs to the n-th element of the sub-vector (LSB first); a set bit is +1;
   * row scales: one per (row, group of g_r consecutive columns); salient row scales: one per (row, group of g_s
     consecutive VCM dense columns);

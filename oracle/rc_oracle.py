@@ -17,7 +17,7 @@ What it follows (FluxBin, arXiv 2608.15602):
     hybrid procedure (App. algorithm "FluxBin-Hybrid"): per block of g columns saliency search, global bases, salient
     refinement of the residual on the salient columns.
 
-Readings where the paper is silent (each is also listed in the design doc):
+Readings where the paper is silent:
   * greedy initialization of base k from the residual R: B = sign(R) on the mask (sign(0) = +1), 0 off it; the column
     scale starts at 1, then the row scale and the column scale take one least-squares update each (Prop. 3.2, in that
     order); R loses the base's contribution;
