@@ -152,15 +152,21 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     const int early_env = env_int("FLUXBIN_EARLY", -1);
     const int64_t sign_bytes = int64_t(L.NSC) * 2 * L.Mp * 16;
     p->early = early_env >= 0 ? early_env != 0 : sign_bytes <= (int64_t(32) << 20);
-    // 1024-thread workgroups, one per CU, amortize each table over the most rows and keep the fewest, longest
-    // pipelines; layers with fewer than one 1024-row unit per CU use smaller workgroups (more, shorter units).
+    // mu = 8: 1024-thread workgroups, one per CU, amortize each table over the most rows and keep the fewest,
+    // longest pipelines, which pays once a layer has at least four 1024-row units per CU (the 70B MLP layers: 0.5 us
+    // faster than 512 threads). Below that, 512-thread workgroups (up to two per CU) keep more CUs busy: measured
+    // 11008x4096 10.2 -> 8.7 us (121 -> 242 workgroups of three units), 4096x11008 10.9 -> 9.4, 8192x8192 with two
+    // bases 11.5 -> 11.1, 10240x8192 with three bases 13.6 -> 13.1; 256 threads were slower on every layer measured
+    // (1024x8192: 9.8 us against 8.4 at 512).
     // mu = 4 does twice the lookups per row and column of mu = 8; there two 512-thread workgroups per CU, each
     // covering the other's barriers, measured 2 to 2.5 us faster than one 1024-thread workgroup on the 8192- and
-    // 28672-row MLP layers: 512 threads at most.
+    // 28672-row MLP layers: 512 threads at most, fewer for layers with fewer than one unit per CU.
     if (nt_env == 256 || nt_env == 512 || nt_env == 1024) {
       p->nt = nt_env;
+    } else if (L.shape.mu == 8) {
+      p->nt = ceil_div(L.shape.M, 1024) * L.NSC >= 4 * int64_t(cus) ? 1024 : 512;
     } else {
-      p->nt = L.shape.mu == 4 ? 512 : 1024;
+      p->nt = 512;
       while (p->nt > 256 && ceil_div(L.shape.M, p->nt) * L.NSC < cus) p->nt /= 2;
     }
     if (per_cu < 1 || per_cu > 8) per_cu = 1024 / p->nt;
@@ -229,8 +235,11 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     return fail(FLUXBIN_ERR_UNSUPPORTED, "layer too large for one launch (%lld work units)", (long long)p->units);
   p->blocks = p->units < target ? p->units : target;
   // small layers: give every workgroup at least a few units, so that its fixed start-up cost is amortized and a split
-  // tile has fewer contributors to reduce
-  const int min_units = env_int("FLUXBIN_MIN_UNITS", 3);
+  // tile has fewer contributors to reduce. Three, or two for mu = 8 where workgroups of two units still number at
+  // most one per CU (4096x4096: 8.2 -> 8.0 us, 1024x8192: 8.6 -> 8.4 us; with more workgroups than CUs some CUs
+  // would run two of them: 11008x4096 8.7 -> 9.9 us).
+  const int min_units_dflt = (L.shape.mu == 8 && ceil_div(p->units, 2) <= cus) ? 2 : 3;
+  const int min_units = env_int("FLUXBIN_MIN_UNITS", min_units_dflt);
   if (min_units > 1 && p->kernel == 0 && p->blocks > 1 && ceil_div(p->units, p->blocks) < min_units)
     p->blocks = ceil_div(p->units, int64_t(min_units)) > 0 ? ceil_div(p->units, int64_t(min_units)) : 1;
   // the batch-1 kernel stages the folded activations of all its units at once: at most b1_max_units(nt) per workgroup
