@@ -315,11 +315,14 @@ def small_batch_us(specs, batches, launches=40):
         for i, it in enumerate(b.items):
             s = it["spec"]
             um, ul = us_k["mfma"][i], us_k["lut"][i]
-            us = um if B > 4 else ul   # the launch plan's choice for mu = 8
+            # the launch plan's choice for mu = 8: matrix cores above B = 4, and at every B on layers with fewer than
+            # four 1024-row units per CU
+            small = -(-s.M // 1024) * it["packs"][0].layer.NSC < 4 * torch.cuda.get_device_properties(0).multi_processor_count
+            us = um if (B > 4 or small) else ul
             out[f"{s.name}_B{B}"] = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
                                      "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
                                      "matrix_core_kernel_us": round(um, 3), "lut_batch_kernel_us": round(ul, 3),
-                                     "default_kernel": "matrix cores" if B > 4 else "LUT batch"}
+                                     "default_kernel": "matrix cores" if (B > 4 or small) else "LUT batch"}
         del b
         torch.cuda.empty_cache()
     return out
@@ -471,7 +474,7 @@ def main():
     ap.add_argument("--g-r", choices=["128", "N"], default="128")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 and small-batch per-call figures")
+    ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 and small-batch per-call figures (70B and 7B MLP layers)")
     ap.add_argument("--no-decoder", action="store_true", help="skip the 70B decoder-layer graph figures")
     ap.add_argument("--no-variants", action="store_true", help="skip the kernel-variant figures (mu 4, pure global)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -556,6 +559,7 @@ def main():
         out["config"]["attn_4096x4096_us_per_gemv"] = round(us, 3)
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
         out["config"]["small_batch"] = small_batch_us(specs, (2, 4, 8, 16))
+        out["config"]["small_batch_mlp7b"] = small_batch_us(config_layers("c3_mlp7b", args.g_r), (2, 4, 8))
     if not args.no_decoder:
         out["config"]["decoder_layer_70b"] = decoder_layer_us(args.g_r)
     if not args.no_variants:

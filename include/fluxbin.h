@@ -169,6 +169,9 @@ fluxbin_status fluxbin_layer_from_header(const void* header_host, void* d_packed
  * Workspace for split reductions of one GEMV/GEMM call with batch B (1..16): partial sums of output rows and one
  * 32-bit counter per row tile. Before its first use the workspace must be zero-filled (fluxbin_workspace_init); every
  * call leaves the counters at zero again. Calls sharing a workspace must not overlap in time.
+ * The counters sit in a region of the same size for every batch size of a layer, so calls of one layer with any
+ * B may share one workspace (of the size queried for the largest B). A workspace used for another layer must first
+ * be zero-filled again: the other layer's partial sums may cover this layer's counters.
  */
 fluxbin_status fluxbin_workspace_query(const fluxbin_layer* layer, int32_t B, size_t* bytes);
 fluxbin_status fluxbin_workspace_init(void* d_workspace, size_t bytes, hipStream_t stream);

@@ -124,13 +124,20 @@ static int env_int(const char* name, int dflt) {
 
 // Small-batch kernel choice. The matrix-core kernel's cost per sign bit (decode) is the same for every B <= 16; the mu = 8
 // LUT batch kernel's table work grows with B. Measured on the 70B MLP layers (us per call, matrix cores / LUT):
-// B = 2: 54 / 44-49, B = 4: 55 / 45-50, B = 8: 58-68 / 83-91, B = 16: 73-96 / 162-172. So mu = 8 uses the LUT kernel up
-// to B = 4 and the matrix cores above; mu = 4 (whose LUT path for B >= 2 is the generic kernel) always the matrix cores.
-// FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
-static bool use_mfma(const fluxbin_layer& L, int B) {
+// B = 2: 52 / 38-40, B = 4: 52 / 45-50, B = 8: 55-60 / 84-92, B = 16: 63-79 / 162-174. So mu = 8 uses the LUT kernel up
+// to B = 4 and the matrix cores above, on layers with at least four 1024-row units per CU. Smaller layers leave the
+// LUT batch kernel's 1024-row workgroups too few to fill the chip, and there the matrix cores (256-row tiles) win at
+// every B (7B MLP layers, B = 2: 17.2 / 17.7 and 18.9 / 19.1; B = 4: 18.9 / 22.6 and 19.6 / 26.3). mu = 4 (whose LUT
+// path for B >= 2 is the generic kernel) always uses the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and
+// measurements).
+static bool use_mfma(const fluxbin_layer& L, int B, int cus) {
   const int forced = env_int("FLUXBIN_MFMA", -1);
   if (forced == 0 || forced == 1) return forced == 1;
-  return L.shape.mu == 4 || B > 4;
+  return L.shape.mu == 4 || B > 4 || ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
+}
+
+static uint64_t layer_counter_bytes(int64_t M) {
+  return round_up256(uint64_t(ceil_div(M, 256) + 4) * uint64_t(kCounterStride) * 4u);
 }
 
 fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
@@ -172,7 +179,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (per_cu < 1 || per_cu > 8) per_cu = 1024 / p->nt;
     p->bg = 1;
     p->n_groups = 1;
-  } else if (B >= 2 && !force_generic && use_mfma(L, B)) {
+  } else if (B >= 2 && !force_generic && use_mfma(L, B, cus)) {
     // small batch on the matrix cores: the sign decode per bit is shared by all batch rows (B <= 16 fit one MFMA tile)
     p->kernel = 3;
     p->nt = 256;
@@ -250,7 +257,14 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   p->ws_counters_off = 0;
   // the small-batch kernel runs one row of workgroups per group of four batch rows, each with its own counters
   const uint64_t counter_sets = p->kernel == 2 ? uint64_t(p->n_groups) : 1u;
-  p->ws_partials_off = counter_sets * round_up256(uint64_t(p->n_tiles) * uint64_t(kCounterStride) * 4u);
+  const uint64_t counter_bytes = counter_sets * round_up256(uint64_t(p->n_tiles) * uint64_t(kCounterStride) * 4u);
+  // The counter region is the same for every launch plan of the layer: room for ceil(M/256) + 4 tile counters (the
+  // most any plan uses: 256-row tiles, or four sets of 1024-row tiles). So no plan's partial sums overlap another
+  // plan's counters, and calls of one layer with any batch size can share a workspace.
+  p->ws_partials_off = layer_counter_bytes(L.shape.M);
+  if (counter_bytes > p->ws_partials_off)
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "launch plan needs %llu bytes of tile counters, the layer's region holds %llu",
+                (unsigned long long)counter_bytes, (unsigned long long)p->ws_partials_off);
   p->ws_bytes = p->ws_partials_off + uint64_t(p->blocks) * 2u * uint64_t(p->rows) * uint64_t(p->bpad) * 4u;
   return FLUXBIN_OK;
 }

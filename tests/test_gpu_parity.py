@@ -417,3 +417,29 @@ def test_graph_replays_match_eager():
                 assert torch.equal(y, y_eager), (spec.name, B, r)
                 fb.fluxbin_lut_gemv(packed, x[0], out_fp32=True, workspace=ws)   # eager work between replays
                 torch.cuda.synchronize()
+
+
+def test_workspace_shared_by_batch_sizes():
+    """One workspace (the largest size queried) serves calls of one layer at every batch size and on every kernel, in
+    any order: the tile counters of every launch plan lie in one region that no plan's partial sums cover, so each
+    result equals the result on a fresh workspace."""
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    log("case workspace shared by batch sizes")
+    spec = LayerSpec("wsshare", M=3000, N=2048, Kb=2, Ks=1, mu=8, S=70, g_r=128, g_s=70, seed=33)
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    runs = [(1, {}), (3, {}), (2, {"FLUXBIN_MFMA": "0"}), (16, {}), (5, {"FLUXBIN_GENERIC": "1"}),
+            (4, {"FLUXBIN_MFMA": "0"}), (1, {"FLUXBIN_NT": "1024"}), (8, {"FLUXBIN_MFMA": "0"})]
+    n = max(_with_env(env, lambda: fb.fluxbin_workspace_query(packed, B)) for B, env in runs)
+    shared = torch.empty((n + 255) // 256 * 256, dtype=torch.uint8, device="cuda")
+    fb.fluxbin_workspace_init(shared)
+    xs = {B: make_activations(L, B) for B, _ in runs}
+    fresh = {i: _with_env(env, lambda: run_gemm(packed, xs[B], out_fp32=True, ws=fb.make_workspace(packed, B)))
+             for i, (B, env) in enumerate(runs)}
+    _check(fresh[1], oracle.gemv_dense(L, xs[3]), "B = 3 on a fresh workspace")
+    for order in (runs, runs[::-1]):
+        for B, env in order:
+            i = runs.index((B, env))
+            y = _with_env(env, lambda: run_gemm(packed, xs[B], out_fp32=True, ws=shared))
+            assert np.array_equal(y, fresh[i]), (B, env)
