@@ -218,8 +218,13 @@ __device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
 // batch rows and depth units of sign data requested ahead; false if no instance exists.
 bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, hipStream_t stream);
 
+// Split tiles of a launch whose kernel stored every contributor's partial sums and skipped the tile counters, reduced
+// by a second kernel over the whole chip (fluxbin_gemv.hip): bp padded batch rows, R rows per tile (a multiple of 256).
+void launch_reduce_split(const GemmArgs& a, int bp, int R, hipStream_t stream);
+
 // Matrix-core small-batch kernel (fluxbin_gemm_mfma.hip): 256-row tiles, partial sums padded to bpad (4, 8 or 16)
-// batch rows, data requested depth (2 or 3) units ahead; false if no instance exists.
-bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, hipStream_t stream);
+// batch rows, data requested depth (2 or 3) units ahead; with reduce2 (depth 2) the split tiles are reduced by a
+// second kernel instead of the tile counters; false if no instance exists.
+bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, bool reduce2, hipStream_t stream);
 
 }  // namespace fluxbin

@@ -308,7 +308,7 @@ struct MfKernel {
   }
 };
 
-template <int BP, int MU, int D>
+template <int BP, int MU, int D, bool R2>
 __global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
   using K = MfKernel<BP, MU, D>;
   __shared__ __attribute__((aligned(16))) uint32_t sx[2 * kMfXUnit];
@@ -388,36 +388,47 @@ __global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
   mf_stage_write<BP>(a, ur[0], sx, sa, ln.t);
   __syncthreads();
   K::template step<0>(a, s, ur, meta_next, s_planes, sx, sa, scr, ln, xrow);
-  const int pend0 = s.first_shared ? s.first_tile : s.last_tile;
-  publish_pending<kMfNT, 1, BP>(a, pend0, s.last_tile, s.n_pending, &s_flag);
+  if constexpr (!R2) {
+    const int pend0 = s.first_shared ? s.first_tile : s.last_tile;
+    publish_pending<kMfNT, 1, BP>(a, pend0, s.last_tile, s.n_pending, &s_flag);
+  }
 }
 
-template <int BP, int D>
+template <int BP, int D, bool R2>
 bool launch_mfma_bp(const GemmArgs& a, int mu, hipStream_t stream) {
   const dim3 grid(unsigned(a.blocks)), block(kMfNT);
   if (mu == 8)
-    hipLaunchKernelGGL((k_gemm_mfma<BP, 8, D>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((k_gemm_mfma<BP, 8, D, R2>), grid, block, 0, stream, a);
   else if (mu == 4)
-    hipLaunchKernelGGL((k_gemm_mfma<BP, 4, D>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((k_gemm_mfma<BP, 4, D, R2>), grid, block, 0, stream, a);
   else
     return false;
+  if constexpr (R2) launch_reduce_split(a, BP, kMfR, stream);
   return true;
 }
 
 }  // namespace
 
-bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, hipStream_t stream) {
+bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, bool reduce2, hipStream_t stream) {
+  if (reduce2 && depth == 2) {   // split tiles reduced by a second kernel (depth 2 only)
+    switch (bpad) {
+      case 4: return launch_mfma_bp<4, 2, true>(a, mu, stream);
+      case 8: return launch_mfma_bp<8, 2, true>(a, mu, stream);
+      case 16: return launch_mfma_bp<16, 2, true>(a, mu, stream);
+    }
+    return false;
+  }
   // 16 batch rows hold 16 more registers per unit in flight: two units ahead (three would spill)
   if (depth == 3 && bpad != 16) {
     switch (bpad) {
-      case 4: return launch_mfma_bp<4, 3>(a, mu, stream);
-      case 8: return launch_mfma_bp<8, 3>(a, mu, stream);
+      case 4: return launch_mfma_bp<4, 3, false>(a, mu, stream);
+      case 8: return launch_mfma_bp<8, 3, false>(a, mu, stream);
     }
   } else if (depth == 2 || depth == 3) {
     switch (bpad) {
-      case 4: return launch_mfma_bp<4, 2>(a, mu, stream);
-      case 8: return launch_mfma_bp<8, 2>(a, mu, stream);
-      case 16: return launch_mfma_bp<16, 2>(a, mu, stream);
+      case 4: return launch_mfma_bp<4, 2, false>(a, mu, stream);
+      case 8: return launch_mfma_bp<8, 2, false>(a, mu, stream);
+      case 16: return launch_mfma_bp<16, 2, false>(a, mu, stream);
     }
   }
   return false;

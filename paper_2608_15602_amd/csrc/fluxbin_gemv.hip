@@ -574,6 +574,45 @@ __global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
   publish_pending<NT, RPT, 1>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
 
+// Split tiles reduced by a second kernel over the whole chip, after a kernel that stored every contributor's partial
+// sums and left the tile counters alone (the matrix-core small-batch kernel): one 256-thread workgroup per (split
+// tile, padded batch row, 256 rows), one thread per row and batch row. The contributors' partial sums are added in
+// workgroup order from +0, the order (hence the bits) of the counter protocol's reducer. With several batch rows a
+// tile's partial sums are tens to hundreds of KB, which the counter protocol's one reducing workgroup reads through a
+// single CU in dependent rounds; here they are read by all CUs at once. (For batch 1 the gap between the two kernels
+// costs more than the counter protocol's reduction: measured 1.3-1.5 us slower on 4096- to 11008-row layers.)
+__global__ void __launch_bounds__(256) k_reduce_split(GemmArgs a, int bp, int R) {
+  constexpr int CH = 16;
+  const int q = R >> 8;   // 256-row parts of a tile
+  const int per_tile = bp * q;
+  const int tile = int(blockIdx.x) / per_tile;
+  const int rem = int(blockIdx.x) - tile * per_tile;
+  const int b = rem / q;
+  if (b >= a.B || !tile_is_shared(a, tile)) return;   // unshared tiles were stored by their owner
+  const int r = (rem - b * q) * 256 + int(threadIdx.x);
+  const int b_first = owner_of(a, tile * a.steps);
+  const int n_c = owner_of(a, (tile + 1) * a.steps - 1) - b_first + 1;
+  const bool first_in_slot1 = first_unit(a, b_first) < tile * a.steps;   // its range starts in an earlier tile
+  float sum = 0.f;
+  for (int c0 = 0; c0 < n_c; c0 += CH) {
+    float v[CH];
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const int c = c0 + k;
+      const int slot = (b_first + c) * 2 + ((c == 0 && first_in_slot1) ? 1 : 0);
+      v[k] = c < n_c ? a.partials[(int64_t(slot) * bp + b) * R + r] : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < CH; ++k) sum += v[k];
+  }
+  const int64_t row = int64_t(tile) * R + r;
+  if (row < a.M) store_y(a, b, row, sum);
+}
+
+void launch_reduce_split(const GemmArgs& a, int bp, int R, hipStream_t stream) {
+  hipLaunchKernelGGL(k_reduce_split, dim3(unsigned(a.n_tiles * bp * (R >> 8))), dim3(256), 0, stream, a, bp, R);
+}
+
 // Stream probe: the batch-1 kernel's sign and row-scale requests (same plan, cursor, ring depth and per-unit barrier)
 // without the table work; each unit's words are folded into a checksum so the loads are not removed.
 template <int NT, int D>
@@ -988,7 +1027,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   } else if (p.kernel == 2) {
     ok = launch_gemm_batch(a, p.n_groups, p.depth, p.bg, stream);
   } else if (p.kernel == 3) {
-    ok = launch_gemm_mfma(a, p.bpad, int(L.shape.mu), p.depth, stream);
+    ok = launch_gemm_mfma(a, p.bpad, int(L.shape.mu), p.depth, p.reduce2, stream);
   } else if (L.shape.mu == 8) {
     ok = launch_gen_mu<8>(a, p, stream);
   } else {

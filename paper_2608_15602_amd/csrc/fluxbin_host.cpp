@@ -122,18 +122,18 @@ static int env_int(const char* name, int dflt) {
   return std::atoi(v);
 }
 
-// Small-batch kernel choice. The matrix-core kernel's cost per sign bit (decode) is the same for every B <= 16; the mu = 8
-// LUT batch kernel's table work grows with B. Measured on the 70B MLP layers (us per call, matrix cores / LUT):
-// B = 2: 52 / 38-40, B = 4: 52 / 45-50, B = 8: 55-60 / 84-92, B = 16: 63-79 / 162-174. So mu = 8 uses the LUT kernel up
-// to B = 4 and the matrix cores above, on layers with at least four 1024-row units per CU. Smaller layers leave the
-// LUT batch kernel's 1024-row workgroups too few to fill the chip, and there the matrix cores (256-row tiles) win at
-// every B (7B MLP layers, B = 2: 17.2 / 17.7 and 18.9 / 19.1; B = 4: 18.9 / 22.6 and 19.6 / 26.3). mu = 4 (whose LUT
-// path for B >= 2 is the generic kernel) always uses the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and
-// measurements).
+// Small-batch kernel choice. The matrix-core kernel's cost per sign bit (decode) is the same for every B <= 16 (B <= 4
+// share one padded instance); the mu = 8 LUT batch kernel's table work grows with B. Measured on the 70B MLP layers (us
+// per call, up / down; matrix cores with the second-kernel reduction / LUT): B = 2: 42.6 / 43.6 against 37.5 / 39.9,
+// B = 4: 42.6 / 43.6 against 45.9 / 49.8, B = 8: 46.5 / 47.1 against 84 / 92. So mu = 8 uses the LUT kernel at B = 2
+// and the matrix cores above, on layers with at least four 1024-row units per CU. Smaller layers leave the LUT batch
+// kernel's 1024-row workgroups too few to fill the chip, and there the matrix cores (256-row tiles) win at every B (7B
+// MLP layers, B = 2: 17.2 / 18.7 against 17.7 / 19.1). mu = 4 (whose LUT path for B >= 2 is the generic kernel) always
+// uses the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
 static bool use_mfma(const fluxbin_layer& L, int B, int cus) {
   const int forced = env_int("FLUXBIN_MFMA", -1);
   if (forced == 0 || forced == 1) return forced == 1;
-  return L.shape.mu == 4 || B > 4 || ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
+  return L.shape.mu == 4 || B > 2 || ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
 }
 
 static uint64_t layer_counter_bytes(int64_t M) {
@@ -189,6 +189,10 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     p->depth = depth_env == 3 ? 3 : 2;
     p->bg = B <= 4 ? 4 : (B <= 8 ? 8 : 16);
     p->n_groups = 1;
+    // split tiles reduced by a second kernel (FLUXBIN_MFMA_R2=0: by the tile counters, as the other kernels): measured
+    // on the 70B MLP layers, up / down, 58.6 / 78.7 -> 57.2 / 59.3 us at B = 16, 48.0 / 57.7 -> 46.5 / 47.1 at B = 8,
+    // 45.5 / 48.8 -> 42.6 / 43.6 at B = 4; 7B MLP layers 18.8 / 19.0 -> 15.1 / 17.1 at B = 4
+    p->reduce2 = p->depth == 2 && env_int("FLUXBIN_MFMA_R2", 1) != 0;
     if (per_cu < 1 || per_cu > 8) per_cu = 3;   // three 256-thread workgroups per CU (the kernel's occupancy)
   } else if (L.shape.mu == 8 && B >= 2 && !force_generic) {
     // small batch: 1024-row tiles, one super-chunk per unit (the batch-1 sign stream), batch in groups of four rows

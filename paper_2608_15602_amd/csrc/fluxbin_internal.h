@@ -97,6 +97,7 @@ struct Plan {
   int bpad;         // bg * n_groups
   int depth;        // units of sign data requested ahead of the one looked up
   bool early;       // batch-1 kernel: request sign data before staging the activations (small layers)
+  bool reduce2;     // matrix-core kernel: split tiles reduced by a second kernel over the whole chip
   uint64_t ws_counters_off, ws_partials_off, ws_bytes;
 };
 
