@@ -306,7 +306,7 @@ __device__ __forceinline__ void bat_units(const GemmArgs& a, BatState<NB>& st, B
   }
 }
 
-template <int D, int NB>
+template <int D, int NB, bool R2>
 __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   __shared__ __attribute__((aligned(16))) float tbl[2 * Bat::TBL];   // 128 KB: buffer 0 chunk 0, buffer 1 chunk 1
   __shared__ __attribute__((aligned(16))) float xs[2 * Bat::XS];      // staged activations, two units
@@ -418,25 +418,33 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   bat_build<NB>(tbl, xs);   // unit 0, chunk 0
   __syncthreads();
   bat_units<D, 0, NB>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
-  const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
-  publish_pending<1024, 1, NB>(a, pend0, st.last_tile, st.n_pending, &s_flag);
+  if constexpr (!R2) {   // else the split tiles are reduced by k_reduce_split after this kernel
+    const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
+    publish_pending<1024, 1, NB>(a, pend0, st.last_tile, st.n_pending, &s_flag);
+  }
 }
 
 template <int NB>
-static bool launch_batch_nb(const GemmArgs& a, int n_groups, int depth, hipStream_t stream) {
+static bool launch_batch_nb(const GemmArgs& a, int n_groups, int depth, bool reduce2, hipStream_t stream) {
   const dim3 grid(unsigned(a.blocks), unsigned(n_groups));
+  if (reduce2) {   // one batch group, depth 1 (launch plan): the partial sums are laid out as k_reduce_split reads them
+    if (n_groups != 1 || depth != 1) return false;
+    hipLaunchKernelGGL((k_gemm_mu8_batch<1, NB, true>), grid, dim3(1024), 0, stream, a);
+    launch_reduce_split(a, NB, 1024, stream);
+    return true;
+  }
   switch (depth) {
-    case 1: hipLaunchKernelGGL((k_gemm_mu8_batch<1, NB>), grid, dim3(1024), 0, stream, a); return true;
-    case 2: hipLaunchKernelGGL((k_gemm_mu8_batch<2, NB>), grid, dim3(1024), 0, stream, a); return true;
-    case 3: hipLaunchKernelGGL((k_gemm_mu8_batch<3, NB>), grid, dim3(1024), 0, stream, a); return true;
+    case 1: hipLaunchKernelGGL((k_gemm_mu8_batch<1, NB, false>), grid, dim3(1024), 0, stream, a); return true;
+    case 2: hipLaunchKernelGGL((k_gemm_mu8_batch<2, NB, false>), grid, dim3(1024), 0, stream, a); return true;
+    case 3: hipLaunchKernelGGL((k_gemm_mu8_batch<3, NB, false>), grid, dim3(1024), 0, stream, a); return true;
   }
   return false;
 }
 
-bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, hipStream_t stream) {
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, bool reduce2, hipStream_t stream) {
   if (n_groups < 1 || n_groups > 4) return false;
-  if (nb == 2) return n_groups == 1 && launch_batch_nb<2>(a, n_groups, depth, stream);
-  if (nb == 4) return launch_batch_nb<4>(a, n_groups, depth, stream);
+  if (nb == 2) return n_groups == 1 && launch_batch_nb<2>(a, n_groups, depth, reduce2, stream);
+  if (nb == 4) return launch_batch_nb<4>(a, n_groups, depth, reduce2, stream);
   return false;
 }
 

@@ -1025,7 +1025,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
       default: ok = false;
     }
   } else if (p.kernel == 2) {
-    ok = launch_gemm_batch(a, p.n_groups, p.depth, p.bg, stream);
+    ok = launch_gemm_batch(a, p.n_groups, p.depth, p.bg, p.reduce2, stream);
   } else if (p.kernel == 3) {
     ok = launch_gemm_mfma(a, p.bpad, int(L.shape.mu), p.depth, p.reduce2, stream);
   } else if (L.shape.mu == 8) {

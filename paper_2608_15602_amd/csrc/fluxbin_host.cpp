@@ -122,18 +122,19 @@ static int env_int(const char* name, int dflt) {
   return std::atoi(v);
 }
 
-// Small-batch kernel choice. The matrix-core kernel's cost per sign bit (decode) is the same for every B <= 16 (B <= 4
-// share one padded instance); the mu = 8 LUT batch kernel's table work grows with B. Measured on the 70B MLP layers (us
-// per call, up / down; matrix cores with the second-kernel reduction / LUT): B = 2: 42.6 / 43.6 against 37.5 / 39.9,
-// B = 4: 42.6 / 43.6 against 45.9 / 49.8, B = 8: 46.5 / 47.1 against 84 / 92. So mu = 8 uses the LUT kernel at B = 2
-// and the matrix cores above, on layers with at least four 1024-row units per CU. Smaller layers leave the LUT batch
-// kernel's 1024-row workgroups too few to fill the chip, and there the matrix cores (256-row tiles) win at every B (7B
-// MLP layers, B = 2: 17.2 / 18.7 against 17.7 / 19.1). mu = 4 (whose LUT path for B >= 2 is the generic kernel) always
-// uses the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
+// Small-batch kernel choice (both kernels reduce split tiles with the second kernel). The matrix-core kernel's cost per
+// sign bit (decode) is the same for every B <= 16 (B <= 4 share one padded instance); the mu = 8 LUT batch kernel's
+// table work grows with B. Measured (us per call, up / down, LUT batch / matrix cores): 70B MLP layers B = 2 32.9 / 34.5
+// against 53.4 / 46.4, B = 4 42.1 / 42.4 against 51.9 / 48.0, B = 8 84.6 / 91.5 against 55.0 / 51.3; 7B MLP layers
+// (fewer than four 1024-row units per CU, where the LUT batch kernel's 1024-row workgroups do not fill the chip)
+// B = 2 14.4 / 17.4 against 15.3 / 17.8, B = 4 16.3 / 18.9 against 16.0 / 18.4. So mu = 8 uses the LUT batch kernel up
+// to B = 4 on large layers and at B = 2 on small ones, the matrix cores otherwise; mu = 4 (whose LUT path for B >= 2
+// is the generic kernel) always the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
 static bool use_mfma(const fluxbin_layer& L, int B, int cus) {
   const int forced = env_int("FLUXBIN_MFMA", -1);
   if (forced == 0 || forced == 1) return forced == 1;
-  return L.shape.mu == 4 || B > 2 || ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
+  const bool small = ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
+  return L.shape.mu == 4 || B > 4 || (B > 2 && small);
 }
 
 static uint64_t layer_counter_bytes(int64_t M) {
@@ -203,6 +204,9 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     p->depth = (depth_env == 2 || depth_env == 3) ? depth_env : 1;
     p->bg = B == 2 ? 2 : 4;
     p->n_groups = B <= 4 ? 1 : (B <= 8 ? 2 : 4);
+    // one batch group: split tiles reduced by a second kernel (FLUXBIN_BAT_R2=0: by the tile counters). Measured on the
+    // 70B MLP layers, up / down: B = 2 37.6 / 40.6 -> 33.8 / 35.0 us, B = 4 46.0 / 50.2 -> 40.3 / 41.7 us
+    p->reduce2 = p->n_groups == 1 && p->depth == 1 && env_int("FLUXBIN_BAT_R2", 1) != 0;
     if (per_cu < 1 || per_cu > 8) per_cu = 1;
   } else {
     p->kernel = 1;

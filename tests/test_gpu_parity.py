@@ -465,3 +465,21 @@ def test_mfma_second_kernel_reduction_equals_counters(B, mu):
     assert np.array_equal(y_r, y_c), int(np.sum(y_r != y_c))
     _check(y_r, oracle.gemv_dense(L, x), "second-kernel reduction vs oracle")
 
+
+
+@pytest.mark.parametrize("B", [2, 3, 4])
+def test_lut_batch_second_kernel_reduction_equals_counters(B):
+    """The LUT batch kernel's split tiles reduced by the second kernel give the counter protocol's y bit for bit, on a
+    layer whose 1024-row tiles have about a hundred contributors each, and match the oracle."""
+    from paper_2608_15602_amd import fluxbin as fb
+    spec = LayerSpec("batr2", M=3000, N=8192, Kb=3, Ks=1, mu=8, S=100, g_r=128, g_s=100, seed=35)
+    log(f"case LUT batch second-kernel reduction B={B}")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    x = make_activations(L, B)
+    y = {}
+    for r2 in ("0", "1"):
+        y[r2] = _with_env({"FLUXBIN_MFMA": "0", "FLUXBIN_BAT_R2": r2},
+                          lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
+    assert np.array_equal(y["1"], y["0"]), int(np.sum(y["1"] != y["0"]))
+    _check(y["1"], oracle.gemv_dense(L, x), "LUT batch second-kernel reduction vs oracle")
