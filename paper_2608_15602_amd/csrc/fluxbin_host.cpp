@@ -262,6 +262,14 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     p->blocks = ceil_div(p->units, int64_t(b1_max_units(p->nt)));
   if (p->kernel == 2 && ceil_div(p->units, p->blocks) > kBatMaxUnits) p->blocks = ceil_div(p->units, kBatMaxUnits);
   if (p->kernel == 3 && ceil_div(p->units, p->blocks) > kMfMaxUnits) p->blocks = ceil_div(p->units, kMfMaxUnits);
+  // More workgroups than the chip holds at once (the caps above on large layers): whole waves of workgroups, each with
+  // fewer units, instead of one full wave and a small second one that leaves most CUs idle (57344x8192 with 2 bases at
+  // B = 4: 304 one-per-CU workgroups of 12 units -> 512 of 7.1).
+  const int64_t resident = int64_t(cus) * per_cu;
+  if (p->kernel != 1 && blocks_env <= 0 && p->blocks > resident) {
+    const int64_t whole = ceil_div(p->blocks, resident) * resident;
+    p->blocks = whole < p->units ? whole : p->units;
+  }
   p->ws_counters_off = 0;
   // the small-batch kernel runs one row of workgroups per group of four batch rows, each with its own counters
   const uint64_t counter_sets = p->kernel == 2 ? uint64_t(p->n_groups) : 1u;
