@@ -190,7 +190,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     p->depth = depth_env == 3 ? 3 : 2;
     p->bg = B <= 4 ? 4 : (B <= 8 ? 8 : 16);
     p->n_groups = 1;
-    // split tiles reduced by a second kernel (FLUXBIN_MFMA_R2=0: by the tile counters, as the other kernels): measured
+    // split tiles reduced by a second kernel (FLUXBIN_MFMA_R2=0: by the tile counters, as at batch 1): measured
     // on the 70B MLP layers, up / down, 58.6 / 78.7 -> 57.2 / 59.3 us at B = 16, 48.0 / 57.7 -> 46.5 / 47.1 at B = 8,
     // 45.5 / 48.8 -> 42.6 / 43.6 at B = 4; 7B MLP layers 18.8 / 19.0 -> 15.1 / 17.1 at B = 4
     p->reduce2 = p->depth == 2 && env_int("FLUXBIN_MFMA_R2", 1) != 0;
