@@ -23,6 +23,13 @@
  *   - Every call validates its arguments on the host before any launch and returns a status; on failure nothing is
  *     launched and fluxbin_last_error_message() (thread-local) describes the problem.
  *   - Results are deterministic: the same inputs on the same device give bitwise identical outputs (no float atomics).
+ *     The split of the work over workgroups (the launch plan), and with it the fp32 summation order, depends on the
+ *     device's CU count and on these tuning variables, read at every call (for tests and measurements; unset by
+ *     default): FLUXBIN_NT (batch-1 workgroup size 256/512/1024), FLUXBIN_MIN_UNITS, FLUXBIN_BLOCKS,
+ *     FLUXBIN_BLOCKS_PER_CU, FLUXBIN_DEPTH / FLUXBIN_MFMA_DEPTH (units of data in flight), FLUXBIN_EARLY (batch-1
+ *     request order), FLUXBIN_RPT, FLUXBIN_MFMA=0/1 (small-batch kernel choice), FLUXBIN_GENERIC=1 (generic kernel),
+ *     FLUXBIN_MFMA_R2=0 / FLUXBIN_BAT_R2=0 (small-batch split tiles reduced by tile counters instead of a second
+ *     kernel). Any plan gives the same product up to fp32 summation order.
  *   - Calls that share a workspace must not overlap in time (same stream, or ordered by the caller).
  */
 #ifndef FLUXBIN_H_
