@@ -250,10 +250,10 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     return fail(FLUXBIN_ERR_UNSUPPORTED, "layer too large for one launch (%lld work units)", (long long)p->units);
   p->blocks = p->units < target ? p->units : target;
   // small layers: give every workgroup at least a few units, so that its fixed start-up cost is amortized and a split
-  // tile has fewer contributors to reduce. Three, or two for mu = 8 where workgroups of two units still number at
-  // most one per CU (4096x4096: 8.2 -> 8.0 us, 1024x8192: 8.6 -> 8.4 us; with more workgroups than CUs some CUs
-  // would run two of them: 11008x4096 8.7 -> 9.9 us).
-  const int min_units_dflt = (L.shape.mu == 8 && ceil_div(p->units, 2) <= cus) ? 2 : 3;
+  // tile has fewer contributors to reduce. Three, or two where workgroups of two units still number at most one per
+  // CU (4096x4096: 8.2 -> 8.0 us at mu = 8, 8.5 -> 8.2 us at mu = 4; 1024x8192: 8.6 -> 8.4 us; with more workgroups
+  // than CUs some CUs would run two of them: 11008x4096 8.7 -> 9.9 us).
+  const int min_units_dflt = ceil_div(p->units, 2) <= cus ? 2 : 3;
   const int min_units = env_int("FLUXBIN_MIN_UNITS", min_units_dflt);
   if (min_units > 1 && p->kernel == 0 && p->blocks > 1 && ceil_div(p->units, p->blocks) < min_units)
     p->blocks = ceil_div(p->units, int64_t(min_units)) > 0 ? ceil_div(p->units, int64_t(min_units)) : 1;
