@@ -304,25 +304,19 @@ def small_batch_us(specs, batches, launches=40):
     for B in batches:
         b = Bench(specs, B, COPIES_BYTES_PER_LAYER * len(specs))
         us_k = {}
-        for kern, flag in (("mfma", "1"), ("lut", "0")):
-            os.environ["FLUXBIN_MFMA"] = flag
-            try:
+        for kern, flag in (("mfma", 1), ("lut", 0), ("default", None)):
+            with b.fb.tuning(**({} if flag is None else {"mfma": flag})):
                 for it in b.items:
                     it["ws"] = b.fb.make_workspace(it["packs"][0], B)
                 us_k[kern] = b.per_launch_us(launches, 3)
-            finally:
-                os.environ.pop("FLUXBIN_MFMA", None)
         for i, it in enumerate(b.items):
             s = it["spec"]
-            um, ul = us_k["mfma"][i], us_k["lut"][i]
-            # the launch plan's choice for mu = 8: matrix cores above B = 4, and above B = 2 on layers with fewer than
-            # four 1024-row units per CU
-            small = -(-s.M // 1024) * it["packs"][0].layer.NSC < 4 * torch.cuda.get_device_properties(0).multi_processor_count
-            us = um if (B > 4 or (B > 2 and small)) else ul
+            um, ul, us = us_k["mfma"][i], us_k["lut"][i], us_k["default"][i]
+            plan = b.fb.fluxbin_plan_query(it["packs"][0], B)   # the launch plan's own choice (no forcing)
             out[f"{s.name}_B{B}"] = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
                                      "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
                                      "matrix_core_kernel_us": round(um, 3), "lut_batch_kernel_us": round(ul, 3),
-                                     "default_kernel": "matrix cores" if (B > 4 or (B > 2 and small)) else "LUT batch"}
+                                     "default_kernel": plan["kernel_name"]}
         del b
         torch.cuda.empty_cache()
     return out

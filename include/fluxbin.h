@@ -24,12 +24,10 @@
  *     launched and fluxbin_last_error_message() (thread-local) describes the problem.
  *   - Results are deterministic: the same inputs on the same device give bitwise identical outputs (no float atomics).
  *     The split of the work over workgroups (the launch plan), and with it the fp32 summation order, depends on the
- *     device's CU count and on these tuning variables, read at every call (for tests and measurements; unset by
- *     default): FLUXBIN_NT (batch-1 workgroup size 256/512/1024), FLUXBIN_MIN_UNITS, FLUXBIN_BLOCKS,
- *     FLUXBIN_BLOCKS_PER_CU, FLUXBIN_DEPTH / FLUXBIN_MFMA_DEPTH (units of data in flight), FLUXBIN_EARLY (batch-1
- *     request order), FLUXBIN_RPT, FLUXBIN_MFMA=0/1 (small-batch kernel choice), FLUXBIN_GENERIC=1 (generic kernel),
- *     FLUXBIN_MFMA_R2=0 / FLUXBIN_BAT_R2=0 (small-batch split tiles reduced by tile counters instead of a second
- *     kernel). Any plan gives the same product up to fp32 summation order.
+ *     device's CU count and on the process-wide launch-plan tuning (fluxbin_tuning below: library defaults unless a
+ *     caller changes them with fluxbin_set_tuning; the FLUXBIN_* environment variables named there are read once, at
+ *     the library's first plan). Any plan gives the same product up to fp32 summation order; fluxbin_plan_query tells
+ *     which kernel and plan a call would use.
  *   - Calls that share a workspace must not overlap in time (same stream, or ordered by the caller).
  */
 #ifndef FLUXBIN_H_
@@ -204,6 +202,42 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
 fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx,
                                            void* d_y, int64_t ldy, int32_t y_is_fp32, void* d_workspace,
                                            size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Launch-plan tuning, for tests and measurements (the defaults are the library's measured choices). Process-wide: the
+ * first plan made in a process initializes it from the environment variable named after each field (unset: default);
+ * afterwards only fluxbin_set_tuning changes it (NULL restores the defaults). A plan takes one consistent copy, so
+ * a change applies to the calls made after it returns. Fields and their defaults:
+ *   nt             FLUXBIN_NT             batch-1 workgroup size 256 / 512 / 1024; 0: chosen by layer size
+ *   min_units      FLUXBIN_MIN_UNITS      batch-1 minimum units per workgroup; -1: chosen by layer size
+ *   blocks         FLUXBIN_BLOCKS         grid size target; 0: CU count times workgroups per CU
+ *   blocks_per_cu  FLUXBIN_BLOCKS_PER_CU  workgroups per CU (1..8); 0: the kernel's occupancy
+ *   depth          FLUXBIN_DEPTH          LUT kernels' units of sign data requested ahead (1..3); 0: 1
+ *   mfma_depth     FLUXBIN_MFMA_DEPTH     matrix-core kernel's units requested ahead (2 or 3); 0: 2
+ *   early          FLUXBIN_EARLY          batch-1 request order (1: signs before the activations); -1: by layer size
+ *   rpt            FLUXBIN_RPT            generic kernel rows per thread (1, 2, 4); 0: chosen by layer size
+ *   mfma           FLUXBIN_MFMA           small-batch kernel: 1 matrix cores, 0 LUT tables; -1: chosen by B and size
+ *   generic        FLUXBIN_GENERIC        1: the generic kernel for every batch size
+ *   mfma_r2        FLUXBIN_MFMA_R2        0: matrix-core split tiles reduced by tile counters, not a second kernel
+ *   bat_r2         FLUXBIN_BAT_R2         0: LUT batch kernel split tiles reduced by tile counters
+ */
+typedef struct {
+  int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2;
+} fluxbin_tuning;
+fluxbin_status fluxbin_get_tuning(fluxbin_tuning* out);
+fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
+
+/*
+ * The launch plan a GEMV/GEMM call of batch B on this layer would use on the current device with the current tuning.
+ *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel.
+ * Host only apart from reading the device's CU count; launches nothing.
+ */
+typedef struct {
+  int32_t kernel, threads, rows_per_tile, depth, batch_groups, second_kernel_reduction, early, reserved;
+  int64_t tiles, units, workgroups;
+  uint64_t workspace_bytes;
+} fluxbin_plan_info;
+fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin_plan_info* out);
 
 /*
  * Test support. fluxbin_debug_indices writes the LUT index p read for every (chunk c < NCP, row i < M, sub-vector

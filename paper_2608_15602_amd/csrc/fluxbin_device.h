@@ -181,6 +181,11 @@ __device__ __forceinline__ void reduce_tile(const GemmArgs& a, int64_t tile) {
 // its first and its last tile). Lanes 0 and 1 of the first wave bump the two counters with one instruction, so the two
 // round trips are one; a counter that reaches the number of contributors makes this workgroup the one that reduces
 // that tile.
+// Ordering (HIP's scoped memory model): every thread's partial-sum stores happen before the barrier (workgroup-scope
+// release, and a wait for all of the thread's memory operations); the counter bump is an agent-scope acquire-release
+// read-modify-write, so the stores of all threads of the workgroup are visible at agent scope to whichever workgroup
+// later reads the count they completed; the reducing workgroup's threads take an agent-scope acquire after the barrier
+// that hands them the decision, before they load the partial sums.
 template <int NT, int RPT, int BP>
 __device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0, int pending1, int n_pending,
                                                 int* s_flag) {
@@ -193,7 +198,7 @@ __device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0,
     const int tile = lane == 0 ? pending0 : pending1;
     bool last = false;
     if (lane < n_pending) {
-      const uint32_t prev = __hip_atomic_fetch_add(a.counters + int64_t(tile) * kCounterStride, 1u, __ATOMIC_RELAXED,
+      const uint32_t prev = __hip_atomic_fetch_add(a.counters + int64_t(tile) * kCounterStride, 1u, __ATOMIC_ACQ_REL,
                                                     __HIP_MEMORY_SCOPE_AGENT);
       const int bf = owner_of(a, tile * a.steps);
       const int bl = owner_of(a, (tile + 1) * a.steps - 1);
@@ -204,6 +209,8 @@ __device__ __forceinline__ void publish_pending(const GemmArgs& a, int pending0,
   }
   __syncthreads();
   const int flags = *s_flag;
+  if (flags == 0) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (flags & 1) reduce_tile<NT, RPT, BP>(a, pending0);
   if (flags & 2) reduce_tile<NT, RPT, BP>(a, pending1);
 }

@@ -31,11 +31,10 @@ fluxbin_status hip_fail(int err, const char* what) {
 
 int device_cu_count() {
   static std::mutex mu;
-  static std::vector<int> cache;
+  static int cache[64] = {};   // per device index
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
   std::lock_guard<std::mutex> lock(mu);
-  if (dev >= static_cast<int>(cache.size())) cache.resize(dev + 1, 0);
   if (cache[dev] == 0) {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return -1;
@@ -116,10 +115,59 @@ static fluxbin_status check_layer(const fluxbin_layer* L) {
   return FLUXBIN_OK;
 }
 
+// ---- launch-plan tuning: read from the FLUXBIN_* environment once per process, then only changed through
+// fluxbin_set_tuning (tests and measurements); every plan takes one consistent snapshot ----
+static fluxbin_tuning tuning_defaults() {
+  fluxbin_tuning t;
+  std::memset(&t, 0, sizeof(t));
+  t.nt = 0;
+  t.min_units = -1;
+  t.blocks = 0;
+  t.blocks_per_cu = 0;
+  t.depth = 0;
+  t.mfma_depth = 0;
+  t.early = -1;
+  t.rpt = 0;
+  t.mfma = -1;
+  t.generic = 0;
+  t.mfma_r2 = 1;
+  t.bat_r2 = 1;
+  return t;
+}
+
 static int env_int(const char* name, int dflt) {
   const char* v = std::getenv(name);
   if (!v || !*v) return dflt;
   return std::atoi(v);
+}
+
+static std::mutex g_tuning_mu;
+static bool g_tuning_init = false;
+static fluxbin_tuning g_tuning;
+
+static void tuning_init_locked() {
+  if (g_tuning_init) return;
+  fluxbin_tuning t = tuning_defaults();
+  t.nt = env_int("FLUXBIN_NT", t.nt);
+  t.min_units = env_int("FLUXBIN_MIN_UNITS", t.min_units);
+  t.blocks = env_int("FLUXBIN_BLOCKS", t.blocks);
+  t.blocks_per_cu = env_int("FLUXBIN_BLOCKS_PER_CU", t.blocks_per_cu);
+  t.depth = env_int("FLUXBIN_DEPTH", t.depth);
+  t.mfma_depth = env_int("FLUXBIN_MFMA_DEPTH", t.mfma_depth);
+  t.early = env_int("FLUXBIN_EARLY", t.early);
+  t.rpt = env_int("FLUXBIN_RPT", t.rpt);
+  t.mfma = env_int("FLUXBIN_MFMA", t.mfma);
+  t.generic = env_int("FLUXBIN_GENERIC", t.generic);
+  t.mfma_r2 = env_int("FLUXBIN_MFMA_R2", t.mfma_r2);
+  t.bat_r2 = env_int("FLUXBIN_BAT_R2", t.bat_r2);
+  g_tuning = t;
+  g_tuning_init = true;
+}
+
+static fluxbin_tuning tuning_snapshot() {
+  std::lock_guard<std::mutex> lock(g_tuning_mu);
+  tuning_init_locked();
+  return g_tuning;
 }
 
 // Small-batch kernel choice (both kernels reduce split tiles with the second kernel). The matrix-core kernel's cost per
@@ -130,8 +178,8 @@ static int env_int(const char* name, int dflt) {
 // B = 2 14.4 / 17.4 against 15.3 / 17.8, B = 4 16.3 / 18.9 against 16.0 / 18.4. So mu = 8 uses the LUT batch kernel up
 // to B = 4 on large layers and at B = 2 on small ones, the matrix cores otherwise; mu = 4 (whose LUT path for B >= 2
 // is the generic kernel) always the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
-static bool use_mfma(const fluxbin_layer& L, int B, int cus) {
-  const int forced = env_int("FLUXBIN_MFMA", -1);
+static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tuning& tu) {
+  const int forced = tu.mfma;
   if (forced == 0 || forced == 1) return forced == 1;
   const bool small = ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
   return L.shape.mu == 4 || B > 4 || (B > 2 && small);
@@ -145,19 +193,20 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int cus = device_cu_count();
   if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
   std::memset(p, 0, sizeof(*p));
-  const int force_generic = env_int("FLUXBIN_GENERIC", 0);
-  const int rpt_env = env_int("FLUXBIN_RPT", 0);
-  int per_cu = env_int("FLUXBIN_BLOCKS_PER_CU", 0);
+  const fluxbin_tuning tu = tuning_snapshot();
+  const int force_generic = tu.generic;
+  const int rpt_env = tu.rpt;
+  int per_cu = tu.blocks_per_cu;
   p->nt = 256;
   if (B == 1 && !force_generic) {   // batch-1 kernel (mu = 8 or 4)
     p->kernel = 0;
-    const int nt_env = env_int("FLUXBIN_NT", 0);
+    const int nt_env = tu.nt;
     // units of sign data requested ahead of the one being looked up: one (two units, 64 KB per CU, in flight) already
     // keeps HBM saturated; deeper rings only add queueing and prologue latency
-    const int depth_env = env_int("FLUXBIN_DEPTH", 1);
+    const int depth_env = tu.depth;
     p->depth = (depth_env == 2 || depth_env == 3) ? depth_env : 1;
     // layers whose sign stream is small for the chip overlap the activation and sign round trips (see the kernel)
-    const int early_env = env_int("FLUXBIN_EARLY", -1);
+    const int early_env = tu.early;
     const int64_t sign_bytes = int64_t(L.NSC) * 2 * L.Mp * 16;
     p->early = early_env >= 0 ? early_env != 0 : sign_bytes <= (int64_t(32) << 20);
     // mu = 8: 1024-thread workgroups, one per CU, amortize each table over the most rows and keep the fewest,
@@ -180,33 +229,33 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (per_cu < 1 || per_cu > 8) per_cu = 1024 / p->nt;
     p->bg = 1;
     p->n_groups = 1;
-  } else if (B >= 2 && !force_generic && use_mfma(L, B, cus)) {
+  } else if (B >= 2 && !force_generic && use_mfma(L, B, cus, tu)) {
     // small batch on the matrix cores: the sign decode per bit is shared by all batch rows (B <= 16 fit one MFMA tile)
     p->kernel = 3;
     p->nt = 256;
     p->rpt = 1;   // four 16-row blocks per wavefront: 256-row tiles
     // units of data requested ahead: two (measured 2-8 us faster than three on the 70B MLP layers at B = 2..16)
-    const int depth_env = env_int("FLUXBIN_MFMA_DEPTH", 2);
+    const int depth_env = tu.mfma_depth;
     p->depth = depth_env == 3 ? 3 : 2;
     p->bg = B <= 4 ? 4 : (B <= 8 ? 8 : 16);
     p->n_groups = 1;
     // split tiles reduced by a second kernel (FLUXBIN_MFMA_R2=0: by the tile counters, as at batch 1): measured
     // on the 70B MLP layers, up / down, 58.6 / 78.7 -> 57.2 / 59.3 us at B = 16, 48.0 / 57.7 -> 46.5 / 47.1 at B = 8,
     // 45.5 / 48.8 -> 42.6 / 43.6 at B = 4; 7B MLP layers 18.8 / 19.0 -> 15.1 / 17.1 at B = 4
-    p->reduce2 = p->depth == 2 && env_int("FLUXBIN_MFMA_R2", 1) != 0;
+    p->reduce2 = p->depth == 2 && tu.mfma_r2 != 0;
     if (per_cu < 1 || per_cu > 8) per_cu = 3;   // three 256-thread workgroups per CU (the kernel's occupancy)
   } else if (L.shape.mu == 8 && B >= 2 && !force_generic) {
     // small batch: 1024-row tiles, one super-chunk per unit (the batch-1 sign stream), batch in groups of four rows
     // (two for B = 2: half the table entries and lookup additions of a padded group of four)
     p->kernel = 2;
     p->nt = 1024;
-    const int depth_env = env_int("FLUXBIN_DEPTH", 1);
+    const int depth_env = tu.depth;
     p->depth = (depth_env == 2 || depth_env == 3) ? depth_env : 1;
     p->bg = B == 2 ? 2 : 4;
-    p->n_groups = B <= 4 ? 1 : (B <= 8 ? 2 : 4);
+    p->n_groups = int(ceil_div(B, 4));   // every group holds at least one batch row (the grid's y extent)
     // one batch group: split tiles reduced by a second kernel (FLUXBIN_BAT_R2=0: by the tile counters). Measured on the
     // 70B MLP layers, up / down: B = 2 37.6 / 40.6 -> 33.8 / 35.0 us, B = 4 46.0 / 50.2 -> 40.3 / 41.7 us
-    p->reduce2 = p->n_groups == 1 && p->depth == 1 && env_int("FLUXBIN_BAT_R2", 1) != 0;
+    p->reduce2 = p->n_groups == 1 && p->depth == 1 && tu.bat_r2 != 0;
     if (per_cu < 1 || per_cu > 8) per_cu = 1;
   } else {
     p->kernel = 1;
@@ -215,7 +264,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (p->n_groups == 3) p->n_groups = 4;  // instantiated batch paddings: 1, 2, 4, 8, 16
     if (per_cu < 1 || per_cu > 8) per_cu = 2;
   }
-  const int blocks_env = env_int("FLUXBIN_BLOCKS", 0);   // tuning override: grid size target
+  const int blocks_env = tu.blocks;   // tuning override: grid size target
   const int64_t target = blocks_env > 0 ? blocks_env : int64_t(cus) * per_cu;
   p->bpad = p->bg * p->n_groups;
   const int64_t steps = p->kernel == 1 ? (2 * L.NSC) * p->n_groups : L.NSC;
@@ -254,7 +303,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   // CU (4096x4096: 8.2 -> 8.0 us at mu = 8, 8.5 -> 8.2 us at mu = 4; 1024x8192: 8.6 -> 8.4 us; with more workgroups
   // than CUs some CUs would run two of them: 11008x4096 8.7 -> 9.9 us).
   const int min_units_dflt = ceil_div(p->units, 2) <= cus ? 2 : 3;
-  const int min_units = env_int("FLUXBIN_MIN_UNITS", min_units_dflt);
+  const int min_units = tu.min_units >= 0 ? tu.min_units : min_units_dflt;
   if (min_units > 1 && p->kernel == 0 && p->blocks > 1 && ceil_div(p->units, p->blocks) < min_units)
     p->blocks = ceil_div(p->units, int64_t(min_units)) > 0 ? ceil_div(p->units, int64_t(min_units)) : 1;
   // the batch-1 kernel stages the folded activations of all its units at once: at most b1_max_units(nt) per workgroup
@@ -525,4 +574,45 @@ fluxbin_status fluxbin_stream_probe(const fluxbin_layer* layer, uint32_t* d_sink
   return launch_stream_probe(*layer, p, d_sink, stream);
 }
 
+fluxbin_status fluxbin_get_tuning(fluxbin_tuning* out) {
+  g_msg[0] = 0;
+  if (!out) return fail(FLUXBIN_ERR_INVALID_ARG, "out is NULL");
+  *out = tuning_snapshot();
+  return FLUXBIN_OK;
+}
+
+fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t) {
+  g_msg[0] = 0;
+  std::lock_guard<std::mutex> lock(g_tuning_mu);
+  g_tuning = t ? *t : tuning_defaults();
+  g_tuning_init = true;
+  return FLUXBIN_OK;
+}
+
+fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin_plan_info* out) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_layer(layer);
+  if (st != FLUXBIN_OK) return st;
+  if (!out) return fail(FLUXBIN_ERR_INVALID_ARG, "out is NULL");
+  if (B < 1 || B > kMaxBatch) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, 16]", B);
+  Plan p;
+  st = make_plan(*layer, B, &p);
+  if (st != FLUXBIN_OK) return st;
+  std::memset(out, 0, sizeof(*out));
+  out->kernel = p.kernel;
+  out->threads = p.nt;
+  out->rows_per_tile = p.rows;
+  out->depth = p.depth;
+  out->batch_groups = p.n_groups;
+  out->second_kernel_reduction = p.reduce2 ? 1 : 0;
+  out->early = p.early ? 1 : 0;
+  out->reserved = 0;
+  out->tiles = p.n_tiles;
+  out->units = p.units;
+  out->workgroups = p.blocks;
+  out->workspace_bytes = p.ws_bytes;
+  return FLUXBIN_OK;
+}
+
 }  // extern "C"
+

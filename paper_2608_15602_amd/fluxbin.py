@@ -25,8 +25,11 @@ EXPORTS = (
     "fluxbin_status_string", "fluxbin_last_error_message", "fluxbin_pack_query", "fluxbin_pack",
     "fluxbin_layer_from_header", "fluxbin_workspace_query", "fluxbin_workspace_init", "fluxbin_lut_gemv",
     "fluxbin_lut_gemm_smallbatch", "fluxbin_debug_indices", "fluxbin_unpack_canonical", "fluxbin_stream_probe",
-    "fluxbin_rc_workspace_query", "fluxbin_rc_decompose", "fluxbin_structural_search",
+    "fluxbin_rc_workspace_query", "fluxbin_rc_decompose", "fluxbin_structural_search", "fluxbin_get_tuning",
+    "fluxbin_set_tuning", "fluxbin_plan_query",
 )
+
+KERNEL_NAMES = {0: "batch1", 1: "generic", 2: "lut_batch", 3: "mfma"}
 
 
 class FluxbinError(RuntimeError):
@@ -54,6 +57,19 @@ class Layer(ctypes.Structure):
                 ("Mp", ctypes.c_int64), ("Gr", ctypes.c_int64), ("Gs", ctypes.c_int64), ("NRP", ctypes.c_int64),
                 ("off_signs", ctypes.c_uint64), ("off_rscale", ctypes.c_uint64), ("off_colscale", ctypes.c_uint64),
                 ("off_xidx", ctypes.c_uint64), ("off_chunk_plane", ctypes.c_uint64), ("off_sal_idx", ctypes.c_uint64)]
+
+
+class Tuning(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("nt", "min_units", "blocks", "blocks_per_cu", "depth", "mfma_depth",
+                                             "early", "rpt", "mfma", "generic", "mfma_r2", "bat_r2")]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("threads", ctypes.c_int32), ("rows_per_tile", ctypes.c_int32),
+                ("depth", ctypes.c_int32), ("batch_groups", ctypes.c_int32),
+                ("second_kernel_reduction", ctypes.c_int32), ("early", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("tiles", ctypes.c_int64), ("units", ctypes.c_int64), ("workgroups", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_uint64)]
 
 
 _lib = None
@@ -86,6 +102,9 @@ def lib() -> ctypes.CDLL:
         L.fluxbin_rc_decompose.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, i32, i32, i64, ctypes.c_double,
                                            vp, vp, vp, vp, sz, vp]
         L.fluxbin_structural_search.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp]
+        L.fluxbin_get_tuning.argtypes = [ctypes.POINTER(Tuning)]
+        L.fluxbin_set_tuning.argtypes = [ctypes.POINTER(Tuning)]
+        L.fluxbin_plan_query.argtypes = [ctypes.POINTER(Layer), i32, ctypes.POINTER(PlanInfo)]
         for name in EXPORTS:
             if name not in ("fluxbin_status_string", "fluxbin_last_error_message"):
                 getattr(L, name).restype = ctypes.c_int
@@ -179,11 +198,30 @@ def make_workspace(layer: PackedLayer, B: int = 1, stream=None):
     return ws
 
 
+def _check_io(layer: PackedLayer, x, y, out_fp32: bool, B: int) -> None:
+    """The library takes raw pointers: dtype, device, length and inner stride are checked here, before the call."""
+    import torch
+    s = layer.shape
+    dev = layer.buf.device
+    if x.dtype != torch.float16 or x.device != dev or x.stride(-1) != 1:
+        raise FluxbinError(FLUXBIN_ERR_INVALID_ARG, f"x must be fp16 on {dev} with unit inner stride")
+    if x.shape[-1] < s.N or (x.dim() == 2 and x.shape[0] < B):
+        raise FluxbinError(FLUXBIN_ERR_INVALID_ARG, f"x has shape {tuple(x.shape)}, needs [{B}, >= {s.N}]")
+    want = torch.float32 if out_fp32 else torch.float16
+    if y.dtype != want or y.device != dev or y.stride(-1) != 1:
+        raise FluxbinError(FLUXBIN_ERR_INVALID_ARG, f"y must be {want} on {dev} with unit inner stride")
+    if y.shape[-1] < s.M or (y.dim() == 2 and y.shape[0] < B):
+        raise FluxbinError(FLUXBIN_ERR_INVALID_ARG, f"y has shape {tuple(y.shape)}, needs [{B}, >= {s.M}]")
+
+
 def fluxbin_lut_gemv(layer: PackedLayer, x, y=None, out_fp32: bool = False, workspace=None, stream=None):
     import torch
     M = layer.shape.M
     if y is None:
         y = torch.empty(M, dtype=torch.float32 if out_fp32 else torch.float16, device=x.device)
+    if x.dim() != 1 or y.dim() != 1:
+        raise FluxbinError(FLUXBIN_ERR_INVALID_ARG, "fluxbin_lut_gemv takes one activation vector x [N] and y [M]")
+    _check_io(layer, x, y, out_fp32, 1)
     if workspace is None:
         workspace = make_workspace(layer, 1, stream)
     _check(lib().fluxbin_lut_gemv(ctypes.byref(layer.layer), x.data_ptr(), y.data_ptr(), 1 if out_fp32 else 0,
@@ -198,6 +236,9 @@ def fluxbin_lut_gemm_smallbatch(layer: PackedLayer, x, y=None, out_fp32: bool = 
     M = layer.shape.M
     if y is None:
         y = torch.empty(B, M, dtype=torch.float32 if out_fp32 else torch.float16, device=x.device)
+    if x.dim() != 2 or y.dim() != 2:
+        raise FluxbinError(FLUXBIN_ERR_INVALID_ARG, "fluxbin_lut_gemm_smallbatch takes x [B, N] and y [B, M]")
+    _check_io(layer, x, y, out_fp32, B)
     if workspace is None:
         workspace = make_workspace(layer, B, stream)
     _check(lib().fluxbin_lut_gemm_smallbatch(ctypes.byref(layer.layer), int(B), x.data_ptr(), int(x.stride(0)),
@@ -271,3 +312,49 @@ def fluxbin_structural_search(W, hinv_diag, g: int, s: int, stream=None):
                                            scores.data_ptr(), idx.data_ptr(), mask.data_ptr(), _stream(stream)))
     return scores, idx, mask
 
+
+
+def fluxbin_get_tuning() -> Dict[str, int]:
+    t = Tuning()
+    _check(lib().fluxbin_get_tuning(ctypes.byref(t)))
+    return {n: getattr(t, n) for n, _ in Tuning._fields_}
+
+
+def fluxbin_set_tuning(values: Optional[Dict[str, int]]) -> None:
+    """Set the process-wide launch-plan tuning (None: the library defaults)."""
+    if values is None:
+        _check(lib().fluxbin_set_tuning(None))
+        return
+    t = Tuning(**{n: int(values[n]) for n, _ in Tuning._fields_})
+    _check(lib().fluxbin_set_tuning(ctypes.byref(t)))
+
+
+class tuning:
+    """Context manager: the current tuning with some fields overridden, restored on exit.
+    Example: ``with fluxbin.tuning(mfma=0): ...`` runs the LUT batch kernel for every small batch."""
+
+    def __init__(self, **overrides):
+        self.overrides = overrides
+
+    def __enter__(self):
+        self.saved = fluxbin_get_tuning()
+        new = dict(self.saved)
+        for k, v in self.overrides.items():
+            if k not in new:
+                raise KeyError(f"unknown tuning field {k}")
+            new[k] = int(v)
+        fluxbin_set_tuning(new)
+        return self
+
+    def __exit__(self, *exc):
+        fluxbin_set_tuning(self.saved)
+        return False
+
+
+def fluxbin_plan_query(layer: PackedLayer, B: int = 1) -> Dict[str, object]:
+    """The launch plan a call with batch B would use (kernel name, workgroups, ...)."""
+    p = PlanInfo()
+    _check(lib().fluxbin_plan_query(ctypes.byref(layer.layer), int(B), ctypes.byref(p)))
+    out = {n: getattr(p, n) for n, _ in PlanInfo._fields_ if n != "reserved"}
+    out["kernel_name"] = KERNEL_NAMES.get(p.kernel, str(p.kernel))
+    return out

@@ -240,3 +240,27 @@ def test_decomposition_sizes_and_bad_arguments(L):
     assert ss(X, A, 64, 256, 2048, 8, C, S, None, None) == fb.FLUXBIN_ERR_UNSUPPORTED   # group > 1024
     assert ss(X, A, 64, 256, 128, 200, C, S, None, None) == fb.FLUXBIN_ERR_INVALID_ARG  # s > g
     assert ss(X, A, 64, 256, 128, 0, C, S, None, None) == fb.FLUXBIN_ERR_INVALID_ARG
+
+
+def test_tuning_is_explicit_process_state(L):
+    """The launch-plan tuning is read from the environment once and otherwise changed only by fluxbin_set_tuning; the
+    context manager restores the previous values."""
+    t0 = fb.fluxbin_get_tuning()
+    assert set(t0) == {n for n, _ in fb.Tuning._fields_}
+    with fb.tuning(mfma=0, nt=512):
+        t1 = fb.fluxbin_get_tuning()
+        assert t1["mfma"] == 0 and t1["nt"] == 512
+    assert fb.fluxbin_get_tuning() == t0
+    fb.fluxbin_set_tuning(None)
+    d = fb.fluxbin_get_tuning()
+    assert d["mfma"] == -1 and d["min_units"] == -1 and d["early"] == -1 and d["mfma_r2"] == 1 and d["bat_r2"] == 1
+    fb.fluxbin_set_tuning(t0)
+    with pytest.raises(KeyError):
+        with fb.tuning(no_such_field=1):
+            pass
+    assert L.fluxbin_get_tuning(None) == fb.FLUXBIN_ERR_INVALID_ARG
+
+
+def test_plan_query_validates_on_the_host(L):
+    info = fb.PlanInfo()
+    assert L.fluxbin_plan_query(None, 1, ctypes.byref(info)) == fb.FLUXBIN_ERR_INVALID_ARG

@@ -3,8 +3,6 @@
 Bar: packing and LUT indices bit-exact; outputs within |y - y*| <= 2e-3 * max(|y*|, 1e-3 * max|y*| of the row)
 (fp32 accumulation; x * alpha_c exact in fp32; fp16 output rounding 2^-11 relative). Full-size layers are checked on
 sampled rows that the oracle computes one by one; the smaller ones on every row."""
-import os
-
 import numpy as np
 import pytest
 
@@ -255,22 +253,14 @@ def test_mu4_batch1_kernel_matches_oracle_and_generic(spec):
     """mu = 4 at batch 1 runs the batch-1 kernel (16-entry tables); it matches the oracle on every row and the
     generic kernel's result within the tolerance."""
     L, packed, x, y = _parity(spec, 1, out_fp32=True)
-    os.environ["FLUXBIN_GENERIC"] = "1"
-    try:
-        y_gen = run_gemm(packed, x, out_fp32=True)
-    finally:
-        del os.environ["FLUXBIN_GENERIC"]
+    y_gen = _with_env({"FLUXBIN_GENERIC": "1"}, lambda: run_gemm(packed, x, out_fp32=True))
     _check(y, y_gen, "batch-1 kernel vs generic kernel")
 
 
 def test_fp32_output_and_generic_kernel_at_batch1():
     spec = LayerSpec("gen", M=2000, N=1024, Kb=2, Ks=1, mu=8, S=40, g_r=128, g_s=40, seed=21)
     L, packed, x, y = _parity(spec, 1, out_fp32=True)
-    os.environ["FLUXBIN_GENERIC"] = "1"
-    try:
-        y2 = run_gemm(packed, x, out_fp32=True)
-    finally:
-        del os.environ["FLUXBIN_GENERIC"]
+    y2 = _with_env({"FLUXBIN_GENERIC": "1"}, lambda: run_gemm(packed, x, out_fp32=True))
     _check(y2, oracle.gemv_dense(L, x), "generic kernel at batch 1")
 
 
@@ -282,18 +272,17 @@ SMALL_BATCH_KERNELS = {"mfma": {"FLUXBIN_MFMA": "1"}, "lut_batch": {"FLUXBIN_MFM
 
 
 def _with_env(env, fn):
-    for k, v in env.items():
-        os.environ[k] = v
-    try:
+    """Run fn with launch-plan tuning fields overridden (named like their FLUXBIN_* environment variables), restored
+    afterwards (fluxbin_set_tuning: the library reads the environment only once per process)."""
+    from paper_2608_15602_amd import fluxbin as fb
+    kw = {k[len("FLUXBIN_"):].lower(): int(v) for k, v in env.items()}
+    with fb.tuning(**kw):
         return fn()
-    finally:
-        for k in env:
-            os.environ.pop(k, None)
 
 
 @pytest.mark.parametrize("kernel", list(SMALL_BATCH_KERNELS))
 @pytest.mark.parametrize("mu", [8, 4])
-@pytest.mark.parametrize("B", [2, 5, 16])
+@pytest.mark.parametrize("B", [2, 5, 9, 12, 16])
 def test_batch_rows_equal_batch1(B, mu, kernel):
     """Each batch row of every small-batch kernel matches the oracle (rows of several split tiles, a ragged last
     tile, B not a multiple of four)."""
