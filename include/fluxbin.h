@@ -204,6 +204,20 @@ fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B
                                            size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * fluxbin_lut_gemv for callers that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same product, launch plan and kernels as fluxbin_lut_gemv (bitwise the same
+ * y), with the split-tile workspace taken from a static device array of FLUXBIN_NOALLOC_SCRATCH_BYTES that every
+ * device the library runs on holds until the process ends. The call allocates nothing. Limits: M <= 64512 rows and
+ * a launch plan needing at most FLUXBIN_NOALLOC_SCRATCH_BYTES of workspace, else FLUXBIN_ERR_UNSUPPORTED (nothing
+ * launched). The first call on a device zero-fills that device's array on `stream`; every completed call leaves its
+ * tile counters at zero again. All calls on one device share its array: calls that overlap in time on one device
+ * (different streams, or different host threads without ordering) race and may return wrong results.
+ */
+#define FLUXBIN_NOALLOC_SCRATCH_BYTES (8u << 20)
+fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16_t* d_x, void* d_y, int32_t y_is_fp32,
+                                        hipStream_t stream);
+
+/*
  * Launch-plan tuning, for tests and measurements (the defaults are the library's measured choices). Process-wide: the
  * first plan made in a process initializes it from the environment variable named after each field (unset: default);
  * afterwards only fluxbin_set_tuning changes it (NULL restores the defaults). A plan takes one consistent copy, so

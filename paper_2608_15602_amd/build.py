@@ -20,7 +20,7 @@ OBJDIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfluxbin.so")
 
 SOURCES = ["fluxbin_host.cpp", "fluxbin_pack.hip", "fluxbin_gemv.hip", "fluxbin_gemm_batch.hip",
-           "fluxbin_gemm_mfma.hip", "fluxbin_rc.hip"]
+           "fluxbin_gemm_mfma.hip", "fluxbin_rc.hip", "fluxbin_noalloc.hip"]
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are kept out of the generated code (plain float code only).

@@ -31,7 +31,7 @@ fluxbin_status hip_fail(int err, const char* what) {
 
 int device_cu_count() {
   static std::mutex mu;
-  static int cache[64] = {};   // per device index
+  static int cache[64] = {};   // per device index (no allocation: fluxbin_lut_gemv_noalloc plans through this)
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
   std::lock_guard<std::mutex> lock(mu);
@@ -542,6 +542,19 @@ fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B
                                            size_t workspace_bytes, hipStream_t stream) {
   g_msg[0] = 0;
   return gemm_common(layer, B, d_x, ldx, d_y, ldy, y_is_fp32, d_workspace, workspace_bytes, stream);
+}
+
+fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16_t* d_x, void* d_y, int32_t y_is_fp32,
+                                        hipStream_t stream) {
+  g_msg[0] = 0;
+  fluxbin_status st = check_layer(layer);
+  if (st != FLUXBIN_OK) return st;
+  if (!d_x || !d_y) return fail(FLUXBIN_ERR_INVALID_ARG, "x or y is NULL");
+  if (y_is_fp32 != 0 && y_is_fp32 != 1) return fail(FLUXBIN_ERR_INVALID_ARG, "y_is_fp32 must be 0 or 1");
+  const size_t xb = size_t(layer->shape.N) * 2;
+  const size_t yb = size_t(layer->shape.M) * (y_is_fp32 ? 4 : 2);
+  if (ranges_overlap(d_x, xb, d_y, yb)) return fail(FLUXBIN_ERR_INVALID_ARG, "x and y overlap");
+  return gemv_noalloc(*layer, d_x, d_y, y_is_fp32, stream);
 }
 
 fluxbin_status fluxbin_debug_indices(const fluxbin_layer* layer, uint8_t* d_p, hipStream_t stream) {

@@ -23,6 +23,10 @@ constexpr int kMfMaxUnits = 16;         // units per workgroup of the matrix-cor
 #define FLUXBIN_COUNTER_STRIDE 64
 #endif
 constexpr int kCounterStride = FLUXBIN_COUNTER_STRIDE;
+// Static scratch of fluxbin_lut_gemv_noalloc: a fixed region of tile counters (room for every layer with at most
+// kNoallocMaxM rows), then partial sums.
+constexpr uint64_t kNoallocCounterBytes = 65536;
+constexpr int64_t kNoallocMaxM = int64_t(kNoallocCounterBytes / (uint64_t(kCounterStride) * 4u) - 4) * 256;
 
 struct Derived {
   int64_t Npad, ncg, Sv, ncs, NC, NSC, NCP, V, Mp, Gr, Gs, NRP;
@@ -110,6 +114,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
                            void* d_y, int64_t ldy, int y_fp32, void* d_ws, hipStream_t stream);
 fluxbin_status launch_fill_zero(void* d, size_t bytes, hipStream_t stream);
 fluxbin_status launch_stream_probe(const fluxbin_layer& L, const Plan& p, uint32_t* d_sink, hipStream_t stream);
+fluxbin_status gemv_noalloc(const fluxbin_layer& L, const uint16_t* d_x, void* d_y, int y_fp32, hipStream_t stream);
 fluxbin_status launch_debug_indices(const fluxbin_layer& L, uint8_t* d_p, hipStream_t stream);
 fluxbin_status launch_unpack(const fluxbin_layer& L, uint32_t* d_signs, uint32_t* d_dense, hipStream_t stream);
 

@@ -26,8 +26,9 @@ EXPORTS = (
     "fluxbin_layer_from_header", "fluxbin_workspace_query", "fluxbin_workspace_init", "fluxbin_lut_gemv",
     "fluxbin_lut_gemm_smallbatch", "fluxbin_debug_indices", "fluxbin_unpack_canonical", "fluxbin_stream_probe",
     "fluxbin_rc_workspace_query", "fluxbin_rc_decompose", "fluxbin_structural_search", "fluxbin_get_tuning",
-    "fluxbin_set_tuning", "fluxbin_plan_query",
+    "fluxbin_set_tuning", "fluxbin_plan_query", "fluxbin_lut_gemv_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 8 << 20
 
 KERNEL_NAMES = {0: "batch1", 1: "generic", 2: "lut_batch", 3: "mfma"}
 
@@ -105,6 +106,7 @@ def lib() -> ctypes.CDLL:
         L.fluxbin_get_tuning.argtypes = [ctypes.POINTER(Tuning)]
         L.fluxbin_set_tuning.argtypes = [ctypes.POINTER(Tuning)]
         L.fluxbin_plan_query.argtypes = [ctypes.POINTER(Layer), i32, ctypes.POINTER(PlanInfo)]
+        L.fluxbin_lut_gemv_noalloc.argtypes = [ctypes.POINTER(Layer), vp, vp, i32, vp]
         for name in EXPORTS:
             if name not in ("fluxbin_status_string", "fluxbin_last_error_message"):
                 getattr(L, name).restype = ctypes.c_int
@@ -226,6 +228,16 @@ def fluxbin_lut_gemv(layer: PackedLayer, x, y=None, out_fp32: bool = False, work
         workspace = make_workspace(layer, 1, stream)
     _check(lib().fluxbin_lut_gemv(ctypes.byref(layer.layer), x.data_ptr(), y.data_ptr(), 1 if out_fp32 else 0,
                                   workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+    return y
+
+
+def fluxbin_lut_gemv_noalloc(layer: PackedLayer, x, y, out_fp32: bool = False, stream=None):
+    """fluxbin_lut_gemv without a workspace (the library's static device scratch); y must be preallocated."""
+    if x.dim() != 1 or y.dim() != 1:
+        raise FluxbinError(FLUXBIN_ERR_INVALID_ARG, "fluxbin_lut_gemv_noalloc takes x [N] and y [M]")
+    _check_io(layer, x, y, out_fp32, 1)
+    _check(lib().fluxbin_lut_gemv_noalloc(ctypes.byref(layer.layer), x.data_ptr(), y.data_ptr(), 1 if out_fp32 else 0,
+                                          _stream(stream)))
     return y
 
 

@@ -261,6 +261,9 @@ def test_tuning_is_explicit_process_state(L):
     assert L.fluxbin_get_tuning(None) == fb.FLUXBIN_ERR_INVALID_ARG
 
 
-def test_plan_query_validates_on_the_host(L):
+def test_plan_query_and_noalloc_validate_on_the_host(L):
     info = fb.PlanInfo()
     assert L.fluxbin_plan_query(None, 1, ctypes.byref(info)) == fb.FLUXBIN_ERR_INVALID_ARG
+    X = ctypes.c_void_p(1 << 20)
+    Y = ctypes.c_void_p(1 << 24)
+    assert L.fluxbin_lut_gemv_noalloc(None, X, Y, 0, None) == fb.FLUXBIN_ERR_INVALID_ARG
