@@ -62,11 +62,14 @@ const char* fluxbin_last_error_message(void);
  *        App. C.2).
  *   Kb   global bases, 1..4.            Ks   salient bases, 0..4 (the paper uses Ks = Kb; the hybrid configs here 1).
  *   mu   LUT sub-vector length, 4 or 8 (Sec. 3.2 and App. E.2 use both; 8 is the paper's default).
- *   g_r  global row-scale group in columns: one row scale per (row, base, group of g_r consecutive columns)
- *        ("one row scale per weight group", Sec. 3.1). Supported: a multiple of 128, or g_r >= N (one per row).
+ *   g_r  global row-scale group in columns: each row of each global base has its own scale for every run of g_r
+ *        consecutive columns (Sec. 3.1; the 16*M*N/g storage term of App. C.2). A multiple of mu that divides 128
+ *        (the paper's g = 64), a multiple of 128 (g = 128, 256), or g_r >= N (one per row).
  *   S    number of salient columns, 0..N (N_sal in the paper).
  *   g_s  salient row-scale group in VCM dense columns: one salient row scale per (row, salient base, group of g_s
- *        consecutive dense columns). Supported: a multiple of 128, or g_s >= S. Ignored when S == 0 or Ks == 0.
+ *        consecutive dense columns). The paper's structured selection (s salient columns in every block of g input
+ *        columns, Sec. 3.1, Alg. FluxBin-Hybrid) with one salient row scale per (row, block) is g_s = s. Same rule as
+ *        g_r (with S for N); ignored when S == 0 or Ks == 0.
  */
 typedef struct {
   int64_t M, N;
@@ -119,37 +122,46 @@ typedef struct {
 } fluxbin_layer;
 
 /*
- * PACKED FORMAT (version 1). Written by fluxbin_pack, read by the GEMV kernels.
+ * PACKED FORMAT (version 2). Written by fluxbin_pack, read by the GEMV kernels.
  *
  * Virtual columns. The global bases' columns and the salient bases' VCM dense columns (Def. VCM, Eq. 12: salient
  * column t of the dense block is input column I_sal[t]) are laid end to end in chunks of 128 columns:
  *   Npad = ceil(N/128)*128 and ncg = Npad/128 chunks per global base;
  *   Sv = ceil(S/128)*128 (0 if S == 0 or Ks == 0) and ncs = Sv/128 chunks per salient base;
- *   NC = Kb*ncg + Ks*ncs chunks, NSC = ceil(NC/2) super-chunks of two chunks, NCP = 2*NSC (an odd NC gets one
- *   all-zero pad chunk), V = 128*NCP virtual columns.
- * Chunk c < Kb*ncg is global base k = c / ncg, input columns ((c % ncg)*128 + r); chunk Kb*ncg <= c < NC is salient
- * base k = (c - Kb*ncg) / ncs, dense columns t = ((c - Kb*ncg) % ncs)*128 + r, input column I_sal[t]. A virtual column
- * with no source (r past N, t past S, the pad chunk) has sign bit 0, column scale 0 and activation index 0xFFFF; it
+ *   row scales per chunk and row: Gcg = 128/g_r for the global chunks when g_r < 128 and g_r < N ("fine" groups),
+ *   else 1 ("coarse"); Gcs likewise from g_s and S for the salient chunks;
+ *   ngcp = Kb*ncg global chunks, plus one inert separator chunk when Kb*ncg is odd, there is a salient part and
+ *   Gcg != Gcs (so that the two chunks of a super-chunk share one scale layout);
+ *   NC = ngcp + Ks*ncs chunks, NSC = ceil(NC/2) super-chunks of two chunks, NCP = 2*NSC (an odd NC gets one
+ *   all-zero pad chunk), V = 128*NCP virtual columns; nfc = ngcp with a salient part, else NCP: chunks c >= nfc use
+ *   the salient scale layout (Gcs), the others the global one (Gcg).
+ * Chunk c < Kb*ncg is global base k = c / ncg, input columns ((c % ncg)*128 + r); chunk ngcp <= c < NC is salient
+ * base k = (c - ngcp) / ncs, dense columns t = ((c - ngcp) % ncs)*128 + r, input column I_sal[t]. A virtual column
+ * with no source (r past N, t past S, a pad chunk) has sign bit 0, column scale 0 and activation index 0xFFFF; it
  * contributes exactly zero.
  *
  * Sections (each starts at a multiple of 256 bytes, in this order after the 256-byte header):
  *   signs       [NSC][2][Mp][16] bytes, Mp = ceil(M/64)*64. Each 16-byte entry is one chunk of one row: 128 sign
- *               bits, split into sub-vectors of mu bits (bit n of a sub-vector is its n-th column; set = +1).
- *               mu = 8: slot h of super-chunk sc for row i holds chunk 2*sc + (h XOR [i mod 32 >= 16]); its byte q is
- *               the chunk's sub-vector u = (q + i) mod 16.
- *               mu = 4: slot h holds chunk 2*sc + h; its nibble q (byte q/2, low nibble first) is the chunk's
- *               sub-vector u = (q + i) mod 32.
- *               Rows i >= M are zero. (The rotation by the row index lets the 32 lanes of a half-wavefront read 32
- *               different tables at the same step, so every LDS bank is hit once.)
- *   rscale      fp16 [NRP][Mp], NRP = Kb*G_r + Ks*G_s: plane k*G_r + g holds alpha_r^(k)[:, g]; plane
- *               Kb*G_r + k*G_s + g holds alpha_sr^(k)[:, g]; rows >= M are zero.
+ *               bits, split into P = 128/mu sub-vectors of mu bits (bit n of a sub-vector is its n-th column; set =
+ *               +1), stored at rotated positions: with G the chunk's scales per row and n = P/G, position q of row i
+ *               holds sub-vector ((floor(q/n) + floor(i/n)) mod G)*n + ((q mod n) + i) mod n (for G = 1 and G = P
+ *               simply (q + i) mod P): the groups are rotated by floor(i/n) and the positions inside a group by i.
+ *               mu = 8: slot h of super-chunk sc for row i holds chunk 2*sc + (h XOR [i mod 32 >= 16]); byte q is
+ *               position q. mu = 4: slot h holds chunk 2*sc + h; nibble q (byte q/2, low nibble first) is position q.
+ *               Rows i >= M are zero. (The rotation lets the 32 lanes of a half-wavefront read 32 different tables at
+ *               the same step, so every LDS bank is hit once, and keeps each group's positions contiguous.)
+ *   rscale      fp16 [NRP][Mp] planes. Global part (Pg planes): coarse, plane k*G_r + g holds alpha_r^(k)[:, g]
+ *               (G_r = ceil(N/g_r), Pg = Kb*G_r); fine, chunk l of base k owns the Gcg planes from (k*ncg + l)*Gcg,
+ *               read as [Mp][Gcg]: slot b of row i holds the scale of the chunk's group (b + floor(i/n)) mod Gcg,
+ *               i.e. of the positions b*n .. b*n+n-1 (Pg = Kb*ncg*Gcg). Salient part, after the global planes: the
+ *               same with alpha_sr, G_s = ceil(S/g_s), ncs, Gcs. Groups past the last one and rows >= M are zero.
  *   colscale    fp16 [V]: alpha_c^(k)[j] for global columns, alpha_sc^(k)[I_sal[t]] (= alpha_scd, Eq. 13) for salient
  *               dense columns, 0 for columns without a source.
  *   xidx        uint16 [V]: the input column j whose activation the virtual column reads, 0xFFFF for none.
- *   chunk_plane int32 [NCP]: rscale plane of each chunk (the pad chunk has 0).
+ *   chunk_plane int32 [NCP]: first rscale plane of each chunk (a pad chunk has the planes of the chunk before it).
  *   sal_idx     uint16 [max(S,1)]: I_sal as 16-bit indices (App. C.2); a single 0 when S == 0.
  */
-#define FLUXBIN_FORMAT_VERSION 1u
+#define FLUXBIN_FORMAT_VERSION 2u
 #define FLUXBIN_HEADER_BYTES 256u
 
 /* Bytes of the packed buffer for a shape. Host only; validates the shape. */
@@ -197,7 +209,8 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
  * Two kernels compute it: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4) and a matrix-core
  * kernel (mu = 4, or B > 4) that decodes the sign bits into fp16 +-|alpha_c| tiles and multiplies them with the
  * activations on the MFMA units (the products are exact in the fp32 accumulation, as in the LUT path; the row scale is
- * applied per 128-column chunk). Both are deterministic; their results differ only by fp32 summation order.
+ * applied per 128-column chunk). Layers with fine row-scale groups (g_r or g_s below 128) run the generic LUT kernel
+ * for B >= 2. All are deterministic; their results differ only by fp32 summation order.
  */
 fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx,
                                            void* d_y, int64_t ldy, int32_t y_is_fp32, void* d_workspace,

@@ -17,37 +17,71 @@ from .fluxbin_oracle import sign_bits
 
 CHUNK = 128
 MAGIC = 0x42584C46
-VERSION = 1
+VERSION = 2
 
 
 def derived(spec) -> Dict[str, int]:
-    """Derived sizes of the packed format."""
+    """Derived sizes of the packed format.
+
+    A chunk's row scales are "coarse" (one plane of one scale per row, shared by every chunk of the same scale group)
+    when its group size is at least 128 columns or covers the whole extent, else "fine": 128 // g scales per row and
+    chunk (Gcg for the global chunks, Gcs for the salient ones). When the two kinds differ and the global chunk count
+    is odd, one inert chunk separates them, so that no pair of chunks (super-chunk) mixes the two layouts."""
     M, N, Kb, Ks, S = spec.M, spec.N, spec.Kb, spec.Ks, spec.S
+    sal = S > 0 and Ks > 0
     Npad = -(-N // CHUNK) * CHUNK
-    Sv = (-(-S // CHUNK) * CHUNK) if (S > 0 and Ks > 0) else 0
+    Sv = (-(-S // CHUNK) * CHUNK) if sal else 0
     ncg, ncs = Npad // CHUNK, Sv // CHUNK
-    NC = Kb * ncg + Ks * ncs
+
+    def per_chunk(g, extent):
+        return CHUNK // g if (g < CHUNK and g < extent) else 1
+
+    Gcg = per_chunk(spec.g_r, N)
+    Gcs = per_chunk(spec.g_s, S) if sal else 1
+    ngcp = Kb * ncg + (1 if (sal and Gcg != Gcs and (Kb * ncg) % 2 == 1) else 0)
+    NC = ngcp + Ks * ncs
     NSC = -(-NC // 2)
     NCP = 2 * NSC
     Gr = -(-N // spec.g_r)
-    Gs = (-(-S // spec.g_s)) if (S > 0 and Ks > 0) else 0
+    Gs = (-(-S // spec.g_s)) if sal else 0
+    Pg = Kb * Gr if Gcg == 1 else Kb * ncg * Gcg
+    Ps = (Ks * Gs if Gcs == 1 else Ks * ncs * Gcs) if sal else 0
     return dict(Npad=Npad, Sv=Sv, ncg=ncg, ncs=ncs, NC=NC, NSC=NSC, NCP=NCP, V=CHUNK * NCP,
-                Mp=-(-M // 64) * 64, Gr=Gr, Gs=Gs, NRP=Kb * Gr + Ks * Gs)
+                Mp=-(-M // 64) * 64, Gr=Gr, Gs=Gs, NRP=Pg + Ps, Gcg=Gcg, Gcs=Gcs, ngcp=ngcp,
+                nfc=ngcp if sal else NCP, Pg=Pg)
+
+
+def chunk_G(spec, c: int) -> int:
+    """Row scales per row of chunk c: the salient layout from the first salient chunk on (pad chunks included)."""
+    d = derived(spec)
+    return d["Gcg"] if c < d["nfc"] else d["Gcs"]
 
 
 def chunk_info(spec, c: int):
-    """(kind, plane k, first local column, row-scale plane) of chunk c. kind is 'g', 's' or 'pad'."""
+    """(kind, base k, first local column, first row-scale plane) of chunk c; kind is 'g', 's' or 'pad'. A pad chunk
+    (the separator, or the last chunk of an odd count) uses the planes of the chunk before it."""
     d = derived(spec)
     if c < spec.Kb * d["ncg"]:
         k, lc = divmod(c, d["ncg"])
-        grp = (lc * CHUNK) // spec.g_r
-        return "g", k, lc * CHUNK, k * d["Gr"] + grp
-    c2 = c - spec.Kb * d["ncg"]
-    if c2 < spec.Ks * d["ncs"]:
+        plane = k * d["Gr"] + (lc * CHUNK) // spec.g_r if d["Gcg"] == 1 else (k * d["ncg"] + lc) * d["Gcg"]
+        return "g", k, lc * CHUNK, plane
+    c2 = c - d["ngcp"]
+    if c >= d["ngcp"] and c2 < spec.Ks * d["ncs"]:
         k, lc = divmod(c2, d["ncs"])
-        grp = (lc * CHUNK) // spec.g_s
-        return "s", k, lc * CHUNK, spec.Kb * d["Gr"] + k * d["Gs"] + grp
-    return "pad", 0, 0, 0
+        if d["Gcs"] == 1:
+            plane = d["Pg"] + k * d["Gs"] + (lc * CHUNK) // spec.g_s
+        else:
+            plane = d["Pg"] + (k * d["ncs"] + lc) * d["Gcs"]
+        return "s", k, lc * CHUNK, plane
+    return "pad", 0, 0, chunk_info(spec, c - 1)[3]
+
+
+def position_subvector(q: int, i: int, spc: int, G: int) -> int:
+    """Sub-vector held at position q of row i's entry of a chunk with G scale groups (spc positions): with n = spc / G
+    positions per group, position block q // n holds group (q // n + i // n) mod G and, inside it, sub-vector
+    (q mod n + i) mod n of that group."""
+    n = spc // G
+    return ((q // n + i // n) % G) * n + ((q % n + i) % n)
 
 
 def virtual_columns(L) -> Dict[str, np.ndarray]:
@@ -100,9 +134,10 @@ def device_signs(L, rows: Optional[Sequence[int]] = None) -> np.ndarray:
     """Device sign section restricted to ``rows``: uint8 [NSC, 2, len(rows), 16].
 
     mu = 8: slot h of super-chunk sc for row i holds chunk 2 sc + (h xor [i mod 32 >= 16]); its byte q is the chunk's
-    sub-vector byte u = (q + i) mod 16, where sub-vector byte u packs columns 8u..8u+7 of the chunk, LSB first.
+    sub-vector byte u = position_subvector(q, i, 16, G) (G = 1: (q + i) mod 16), where sub-vector byte u packs columns
+    8u..8u+7 of the chunk, LSB first.
     mu = 4: slot h holds chunk 2 sc + h; its nibble q (byte q // 2, low nibble first) is the chunk's sub-vector nibble
-    u = (q + i) mod 32, packing columns 4u..4u+3, LSB first."""
+    u = position_subvector(q, i, 32, G), packing columns 4u..4u+3, LSB first."""
     s = L.spec
     d = derived(s)
     if rows is None:
@@ -116,16 +151,18 @@ def device_signs(L, rows: Optional[Sequence[int]] = None) -> np.ndarray:
         for sc in range(d["NSC"]):
             for h in range(2):
                 c = 2 * sc + (h ^ hb)                                                  # per row
+                G = np.array([chunk_G(s, int(cc)) for cc in c], dtype=np.int64)
                 for q in range(16):
-                    u = (q + rows) % 16
+                    u = position_subvector(q, rows, 16, G)
                     out[sc, h, :, q] = sub[np.arange(rows.size), c, u]
     elif s.mu == 4:
         sub = (vb.reshape(rows.size, d["NCP"], 32, 4) << np.arange(4)).sum(-1)      # [R, NCP, 32]
         for sc in range(d["NSC"]):
             for h in range(2):
                 c = 2 * sc + h
+                G = chunk_G(s, c)
                 for q in range(32):
-                    u = (q + rows) % 32
+                    u = position_subvector(q, rows, 32, G)
                     nib = sub[np.arange(rows.size), c, u]
                     out[sc, h, :, q // 2] |= (nib << (4 * (q % 2))).astype(np.uint8)
     else:
@@ -134,17 +171,41 @@ def device_signs(L, rows: Optional[Sequence[int]] = None) -> np.ndarray:
 
 
 def device_rscale(L) -> np.ndarray:
-    """Row-scale section: uint16 [NRP, Mp]; plane k*Gr + grp holds alpha_r^(k)[:, grp], plane Kb*Gr + k*Gs + grp holds
-    alpha_sr^(k)[:, grp]; rows >= M are zero."""
+    """Row-scale section: uint16 [NRP, Mp]. Coarse layout: plane k*Gr + grp holds alpha_r^(k)[:, grp] (salient: plane
+    Pg + k*Gs + grp holds alpha_sr^(k)[:, grp]). Fine layout: chunk lc of base k owns the G planes starting at
+    (k*nc + lc)*G (salient: after Pg), read as [Mp][G]: slot b of row i is the scale of the chunk's group
+    (b + i // n) mod G, n = (128 / mu) / G, i.e. of the sub-vectors at positions b*n .. b*n + n - 1 of the row's entry.
+    Groups past the last one, and rows >= M, are zero."""
     s = L.spec
     d = derived(s)
     out = np.zeros((d["NRP"], d["Mp"]), dtype=np.uint16)
-    for k in range(s.Kb):
-        for g in range(d["Gr"]):
-            out[k * d["Gr"] + g, :s.M] = L.alpha_r[k, :, g]
-    for k in range(s.Ks if d["Gs"] else 0):
-        for g in range(d["Gs"]):
-            out[s.Kb * d["Gr"] + k * d["Gs"] + g, :s.M] = L.alpha_sr[k, :, g]
+    flat = out.reshape(-1)
+    spc = CHUNK // s.mu
+
+    def fine(base_plane, alpha, ngroups, nc, G, K):
+        n = spc // G
+        for k in range(K):
+            for lc in range(nc):
+                blk0 = (base_plane + (k * nc + lc) * G) * d["Mp"]
+                for i in range(s.M):
+                    for b in range(G):
+                        grp = lc * G + (b + i // n) % G
+                        if grp < ngroups:
+                            flat[blk0 + i * G + b] = alpha[k, i, grp]
+
+    if d["Gcg"] == 1:
+        for k in range(s.Kb):
+            for g in range(d["Gr"]):
+                out[k * d["Gr"] + g, :s.M] = L.alpha_r[k, :, g]
+    else:
+        fine(0, L.alpha_r, d["Gr"], d["ncg"], d["Gcg"], s.Kb)
+    if d["Gs"]:
+        if d["Gcs"] == 1:
+            for k in range(s.Ks):
+                for g in range(d["Gs"]):
+                    out[d["Pg"] + k * d["Gs"] + g, :s.M] = L.alpha_sr[k, :, g]
+        else:
+            fine(d["Pg"], L.alpha_sr, d["Gs"], d["ncs"], d["Gcs"], s.Ks)
     return out
 
 
@@ -168,14 +229,14 @@ def undo_device_signs(dev: np.ndarray, spec, rows: Sequence[int]) -> np.ndarray:
                 if spec.mu == 8:
                     c = 2 * sc + (h ^ int((i % 32) >= 16))
                     for q in range(16):
-                        u = (q + int(i)) % 16
+                        u = position_subvector(q, int(i), 16, chunk_G(spec, c))
                         byte = int(dev[sc, h, ri, q])
                         for n in range(8):
                             vb[ri, c, 8 * u + n] = (byte >> n) & 1
                 else:
                     c = 2 * sc + h
                     for q in range(32):
-                        u = (q + int(i)) % 32
+                        u = position_subvector(q, int(i), 32, chunk_G(spec, c))
                         nib = (int(dev[sc, h, ri, q // 2]) >> (4 * (q % 2))) & 15
                         for n in range(4):
                             vb[ri, c, 4 * u + n] = (nib >> n) & 1

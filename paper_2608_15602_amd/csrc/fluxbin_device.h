@@ -29,6 +29,8 @@ struct GemmArgs {
   int32_t N;         // input columns
   int32_t ncg;       // chunks per global base
   int32_t ngc;       // global chunks (Kb * ncg); chunks >= ngc are salient or padding
+  int32_t nfc;       // first chunk with the salient chunks' row-scale layout
+  int32_t Gcg, Gcs;  // row scales per chunk and row: global / salient layout (1, or 2..32 for fine groups)
 };
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

@@ -58,8 +58,9 @@ static fluxbin_status check_shape(const fluxbin_shape* s) {
   if (s->g_r < 1) return fail(FLUXBIN_ERR_INVALID_ARG, "g_r = %lld must be >= 1", (long long)s->g_r);
   if (s->g_r < s->N && s->g_r % s->mu != 0)
     return fail(FLUXBIN_ERR_INVALID_ARG, "g_r = %lld must hold whole sub-vectors of mu = %d", (long long)s->g_r, s->mu);
-  if (s->g_r < s->N && s->g_r % kChunk != 0)
-    return fail(FLUXBIN_ERR_UNSUPPORTED, "g_r = %lld: supported are multiples of 128 or g_r >= N", (long long)s->g_r);
+  if (s->g_r < s->N && s->g_r % kChunk != 0 && kChunk % s->g_r != 0)
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "g_r = %lld: supported are divisors of 128, multiples of 128, or g_r >= N",
+                (long long)s->g_r);
   if (s->S < 0 || s->S > s->N)
     return fail(FLUXBIN_ERR_INVALID_ARG, "S = %lld out of range [0, N]", (long long)s->S);
   if (s->S > 0 && s->Ks > 0) {
@@ -67,8 +68,8 @@ static fluxbin_status check_shape(const fluxbin_shape* s) {
     if (s->g_s < s->S && s->g_s % s->mu != 0)
       return fail(FLUXBIN_ERR_INVALID_ARG, "g_s = %lld must hold whole sub-vectors of mu = %d", (long long)s->g_s,
                   s->mu);
-    if (s->g_s < s->S && s->g_s % kChunk != 0)
-      return fail(FLUXBIN_ERR_UNSUPPORTED, "g_s = %lld: supported are multiples of 128 or g_s >= S",
+    if (s->g_s < s->S && s->g_s % kChunk != 0 && kChunk % s->g_s != 0)
+      return fail(FLUXBIN_ERR_UNSUPPORTED, "g_s = %lld: supported are divisors of 128, multiples of 128, or g_s >= S",
                   (long long)s->g_s);
   }
   return FLUXBIN_OK;
@@ -197,8 +198,13 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int force_generic = tu.generic;
   const int rpt_env = tu.rpt;
   int per_cu = tu.blocks_per_cu;
+  // Fine row-scale groups (groups shorter than a chunk): the batch-1 kernel's instances for them have mu = 8, one unit
+  // ahead and 512 or 1024 threads; every other case with fine groups runs the generic kernel (the matrix-core and LUT
+  // batch kernels apply one row scale per chunk).
+  const Derived dv = derive(L.shape);
+  const bool fine = dv.Gcg > 1 || dv.Gcs > 1;
   p->nt = 256;
-  if (B == 1 && !force_generic) {   // batch-1 kernel (mu = 8 or 4)
+  if (B == 1 && !force_generic && !(fine && L.shape.mu != 8)) {   // batch-1 kernel (mu = 8 or 4)
     p->kernel = 0;
     const int nt_env = tu.nt;
     // units of sign data requested ahead of the one being looked up: one (two units, 64 KB per CU, in flight) already
@@ -220,16 +226,18 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     // 28672-row MLP layers: 512 threads at most, fewer for layers with fewer than one unit per CU.
     if (nt_env == 256 || nt_env == 512 || nt_env == 1024) {
       p->nt = nt_env;
+      if (fine && p->nt == 256) p->nt = 512;
     } else if (L.shape.mu == 8) {
       p->nt = ceil_div(L.shape.M, 1024) * L.NSC >= 4 * int64_t(cus) ? 1024 : 512;
     } else {
       p->nt = 512;
       while (p->nt > 256 && ceil_div(L.shape.M, p->nt) * L.NSC < cus) p->nt /= 2;
     }
+    if (fine) p->depth = 1;
     if (per_cu < 1 || per_cu > 8) per_cu = 1024 / p->nt;
     p->bg = 1;
     p->n_groups = 1;
-  } else if (B >= 2 && !force_generic && use_mfma(L, B, cus, tu)) {
+  } else if (B >= 2 && !force_generic && !fine && use_mfma(L, B, cus, tu)) {
     // small batch on the matrix cores: the sign decode per bit is shared by all batch rows (B <= 16 fit one MFMA tile)
     p->kernel = 3;
     p->nt = 256;
@@ -244,7 +252,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     // 45.5 / 48.8 -> 42.6 / 43.6 at B = 4; 7B MLP layers 18.8 / 19.0 -> 15.1 / 17.1 at B = 4
     p->reduce2 = p->depth == 2 && tu.mfma_r2 != 0;
     if (per_cu < 1 || per_cu > 8) per_cu = 3;   // three 256-thread workgroups per CU (the kernel's occupancy)
-  } else if (L.shape.mu == 8 && B >= 2 && !force_generic) {
+  } else if (L.shape.mu == 8 && B >= 2 && !force_generic && !fine) {
     // small batch: 1024-row tiles, one super-chunk per unit (the batch-1 sign stream), batch in groups of four rows
     // (two for B = 2: half the table entries and lookup additions of a padded group of four)
     p->kernel = 2;

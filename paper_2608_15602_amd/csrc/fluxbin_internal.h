@@ -30,10 +30,22 @@ constexpr int64_t kNoallocMaxM = int64_t(kNoallocCounterBytes / (uint64_t(kCount
 
 struct Derived {
   int64_t Npad, ncg, Sv, ncs, NC, NSC, NCP, V, Mp, Gr, Gs, NRP;
+  // Row scales per chunk and row: 1 (a "coarse" chunk: one scale plane, possibly shared by several chunks) or
+  // 128 / g for a group size g below 128 (a "fine" chunk: its own block of Gc scales per row). Gcg for the global
+  // chunks, Gcs for the salient ones.
+  int64_t Gcg, Gcs;
+  int64_t ngcp;   // chunks before the first salient chunk: Kb * ncg global chunks, plus one inert separator chunk
+                  // when Kb * ncg is odd and Gcg != Gcs (so that no super-chunk mixes two scale layouts)
+  int64_t nfc;    // first chunk that uses the salient chunks' scale layout (ngcp with a salient part, else NCP)
+  int64_t Pg;     // row-scale planes of the global bases (the salient planes follow)
 };
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline uint64_t round_up256(uint64_t v) { return (v + 255u) & ~uint64_t(255u); }
+
+// Scales per chunk for a row-scale group of g columns over `extent` columns: fine (128 / g) when the group is shorter
+// than both a chunk and the extent, else coarse (1).
+inline int64_t chunk_scales(int64_t g, int64_t extent) { return (g < kChunk && g < extent) ? kChunk / g : 1; }
 
 inline Derived derive(const fluxbin_shape& s) {
   Derived d{};
@@ -42,14 +54,19 @@ inline Derived derive(const fluxbin_shape& s) {
   const bool sal = s.S > 0 && s.Ks > 0;
   d.Sv = sal ? ceil_div(s.S, kChunk) * kChunk : 0;
   d.ncs = d.Sv / kChunk;
-  d.NC = s.Kb * d.ncg + s.Ks * d.ncs;
+  d.Gcg = chunk_scales(s.g_r, s.N);
+  d.Gcs = sal ? chunk_scales(s.g_s, s.S) : 1;
+  d.ngcp = s.Kb * d.ncg + ((sal && d.Gcg != d.Gcs && (s.Kb * d.ncg) % 2 == 1) ? 1 : 0);
+  d.NC = d.ngcp + s.Ks * d.ncs;
   d.NSC = ceil_div(d.NC, 2);
   d.NCP = 2 * d.NSC;
+  d.nfc = sal ? d.ngcp : d.NCP;
   d.V = kChunk * d.NCP;
   d.Mp = ceil_div(s.M, 64) * 64;
   d.Gr = ceil_div(s.N, s.g_r);
   d.Gs = sal ? ceil_div(s.S, s.g_s) : 0;
-  d.NRP = s.Kb * d.Gr + s.Ks * d.Gs;
+  d.Pg = d.Gcg == 1 ? s.Kb * d.Gr : s.Kb * d.ncg * d.Gcg;
+  d.NRP = d.Pg + (sal ? (d.Gcs == 1 ? s.Ks * d.Gs : s.Ks * d.ncs * d.Gcs) : 0);
   return d;
 }
 

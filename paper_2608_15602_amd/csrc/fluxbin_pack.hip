@@ -22,6 +22,7 @@ struct PackArgs {
   int64_t M, N, W, g_r, S, g_s;
   int32_t Kb, Ks, mu, pad0;
   int64_t Npad, ncg, Sv, ncs, NC, NSC, NCP, V, Mp, Gr, Gs, NRP;
+  int64_t Gcg, Gcs, ngcp, nfc, Pg;
   uint64_t off_signs, off_rscale, off_colscale, off_xidx, off_chunk_plane, off_sal_idx;
 };
 
@@ -29,14 +30,20 @@ struct HeaderWords {
   uint32_t w[64];
 };
 
-// Kind of chunk c: 0 global, 1 salient, 2 pad; plane k and the first local column.
+// Kind of chunk c: 0 global, 1 salient, 2 pad (the separator after the global chunks, or the last chunk of an odd
+// count); base k and the first local column.
 __device__ inline int chunk_kind(const PackArgs& a, int64_t c, int64_t* k, int64_t* col0) {
   if (c < a.Kb * a.ncg) {
     *k = c / a.ncg;
     *col0 = (c % a.ncg) * kChunk;
     return 0;
   }
-  const int64_t c2 = c - a.Kb * a.ncg;
+  if (c < a.ngcp) {
+    *k = 0;
+    *col0 = 0;
+    return 2;
+  }
+  const int64_t c2 = c - a.ngcp;
   if (c2 < a.Ks * a.ncs) {
     *k = c2 / a.ncs;
     *col0 = (c2 % a.ncs) * kChunk;
@@ -45,6 +52,27 @@ __device__ inline int chunk_kind(const PackArgs& a, int64_t c, int64_t* k, int64
   *k = 0;
   *col0 = 0;
   return 2;
+}
+
+// Row scales per chunk c and row (1: one plane; G > 1: a block of G scales per row), by the chunk's scale layout.
+__device__ inline int64_t chunk_G(const PackArgs& a, int64_t c) { return c < a.nfc ? a.Gcg : a.Gcs; }
+
+// Sub-vector held at position q of row i's 16-byte entry of a chunk with G scale groups (spc = 128/mu positions,
+// n = spc/G per group): the groups are rotated by floor(i/n) and the positions within a group by i, so that any
+// spc consecutive rows read spc different sub-vectors at every position (G = 1: (q + i) mod spc).
+__device__ inline int sub_at(int q, int64_t i, int spc, int G) {
+  const int n = spc / G;
+  const int blk = int(((q / n) + (i / n)) % G);
+  const int w = int(((q % n) + i) % n);
+  return blk * n + w;
+}
+
+// Inverse of sub_at: the position of sub-vector u.
+__device__ inline int pos_of(int u, int64_t i, int spc, int G) {
+  const int n = spc / G;
+  const int blk = int((((u / n) - (i / n)) % G + G) % G);
+  const int w = int((((u % n) - i) % n + n) % n);
+  return blk * n + w;
 }
 
 // The 128 virtual sign bits of chunk c for row i (bit r of the result <-> virtual column 128 c + r).
@@ -89,16 +117,18 @@ __global__ void k_pack_signs(PackArgs a) {
   if (a.mu == 8) {
     const int64_t c = 2 * sc + (h ^ ((i & 31) >= 16 ? 1 : 0));
     chunk_bits(a, c, i, bits);
+    const int G = int(chunk_G(a, c));
     for (int q = 0; q < 16; ++q) {
-      const int u = int((q + i) & 15);
+      const int u = sub_at(q, i, 16, G);
       const uint32_t byte = (bits[u >> 2] >> (8 * (u & 3))) & 0xFFu;
       o[q >> 2] |= byte << (8 * (q & 3));
     }
   } else {
     const int64_t c = 2 * sc + h;
     chunk_bits(a, c, i, bits);
+    const int G = int(chunk_G(a, c));
     for (int q = 0; q < 32; ++q) {
-      const int u = int((q + i) & 31);
+      const int u = sub_at(q, i, 32, G);
       const uint32_t nib = (bits[u >> 3] >> (4 * (u & 7))) & 0xFu;
       o[q >> 3] |= nib << (4 * (q & 7));
     }
@@ -107,21 +137,39 @@ __global__ void k_pack_signs(PackArgs a) {
   *dst = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
-// One thread per (row-scale plane, row < Mp).
+// One thread per (row-scale plane, row < Mp). Coarse planes hold one scale per row; a fine chunk's block of G planes
+// holds, for each row, G consecutive scales: slot b is the scale of the chunk's group (b + floor(i/n)) mod G (n = spc/G
+// sub-vectors per group), i.e. the group read at positions b*n .. b*n+n-1 of the row's rotated entry.
 __global__ void k_pack_rscale(PackArgs a) {
   const int64_t e = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (e >= a.NRP * a.Mp) return;
-  const int64_t i = e % a.Mp;
-  const int64_t plane = e / a.Mp;
+  const bool salient = e >= a.Pg * a.Mp;
+  const int64_t G = salient ? a.Gcs : a.Gcg;
+  const int64_t e2 = salient ? e - a.Pg * a.Mp : e;
   uint16_t v = 0;
-  if (i < a.M) {
-    if (plane < a.Kb * a.Gr) {
-      const int64_t k = plane / a.Gr, g = plane % a.Gr;
-      v = a.alpha_r[(k * a.M + i) * a.Gr + g];
-    } else {
-      const int64_t p2 = plane - a.Kb * a.Gr;
-      const int64_t k = p2 / a.Gs, g = p2 % a.Gs;
-      v = a.alpha_sr[(k * a.M + i) * a.Gs + g];
+  if (G == 1) {
+    const int64_t i = e2 % a.Mp;
+    const int64_t plane = e2 / a.Mp;
+    if (i < a.M) {
+      if (!salient) {
+        const int64_t k = plane / a.Gr, g = plane % a.Gr;
+        v = a.alpha_r[(k * a.M + i) * a.Gr + g];
+      } else {
+        const int64_t k = plane / a.Gs, g = plane % a.Gs;
+        v = a.alpha_sr[(k * a.M + i) * a.Gs + g];
+      }
+    }
+  } else {
+    const int64_t blk = e2 / (a.Mp * G);                 // (base, chunk within the base)
+    const int64_t i = (e2 % (a.Mp * G)) / G;
+    const int64_t b = e2 % G;
+    const int64_t nc = salient ? a.ncs : a.ncg;
+    const int64_t k = blk / nc, lc = blk % nc;
+    const int64_t n = (kChunk / a.mu) / G;
+    const int64_t grp = lc * G + (b + i / n) % G;
+    if (i < a.M) {
+      if (!salient && grp < a.Gr) v = a.alpha_r[(k * a.M + i) * a.Gr + grp];
+      if (salient && grp < a.Gs) v = a.alpha_sr[(k * a.M + i) * a.Gs + grp];
     }
   }
   reinterpret_cast<uint16_t*>(a.base + a.off_rscale)[e] = v;
@@ -150,12 +198,16 @@ __global__ void k_pack_columns(PackArgs a) {
     reinterpret_cast<uint16_t*>(a.base + a.off_xidx)[v] = xi;
   }
   if (v < a.NCP) {
+    // first row-scale plane of chunk v; a pad chunk uses the planes of the chunk before it (its signs and column
+    // scales are zero, so any finite scale gives it exactly zero)
+    int64_t c = v;
     int64_t k, col0;
-    const int kind = chunk_kind(a, v, &k, &col0);
-    int32_t plane = 0;
-    if (kind == 0) plane = int32_t(k * a.Gr + col0 / a.g_r);
-    if (kind == 1) plane = int32_t(a.Kb * a.Gr + k * a.Gs + col0 / a.g_s);
-    reinterpret_cast<int32_t*>(a.base + a.off_chunk_plane)[v] = plane;
+    int kind = chunk_kind(a, c, &k, &col0);
+    while (kind == 2 && c > 0) kind = chunk_kind(a, --c, &k, &col0);
+    int64_t plane = 0;
+    if (kind == 0) plane = a.Gcg == 1 ? k * a.Gr + col0 / a.g_r : (k * a.ncg + col0 / kChunk) * a.Gcg;
+    if (kind == 1) plane = a.Pg + (a.Gcs == 1 ? k * a.Gs + col0 / a.g_s : (k * a.ncs + col0 / kChunk) * a.Gcs);
+    reinterpret_cast<int32_t*>(a.base + a.off_chunk_plane)[v] = int32_t(plane);
   }
   const int64_t ns = a.S > 1 ? a.S : 1;
   if (v < ns) {
@@ -169,18 +221,21 @@ __global__ void k_write_header(HeaderWords h, uint32_t* dst) {
 }
 
 // Reads one virtual sign bit (chunk c, column r of the chunk, row i) back from the device layout.
-__device__ inline uint32_t device_bit(const uint8_t* signs, int64_t Mp, int mu, int64_t c, int r, int64_t i) {
+__device__ inline uint32_t device_bit(const PackArgs& a, const uint8_t* signs, int64_t c, int r, int64_t i) {
+  const int64_t Mp = a.Mp;
+  const int mu = a.mu;
+  const int G = int(chunk_G(a, c));
   const int64_t sc = c >> 1;
   if (mu == 8) {
     const int64_t h = (c & 1) ^ ((i & 31) >= 16 ? 1 : 0);
     const int u = r >> 3, n = r & 7;
-    const int q = int((u - i) & 15);
+    const int q = pos_of(u, i, 16, G);
     const uint8_t byte = signs[((sc * 2 + h) * Mp + i) * 16 + q];
     return (byte >> n) & 1u;
   }
   const int64_t h = c & 1;
   const int u = r >> 2, n = r & 3;
-  const int q = int((u - i) & 31);
+  const int q = pos_of(u, i, 32, G);
   const uint8_t byte = signs[((sc * 2 + h) * Mp + i) * 16 + (q >> 1)];
   return (byte >> (4 * (q & 1) + n)) & 1u;
 }
@@ -199,7 +254,7 @@ __global__ void k_unpack(PackArgs a, uint32_t* d_signs, uint32_t* d_dense) {
       const int64_t j = 32 * w + b;
       if (j >= a.N) break;
       const int64_t vcol = k * a.Npad + j;
-      word |= device_bit(signs, a.Mp, a.mu, vcol / kChunk, int(vcol % kChunk), i) << b;
+      word |= device_bit(a, signs, vcol / kChunk, int(vcol % kChunk), i) << b;
     }
     d_signs[e] = word;
   } else if (e < ng + ns) {
@@ -209,8 +264,8 @@ __global__ void k_unpack(PackArgs a, uint32_t* d_signs, uint32_t* d_dense) {
     for (int b = 0; b < 32; ++b) {
       const int64_t t = 32 * w + b;
       if (t >= a.S) break;
-      const int64_t vcol = a.Kb * a.Npad + k * a.Sv + t;
-      word |= device_bit(signs, a.Mp, a.mu, vcol / kChunk, int(vcol % kChunk), i) << b;
+      const int64_t vcol = a.ngcp * kChunk + k * a.Sv + t;
+      word |= device_bit(a, signs, vcol / kChunk, int(vcol % kChunk), i) << b;
     }
     d_dense[f] = word;
   }
@@ -234,12 +289,13 @@ __global__ void k_debug_indices(PackArgs a, uint8_t* d_p) {
   const int64_t sc = c >> 1;
   int64_t h;
   int q;
+  const int G = int(chunk_G(a, c));
   if (a.mu == 8) {
     h = (c & 1) ^ ((i & 31) >= 16 ? 1 : 0);
-    q = int((u - i) & 15);
+    q = pos_of(u, i, 16, G);
   } else {
     h = c & 1;
-    q = int((u - i) & 31);
+    q = pos_of(u, i, 32, G);
   }
   const uint4 entry = reinterpret_cast<const uint4*>(a.base + a.off_signs)[(sc * 2 + h) * a.Mp + i];
   d_p[e] = uint8_t(pattern_at(entry, q, a.mu));
@@ -276,6 +332,11 @@ static PackArgs make_args(const fluxbin_layer& L) {
   a.Gr = d.Gr;
   a.Gs = d.Gs;
   a.NRP = d.NRP;
+  a.Gcg = d.Gcg;
+  a.Gcs = d.Gcs;
+  a.ngcp = d.ngcp;
+  a.nfc = d.nfc;
+  a.Pg = d.Pg;
   a.off_signs = L.off_signs;
   a.off_rscale = L.off_rscale;
   a.off_colscale = L.off_colscale;

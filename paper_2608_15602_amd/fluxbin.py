@@ -17,7 +17,7 @@ FLUXBIN_ERR_INVALID_ARG = 1
 FLUXBIN_ERR_UNSUPPORTED = 2
 FLUXBIN_ERR_BUFFER_TOO_SMALL = 3
 FLUXBIN_ERR_HIP = 4
-FORMAT_VERSION = 1
+FORMAT_VERSION = 2
 HEADER_BYTES = 256
 
 # Entry points declared in include/fluxbin.h.

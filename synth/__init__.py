@@ -15,4 +15,6 @@ from .layers import (  # noqa: F401
     fused_decoder_layers,
     make_weight_matrix,
     vcm_off_equivalent,
+    paper_config,
+    kernel_latency_layers,
 )

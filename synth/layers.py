@@ -49,6 +49,8 @@ class LayerSpec:
     outlier_frac: float = 0.0
     seed: int = 0
     layer_id: int = 0
+    sal_block: int = 0   # > 0: the paper's structured selection, S / ceil(N / sal_block) columns in every block of
+                         # sal_block input columns (else S columns drawn uniformly over all N)
 
     @property
     def G_r(self) -> int:
@@ -102,7 +104,20 @@ def make_layer(spec: LayerSpec) -> SyntheticLayer:
     signs = _random_sign_words(rng, Kb, M, N)
     alpha_r = _f16_bits(np.abs(rng.normal(0.0, 0.05, size=(Kb, M, spec.G_r))))
     alpha_c = _f16_bits(rng.lognormal(0.0, 0.3, size=(Kb, N)))
-    sal_idx = np.sort(rng.choice(N, size=S, replace=False)).astype(np.int32) if S > 0 else np.zeros(0, np.int32)
+    if S > 0 and spec.sal_block > 0:
+        nb = -(-N // spec.sal_block)
+        per = S // nb
+        if per * nb != S:
+            raise ValueError("structured selection needs S = s * ceil(N / sal_block)")
+        parts = []
+        for b0 in range(0, N, spec.sal_block):
+            cols = np.arange(b0, min(N, b0 + spec.sal_block))
+            parts.append(np.sort(rng.choice(cols, size=min(per, cols.size), replace=False)))
+        sal_idx = np.concatenate(parts).astype(np.int32)
+    elif S > 0:
+        sal_idx = np.sort(rng.choice(N, size=S, replace=False)).astype(np.int32)
+    else:
+        sal_idx = np.zeros(0, np.int32)
     sal_signs = _random_sign_words(rng, Ks, M, N)
     alpha_sr = _f16_bits(np.abs(rng.normal(0.0, 0.05, size=(Ks, M, spec.G_s))))
     alpha_sc = _f16_bits(rng.lognormal(0.0, 0.3, size=(Ks, N)))
@@ -145,6 +160,30 @@ def make_activations(layer: SyntheticLayer, B: int, draw: int = 0) -> np.ndarray
     if layer.outliers.size:
         x[:, layer.outliers] *= 20.0
     return _f16_bits(x)
+
+
+def paper_config(name: str, M: int, N: int, Kb: int, s: int = 0, g: int = 128, mu: int = 8, seed: int = 7,
+                 layer_id: int = 0) -> LayerSpec:
+    """A layer in the paper's {Kb-sS-gG} configuration (Sec. 4, App. C.2): Kb global bases with one row scale per
+    (row, block of g columns); with s > 0 also Ks = Kb salient bases on s columns of every block of g (structured
+    selection, Sec. 3.1), each salient base with one row scale per (row, block), i.e. per s VCM dense columns."""
+    if s == 0:
+        return LayerSpec(name, M=M, N=N, Kb=Kb, Ks=0, mu=mu, S=0, g_r=g, g_s=1, seed=seed, layer_id=layer_id)
+    S = s * (-(-N // g))
+    return LayerSpec(name, M=M, N=N, Kb=Kb, Ks=Kb, mu=mu, S=S, g_r=g, g_s=s, seed=seed, layer_id=layer_id,
+                     sal_block=g)
+
+
+def kernel_latency_layers() -> List[LayerSpec]:
+    """The operator shapes and configurations of the paper's kernel-latency table (App. E.4): out x in 4096x4096,
+    5120x5120, 4096x11008 and 5120x13824, each as 2b-g128, 2b-s8-g128, 2b-s16-g128 and 4b-g128."""
+    out = []
+    lid = 200
+    for M, N in ((4096, 4096), (5120, 5120), (4096, 11008), (5120, 13824)):
+        for tag, Kb, s in (("2b", 2, 0), ("2b-s8", 2, 8), ("2b-s16", 2, 16), ("4b", 4, 0)):
+            out.append(paper_config(f"{M}x{N}_{tag}-g128", M, N, Kb, s, 128, layer_id=lid))
+            lid += 1
+    return out
 
 
 def _attn_mlp(name, M, N, Kb, frac, seed, layer_id, mu=8, g_r=128, outlier_frac=0.0):

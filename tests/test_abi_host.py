@@ -57,6 +57,8 @@ def _spec(sh):
     {}, dict(M=28672, N=8192, Kb=3, S=410, g_s=410), dict(M=8192, N=28672, Kb=3, S=1434, g_s=1434),
     dict(M=512, N=256, mu=4, S=8, g_s=8), dict(M=1, N=1, Kb=1, Ks=0, S=0, g_r=1, g_s=1),
     dict(M=70, N=300, Kb=4, Ks=2, S=300, g_s=128, g_r=256), dict(M=65, N=100, S=0, g_r=100),
+    dict(Ks=2, S=256, g_s=8), dict(Ks=2, S=512, g_s=16), dict(g_r=64, Ks=2, S=256, g_s=8),
+    dict(M=70, N=300, Kb=3, S=40, g_r=64, g_s=16), dict(M=512, N=256, mu=4, S=64, g_s=4, g_r=32),
 ])
 def test_pack_query_matches_format(L, kw):
     sh = _shape(**kw)
@@ -75,10 +77,10 @@ def test_pack_query_matches_format(L, kw):
     (dict(mu=6), fb.FLUXBIN_ERR_UNSUPPORTED),
     (dict(g_r=0), fb.FLUXBIN_ERR_INVALID_ARG),
     (dict(g_r=100), fb.FLUXBIN_ERR_INVALID_ARG),       # not whole sub-vectors of mu = 8
-    (dict(g_r=64), fb.FLUXBIN_ERR_UNSUPPORTED),        # whole sub-vectors, but not a multiple of 128
+    (dict(g_r=96), fb.FLUXBIN_ERR_UNSUPPORTED),        # whole sub-vectors, but neither a divisor nor a multiple of 128
     (dict(S=5000), fb.FLUXBIN_ERR_INVALID_ARG),
     (dict(S=300, g_s=12), fb.FLUXBIN_ERR_INVALID_ARG),
-    (dict(S=300, g_s=64), fb.FLUXBIN_ERR_UNSUPPORTED),
+    (dict(S=300, g_s=192), fb.FLUXBIN_ERR_UNSUPPORTED),
 ])
 def test_pack_query_rejects(L, kw, status):
     n = ctypes.c_size_t(123)
@@ -162,14 +164,15 @@ def _fake_layer(L, spec):
     return out, total
 
 
-def test_layer_from_header(L):
-    spec = LayerSpec("h", M=1000, N=300, Kb=3, Ks=1, mu=8, S=17, g_r=128, g_s=17)
+@pytest.mark.parametrize("g_r,g_s", [(128, 17), (64, 8)])
+def test_layer_from_header(L, g_r, g_s):
+    spec = LayerSpec("h", M=1000, N=300, Kb=3, Ks=1, mu=8, S=17, g_r=g_r, g_s=g_s)
     out, total = _fake_layer(L, spec)
     pb = fmt.packed_bytes(spec)
     d = fmt.derived(spec)
     assert out.off_signs == pb["off_signs"] and out.off_sal_idx == pb["off_sal_idx"]
     assert out.NSC == d["NSC"] and out.Mp == d["Mp"] and out.NRP == d["NRP"]
-    assert out.format_version == 1 and out.bytes == total
+    assert out.format_version == fb.FORMAT_VERSION == 2 and out.bytes == total
     bad = bytearray(_header_bytes(spec))
     bad[0] ^= 1
     assert L.fluxbin_layer_from_header(ctypes.create_string_buffer(bytes(bad), 256), FAKE_DEVICE_PTR, total,

@@ -8,7 +8,7 @@ import pytest
 
 import oracle
 from oracle import format_oracle as fmt
-from synth import CONFIGS, LayerSpec, config_layers, make_activations, make_layer
+from synth import CONFIGS, LayerSpec, config_layers, kernel_latency_layers, make_activations, make_layer, paper_config
 
 from conftest import gpu_available
 from gpu_util import log, pack_layer, run_gemm, sample_rows, x_tensor
@@ -56,6 +56,11 @@ SMALL_SPECS = [
     LayerSpec("mu8_ragged", M=333, N=300, Kb=3, Ks=2, mu=8, S=77, g_r=128, g_s=77, seed=5),
     LayerSpec("mu4_ragged", M=100, N=200, Kb=1, Ks=1, mu=4, S=130, g_r=200, g_s=128, seed=6),
     LayerSpec("no_salient", M=64, N=128, Kb=2, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=7),
+    # fine row-scale groups: g_r = 64 (two scales per global chunk), g_s = 8 (one per mu = 8 sub-vector), 9 global
+    # chunks (odd: separator chunk); mu = 4 with g_r = 32 and g_s = 16; the paper's 2b-s16-g128
+    LayerSpec("fine_mu8", M=333, N=300, Kb=3, Ks=2, mu=8, S=77, g_r=64, g_s=8, seed=8),
+    LayerSpec("fine_mu4", M=100, N=200, Kb=1, Ks=1, mu=4, S=130, g_r=32, g_s=16, seed=9),
+    LayerSpec("fine_s16", M=200, N=1024, Kb=2, Ks=2, mu=8, S=128, g_r=128, g_s=16, seed=10, sal_block=128),
 ]
 
 
@@ -115,7 +120,7 @@ def test_unpack_and_indices_bit_exact(spec):
     if spec.S > 0 and spec.Ks > 0:
         ncs = fmt.derived(spec)["ncs"]
         for k in range(spec.Ks):
-            c0 = spec.Kb * ncg + k * ncs
+            c0 = fmt.derived(spec)["ngcp"] + k * ncs   # after the separator chunk, if any
             sblk = pc[c0:c0 + ncs].transpose(1, 0, 2).reshape(spec.M, -1)
             n = idx["salient"].shape[2]
             assert np.array_equal(sblk[:, :n], idx["salient"][k])
@@ -234,6 +239,13 @@ EDGE_SPECS = [
     LayerSpec("four_bases", M=513, N=1024, Kb=4, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=16),
     LayerSpec("mu4_ragged", M=777, N=260, Kb=2, Ks=1, mu=4, S=20, g_r=260, g_s=20, seed=17),
     LayerSpec("tiny_N", M=70, N=7, Kb=2, Ks=1, mu=4, S=3, g_r=7, g_s=3, seed=18),
+    # fine row-scale groups (group shorter than a 128-column chunk) on the global side, the salient side or both
+    LayerSpec("fine_g64_s8", M=1000, N=300, Kb=3, Ks=2, mu=8, S=77, g_r=64, g_s=8, seed=19),
+    LayerSpec("fine_g8_s16", M=700, N=512, Kb=2, Ks=1, mu=8, S=100, g_r=8, g_s=16, seed=20),
+    LayerSpec("fine_g32_s64", M=300, N=1024, Kb=1, Ks=1, mu=8, S=300, g_r=32, g_s=64, seed=21),
+    LayerSpec("fine_global_only", M=600, N=384, Kb=2, Ks=0, mu=8, S=0, g_r=16, g_s=1, seed=22),
+    LayerSpec("fine_one_row", M=1, N=128, Kb=1, Ks=1, mu=8, S=16, g_r=64, g_s=8, seed=23),
+    LayerSpec("fine_mu4", M=333, N=260, Kb=2, Ks=1, mu=4, S=40, g_r=16, g_s=4, seed=24),
 ]
 
 
@@ -242,6 +254,22 @@ EDGE_SPECS = [
 def test_edge_shapes(spec, B):
     """B = 1: batch-1 kernels; B = 3: LUT batch kernel (mu = 8) or matrix cores (mu = 4); B = 9: matrix cores."""
     _parity(spec, B)
+
+
+@pytest.mark.parametrize("spec", kernel_latency_layers(), ids=lambda s: s.name)
+def test_paper_kernel_latency_configs_full_size(spec):
+    """The operator shapes and configurations of the paper's kernel-latency table (App. E.4): 2b-g128, 2b-s8-g128
+    (structured selection of 8 salient columns per 128, one salient row scale per row and block, Ks = Kb = 2),
+    2b-s16-g128 and 4b-g128 at full size in the benchmark's launch configuration, sampled rows against the oracle."""
+    rows = sample_rows(spec.M, 384, seed=spec.layer_id)
+    _parity(spec, 1, rows=rows)
+
+
+@pytest.mark.parametrize("B", [2, 4])
+def test_paper_config_small_batch(B):
+    """A paper-configuration layer (fine salient row-scale groups) at small batch: the generic kernel."""
+    spec = paper_config("2b-s8-g128_small", 1536, 2048, 2, 8, 128)
+    _parity(spec, B, out_fp32=True)
 
 
 @pytest.mark.parametrize("spec", [
@@ -379,7 +407,8 @@ def test_graph_replays_match_eager():
     log("case graph replay")
     outs = []
     specs = [LayerSpec("g1", M=3000, N=2048, Kb=2, Ks=1, mu=8, S=70, g_r=128, g_s=70, seed=31),
-             LayerSpec("g2", M=700, N=512, Kb=2, Ks=1, mu=4, S=9, g_r=512, g_s=9, seed=32)]
+             LayerSpec("g2", M=700, N=512, Kb=2, Ks=1, mu=4, S=9, g_r=512, g_s=9, seed=32),
+             LayerSpec("g3", M=2000, N=1024, Kb=2, Ks=2, mu=8, S=128, g_r=64, g_s=16, seed=33, sal_block=128)]
     for spec in specs:
         L = make_layer(spec)
         packed = pack_layer(L)
