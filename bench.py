@@ -411,12 +411,13 @@ def vcm_ablation_us(g_r: str, launches: int = 40):
     return out
 
 
-def decomposition_ms(M: int = 8192, N: int = 8192, g: int = 128, s: int = 8, Kb: int = 2, Ks: int = 1, T: int = 10,
+def decomposition_ms(M: int = 8192, N: int = 8192, g: int = 128, s: int = 8, Kb: int = 2, Ks: int = 2, T: int = 10,
                      oracle_rows: int = 512):
-    """The weight decomposition (FluxBin-Hybrid with a diagonal inverse Hessian: saliency search, Kb global bases per
-    g-column block, Ks salient bases on s columns per block, T alternating rounds) of a synthetic M x N fp32 matrix on
-    the GPU (HIP events around the three library calls, median of 3), and the fp64 oracle on an oracle_rows x N
-    slice of it on the host (one run), reported per million weights."""
+    """The weight decomposition in the paper's 2b-s8-g128 configuration (Alg. FluxBin-Hybrid with a diagonal inverse
+    Hessian: per g-column block the s most salient columns, Kb global bases, Ks salient bases of the block's residual
+    on those columns, one row scale per row and block on both branches, T alternating rounds) of a synthetic M x N fp32
+    matrix on the GPU (HIP events around the three library calls, median of 3), and the fp64 oracle on an
+    oracle_rows x N slice of it on the host (one run), reported per million weights."""
     import numpy as np
     import torch
     from oracle import rc_oracle as rc
@@ -429,7 +430,7 @@ def decomposition_ms(M: int = 8192, N: int = 8192, g: int = 128, s: int = 8, Kb:
     def run():
         _, _, mask = fb.fluxbin_structural_search(Wt, ht, g, s)
         gs, gar, gac = fb.fluxbin_rc_decompose(Wt, Kb, T, g)
-        fb.fluxbin_rc_decompose(Wt, Ks, T, N, mask=mask, prior=(gs, gar, gac, g))
+        fb.fluxbin_rc_decompose(Wt, Ks, T, g, mask=mask, prior=(gs, gar, gac, g))
 
     run()
     torch.cuda.synchronize()

@@ -26,8 +26,10 @@ Readings where the paper is silent:
   * ties in the sign search keep the first combination in the order c = 0..2^K-1, where bit k of c set means b_k = +1;
   * one row scale per (row, block of g columns): the blocks are decomposed independently (with a diagonal inverse
     Hessian the GPTQ error compensation between blocks is exactly zero, the synthetic setting used here);
-  * the salient refinement is decomposed over all salient columns at once (one salient row scale per row), the
-    grouping the packed format supports for an unstructured dense salient block (g_s >= S);
+  * the salient refinement follows the hybrid procedure block by block: within each block of g columns, RC_Decomp of
+    the block's residual (after its global bases) on the block's salient mask, so every salient base has one row
+    scale per (row, block), the 16*M*N/g term of the storage analysis (App. C.2); in the packed format's dense salient
+    columns that is one scale per s columns (g_s = s);
   * the top-s selection orders columns by decreasing saliency, equal scores by increasing column index;
   * eps = 1e-12 (the paper names a stability constant without a value).
 """
@@ -149,14 +151,35 @@ def structural_search(W: np.ndarray, hinv_diag: np.ndarray, g: int, s: int) -> n
 
 def hybrid_quantize(W: np.ndarray, hinv_diag: np.ndarray, g: int, s: int, Kb: int, Ks: int, T: int,
                     eps: float = EPS) -> Dict[str, np.ndarray]:
-    """FluxBin-Hybrid with a diagonal inverse Hessian: salient columns by structural search, global bases by RC_Decomp
-    per block, salient bases by RC_Decomp of the residual on the salient columns (one salient row scale per row)."""
+    """FluxBin-Hybrid (App. algorithm "FluxBin-Hybrid") with a diagonal inverse Hessian, block by block over the
+    column blocks of g: (1) structural search picks the block's s salient columns; (2) RC_Decomp of the block into Kb
+    global bases (all columns); (3) RC_Decomp of the block's residual into Ks salient bases on the block's mask. The
+    error compensation between blocks (step 4) is zero for a diagonal inverse Hessian, so the blocks are independent.
+    Returns the salient columns and, per branch, the bases of all blocks side by side: signs [K, M, N], row scales
+    [K, M, ceil(N/g)] (one per row and block), column scales [K, N]."""
     W = np.asarray(W, dtype=np.float64)
     M, N = W.shape
-    sal = structural_search(W, hinv_diag, g, s)
-    glob = rc_decomp(W, np.ones(N, dtype=bool), Kb, T, g, eps)
-    R = W - reconstruct(glob["B"], glob["alpha_r"], glob["alpha_c"], g)
-    mask = np.zeros(N, dtype=bool)
-    mask[sal] = True
-    salr = rc_decomp(R, mask, Ks, T, N, eps) if Ks > 0 else None
-    return dict(sal_idx=sal, glob=glob, sal=salr)
+    G = -(-N // g)
+    sal_parts = []
+    glob = dict(B=np.zeros((Kb, M, N), dtype=np.int8), alpha_r=np.zeros((Kb, M, G)), alpha_c=np.zeros((Kb, N)))
+    salr = (dict(B=np.zeros((Ks, M, N), dtype=np.int8), alpha_r=np.zeros((Ks, M, G)), alpha_c=np.zeros((Ks, N)))
+            if Ks > 0 else None)
+    for blk in range(G):
+        cols = slice(blk * g, min(N, (blk + 1) * g))
+        Wb = W[:, cols]
+        nb = Wb.shape[1]
+        idx = structural_search(Wb, np.asarray(hinv_diag, dtype=np.float64)[cols], nb, s)   # step 1
+        sal_parts.append(idx + blk * g)
+        gb = rc_decomp(Wb, np.ones(nb, dtype=bool), Kb, T, nb, eps)                      # step 2
+        glob["B"][:, :, cols] = gb["B"]
+        glob["alpha_r"][:, :, blk] = gb["alpha_r"][:, :, 0]
+        glob["alpha_c"][:, cols] = gb["alpha_c"]
+        if Ks > 0:                                                                        # step 3
+            Rb = Wb - reconstruct(gb["B"], gb["alpha_r"], gb["alpha_c"], nb)
+            mb = np.zeros(nb, dtype=bool)
+            mb[idx] = True
+            sb = rc_decomp(Rb, mb, Ks, T, nb, eps)
+            salr["B"][:, :, cols] = sb["B"]
+            salr["alpha_r"][:, :, blk] = sb["alpha_r"][:, :, 0]
+            salr["alpha_c"][:, cols] = sb["alpha_c"]
+    return dict(sal_idx=np.concatenate(sal_parts).astype(np.int64), glob=glob, sal=salr)

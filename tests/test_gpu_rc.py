@@ -70,12 +70,13 @@ def test_rc_decompose_matches_oracle(K):
 
 
 def test_rc_decompose_masked_with_prior_matches_oracle():
-    """The salient refinement of FluxBin-Hybrid: the residual of a 2-base global decomposition, decomposed on a column
-    mask by one base with one row scale per row."""
+    """The salient refinement of FluxBin-Hybrid: the residual of a 2-base global decomposition, decomposed on the
+    salient column mask by two bases with one row scale per (row, block of g columns), as Alg. FluxBin-Hybrid does
+    block by block."""
     import torch
     M, N, g = 128, 256, 64
     W, hinv = make_weight_matrix(M, N, seed=41, outlier_frac=0.02)
-    ref = rc.hybrid_quantize(W.astype(np.float64), hinv, g=g, s=4, Kb=2, Ks=1, T=3)
+    ref = rc.hybrid_quantize(W.astype(np.float64), hinv, g=g, s=4, Kb=2, Ks=2, T=3)
     gs, gar, gac = _gpu_rc(W, 2, 3, g)
     from paper_2608_15602_amd import fluxbin as fb
     Wt = torch.from_numpy(W).cuda()
@@ -83,7 +84,7 @@ def test_rc_decompose_masked_with_prior_matches_oracle():
     torch.cuda.synchronize()
     assert np.array_equal(idx.cpu().numpy().astype(np.int64), ref["sal_idx"]), "salient columns differ"
     _close(scores.cpu().numpy(), rc.saliency(W.astype(np.float64), hinv), "saliency", rtol=1e-12)
-    ss, sar, sac = fb.fluxbin_rc_decompose(Wt, 1, 3, N, mask=mask, prior=(gs, gar, gac, g))
+    ss, sar, sac = fb.fluxbin_rc_decompose(Wt, 2, 3, g, mask=mask, prior=(gs, gar, gac, g))
     torch.cuda.synchronize()
     assert np.array_equal(gs.cpu().numpy().view(np.uint32), _bits(ref["glob"]["B"])), "global signs differ"
     assert np.array_equal(ss.cpu().numpy().view(np.uint32), _bits(ref["sal"]["B"])), "salient signs differ"
@@ -107,10 +108,11 @@ def test_structural_search_matches_oracle():
 
 
 def test_decomposed_layer_through_pack_and_gemv():
-    """A 2048 x 2048 weight matrix decomposed on the GPU (saliency, 2 global bases per 128-column block, 1 salient base
-    on 8 columns per block), scales rounded to fp16, packed and multiplied (B = 1 and 4) by the library: the result
-    matches the GEMV oracle on the same layer; the signs match the decomposition oracle, and the hybrid error is below
-    the global one."""
+    """A 2048 x 2048 weight matrix decomposed on the GPU in the paper's 2b-s8-g128 configuration (Alg. FluxBin-Hybrid:
+    per 128-column block 8 salient columns, 2 global bases, 2 salient bases of the block's residual on them, one row
+    scale per row and block on both branches), scales rounded to fp16, packed with one salient row scale per 8 dense
+    columns (g_s = 8) and multiplied (B = 1 and 4) by the library: the result matches the GEMV oracle on the same
+    layer; the signs match the decomposition oracle, and the hybrid error is below the global one."""
     import torch
     from paper_2608_15602_amd import fluxbin as fb
     from gpu_util import pack_layer, run_gemm
@@ -119,15 +121,16 @@ def test_decomposed_layer_through_pack_and_gemv():
     Wt = torch.from_numpy(W).cuda()
     _, idx, mask = fb.fluxbin_structural_search(Wt, torch.from_numpy(hinv).cuda(), g, s)
     gs, gar, gac = fb.fluxbin_rc_decompose(Wt, 2, T, g)
-    ss, sar, sac = fb.fluxbin_rc_decompose(Wt, 1, T, N, mask=mask, prior=(gs, gar, gac, g))
+    ss, sar, sac = fb.fluxbin_rc_decompose(Wt, 2, T, g, mask=mask, prior=(gs, gar, gac, g))
     torch.cuda.synchronize()
-    ref = rc.hybrid_quantize(W.astype(np.float64), hinv, g=g, s=s, Kb=2, Ks=1, T=T)
+    ref = rc.hybrid_quantize(W.astype(np.float64), hinv, g=g, s=s, Kb=2, Ks=2, T=T)
     assert np.array_equal(gs.cpu().numpy().view(np.uint32), _bits(ref["glob"]["B"])), "global signs differ"
     assert np.array_equal(ss.cpu().numpy().view(np.uint32), _bits(ref["sal"]["B"])), "salient signs differ"
     sal = idx.cpu().numpy().astype(np.int32)
     S = len(sal)
     f16 = lambda a: np.ascontiguousarray(a.astype(np.float16)).view(np.uint16)
-    spec = LayerSpec("decomposed", M=M, N=N, Kb=2, Ks=1, mu=8, S=S, g_r=g, g_s=S, seed=0)
+    assert S == s * (N // g)
+    spec = LayerSpec("decomposed", M=M, N=N, Kb=2, Ks=2, mu=8, S=S, g_r=g, g_s=s, seed=0)
     L = SyntheticLayer(spec=spec, signs=gs.cpu().numpy().view(np.uint32), alpha_r=f16(gar.cpu().numpy()),
                        alpha_c=f16(gac.cpu().numpy()), sal_idx=sal, sal_signs=ss.cpu().numpy().view(np.uint32),
                        alpha_sr=f16(sar.cpu().numpy()), alpha_sc=f16(sac.cpu().numpy()),
@@ -141,7 +144,7 @@ def test_decomposed_layer_through_pack_and_gemv():
         log(f"  decomposed layer B={B}: normwise {r['normwise']:.2e}")
         assert r["ok"], r
     Wg = rc.reconstruct(ref["glob"]["B"], ref["glob"]["alpha_r"], ref["glob"]["alpha_c"], g)
-    Wh = Wg + rc.reconstruct(ref["sal"]["B"], ref["sal"]["alpha_r"], ref["sal"]["alpha_c"], N)
+    Wh = Wg + rc.reconstruct(ref["sal"]["B"], ref["sal"]["alpha_r"], ref["sal"]["alpha_c"], g)
     assert ((W - Wh) ** 2).sum() < ((W - Wg) ** 2).sum()
 
 

@@ -130,7 +130,7 @@ def test_hybrid_refines_the_salient_columns():
     hinv = np.ones(N)
     h = rc.hybrid_quantize(W, hinv, g=g, s=2, Kb=2, Ks=1, T=5)
     Wg = rc.reconstruct(h["glob"]["B"], h["glob"]["alpha_r"], h["glob"]["alpha_c"], g)
-    Ws = rc.reconstruct(h["sal"]["B"], h["sal"]["alpha_r"], h["sal"]["alpha_c"], N)
+    Ws = rc.reconstruct(h["sal"]["B"], h["sal"]["alpha_r"], h["sal"]["alpha_c"], g)
     sal = h["sal_idx"]
     assert 3 in sal and 40 in sal and len(sal) == 2 * (N // g)
     off = np.setdiff1d(np.arange(N), sal)
@@ -138,3 +138,59 @@ def test_hybrid_refines_the_salient_columns():
     err_g = ((W - Wg)[:, sal] ** 2).sum()
     err_h = ((W - Wg - Ws)[:, sal] ** 2).sum()
     assert err_h < 0.7 * err_g
+
+
+def test_hybrid_salient_scales_are_per_block_closed_form():
+    """Alg. FluxBin-Hybrid decomposes the salient residual block by block, so each salient base has one row scale per
+    (row, block of g columns). With T = 0 rounds and one salient base the greedy initialization has a closed form: on
+    the block's salient columns B_s = sign(R), the row scale is the mean |R| of the row over those columns (Prop. 3.2
+    with unit column scales), and the column scale is sum_i a_i |R_ij| / sum_i a_i^2. Computed here directly from the
+    global residual; a salient decomposition pooled over all blocks (one scale per row) gives other values."""
+    rng = _rng(11)
+    M, N, g, s = 6, 32, 8, 3
+    W = rng.normal(size=(M, N))
+    hinv = rng.uniform(0.5, 2.0, size=N)
+    h = rc.hybrid_quantize(W, hinv, g=g, s=s, Kb=1, Ks=1, T=0)
+    R = W - rc.reconstruct(h["glob"]["B"], h["glob"]["alpha_r"], h["glob"]["alpha_c"], g)
+    sal = h["sal_idx"]
+    assert h["sal"]["alpha_r"].shape == (1, M, N // g)
+    for b in range(N // g):
+        cols = [j for j in sal if b * g <= j < (b + 1) * g]
+        assert len(cols) == s
+        Rb = R[:, cols]
+        a = np.abs(Rb).mean(axis=1)
+        assert np.allclose(h["sal"]["alpha_r"][0, :, b], a, rtol=1e-10, atol=0)   # eps = 1e-12 in the quotients
+        c = (a[:, None] * np.abs(Rb)).sum(axis=0) / (a * a).sum()
+        assert np.allclose(h["sal"]["alpha_c"][0, cols], c, rtol=1e-10, atol=0)
+        assert np.array_equal(h["sal"]["B"][0][:, cols], np.where(Rb >= 0, 1, -1))
+    pooled = np.abs(R[:, sal]).mean(axis=1)
+    assert not np.allclose(h["sal"]["alpha_r"][0, :, 0], pooled)
+
+
+def test_hybrid_equals_its_blocks():
+    """With a diagonal inverse Hessian the GPTQ compensation between blocks is zero, so the hybrid decomposition of W is
+    the side-by-side concatenation of the hybrid decompositions of its column blocks (each a single block)."""
+    rng = _rng(12)
+    M, N, g, s = 20, 48, 16, 4
+    W = rng.normal(size=(M, N))
+    W[:, [5, 30]] *= 8.0
+    hinv = rng.uniform(0.5, 2.0, size=N)
+    h = rc.hybrid_quantize(W, hinv, g=g, s=s, Kb=2, Ks=2, T=3)
+    for b in range(N // g):
+        cols = slice(b * g, (b + 1) * g)
+        hb = rc.hybrid_quantize(W[:, cols], hinv[cols], g=g, s=s, Kb=2, Ks=2, T=3)
+        assert np.array_equal(hb["sal_idx"] + b * g, h["sal_idx"][b * s:(b + 1) * s])
+        for br in ("glob", "sal"):
+            assert np.array_equal(hb[br]["B"], h[br]["B"][:, :, cols])
+            assert np.array_equal(hb[br]["alpha_r"][:, :, 0], h[br]["alpha_r"][:, :, b])
+            assert np.array_equal(hb[br]["alpha_c"], h[br]["alpha_c"][:, cols])
+    # and the same as RC_Decomp over all blocks at once (its row scales are per block too)
+    glob = rc.rc_decomp(W, np.ones(N, bool), 2, 3, g)
+    assert np.array_equal(glob["B"], h["glob"]["B"])
+    assert np.allclose(glob["alpha_r"], h["glob"]["alpha_r"], rtol=1e-13, atol=0)
+    mask = np.zeros(N, bool)
+    mask[h["sal_idx"]] = True
+    R = W - rc.reconstruct(glob["B"], glob["alpha_r"], glob["alpha_c"], g)
+    salr = rc.rc_decomp(R, mask, 2, 3, g)
+    assert np.array_equal(salr["B"], h["sal"]["B"])
+    assert np.allclose(salr["alpha_r"], h["sal"]["alpha_r"], rtol=1e-10, atol=1e-14)
