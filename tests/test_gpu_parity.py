@@ -169,9 +169,10 @@ def test_config4_mlp70b(g_r):
         _parity(spec, 1, rows=sample_rows(spec.M, 768))
 
 
-def test_config5_layer70b():
+@pytest.mark.parametrize("g_r", ["128", "N"])
+def test_config5_layer70b(g_r):
     import torch
-    for spec in config_layers("c5_layer70b", "128"):
+    for spec in config_layers("c5_layer70b", g_r):
         L = make_layer(spec)
         packed = pack_layer(L)
         for B in CONFIGS["c5_layer70b"]["batches"]:
@@ -501,3 +502,78 @@ def test_lut_batch_second_kernel_reduction_equals_counters(B):
                           lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
     assert np.array_equal(y["1"], y["0"]), int(np.sum(y["1"] != y["0"]))
     _check(y["1"], oracle.gemv_dense(L, x), "LUT batch second-kernel reduction vs oracle")
+
+
+
+# ------------------------------------------------------------------------------------------- fp16 subnormal inputs
+
+def _subnormals(rng, shape):
+    """Random fp16 subnormal bit patterns (nonzero exponent-0 values, random sign)."""
+    mag = rng.integers(1, 1024, size=shape).astype(np.uint16)
+    return (mag | (rng.integers(0, 2, size=shape).astype(np.uint16) << 15)).astype(np.uint16)
+
+
+def _subnormal_case(which, mu):
+    spec = LayerSpec(f"sub_{which}_mu{mu}", M=1500, N=1024, Kb=2, Ks=1, mu=mu, S=61, g_r=128, g_s=61, seed=70)
+    L = make_layer(spec)
+    rng = np.random.default_rng(71)
+    B = 9
+    x = make_activations(L, B)
+    if which == "colscale":      # every global and salient column scale subnormal (positive: scales here are > 0)
+        L.alpha_c[:] = _subnormals(rng, L.alpha_c.shape) & 0x7FFF
+        L.alpha_sc[:] = _subnormals(rng, L.alpha_sc.shape) & 0x7FFF
+    elif which == "rowscale":    # every row scale subnormal
+        L.alpha_r[:] = _subnormals(rng, L.alpha_r.shape) & 0x7FFF
+        L.alpha_sr[:] = _subnormals(rng, L.alpha_sr.shape) & 0x7FFF
+    else:                        # every activation subnormal
+        x = _subnormals(rng, x.shape)
+    return L, x
+
+
+@pytest.mark.parametrize("kernel", ["batch1", "lut_batch", "mfma"])
+@pytest.mark.parametrize("which", ["colscale", "rowscale", "x"])
+def test_fp16_subnormals_are_honoured(which, kernel):
+    """Subnormal fp16 column scales, row scales or activations (the reading that subnormals are honoured on both
+    sides): every product and sum stays far above the fp32 subnormal range, so a kernel that flushed fp16 subnormals
+    to zero would return zeros. Batch 1, the LUT batch kernel at B = 3 and the matrix-core kernel at B = 3 and 9,
+    against the fp64 oracle (fp32 output)."""
+    L, x = _subnormal_case(which, 8)
+    packed = pack_layer(L)
+    env = {"batch1": {}, "lut_batch": {"FLUXBIN_MFMA": "0"}, "mfma": {"FLUXBIN_MFMA": "1"}}[kernel]
+    for B in ((1,) if kernel == "batch1" else (3, 9) if kernel == "mfma" else (3,)):
+        log(f"case subnormal {which} kernel={kernel} B={B}")
+        xb = x[:B]
+        y = _with_env(env, lambda: run_gemm(packed, xb, out_fp32=True))
+        y_ref = oracle.gemv_dense(L, xb)
+        assert np.abs(y_ref).max() > 0
+        _check(y, y_ref, f"subnormal {which}, {kernel}, B={B}")
+
+
+@pytest.mark.parametrize("which", ["colscale", "x"])
+def test_fp16_subnormals_mu4(which):
+    """The same at mu = 4 (batch-1 kernel, and the matrix cores at B = 3)."""
+    L, x = _subnormal_case(which, 4)
+    packed = pack_layer(L)
+    for B in (1, 3):
+        log(f"case subnormal mu4 {which} B={B}")
+        y = run_gemm(packed, x[:B], out_fp32=True)
+        _check(y, oracle.gemv_dense(L, x[:B]), f"subnormal mu4 {which} B={B}")
+
+
+@pytest.mark.parametrize("kernel,B", [("lut_batch", 2), ("lut_batch", 4), ("mfma", 3), ("mfma", 16),
+                                      ("generic", 3)])
+def test_small_batch_power_of_two_scaling_is_exact(kernel, B):
+    """y(2x) == 2 y(x) bit for bit on the small-batch kernels (scaling by two commutes with every fp32 rounding when
+    nothing overflows or underflows), and repeated calls are bitwise equal."""
+    spec = LayerSpec("pow2", M=3000, N=2048, Kb=2, Ks=1, mu=8, S=70, g_r=128, g_s=70, seed=72)
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    x = make_activations(L, B)
+    x2 = (oracle.f16_to_f64(x) * 2).astype(np.float16).view(np.uint16)
+    env = {"lut_batch": {"FLUXBIN_MFMA": "0"}, "mfma": {"FLUXBIN_MFMA": "1"}, "generic": {"FLUXBIN_GENERIC": "1"}}[kernel]
+    log(f"case y(2x) == 2 y(x) {kernel} B={B}")
+    y1 = _with_env(env, lambda: run_gemm(packed, x, out_fp32=True))
+    y1b = _with_env(env, lambda: run_gemm(packed, x, out_fp32=True))
+    y2 = _with_env(env, lambda: run_gemm(packed, x2, out_fp32=True))
+    assert np.array_equal(y1, y1b)
+    assert np.array_equal(y2, 2 * y1), int(np.sum(y2 != 2 * y1))
