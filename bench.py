@@ -114,9 +114,10 @@ class Bench:
         torch.cuda.synchronize()
         return e0.elapsed_time(e1)
 
-    def run(self, steps: int, warmup: int):
-        """Warmup steps, then exactly `steps` steps replayed from one HIP graph between two events (synchronized on
-        both sides). Returns the total milliseconds and the wall-clock seconds of the timed region."""
+    def run(self, steps: int, warmup: int, replays: int = 1):
+        """Warmup steps, then a HIP graph of exactly `steps` steps, replayed `replays` times, each replay between two
+        events on the replay stream (synchronized on both sides). Returns the milliseconds of every replay and the
+        wall-clock seconds of all of them."""
         import torch
         for s in range(warmup):
             for it in self.items:
@@ -125,9 +126,9 @@ class Bench:
         g.replay()          # first replay outside the timed region (graph upload)
         torch.cuda.synchronize()
         wall0 = time.perf_counter()
-        total_ms = self.time_graph(g)
+        ms = [self.time_graph(g) for _ in range(replays)]
         wall = time.perf_counter() - wall0
-        return total_ms, wall
+        return ms, wall
 
     def per_launch_us(self, launches: int = 60, reps: int = 5):
         """Average duration of each layer's launch: a graph of `launches` launches of that layer alone (rotating
@@ -340,8 +341,8 @@ def decoder_layer_us(g_r: str, batches=(1, 4, 16), steps: int = 40):
                 if B != b.B:
                     b.set_batch(B)
                 b.run(2, 2)   # warm up graph capture for this batch
-                total_ms, _ = b.run(steps, 2)
-                us = total_ms * 1000.0 / steps
+                ms, _ = b.run(steps, 2, replays=5)
+                us = sorted(ms)[len(ms) // 2] * 1000.0 / steps
                 step_bytes = sum(it["bytes"] for it in b.items)
                 out[f"{variant}{kind}_B{B}"] = {"us_per_layer": round(us, 2),
                                                 "GBps": round(step_bytes / (us * 1e-6) / 1e9, 1),
@@ -370,21 +371,71 @@ def kernel_variants_us(g_r: str, launches: int = 40):
 
 
 def mu_profile_us(g_r: str, launches: int = 40):
-    """mu = 8 against mu = 4 (same weights' shapes and seeds) on the 7B attention and MLP layers, batch 1; mu = 4 runs
-    the generic kernel (one chunk per unit, tables of 16 entries)."""
+    """mu = 8 against mu = 4 (same shapes and seeds) at batch 1 (Sec. 3.2 trades table size against lookups; App. E.2
+    profiles mu on the 7B model): the 7B attention and MLP layers, the 70B MLP layers, and the distinct shapes of the
+    70B decoder layer (q/o 8192x8192, k/v 1024x8192, gate/up 28672x8192, down 8192x28672) in both hybrid variants."""
     import torch
     from synth import config_layers
     out = {}
-    for cfg in ("c2_attn7b", "c3_mlp7b"):
-        for spec in config_layers(cfg, g_r):
+    c5 = [sp for sp in config_layers("c5_layer70b", g_r) if sp.name.split("_", 1)[1] in ("q", "k", "gate", "down")]
+    for cfg, specs in (("c2_attn7b", config_layers("c2_attn7b", g_r)), ("c3_mlp7b", config_layers("c3_mlp7b", g_r)),
+                       ("c4_mlp70b", config_layers("c4_mlp70b", g_r)), ("c5_layer70b", c5)):
+        for spec in specs:
+            row = {"shape_out_x_in": f"{spec.M}x{spec.N}"}
             for mu in (8, 4):
                 sp = spec.with_(mu=mu, name=f"{spec.name}_mu{mu}")
                 b = Bench([sp], 1, COPIES_BYTES_PER_LAYER)
                 us = b.per_launch_us(launches, 3)[0]
-                out[f"{cfg}_{sp.name}"] = {"shape_out_x_in": f"{sp.M}x{sp.N}", "us_per_call": round(us, 3),
-                                           "GBps": round(b.items[0]["bytes"] / (us * 1e-6) / 1e9, 1)}
+                row[f"mu{mu}_us"] = round(us, 3)
+                row[f"mu{mu}_GBps"] = round(b.items[0]["bytes"] / (us * 1e-6) / 1e9, 1)
                 del b
                 torch.cuda.empty_cache()
+            row["mu8_faster"] = row["mu8_us"] < row["mu4_us"]
+            out[f"{cfg}_{spec.name}"] = row
+    return out
+
+
+# The paper's per-operator latencies on its NVIDIA A100 80GB (App. E.4, Table kernel-latency; batch 1, fp16
+# activations, g = 128), in microseconds, by (out, in) shape and configuration: context for the MI355X figures.
+PAPER_A100_KERNEL_US = {
+    (4096, 4096): {"2b": 41, "2b-s8": 47, "2b-s16": 49, "4b": 56},
+    (5120, 5120): {"2b": 63, "2b-s8": 73, "2b-s16": 74, "4b": 87},
+    (4096, 11008): {"2b": 102, "2b-s8": 109, "2b-s16": 111, "4b": 158},
+    (5120, 13824): {"2b": 167, "2b-s8": 166, "2b-s16": 169, "4b": 252},
+}
+# End-to-end decode speedup the paper quotes for LLaMA-2-7B 2b-s8-g128 against FP16 on that GPU (Sec. 4.1, Table
+# llama2-task: 254.39 against 42.94 tokens/s).
+PAPER_E2E_SPEEDUP = 5.92
+
+
+def kernel_latency_grid_us(launches: int = 100):
+    """The paper's kernel-latency table (App. E.4) on MI355X: four operator shapes x {2b, 2b-s8, 2b-s16, 4b}-g128
+    (s8/s16: structured selection of s salient columns per 128, Ks = Kb = 2, one salient row scale per row and
+    block), batch 1, graph-timed back-to-back launches over rotated packed copies (so every launch reads HBM), median of
+    five replays. Next to each the paper's A100 latency, and per shape the cost of the salient refinement relative to
+    the pure 2-base layer (the paper calls it nearly free)."""
+    import torch
+    from synth import kernel_latency_layers
+    out = {}
+    for spec in kernel_latency_layers():
+        b = Bench([spec], 1, COPIES_BYTES_PER_LAYER)
+        us = b.per_launch_us(launches, 5)[0]
+        it = b.items[0]
+        tag = spec.name.split("_", 1)[1].rsplit("-g", 1)[0]
+        a100 = PAPER_A100_KERNEL_US[(spec.M, spec.N)][tag]
+        out[spec.name] = {"us": round(us, 3), "bytes": it["bytes"], "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
+                          "pct_of_8TBps": round(100 * it["bytes"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 1),
+                          "tflop_eq": round(2.0 * spec.M * (spec.N + spec.S) / (us * 1e-6) / 1e12, 2),
+                          "kernel": b.fb.fluxbin_plan_query(it["packs"][0], 1)["kernel_name"],
+                          "paper_A100_us": a100, "speedup_vs_paper_A100": round(a100 / us, 2)}
+        del b
+        torch.cuda.empty_cache()
+    for (M, N) in PAPER_A100_KERNEL_US:
+        base = out[f"{M}x{N}_2b-g128"]["us"]
+        paper = PAPER_A100_KERNEL_US[(M, N)]
+        for tag in ("2b-s8", "2b-s16"):
+            out[f"{M}x{N}_{tag}_over_2b"] = {"mi355x": round(out[f"{M}x{N}_{tag}-g128"]["us"] / base, 3),
+                                             "paper_A100": round(paper[tag] / paper["2b"], 3)}
     return out
 
 
@@ -461,17 +512,44 @@ def small_layer_us(spec, launches=200):
     return us, b.items[0]["bytes"]
 
 
+def summarize_trace(path: str, steps: int, warmup: int, replays: int) -> dict:
+    """Split a rocprofv3 kernel trace (its kernel_trace.csv) of `bench.py --steps K --warmup W` into the run's phases:
+    the batch-1 GEMV dispatches in launch order are W warmup steps (2 each), one graph upload replay (2K), then the
+    `replays` timed replays (2K each); later dispatches belong to the per-layer figures. Returns the average dispatch
+    duration of each phase and, for the timed replays, the median span from a replay's first dispatch start to its last
+    dispatch end (compare with ms_per_step * K)."""
+    import csv
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if "k_gemv_b1" in r["Kernel_Name"]:
+                rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    rows.sort()
+    w, u, t = 2 * warmup, 2 * steps, 2 * steps * replays
+    if len(rows) < w + u + t:
+        raise SystemExit(f"trace has {len(rows)} GEMV dispatches, the headline phase needs {w + u + t}")
+    avg = lambda seg: sum(e - s for s, e in seg) / len(seg) / 1e3
+    timed = rows[w + u:w + u + t]
+    spans = sorted((timed[k * u + u - 1][1] - timed[k * u][0]) / 1e6 for k in range(replays))
+    return {"gemv_dispatches": len(rows), "warmup_avg_us": round(avg(rows[:w]), 3) if w else None,
+            "upload_replay_avg_us": round(avg(rows[w:w + u]), 3), "timed_avg_us": round(avg(timed), 3),
+            "timed_dispatches": t, "timed_replay_span_ms_median": round(spans[len(spans) // 2], 5),
+            "later_avg_us": round(avg(rows[w + u + t:]), 3) if len(rows) > w + u + t else None}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--replays", type=int, default=10, help="timed replays of the K-step graph (the median is reported)")
     ap.add_argument("--g-r", choices=["128", "N"], default="128")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-small", action="store_true", help="skip the 4096x4096 and small-batch per-call figures (70B and 7B MLP layers)")
     ap.add_argument("--no-decoder", action="store_true", help="skip the 70B decoder-layer graph figures")
     ap.add_argument("--no-variants", action="store_true", help="skip the kernel-variant figures (mu 4, pure global)")
+    ap.add_argument("--no-grid", action="store_true", help="skip the paper's kernel-latency grid (App. E.4 shapes)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before anything else, run a plain device-to-device copy of this many MiB three times "
                          "(the reference dispatch for HBM byte counters)")
@@ -479,7 +557,13 @@ def main():
                     help="batch rows of the counter-collection launches (2..16: the small-batch product)")
     ap.add_argument("--eager-launches", type=int, default=0,
                     help="counter-collection mode: launch each layer this many times without graphs, then exit")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="no GPU work: split a rocprofv3 kernel trace of a run with the same --steps/--warmup/--replays "
+                         "into its phases and print the batch-1 GEMV averages")
     args = ap.parse_args()
+    if args.summarize_trace:
+        print(json.dumps(summarize_trace(args.summarize_trace, args.steps, args.warmup, args.replays)))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "the library runs on one GPU; sharding the path over several GPUs is not implemented",
                           "n_gpus": args.gpus}))
@@ -513,13 +597,21 @@ def main():
                           "layers": [it["spec"].name for it in bench.items],
                           "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}}), flush=True)
         return
-    total_ms, wall = bench.run(args.steps, args.warmup)
+    # Headline: a graph of exactly K steps (up then down per step, rotating packed copies), replayed `replays` times,
+    # each replay between HIP events on the replay stream; the median replay gives ms_per_step and value. Both launches
+    # of a step are the batch-1 GEMV kernel, so its average launch duration in the timed region is the step time / 2
+    # (gaps between the graph's launches included), and roofline.achieved comes from the same timing.
+    replay_ms, wall = bench.run(args.steps, args.warmup, replays=args.replays)
+    med_ms = sorted(replay_ms)[len(replay_ms) // 2]
+    step_bytes = sum(it["bytes"] for it in bench.items)
+    value = step_bytes * args.steps / (med_ms * 1e-3) / 1e9
+    launch_us = med_ms * 1e3 / (args.steps * len(bench.items))
+    achieved = (step_bytes / len(bench.items)) / (launch_us * 1e-6) / 1e9
+    print(f"# headline: {args.replays} replays of {args.steps} steps, median {med_ms:.4f} ms", file=sys.stderr,
+          flush=True)
     kern_us = bench.per_launch_us()
     probe_us = bench.stream_probe_us()
     cold_us = bench.cold_launch_us()
-    step_bytes = sum(it["bytes"] for it in bench.items)
-    value = step_bytes * args.steps / (total_ms * 1e-3) / 1e9
-    achieved = step_bytes / (sum(kern_us) * 1e-6) / 1e9
     traffic = measured_traffic()
     per_layer = {}
     for it, us, pus, cus in zip(bench.items, kern_us, probe_us, cold_us):
@@ -535,19 +627,34 @@ def main():
         }
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(total_ms / args.steps, 5), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(med_ms / args.steps, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded Llama-70B-shaped MLP layers; no trained weights)",
-        "config": {"workload": WORKLOAD, "global_batch": 1, "g_r": args.g_r, "layers": per_layer},
+        "config": {"workload": WORKLOAD, "global_batch": 1, "g_r": args.g_r,
+                   "timing": {"replays": args.replays, "replay_ms": [round(t, 4) for t in replay_ms],
+                              "median_replay_ms": round(med_ms, 4), "us_per_launch": round(launch_us, 3)},
+                   "layers": per_layer},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": (sum(traffic[it["spec"].name] for it in bench.items) if traffic else None),
+                     "traffic": (sum(traffic[it["spec"].name] for it in bench.items) // len(bench.items)
+                                 if traffic else None),
                      "traffic_per_launch": traffic,
-                     "kernel": "k_gemv_b1<8,...> (HIP events around graph replays of back-to-back launches)",
+                     "kernel": "k_gemv_b1<8,1024,1,1,false> (both launches of a step); achieved = mean algorithmic "
+                               "bytes per launch / (median replay time / launches per replay)",
                      "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items},
                      "frac_of_stream_probe": round(sum(probe_us) / sum(kern_us), 4)},
         "wall_s_timed": round(wall, 3),
     }
+    if args.g_r == "128":   # the per-row reading (one row scale per row and base): 89.9 MB per 70B MLP layer
+        bn = Bench(config_layers("c4_mlp70b", "N"), 1, COPIES_BYTES_PER_LAYER * 2)
+        us_n = bn.per_launch_us()
+        out["config"]["layers_g_r_N"] = {
+            it["spec"].name: {"us_per_gemv": round(us, 3), "bytes": it["bytes"],
+                              "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
+                              "pct_of_8TBps": round(100 * it["bytes"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 1)}
+            for it, us in zip(bn.items, us_n)}
+        del bn
+        torch.cuda.empty_cache()
     if not args.no_small:
         spec2 = config_layers("c2_attn7b", args.g_r)[0]
         us, b2 = small_layer_us(spec2)
@@ -555,16 +662,26 @@ def main():
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
         out["config"]["small_batch"] = small_batch_us(specs, (2, 4, 8, 16))
         out["config"]["small_batch_mlp7b"] = small_batch_us(config_layers("c3_mlp7b", args.g_r), (2, 4, 8))
+    if not args.no_grid:
+        out["config"]["kernel_latency_grid"] = kernel_latency_grid_us()
     if not args.no_decoder:
         out["config"]["decoder_layer_70b"] = decoder_layer_us(args.g_r)
     if not args.no_variants:
         out["config"]["kernel_variants_28672x8192"] = kernel_variants_us(args.g_r)
         out["config"]["vcm_ablation"] = vcm_ablation_us(args.g_r)
         out["config"]["mu_profile"] = mu_profile_us(args.g_r)
-    if not args.no_variants:
         out["config"]["decomposition"] = decomposition_ms()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(bench, args.cpu_budget)
+    # Context only (another GPU, and an end-to-end figure): the paper's own numbers next to this run's.
+    ctx = {"paper_hardware": "NVIDIA A100 80GB",
+           "paper_e2e_decode_speedup_vs_fp16": PAPER_E2E_SPEEDUP,
+           "paper_e2e_note": "LLaMA-2-7B 2b-s8-g128 against FP16, end to end (Sec. 4.1); not a kernel figure",
+           "paper_a100_kernel_us": {f"{M}x{N}": v for (M, N), v in PAPER_A100_KERNEL_US.items()}}
+    if "cpu_baseline" in out and out["cpu_baseline"].get("value"):
+        ctx["gpu_over_cpu_oracle"] = round(value / out["cpu_baseline"]["value"], 1)
+        ctx["gpu_over_cpu_oracle_note"] = "the oracle is an untuned fp64 correctness reference, not a CPU kernel"
+    out["paper_context"] = ctx
     print(json.dumps(out), flush=True)
 
 

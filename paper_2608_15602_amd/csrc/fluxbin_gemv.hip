@@ -50,14 +50,14 @@ struct B1 {
   static constexpr int KPT = XV / (NT / 256);                           // staged units per thread
 };
 
-template <int RPT, bool FINE = false>
+template <int RPT, int FG = 0>
 struct Ring {
   uint32_t w[RPT][8];   // sign words of the thread's rows: [0..3] first stored chunk, [4..7] second
   uint32_t ra[RPT];     // 32-bit word holding the fp16 row scales of rows (i & ~1, i | 1) for chunk 2sc
   uint32_t rb[RPT];     // same for chunk 2sc+1
-  // layers with fine row-scale groups: the G fp16 scales of the thread's row for each stored slot (slot h at
-  // f[j][8h .. 8h + G/2 - 1]), already in position-block order
-  uint32_t f[FINE ? RPT : 1][FINE ? 16 : 1];
+  // layers with FG (8 or 16) fine salient row-scale groups per chunk: the FG fp16 scales of the thread's row for each
+  // stored slot (slot h at f[j][h*FG/2 ..]), already in position-block order
+  uint32_t f[FG ? RPT : 1][FG ? FG : 1];
 };
 
 // Super-chunk index sc0 + k of a workgroup's unit k, wrapped at the end of the tile: v < steps + XV, so one
@@ -277,8 +277,8 @@ __device__ __forceinline__ void cursor_advance(const GemmArgs& a, Cursor<NT, RPT
 // Issue the loads of the cursor's unit: sign words of both stored chunks (issue_signs) and the row-scale words of both
 // chunks for row-scale planes pa, pb (issue_rscale), with uniform bases and the per-thread row offsets. Nothing here
 // waits for them.
-template <int NT, int RPT, bool FINE>
-__device__ __forceinline__ void issue_signs(const GemmArgs& a, const Cursor<NT, RPT>& c, Ring<RPT, FINE>& rg) {
+template <int NT, int RPT, int FG>
+__device__ __forceinline__ void issue_signs(const GemmArgs& a, const Cursor<NT, RPT>& c, Ring<RPT, FG>& rg) {
   const uint8_t* e0 = c.sbase;
   const uint8_t* e1 = c.sbase + int64_t(a.Mp) * 16;
 #pragma unroll
@@ -290,9 +290,9 @@ __device__ __forceinline__ void issue_signs(const GemmArgs& a, const Cursor<NT, 
   }
 }
 
-template <int NT, int RPT, bool FINE>
+template <int NT, int RPT, int FG>
 __device__ __forceinline__ void issue_rscale(const GemmArgs& a, const Cursor<NT, RPT>& c, int64_t oa, int64_t ob,
-                                             Ring<RPT, FINE>& rg) {
+                                             Ring<RPT, FG>& rg) {
   const uint8_t* ba = reinterpret_cast<const uint8_t*>(a.rscale) + oa;
   const uint8_t* bb = reinterpret_cast<const uint8_t*>(a.rscale) + ob;
 #pragma unroll
@@ -302,31 +302,25 @@ __device__ __forceinline__ void issue_rscale(const GemmArgs& a, const Cursor<NT,
   }
 }
 
-// Fine row-scale groups (G = 2..16 scales per chunk and row): the row's G scales of the chunk held in each stored slot
-// (slot h holds chunk 2sc + (h XOR hb)), from the chunk's block of rows of G consecutive fp16 values (row * 2G bytes
-// in; c.soff = row * 16). G is uniform, so the branch is.
-template <int NT, int RPT>
+// Fine salient row-scale groups (FG = 8 or 16 scales per chunk and row): the row's FG scales of the chunk held in each
+// stored slot (slot h holds chunk 2sc + (h XOR hb)), from the chunk's block of rows of FG consecutive fp16 values
+// (row * 2FG bytes in; c.soff = row * 16): FG/8 16-byte loads per slot.
+template <int NT, int RPT, int FG>
 __device__ __forceinline__ void issue_rscale_fine(const GemmArgs& a, const Cursor<NT, RPT>& c, int64_t oa, int64_t ob,
-                                                  int G, bool hb, Ring<RPT, true>& rg) {
+                                                  bool hb, Ring<RPT, FG>& rg) {
+  static_assert(FG == 8 || FG == 16, "fine instances: 8 or 16 groups per chunk");
   const uint8_t* rs = reinterpret_cast<const uint8_t*>(a.rscale);
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
+    const uint32_t off = c.soff[j] * uint32_t(FG / 8);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const uint8_t* p = rs + ((h != 0) != hb ? ob : oa);
-      uint32_t* d = &rg.f[j][8 * h];
-      if (G == 16) {
-        const uint4 v0 = *reinterpret_cast<const uint4*>(p + c.soff[j] * 2u);
-        const uint4 v1 = *reinterpret_cast<const uint4*>(p + c.soff[j] * 2u + 16u);
-        d[0] = v0.x; d[1] = v0.y; d[2] = v0.z; d[3] = v0.w; d[4] = v1.x; d[5] = v1.y; d[6] = v1.z; d[7] = v1.w;
-      } else if (G == 8) {
-        const uint4 v0 = *reinterpret_cast<const uint4*>(p + c.soff[j]);
-        d[0] = v0.x; d[1] = v0.y; d[2] = v0.z; d[3] = v0.w;
-      } else if (G == 4) {
-        const uint2 v0 = *reinterpret_cast<const uint2*>(p + (c.soff[j] >> 1));
-        d[0] = v0.x; d[1] = v0.y;
-      } else {
-        d[0] = *reinterpret_cast<const uint32_t*>(p + (c.soff[j] >> 2));
+      const uint8_t* p = rs + ((h != 0) != hb ? ob : oa) + off;
+      uint32_t* d = &rg.f[j][h * (FG / 2)];
+#pragma unroll
+      for (int k = 0; k < FG / 8; ++k) {
+        const uint4 v = *reinterpret_cast<const uint4*>(p + 16 * k);
+        d[4 * k] = v.x; d[4 * k + 1] = v.y; d[4 * k + 2] = v.z; d[4 * k + 3] = v.w;
       }
     }
   }
@@ -347,8 +341,8 @@ __device__ __forceinline__ float tree16(float (&v)[16]) {
   return v[0];
 }
 
-template <int NT, int RPT, int BUF, bool FINE>
-__device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT, FINE>& rg, const uint32_t (&c1)[4],
+template <int NT, int RPT, int BUF, int FG>
+__device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT, FG>& rg, const uint32_t (&c1)[4],
                                           const uint32_t (&c2)[4], bool hb, float (&acc)[RPT][1]) {
   const uint32_t sh = (threadIdx.x & 1u) * 16u;   // the rows of a thread have the parity of threadIdx.x
 #pragma unroll
@@ -380,69 +374,51 @@ __device__ __forceinline__ void lookup_b1(const float* lut, const Ring<RPT, FINE
   }
 }
 
-// Per-position fp16 row scales of one stored slot from its G scales (position block b = positions b*n .. b*n+n-1,
-// n = 16/G, has scale slot b): e[d] holds the scales of positions 2d and 2d + 1.
-__device__ __forceinline__ void expand_scales(const uint32_t* f, int G, uint32_t (&e)[8]) {
-  // v_perm_b32 selector bytes 0..3 pick bytes of its second operand: 0x01000100 repeats the low half, 0x03020302 the
-  // high half
-  constexpr uint32_t LO = 0x01000100u, HI = 0x03020302u;
-  if (G == 16) {
-#pragma unroll
-    for (int d = 0; d < 8; ++d) e[d] = f[d];
-  } else if (G == 8) {   // positions 2d, 2d+1 -> slot d
-#pragma unroll
-    for (int d = 0; d < 8; ++d) e[d] = __builtin_amdgcn_perm(0u, f[d >> 1], (d & 1) ? HI : LO);
-  } else if (G == 4) {   // positions 4b..4b+3 -> slot b
-#pragma unroll
-    for (int d = 0; d < 8; ++d) e[d] = __builtin_amdgcn_perm(0u, f[d >> 2], ((d >> 1) & 1) ? HI : LO);
-  } else {               // G = 2: positions 8b..8b+7 -> slot b
-#pragma unroll
-    for (int d = 0; d < 8; ++d) e[d] = __builtin_amdgcn_perm(0u, f[0], (d >> 2) ? HI : LO);
-  }
-}
-
-// Sum of 16 lookups, each times its position's row scale: four chains of four FMAs, then a tree of the chains.
-__device__ __forceinline__ float scaled16(const float (&v)[16], const uint32_t (&e)[8]) {
-  float c[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    float s = 0.f;
-#pragma unroll
-    for (int q = 4 * k; q < 4 * k + 4; ++q) s = __builtin_fmaf(v[q], h2f(uint16_t(e[q >> 1] >> (16 * (q & 1)))), s);
-    c[k] = s;
-  }
-  return (c[0] + c[1]) + (c[2] + c[3]);
-}
-
-// Batch-1 lookups of a unit whose chunks have fine row-scale groups (G scales per chunk and row): the same 2 x 16
-// lookups as lookup_b1 (c1, c2 hold the rotation of this G), each multiplied by its position's scale.
-template <int NT, int RPT, int BUF>
-__device__ __forceinline__ void lookup_b1_fine(const float* lut, const Ring<RPT, true>& rg, const uint32_t (&c1)[4],
-                                               const uint32_t (&c2)[4], int G, float (&acc)[RPT][1]) {
+// Batch-1 lookups of a unit whose chunks have FG fine row-scale groups: the same 2 x 16 lookups as lookup_b1 (c1, c2
+// hold the rotation of FG groups), each multiplied by the scale of its position block (positions q with the same
+// q / (16 / FG)), in four chains of four FMAs per stored slot; one slot at a time, so that only one slot's lookups are
+// live.
+template <int NT, int RPT, int BUF, int FG>
+__device__ __forceinline__ void lookup_b1_fine(const float* lut, const Ring<RPT, FG>& rg, const uint32_t (&c1)[4],
+                                               const uint32_t (&c2)[4], float (&acc)[RPT][1]) {
+  constexpr int N = 16 / FG;   // positions per group
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
-    float v1[16], v2[16];
+    float part[2];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
+    for (int h = 0; h < 2; ++h) {
+      float v[16];
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb) {
-        const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
-        v1[4 * m + bb] = lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][m], c1[m], sel));
-        v2[4 * m + bb] = lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][4 + m], c2[m], sel));
+      for (int m = 0; m < 4; ++m) {
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb) {
+          const uint32_t sel = 0x0c0c0000u | ((4u + bb) << 8) | uint32_t(bb);
+          v[4 * m + bb] = lds_at<BUF>(lut, __builtin_amdgcn_perm(rg.w[j][4 * h + m], h ? c2[m] : c1[m], sel));
+        }
       }
+      const uint32_t* f = &rg.f[j][h * (FG / 2)];
+      float c[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        float sum = 0.f;
+#pragma unroll
+        for (int q = 4 * k; q < 4 * k + 4; ++q) {
+          const int slot = q / N;
+          sum = __builtin_fmaf(v[q], h2f(uint16_t(f[slot >> 1] >> (16 * (slot & 1)))), sum);
+        }
+        c[k] = sum;
+      }
+      part[h] = (c[0] + c[1]) + (c[2] + c[3]);
     }
-    uint32_t e1[8], e2[8];
-    expand_scales(&rg.f[j][0], G, e1);
-    expand_scales(&rg.f[j][8], G, e2);
-    acc[j][0] += scaled16(v1, e1) + scaled16(v2, e2);
+    acc[j][0] += part[0] + part[1];
   }
 }
 
 // mu = 4: chunk h of the unit is in stored slot h; nibble q of its 16 bytes (word q/8, bits 4(q%8)..) is sub-vector
 // (q + i) mod 32 of row i. bm[m] = ((8m + t) mod 32) * 4 is the lane's byte column for word m, and nibble j of the word
 // adds 4j (an immediate offset). Eight lookups per word, summed as a tree.
-template <int NT, int RPT, int BUF, bool FINE>
-__device__ __forceinline__ void lookup_b1_mu4(const float* lut, const Ring<RPT, FINE>& rg, const uint32_t (&bm)[4],
+template <int NT, int RPT, int BUF, int FG>
+__device__ __forceinline__ void lookup_b1_mu4(const float* lut, const Ring<RPT, FG>& rg, const uint32_t (&bm)[4],
                                               float (&acc)[RPT][1]) {
   const uint32_t sh = (threadIdx.x & 1u) * 16u;
   const char* base = reinterpret_cast<const char*>(lut) + BUF * 8192;
@@ -499,12 +475,12 @@ struct B1State {
 // are unrolled at compile time (a workgroup has at most XV units) so that the wait before each lookup covers
 // exactly the loads of unit K.
 // Per-lane LUT address constants of the lookups (see the kernel): c1/c2 for chunks whose positions follow the plain
-// rotation (one row scale per chunk, or 16 per chunk); with fine row-scale groups also the rotation of each side's
-// group count (fg: global chunks, fs: salient chunks; unused when that side has one scale per chunk).
-template <bool FINE>
+// rotation (one row scale per chunk, or 16 per chunk); with fine salient row-scale groups also the rotation of their
+// group count (fs).
+template <int FG>
 struct LaneConsts {
   uint32_t c1[4], c2[4];
-  uint32_t fg1[FINE ? 4 : 1], fg2[FINE ? 4 : 1], fs1[FINE ? 4 : 1], fs2[FINE ? 4 : 1];
+  uint32_t fs1[FG == 8 ? 4 : 1], fs2[FG == 8 ? 4 : 1];   // FG = 16 rotates like one group (c1, c2)
 };
 
 // Bytes (hb << 6) | (s << 2) of the sub-vectors s at positions 4m .. 4m+3 of lane t's rows for a chunk with G scale
@@ -530,33 +506,46 @@ __device__ __forceinline__ void rotation_consts(int t, int G, bool hb, uint32_t 
 // Scales per chunk (1 or the fine count) of super-chunk sc: the salient chunks' layout from chunk nfc on.
 __device__ __forceinline__ int unit_G(const GemmArgs& a, int sc) { return 2 * sc >= a.nfc ? a.Gcs : a.Gcg; }
 
-template <int NT, int RPT, bool FINE>
+// Row-scale loads of the cursor's unit. The fine instances (global chunks with one scale per chunk, salient chunks with
+// FG fine groups) issue the same number of loads per row for every unit: FG = 8: one 16-byte load per slot, or the two
+// scale words of the global layout; FG = 16: two 16-byte loads per slot, or the two scale words plus two loads of a
+// word that stays cached. With the same count on both paths the compiler's waits before each lookup cover exactly the
+// loads of the unit looked up (different counts made it wait for the loads of the unit requested ahead too).
+template <int NT, int RPT, int FG>
 __device__ __forceinline__ void issue_rscale_any(const GemmArgs& a, const Cursor<NT, RPT>& c, int64_t oa, int64_t ob,
-                                                 bool hb, Ring<RPT, FINE>& rg) {
-  if constexpr (FINE) {
-    const int G = unit_G(a, c.sc);
-    if (G > 1) {
-      issue_rscale_fine<NT, RPT>(a, c, oa, ob, G, hb, rg);
-      return;
+                                                 bool hb, Ring<RPT, FG>& rg) {
+  if constexpr (FG > 0) {
+    if (2 * c.sc >= a.nfc) {
+      issue_rscale_fine<NT, RPT, FG>(a, c, oa, ob, hb, rg);
+    } else {
+      issue_rscale<NT, RPT, FG>(a, c, oa, ob, rg);
+      if constexpr (FG == 16) {
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+          rg.f[j][0] = *reinterpret_cast<const uint32_t*>(a.rscale);
+          rg.f[j][8] = *reinterpret_cast<const uint32_t*>(a.rscale + 2);
+        }
+      }
     }
+  } else {
+    issue_rscale<NT, RPT, FG>(a, c, oa, ob, rg);
   }
-  issue_rscale<NT, RPT, FINE>(a, c, oa, ob, rg);
 }
 
-template <int MU, int NT, int RPT, int D, int K, bool FINE>
+template <int MU, int NT, int RPT, int D, int K, int FG>
 __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
-                                         Ring<RPT, FINE> (&ring)[D + 1], float* lut, float* xs,
-                                         const LaneConsts<FINE>& lc, bool hb, const int64_t* s_roff,
+                                         Ring<RPT, FG> (&ring)[D + 1], float* lut, float* xs,
+                                         const LaneConsts<FG>& lc, bool hb, const int64_t* s_roff,
                                          const Staged<NT>& sg, int sc0) {
   constexpr int XV = B1<NT, 1>::XV;
   if constexpr (K < XV) {
     if (K >= st.n) return;
     constexpr int BUF = K & 1;
     constexpr int KI = (K + D) < XV ? (K + D) : XV - 1;   // unit requested (clamped)
-    issue_signs<NT, RPT, FINE>(a, cur, ring[(K + D) % (D + 1)]);
+    issue_signs<NT, RPT, FG>(a, cur, ring[(K + D) % (D + 1)]);
     int64_t oa, ob;
     roff_of(s_roff, KI, st.n, oa, ob);
-    issue_rscale_any<NT, RPT, FINE>(a, cur, oa, ob, hb, ring[(K + D) % (D + 1)]);
+    issue_rscale_any<NT, RPT, FG>(a, cur, oa, ob, hb, ring[(K + D) % (D + 1)]);
     cursor_advance<NT, RPT>(a, cur, K + D + 1 < st.n);
     if (K + 1 < st.n) {
       if constexpr (MU == 8)
@@ -565,19 +554,19 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
         build_b1_mu4<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
     }
     if constexpr (K == 0) stage_write_salient<NT>(a, sg, xs, sc0, st.n, 2, XV);   // built from step 1 on
-    if constexpr (MU == 8 && FINE) {
-      const bool sal = 2 * st.sc >= a.nfc;
-      const int G = sal ? a.Gcs : a.Gcg;
-      if (G == 1)
-        lookup_b1<NT, RPT, BUF, FINE>(lut, ring[K % (D + 1)], lc.c1, lc.c2, hb, st.acc);
-      else if (sal)
-        lookup_b1_fine<NT, RPT, BUF>(lut, ring[K % (D + 1)], lc.fs1, lc.fs2, G, st.acc);
-      else
-        lookup_b1_fine<NT, RPT, BUF>(lut, ring[K % (D + 1)], lc.fg1, lc.fg2, G, st.acc);
+    if constexpr (MU == 8 && FG > 0) {
+      if (2 * st.sc >= a.nfc) {
+        if constexpr (FG == 16)
+          lookup_b1_fine<NT, RPT, BUF, FG>(lut, ring[K % (D + 1)], lc.c1, lc.c2, st.acc);
+        else
+          lookup_b1_fine<NT, RPT, BUF, FG>(lut, ring[K % (D + 1)], lc.fs1, lc.fs2, st.acc);
+      } else {
+        lookup_b1<NT, RPT, BUF, FG>(lut, ring[K % (D + 1)], lc.c1, lc.c2, hb, st.acc);
+      }
     } else if constexpr (MU == 8) {
-      lookup_b1<NT, RPT, BUF, FINE>(lut, ring[K % (D + 1)], lc.c1, lc.c2, hb, st.acc);
+      lookup_b1<NT, RPT, BUF, FG>(lut, ring[K % (D + 1)], lc.c1, lc.c2, hb, st.acc);
     } else {
-      lookup_b1_mu4<NT, RPT, BUF, FINE>(lut, ring[K % (D + 1)], lc.c1, st.acc);
+      lookup_b1_mu4<NT, RPT, BUF, FG>(lut, ring[K % (D + 1)], lc.c1, st.acc);
     }
     if (st.sc == a.steps - 1 || K + 1 == st.n) {
       const bool shared = st.tile == st.first_tile ? st.first_shared : (st.tile == st.last_tile ? st.last_shared : false);
@@ -595,13 +584,17 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
       st.sc = 0;
       ++st.tile;
     }
-    steps_b1<MU, NT, RPT, D, K + 1, FINE>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
+    steps_b1<MU, NT, RPT, D, K + 1, FG>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
   }
 }
 
-template <int MU, int NT, int RPT, int D, bool EARLY, bool FINE>
-__global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
-  static_assert(!FINE || MU == 8, "fine row-scale groups: mu = 8 only (mu = 4 layers with them run the generic kernel)");
+// FG > 0: the instances for layers whose salient chunks have FG = 8 or 16 fine row-scale groups (s = 16 or 8 salient
+// columns per group, their global chunks one scale per chunk); mu = 8 only. Such layers need at most 128 VGPRs for
+// four waves per SIMD (one 1024- or two 512-thread workgroups per CU), which the second launch bound (minimum waves
+// per SIMD) asks of the compiler.
+template <int MU, int NT, int RPT, int D, bool EARLY, int FG>
+__global__ void __launch_bounds__(NT, FG ? 4 : 1) k_gemv_b1(GemmArgs a) {
+  static_assert(FG == 0 || MU == 8, "fine row-scale groups: mu = 8 only (mu = 4 layers with them run the generic kernel)");
   // mu = 8: 64 KB, two buffers interleaved per pattern; mu = 4: two buffers of 8 KB
   __shared__ __attribute__((aligned(16))) float lut[MU == 8 ? 256 * 64 : 2 * 2048];
   constexpr int XV = B1<NT, 1>::XV;
@@ -675,12 +668,12 @@ __global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
   stage_issue<NT>(a, sg, s_unit);
   Cursor<NT, RPT> cur;
   cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
-  Ring<RPT, FINE> ring[D + 1];
+  Ring<RPT, FG> ring[D + 1];
   Cursor<NT, RPT> cur0 = cur;
   if constexpr (!EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);   // n <= XV (launch plan)
 #pragma unroll
   for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
-    issue_signs<NT, RPT, FINE>(a, cur, ring[k]);
+    issue_signs<NT, RPT, FG>(a, cur, ring[k]);
     cursor_advance<NT, RPT>(a, cur, k + 1 < st.n);
   }
   if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);
@@ -688,9 +681,8 @@ __global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
   // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32. Byte bb of c1[m] is
   // (hb << 6) | (s << 2) with s = (t + 4m + bb) mod 16 (the four bytes at once: no byte exceeds 18 before the mask).
   // (mu = 4: c1[m] is the lane's byte column of word m, ((8m + t) mod 32) * 4; c2 and hb are not used.)
-  // Chunks with fine row-scale groups rotate the positions by groups (rotation_consts); a side with one scale per
-  // chunk uses c1, c2.
-  LaneConsts<FINE> lc;
+  // Salient chunks with fine row-scale groups rotate the positions by groups (rotation_consts).
+  LaneConsts<FG> lc;
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     if constexpr (MU == 8) {
@@ -702,10 +694,7 @@ __global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
       lc.c2[m] = 0u;
     }
   }
-  if constexpr (FINE) {
-    rotation_consts(t, a.Gcg, hb, lc.fg1, lc.fg2);
-    rotation_consts(t, a.Gcs, hb, lc.fs1, lc.fs2);
-  }
+  if constexpr (FG == 8) rotation_consts(t, FG, hb, lc.fs1, lc.fs2);
 
   stage_write_salient<NT>(a, sg, xs, sc0, st.n, 0, 2);
   __syncthreads();
@@ -714,7 +703,7 @@ __global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
   for (int k = 0; k < D; ++k) {
     int64_t oa, ob;
     roff_of(s_roff, k, st.n, oa, ob);
-    issue_rscale_any<NT, RPT, FINE>(a, cur0, oa, ob, hb, ring[k]);
+    issue_rscale_any<NT, RPT, FG>(a, cur0, oa, ob, hb, ring[k]);
     cursor_advance<NT, RPT>(a, cur0, k + 1 < st.n);
   }
   if constexpr (MU == 8)
@@ -722,7 +711,7 @@ __global__ void __launch_bounds__(NT) k_gemv_b1(GemmArgs a) {
   else
     build_b1_mu4<NT, 0>(lut, xs);
   __syncthreads();
-  steps_b1<MU, NT, RPT, D, 0, FINE>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
+  steps_b1<MU, NT, RPT, D, 0, FG>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
   const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
   publish_pending<NT, RPT, 1>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
@@ -782,9 +771,9 @@ __global__ void __launch_bounds__(NT) k_stream_probe(GemmArgs a, uint32_t* sink)
   int sck = sc;
 #pragma unroll
   for (int k = 0; k < D; ++k) {
-    issue_signs<NT, 1, false>(a, cur, ring[k]);
+    issue_signs<NT, 1, 0>(a, cur, ring[k]);
     const int32_t p0 = load_uniform_i32(a.chunk_plane, 2 * sck);
-    issue_rscale<NT, 1, false>(a, cur, int64_t(p0) * a.Mp * 2, int64_t(load_uniform_i32(a.chunk_plane, 2 * sck + 1)) * a.Mp * 2,
+    issue_rscale<NT, 1, 0>(a, cur, int64_t(p0) * a.Mp * 2, int64_t(load_uniform_i32(a.chunk_plane, 2 * sck + 1)) * a.Mp * 2,
                         ring[k]);
     cursor_advance<NT, 1>(a, cur, k + 1 < n);
     if (++sck == a.steps) sck = 0;
@@ -793,8 +782,8 @@ __global__ void __launch_bounds__(NT) k_stream_probe(GemmArgs a, uint32_t* sink)
   for (int k = 0; k < B1<NT, 1>::XV; ++k) {   // n <= XV (launch plan); unrolled so the ring stays in registers
     if (k < n) {
       Ring<1>& nx = ring[(k + D) % (D + 1)];
-      issue_signs<NT, 1, false>(a, cur, nx);
-      issue_rscale<NT, 1, false>(a, cur, int64_t(load_uniform_i32(a.chunk_plane, 2 * sck)) * a.Mp * 2,
+      issue_signs<NT, 1, 0>(a, cur, nx);
+      issue_rscale<NT, 1, 0>(a, cur, int64_t(load_uniform_i32(a.chunk_plane, 2 * sck)) * a.Mp * 2,
                           int64_t(load_uniform_i32(a.chunk_plane, 2 * sck + 1)) * a.Mp * 2, nx);
       cursor_advance<NT, 1>(a, cur, k + D + 1 < n);
       if (++sck == a.steps) sck = 0;
@@ -1077,31 +1066,33 @@ __global__ void __launch_bounds__(NT) k_gemm_generic(GemmArgs a) {
 // =====================================================================================================================
 
 template <int MU, int NT, int RPT, bool EARLY>
-static bool launch_b1_d(const GemmArgs& a, int depth, bool fine, hipStream_t stream) {
+static bool launch_b1_d(const GemmArgs& a, int depth, int fg, hipStream_t stream) {
   const dim3 grid(unsigned(a.blocks));
-  if (fine) {   // fine row-scale groups: mu = 8, 512- or 1024-thread workgroups, one unit ahead (launch plan)
+  if (fg) {   // fine salient row-scale groups: mu = 8, 512 or 1024 threads, one unit ahead (launch plan)
     if constexpr (MU == 8 && NT != 256) {
       if (depth != 1) return false;
-      hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 1, EARLY, true>), grid, dim3(NT), 0, stream, a);
+      if (fg == 16) hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 1, EARLY, 16>), grid, dim3(NT), 0, stream, a);
+      else if (fg == 8) hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 1, EARLY, 8>), grid, dim3(NT), 0, stream, a);
+      else return false;
       return true;
     }
     return false;
   }
   if constexpr (MU == 8) {
     switch (depth) {
-      case 2: hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 2, EARLY, false>), grid, dim3(NT), 0, stream, a); return true;
-      case 3: hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 3, EARLY, false>), grid, dim3(NT), 0, stream, a); return true;
+      case 2: hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 2, EARLY, 0>), grid, dim3(NT), 0, stream, a); return true;
+      case 3: hipLaunchKernelGGL((k_gemv_b1<8, NT, RPT, 3, EARLY, 0>), grid, dim3(NT), 0, stream, a); return true;
       default: break;
     }
   }
-  hipLaunchKernelGGL((k_gemv_b1<MU, NT, RPT, 1, EARLY, false>), grid, dim3(NT), 0, stream, a);   // mu = 4: depth 1 only
+  hipLaunchKernelGGL((k_gemv_b1<MU, NT, RPT, 1, EARLY, 0>), grid, dim3(NT), 0, stream, a);   // mu = 4: depth 1 only
   return true;
 }
 
 template <int MU, int NT, int RPT>
-static bool launch_b1(const GemmArgs& a, int depth, bool early, bool fine, hipStream_t stream) {
-  return early ? launch_b1_d<MU, NT, RPT, true>(a, depth, fine, stream)
-               : launch_b1_d<MU, NT, RPT, false>(a, depth, fine, stream);
+static bool launch_b1(const GemmArgs& a, int depth, bool early, int fg, hipStream_t stream) {
+  return early ? launch_b1_d<MU, NT, RPT, true>(a, depth, fg, stream)
+               : launch_b1_d<MU, NT, RPT, false>(a, depth, fg, stream);
 }
 
 template <int MU, int BG, int NG>
@@ -1201,14 +1192,15 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   a.Gcg = int32_t(d.Gcg);
   a.Gcs = int32_t(d.Gcs);
   const bool fine = d.Gcg > 1 || d.Gcs > 1;
+  const int fg = fine ? (d.Gcg == 1 ? int(d.Gcs) : -1) : 0;   // batch-1 fine instances: salient groups only
   if (p.kernel == 0) {
     switch (p.nt) {   // one row per thread (the launch plan's only choice for this kernel)
-      case 256: ok = L.shape.mu == 8 ? launch_b1<8, 256, 1>(a, p.depth, p.early, fine, stream)
-                                     : launch_b1<4, 256, 1>(a, p.depth, p.early, fine, stream); break;
-      case 512: ok = L.shape.mu == 8 ? launch_b1<8, 512, 1>(a, p.depth, p.early, fine, stream)
-                                     : launch_b1<4, 512, 1>(a, p.depth, p.early, fine, stream); break;
-      case 1024: ok = L.shape.mu == 8 ? launch_b1<8, 1024, 1>(a, p.depth, p.early, fine, stream)
-                                      : launch_b1<4, 1024, 1>(a, p.depth, p.early, fine, stream); break;
+      case 256: ok = L.shape.mu == 8 ? launch_b1<8, 256, 1>(a, p.depth, p.early, fg, stream)
+                                     : launch_b1<4, 256, 1>(a, p.depth, p.early, fg, stream); break;
+      case 512: ok = L.shape.mu == 8 ? launch_b1<8, 512, 1>(a, p.depth, p.early, fg, stream)
+                                     : launch_b1<4, 512, 1>(a, p.depth, p.early, fg, stream); break;
+      case 1024: ok = L.shape.mu == 8 ? launch_b1<8, 1024, 1>(a, p.depth, p.early, fg, stream)
+                                      : launch_b1<4, 1024, 1>(a, p.depth, p.early, fg, stream); break;
       default: ok = false;
     }
   } else if (p.kernel == 2) {

@@ -198,13 +198,16 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int force_generic = tu.generic;
   const int rpt_env = tu.rpt;
   int per_cu = tu.blocks_per_cu;
-  // Fine row-scale groups (groups shorter than a chunk): the batch-1 kernel's instances for them have mu = 8, one unit
-  // ahead and 512 or 1024 threads; every other case with fine groups runs the generic kernel (the matrix-core and LUT
-  // batch kernels apply one row scale per chunk).
+  // Fine row-scale groups (groups shorter than a chunk): the batch-1 kernel's instances for them take mu = 8 layers
+  // whose fine groups are on the salient side only (the paper's s8/s16 configurations), one unit ahead, 512 or 1024
+  // threads; every other case with fine groups runs the generic kernel (the matrix-core and LUT batch kernels apply one
+  // row scale per chunk).
   const Derived dv = derive(L.shape);
   const bool fine = dv.Gcg > 1 || dv.Gcs > 1;
+  // the batch-1 instances for fine groups: salient side only, 8 or 16 groups per chunk (s = 16 or 8 at mu = 8)
+  const bool b1_fine_ok = L.shape.mu == 8 && dv.Gcg == 1 && (dv.Gcs == 8 || dv.Gcs == 16);
   p->nt = 256;
-  if (B == 1 && !force_generic && !(fine && L.shape.mu != 8)) {   // batch-1 kernel (mu = 8 or 4)
+  if (B == 1 && !force_generic && (!fine || b1_fine_ok)) {   // batch-1 kernel (mu = 8 or 4)
     p->kernel = 0;
     const int nt_env = tu.nt;
     // units of sign data requested ahead of the one being looked up: one (two units, 64 KB per CU, in flight) already
