@@ -537,6 +537,34 @@ def summarize_trace(path: str, steps: int, warmup: int, replays: int) -> dict:
             "later_avg_us": round(avg(rows[w + u + t:]), 3) if len(rows) > w + u + t else None}
 
 
+def summarize_counters(path: str, launches: int, copy_bytes: int) -> dict:
+    """One rocprofv3 counter pass (counter_collection.csv) of the counter-collection mode (`--copy-calib-mib`,
+    `--eager-launches N`): the counter's value per dispatch (KiB) of the first three device-to-device copies of
+    copy_bytes bytes (the calibration: bytes per counted KiB), and of the batch-1 GEMV dispatches, the first N the up
+    layer and the next N the down layer; returns the calibrated bytes per launch of each layer."""
+    import csv
+    copies, gemv = [], []
+    name = None
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            name = r["Counter_Name"]
+            v = float(r["Counter_Value"])
+            if "copyBuffer" in r["Kernel_Name"]:
+                copies.append((int(r["Dispatch_Id"]), v))
+            elif "k_gemv_b1" in r["Kernel_Name"]:
+                gemv.append((int(r["Dispatch_Id"]), v))
+    copies = [v for _, v in sorted(copies)][:3]
+    gemv = [v for _, v in sorted(gemv)]
+    if len(copies) < 3 or len(gemv) < 2 * launches:
+        raise SystemExit(f"{path}: {len(copies)} copies and {len(gemv)} GEMV dispatches")
+    cal = copy_bytes / (sum(copies) / len(copies))      # bytes per counted KiB
+    mean = lambda xs: sum(xs) / len(xs)
+    up, down = mean(gemv[:launches]), mean(gemv[launches:2 * launches])
+    return {"counter": name, "copy_kib": round(mean(copies), 1), "bytes_per_counted_kib": round(cal, 3),
+            "up_kib": round(up, 1), "down_kib": round(down, 1), "up_bytes": int(round(up * cal)),
+            "down_bytes": int(round(down * cal))}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -557,12 +585,18 @@ def main():
                     help="batch rows of the counter-collection launches (2..16: the small-batch product)")
     ap.add_argument("--eager-launches", type=int, default=0,
                     help="counter-collection mode: launch each layer this many times without graphs, then exit")
+    ap.add_argument("--summarize-counters", metavar="COUNTER_COLLECTION_CSV",
+                    help="no GPU work: calibrated bytes per launch of one rocprofv3 counter pass of the counter mode "
+                         "(with the same --eager-launches and --copy-calib-mib)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="no GPU work: split a rocprofv3 kernel trace of a run with the same --steps/--warmup/--replays "
                          "into its phases and print the batch-1 GEMV averages")
     args = ap.parse_args()
     if args.summarize_trace:
         print(json.dumps(summarize_trace(args.summarize_trace, args.steps, args.warmup, args.replays)))
+        return
+    if args.summarize_counters:
+        print(json.dumps(summarize_counters(args.summarize_counters, args.eager_launches, args.copy_calib_mib << 20)))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "the library runs on one GPU; sharding the path over several GPUs is not implemented",
