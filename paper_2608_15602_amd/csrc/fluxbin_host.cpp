@@ -370,7 +370,11 @@ using namespace fluxbin;
 extern "C" {
 
 const char* fluxbin_status_string(fluxbin_status s) {
-  switch (s) {
+  // C callers may pass any int; read it as one (in C++ a value outside the enumerators' range is not a valid
+  // fluxbin_status, and switching on it directly is undefined)
+  int v;
+  std::memcpy(&v, &s, sizeof(v));
+  switch (v) {
     case FLUXBIN_OK: return "ok";
     case FLUXBIN_ERR_INVALID_ARG: return "invalid argument";
     case FLUXBIN_ERR_UNSUPPORTED: return "unsupported";

@@ -10,7 +10,8 @@ import os
 from typing import Dict, Optional, Tuple
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libfluxbin.so")
+# FLUXBIN_LIBRARY selects another build of the same library (the host-sanitizer build of the CPU tests)
+LIB_PATH = os.environ.get("FLUXBIN_LIBRARY") or os.path.join(HERE, "libfluxbin.so")
 
 FLUXBIN_OK = 0
 FLUXBIN_ERR_INVALID_ARG = 1

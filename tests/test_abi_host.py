@@ -270,3 +270,29 @@ def test_plan_query_and_noalloc_validate_on_the_host(L):
     X = ctypes.c_void_p(1 << 20)
     Y = ctypes.c_void_p(1 << 24)
     assert L.fluxbin_lut_gemv_noalloc(None, X, Y, 0, None) == fb.FLUXBIN_ERR_INVALID_ARG
+
+
+def test_random_shapes_and_headers_are_rejected_cleanly(L):
+    """Random shapes through fluxbin_pack_query and random or corrupted 256-byte headers through
+    fluxbin_layer_from_header: every call returns a status (the host-sanitizer test runs this under ASan/UBSan)."""
+    rng = np.random.default_rng(5)
+    n = ctypes.c_size_t(0)
+    for _ in range(2000):
+        vals = rng.integers(-3, 1 << 17, size=8)
+        sh = fb.make_shape(int(vals[0]), int(vals[1]), int(vals[2] % 7) - 1, int(vals[3] % 7) - 1,
+                           int(vals[4] % 10), int(vals[5]), int(vals[6]), int(vals[7]))
+        st = L.fluxbin_pack_query(ctypes.byref(sh), ctypes.byref(n))
+        assert st in (fb.FLUXBIN_OK, fb.FLUXBIN_ERR_INVALID_ARG, fb.FLUXBIN_ERR_UNSUPPORTED)
+        if st == fb.FLUXBIN_OK:
+            assert n.value == fmt.packed_bytes(_spec(sh))["total"]
+    good = _header_bytes(LayerSpec("h", M=100, N=300, Kb=2, Ks=1, mu=8, S=20, g_r=64, g_s=8))
+    for k in range(500):
+        h = bytearray(good)
+        for _ in range(int(rng.integers(1, 6))):
+            h[int(rng.integers(0, 256))] = int(rng.integers(0, 256))
+        if k % 50 == 0:
+            h = bytearray(rng.integers(0, 256, size=256, dtype=np.uint8).tobytes())
+        st = L.fluxbin_layer_from_header(ctypes.create_string_buffer(bytes(h), 256), FAKE_DEVICE_PTR, 1 << 40,
+                                         ctypes.byref(fb.Layer()))
+        assert st in (fb.FLUXBIN_OK, fb.FLUXBIN_ERR_INVALID_ARG, fb.FLUXBIN_ERR_UNSUPPORTED,
+                      fb.FLUXBIN_ERR_BUFFER_TOO_SMALL)
