@@ -125,9 +125,17 @@ class Bench:
         g = self.graph(steps, warmup)
         g.replay()          # first replay outside the timed region (graph upload)
         torch.cuda.synchronize()
+        # the replays run back to back (an event between consecutive replays, no host synchronization until the
+        # last one), so the device never idles inside the timed region; each replay is timed by its own event pair
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(replays + 1)]
         wall0 = time.perf_counter()
-        ms = [self.time_graph(g) for _ in range(replays)]
+        ev[0].record()
+        for r in range(replays):
+            g.replay()
+            ev[r + 1].record()
+        torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
+        ms = [ev[r].elapsed_time(ev[r + 1]) for r in range(replays)]
         return ms, wall
 
     def per_launch_us(self, launches: int = 60, reps: int = 5):
@@ -631,8 +639,8 @@ def main():
                           "layers": [it["spec"].name for it in bench.items],
                           "bytes_per_launch": {it["spec"].name: it["bytes"] for it in bench.items}}), flush=True)
         return
-    # Headline: a graph of exactly K steps (up then down per step, rotating packed copies), replayed `replays` times,
-    # each replay between HIP events on the replay stream; the median replay gives ms_per_step and value. Both launches
+    # Headline: a graph of exactly K steps (up then down per step, rotating packed copies), replayed `replays` times
+    # back to back, each replay between HIP events on the replay stream; the median replay gives ms_per_step and value. Both launches
     # of a step are the batch-1 GEMV kernel, so its average launch duration in the timed region is the step time / 2
     # (gaps between the graph's launches included), and roofline.achieved comes from the same timing.
     replay_ms, wall = bench.run(args.steps, args.warmup, replays=args.replays)
