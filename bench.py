@@ -304,20 +304,25 @@ def cpu_baseline(bench, budget_s: float):
     return res
 
 
-def small_batch_us(specs, batches, launches=40):
+def small_batch_us(specs, batches, launches=40, rounds=3):
     """Per-call microseconds of the small-batch product on the same layers, graph-timed like the batch-1 figure, for
-    the default kernel (matrix cores: the sign decode per bit is shared by all batch rows) and, on the same packed
-    copies, the LUT batch kernel (batch-interleaved tables, each sign word read once for all batch rows)."""
+    the default kernel choice and, on the same packed copies, each kernel forced: the matrix cores (the sign decode per
+    bit is shared by all batch rows) and the LUT batch kernel (batch-interleaved tables, each sign word read once for
+    all batch rows). The three are measured in turn, `rounds` times, and each figure is the median of its rounds (the
+    first measurement of a process runs at lower clocks)."""
+    import statistics
     import torch
     out = {}
     for B in batches:
         b = Bench(specs, B, COPIES_BYTES_PER_LAYER * len(specs))
-        us_k = {}
-        for kern, flag in (("mfma", 1), ("lut", 0), ("default", None)):
-            with b.fb.tuning(**({} if flag is None else {"mfma": flag})):
-                for it in b.items:
-                    it["ws"] = b.fb.make_workspace(it["packs"][0], B)
-                us_k[kern] = b.per_launch_us(launches, 3)
+        runs = {"mfma": [], "lut": [], "default": []}
+        for _ in range(rounds):
+            for kern, flag in (("mfma", 1), ("lut", 0), ("default", None)):
+                with b.fb.tuning(**({} if flag is None else {"mfma": flag})):
+                    for it in b.items:
+                        it["ws"] = b.fb.make_workspace(it["packs"][0], B)
+                    runs[kern].append(b.per_launch_us(launches, 3))
+        us_k = {k: [statistics.median(v) for v in zip(*r)] for k, r in runs.items()}
         for i, it in enumerate(b.items):
             s = it["spec"]
             um, ul, us = us_k["mfma"][i], us_k["lut"][i], us_k["default"][i]

@@ -206,10 +206,10 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
  * Y[b, :] = W-hat X[b, :] for b < B (1..16), reading every packed sign word once per call and using it for all B rows
  * (batch-independent reuse of the weights, Sec. 3.2 and App. E.2). d_x fp16 with row stride ldx >= N (elements); d_y
  * with row stride ldy >= M (elements of the output type). B = 1 gives the same result as fluxbin_lut_gemv.
- * Two kernels compute it: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4) and a matrix-core
- * kernel (mu = 4, or B > 4) that decodes the sign bits into fp16 +-|alpha_c| tiles and multiplies them with the
- * activations on the MFMA units (the products are exact in the fp32 accumulation, as in the LUT path; the row scale is
- * applied per 128-column chunk). Layers with fine row-scale groups (g_r or g_s below 128) run the generic LUT kernel
+ * Two kernels compute it: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4 on layers with at
+ * least four 1024-row tiles of super-chunks per CU) and a matrix-core kernel (mu = 4, B > 4, or smaller layers) that
+ * decodes the sign bits into fp16 +-alpha_c tiles and multiplies them with the activations on the MFMA units (the
+ * products are exact in the fp32 accumulation, as in the LUT path; the row scale is applied per 128-column chunk). Layers with fine row-scale groups (g_r or g_s below 128) run the generic LUT kernel
  * for B >= 2. All are deterministic; their results differ only by fp32 summation order.
  */
 fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx,

@@ -8,20 +8,20 @@
 // (128 x B) block of activations. Here every 32 columns of that contraction are one v_mfma_f32_16x16x32_f16, and the
 // cost per sign bit is the same for any B <= 16 (the batch occupies the 16 columns of the MFMA tile).
 //
-// Exactness. The A operand is s(i, v) * |colscale[v]|, an fp16 value (the column scale with its sign bit replaced),
-// and the B operand is x[b, xidx[v]] with the sign of colscale[v] folded in, also fp16. Their products are exact in
-// the fp32 accumulation of the matrix core, as x * colscale is exact in fp32 for the LUT kernels (two 11-bit
-// significands). The row scale multiplies each 128-column chunk's fp32 sum once (Eq. 15's order), and y is the fp32
-// sum over chunks. Padding columns have column scale 0 and stage x = 0, so they add exactly zero.
+// Exactness. The A operand is -s(i, v) * colscale[v], an fp16 value (the column scale with its sign bit flipped where
+// the sign bit is set), and the B operand is x[b, xidx[v]], also fp16. Their products are exact in the fp32
+// accumulation of the matrix core, as x * colscale is exact in fp32 for the LUT kernels (two 11-bit significands). The
+// row scale multiplies each 128-column chunk's fp32 sum once (Eq. 15's order), negated, and y is the fp32 sum over
+// chunks. Padding columns have column scale 0 and stage x = 0, so they add exactly zero.
 //
 // Sign decode. By the packed format, row i's 16-byte entry of a chunk holds the chunk's 128 sign bits rotated left by
 // R(i) bits (mu = 8: R = 8 (i mod 16); mu = 4: R = 4 (i mod 32)). Lane (r, g) of a 16-row MFMA block needs canonical
 // bits 32g .. 32g+31 of its row r: two 32-bit words of the entry and one funnel shift give them, whatever the
 // rotation. The K dimension of the contraction is ordered so that element pair k of K step q holds canonical columns
 // (32g + 4q + k, 32g + 4q + k + 16): a left shift of the 32 bits by 15 - (4q + k) puts both sign bits at bit
-// positions 15 and 31, the fp16 sign bits of the pair, so one and-or with the column-scale pair forms the operand
-// (a set bit gives -|colscale|, so the matrix core sums -s; the row scale is applied negated). The words of two row
-// blocks are shifted together as one 64-bit value.
+// positions 15 and 31, the fp16 sign bits of the pair, so one three-input bit operation (v_bitop3_b32: and with the
+// sign-bit mask, xor with the column-scale pair) forms the operand. The words of two row blocks are shifted together as
+// one 64-bit value.
 //
 // Work decomposition (as in the LUT kernels): a tile is 256 rows, 64 per wavefront of a 256-thread workgroup (four
 // 16-row MFMA blocks); a unit is a tile times a super-chunk (256 virtual columns, both stored chunk slots); units are
@@ -33,7 +33,9 @@
 // byte requested twice); a wavefront passes the entries to its MFMA lanes through its own LDS scratch. The
 // activations of a unit (gathered through the VCM index table) are requested together with its signs, because
 // vector loads complete in issue order: a load issued after the sign loads of a later unit could only be used once
-// those had arrived. They are written to a double-buffered LDS staging area one unit before they are multiplied.
+// those had arrived. Each thread gathers one column pair (the two halves of an operand dword) for half of the batch
+// rows and writes them, one unit before they are multiplied and before the multiplication of the current unit (so
+// that their registers are free during it), to a double-buffered LDS staging area as whole dwords, 64 banks per write.
 #include <hip/hip_runtime.h>
 
 #include "fluxbin_device.h"
@@ -45,27 +47,29 @@ namespace {
 typedef _Float16 mf_half8 __attribute__((ext_vector_type(8)));
 typedef float mf_float4 __attribute__((ext_vector_type(4)));
 typedef unsigned int mf_u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int mf_u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short mf_u16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kMfNT = 256;                          // threads per workgroup: four wavefronts of 64 rows
 constexpr int kMfR = 256;                           // rows per tile
 constexpr int kMfXStride = 68;                      // dwords per (chunk, column group, K step) block: 64 + 4 pad
 constexpr int kMfXUnit = 2 * 4 * 4 * kMfXStride;    // dwords of staged activation pairs per unit
 constexpr int kMfAUnit = 2 * 4 * 16;                // dwords of column-scale pairs per unit
-constexpr int kMfScr = 64 * 8;                      // dwords of a wavefront's sign scratch: 64 rows x 32 bytes
+constexpr int kMfScr = 2 * 64 * 4;                  // dwords of a wavefront's sign scratch: 2 chunks x 64 rows x 16 bytes
+constexpr int kMfScrUnit = kMfScr + 64;             // dwords of one unit's sign scratch and 64 words of row scales
+constexpr int kMfScrWave = 2 * kMfScrUnit;          // dwords of a wavefront's scratch: two units (double buffer)
 constexpr int kMfTStride = 68;                      // dwords per batch row of a wavefront's tile-end transpose
-constexpr int kMfScrWave = 16 * kMfTStride;         // dwords of a wavefront's scratch (>= kMfScr + 64 row scales)
-static_assert(kMfScrWave >= kMfScr + 64, "scratch too small");
+constexpr int kMfTRows = 8;                         // batch rows per pass of the transpose (in one unit's scratch)
+static_assert(kMfTRows * kMfTStride <= kMfScrUnit, "transpose pass larger than a unit's scratch");
 
 // Requested data of one unit: the lane's row entries of both chunks (lane l: row 16 (l >> 4) + (l & 15) of the
 // wavefront's 64 rows), one word of row scales (lane l: rows 2 (l & 31) and 2 (l & 31) + 1 of chunk l >> 5), and the
-// lane's staged column: its metadata and x of batch rows 0..BP-1.
+// lane's staged column pair: the metadata of its two columns and their x in its half of the batch rows.
 template <int BP>
 struct MfUnitRegs {
   mf_u32x4 e[2];
   uint32_t r;
-  uint32_t meta;        // xidx | colscale << 16 (thread t owns virtual column t of the unit)
-  uint32_t xv[BP];      // x bits of batch rows 0..BP-1, one register each (rows >= B read row B-1)
+  uint32_t meta[2];     // xidx | colscale << 16 of the thread's columns c and c + 16 (see mf_pair_col)
+  uint16_t xv[BP];      // x bits: xv[2i], xv[2i + 1] = columns c, c + 16 of batch row BP/2 * half + i (rows >= B: row B-1)
 };
 
 struct MfCursor {
@@ -86,21 +90,39 @@ __device__ __forceinline__ uint32_t mf_block_row(const GemmArgs& a, int tile, in
   return uint32_t(r <= a.Mp - 16 ? r : a.Mp - 16);
 }
 
-__device__ __forceinline__ uint32_t mf_load_meta(const GemmArgs& a, int sc, int t) {
-  const int v = sc * 256 + t;
-  return uint32_t(a.xidx[v]) | (uint32_t(a.colscale[v]) << 16);
+// Staging ownership: thread t stages the column pair p = t & 127 of a unit, virtual columns c = 32 (p >> 4) + (p & 15)
+// and c + 16 (chunk c >> 7; the pair is one fp16 pair of the MFMA operands), for half t >> 7 of the batch rows.
+__device__ __forceinline__ int mf_pair_col(int t) { return 32 * ((t & 127) >> 4) + (t & 15); }
+
+// Metadata of the thread's two columns of super-chunk sc, through buffer loads (byte offsets 32-bit: the host checks
+// the index tables' size).
+__device__ __forceinline__ void mf_load_meta(const GemmArgs& a, int sc, int t, uint32_t (&m)[2]) {
+  const __amdgpu_buffer_rsrc_t ri = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.xidx), 0,
+                                                                       a.NSC * 512, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.colscale), 0,
+                                                                       a.NSC * 512, 0x00020000);
+  const int voff = 2 * mf_pair_col(t), soff = sc * 512;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t xi = __builtin_amdgcn_raw_buffer_load_b16(ri, voff + 32 * i, soff, 0);
+    const uint32_t cs = __builtin_amdgcn_raw_buffer_load_b16(rc, voff + 32 * i, soff, 0);
+    m[i] = xi | (cs << 16);
+  }
 }
 
 // Requests unit c's data into u: activations first (u.meta must hold the unit's metadata), then the sign entries and
-// row scales. p0, p1: row-scale planes of the unit's two chunks.
+// row scales. p0, p1: row-scale planes of the unit's two chunks. rx: buffer resources of the thread's BP/2 batch rows
+// of x (range: the row's N columns). A padding column's load is given an offset outside every range (2^31), for which
+// the load returns zero without reading memory: x is never multiplied there, not even by a zero.
 template <int BP, int MU>
 __device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, int32_t p0, int32_t p1, int wave,
-                                         int lane, const uint16_t* const (&xrow)[BP], MfUnitRegs<BP>& u) {
-  {
-    const uint32_t xi = u.meta & 0xFFFFu;
-    const uint32_t col = xi == 0xFFFFu ? 0u : xi;
+                                         int lane, const __amdgpu_buffer_rsrc_t (&rx)[BP / 2], MfUnitRegs<BP>& u) {
 #pragma unroll
-    for (int b = 0; b < BP; ++b) u.xv[b] = xrow[b][col];
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t xi = u.meta[i] & 0xFFFFu;
+    const int voff = xi == 0xFFFFu ? int(0x80000000u) : int(2 * xi);
+#pragma unroll
+    for (int b = 0; b < BP / 2; ++b) u.xv[2 * b + i] = __builtin_amdgcn_raw_buffer_load_b16(rx[b], voff, 0, 0);
   }
   const int rbl = lane >> 4;
   const uint32_t row = mf_block_row(a, c.tile, wave, rbl) + uint32_t(lane & 15);
@@ -120,24 +142,16 @@ __device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, i
                                            (int64_t(plane) * a.Mp + rrow) * 2);
 }
 
-// Writes a staged unit: the activation pairs (sign of the column scale folded in; 0 for padding columns, so that x is
-// never multiplied there, not even by a zero) and the column-scale pairs (magnitudes) in the order the MFMA operands
-// read them. Batch rows b >= B hold row B-1's values: MFMA output column b depends on activation column b only, and
-// columns >= B are never stored.
+// Writes a staged unit: the thread's activation pairs and, for half 0, its column-scale pair (with sign), in the order
+// the MFMA operands read them. Batch rows b >= B hold row B-1's values: MFMA output column b depends on activation
+// column b only, and columns >= B are never stored.
 template <int BP>
-__device__ __forceinline__ void mf_stage_write(const GemmArgs& a, const MfUnitRegs<BP>& u, uint32_t* sx, uint32_t* sa,
-                                               int t) {
-  const int h = t >> 7, cc = t & 127, g = cc >> 5, m = cc & 31, j = m & 15, hf = m >> 4;
-  const int q = j >> 2, k = j & 3;
-  const uint32_t xi = u.meta & 0xFFFFu;
-  const uint16_t cs = uint16_t(u.meta >> 16);
-  const uint16_t flip = cs & 0x8000u;
-  const uint16_t keep = xi != 0xFFFFu ? uint16_t(0xFFFFu) : uint16_t(0);
-  uint16_t* sx16 = reinterpret_cast<uint16_t*>(sx);
-  const int base = ((h * 4 + g) * 4 + q) * kMfXStride + k;
+__device__ __forceinline__ void mf_stage_write(const MfUnitRegs<BP>& u, uint32_t* sx, uint32_t* sa, int t) {
+  const int p = t & 127, hg = p >> 4, j = p & 15, q = j >> 2, k = j & 3, half = t >> 7;
+  uint32_t* dst = sx + (hg * 4 + q) * kMfXStride + k + 4 * (BP / 2) * half;
 #pragma unroll
-  for (int b = 0; b < BP; ++b) sx16[(base + 4 * b) * 2 + hf] = uint16_t((uint16_t(u.xv[b]) ^ flip) & keep);
-  reinterpret_cast<uint16_t*>(sa)[((h * 4 + g) * 16 + j) * 2 + hf] = uint16_t(cs & 0x7FFFu);
+  for (int b = 0; b < BP / 2; ++b) dst[4 * b] = __builtin_bit_cast(uint32_t, mf_u16x2{u.xv[2 * b], u.xv[2 * b + 1]});
+  if (half == 0) sa[hg * 16 + j] = (u.meta[0] >> 16) | (u.meta[1] & 0xFFFF0000u);
 }
 
 // 64-bit left shift by a constant, as one v_lshlrev_b64: it shifts two 32-bit words in the time a 32-bit shift takes
@@ -150,33 +164,38 @@ __device__ __forceinline__ uint64_t mf_shl64(uint64_t v, uint32_t s) {
   return r;
 }
 
+// Writes a unit's sign entries and row-scale word (requested by mf_issue) to the wavefront's scratch of that unit:
+// chunk h's entries at 256 h dwords, one 16-byte entry per row, rows consecutive, then the 64 row-scale words.
+template <int BP>
+__device__ __forceinline__ void mf_stage_signs(const MfUnitRegs<BP>& u, uint32_t* scr, int lane) {
+  *reinterpret_cast<mf_u32x4*>(scr + lane * 4) = u.e[0];
+  *reinterpret_cast<mf_u32x4*>(scr + 256 + lane * 4) = u.e[1];
+  scr[kMfScr + lane] = u.r;
+}
+
 // Multiplies one staged unit into the accumulators. xs/as: the unit's staged activation and column-scale pairs;
-// scr: the wavefront's sign scratch (32 bytes per row: the 16-byte entry, then its first 8 bytes again, so that the two
-// words a lane reads never wrap), followed by 64 words of row scales.
-template <bool SHL64>
-__device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, const mf_u32x4 (&e)[2], uint32_t r,
-                                        uint32_t* scr, int lane, int r16, int g, const uint32_t (&aw)[2], uint32_t sh,
-                                        float (&acc)[4][4]) {
-  uint32_t* srs = scr + kMfScr;
-  srs[lane] = r;
+// scr: the wavefront's scratch of the unit (mf_stage_signs). wa[par][c]: dword offset, within a chunk's entries, of
+// word c of the two a lane reads from its row of block 0 (row blocks of parity par; block rb adds 64 rb). Reading the
+// words separately, with the index wrapped within the entry, needs no copy of an entry's first words after it, and
+// the 64 lanes of one read hit 64 different banks: lane (r, g) reads bank 4r + (its word index), and the word indices
+// of one r are a permutation of 0..3 over g.
+__device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, const uint32_t* scr, int r16, int g,
+                                        const uint32_t (&wa)[2][2], uint32_t sh, float (&acc)[4][4]) {
+  const uint32_t* srs = scr + kMfScr;
+  uint32_t w[2][4];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+      w[h][rb] = __builtin_amdgcn_alignbit(scr[256 * h + 64 * rb + wa[rb & 1][1]],
+                                           scr[256 * h + 64 * rb + wa[rb & 1][0]], sh);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    *reinterpret_cast<mf_u32x4*>(scr + lane * 8) = e[h];
-    *reinterpret_cast<mf_u32x2*>(scr + lane * 8 + 4) = mf_u32x2{e[h][0], e[h][1]};
-    uint32_t w[4];
     uint2 rs[4];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-      const uint32_t* ent = scr + (16 * rb + r16) * 8 + aw[rb & 1];
-      w[rb] = __builtin_amdgcn_alignbit(ent[1], ent[0], sh);
-      rs[rb] = *reinterpret_cast<const uint2*>(srs + h * 32 + 8 * rb + 2 * g);
-    }
+    for (int rb = 0; rb < 4; ++rb) rs[rb] = *reinterpret_cast<const uint2*>(srs + h * 32 + 8 * rb + 2 * g);
     // the words of row blocks 2rp and 2rp + 1 as one 64-bit value (high: 2rp + 1), shifted together below
-    uint64_t w2[2] = {0, 0};
-    if constexpr (SHL64) {
-      w2[0] = (uint64_t(w[1]) << 32) | w[0];
-      w2[1] = (uint64_t(w[3]) << 32) | w[2];
-    }
+    const uint64_t w2[2] = {(uint64_t(w[h][1]) << 32) | w[h][0], (uint64_t(w[h][3]) << 32) | w[h][2]};
     mf_float4 tmp[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -187,15 +206,9 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
         mf_u32x4 av0, av1;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const uint32_t s = uint32_t(15 - (4 * q + k));
-          if constexpr (SHL64) {
-            const uint64_t sft = mf_shl64(w2[rp], s);
-            av0[k] = (uint32_t(sft) & 0x80008000u) | ac[k];
-            av1[k] = (uint32_t(sft >> 32) & 0x80008000u) | ac[k];
-          } else {
-            av0[k] = ((w[2 * rp] << s) & 0x80008000u) | ac[k];
-            av1[k] = ((w[2 * rp + 1] << s) & 0x80008000u) | ac[k];
-          }
+          const uint64_t sft = mf_shl64(w2[rp], uint32_t(15 - (4 * q + k)));
+          av0[k] = (uint32_t(sft) & 0x80008000u) ^ ac[k];
+          av1[k] = (uint32_t(sft >> 32) & 0x80008000u) ^ ac[k];
         }
         const mf_float4 c0 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[2 * rp];
         const mf_float4 c1 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[2 * rp + 1];
@@ -217,30 +230,34 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
 
 // End of a tile's contribution: y for a tile only this workgroup covers, else its partial sums (slot 0 for the
 // workgroup's first tile, 1 for its last), in the layout reduce_tile reads: element (b, row in tile) at b * R + row.
-// Lane (b = r16, g) holds rows 16 rb + 4 g + v of the wavefront's 64; the wavefront first transposes them through its
-// LDS scratch (row block rb of batch row b at b * kMfTStride + 16 rb), so that every store instruction writes 64
-// consecutive rows of one batch row (whole memory lines: scattered 4-byte stores wrote each line several times).
+// Lane (b = r16, g) holds rows 16 rb + 4 g + v of the wavefront's 64; the wavefront first transposes them through the
+// scratch of the unit it has just multiplied (row block rb of batch row b at (b mod 8) * kMfTStride + 16 rb, eight
+// batch rows per pass), so that every store instruction writes 64 consecutive rows of one batch row (whole memory
+// lines: scattered 4-byte stores wrote each line several times).
 template <int BP>
 __device__ __forceinline__ void mf_tile_end(const GemmArgs& a, int tile, bool shared, int slot, int wave, int lane,
                                             int r16, int g, const float (&acc)[4][4], uint32_t* scr) {
+  constexpr int TB = BP < kMfTRows ? BP : kMfTRows;
   float* t = reinterpret_cast<float*>(scr);
-  if (r16 < BP) {
+  float* mine = a.partials + ((int64_t(blockIdx.x) * 2 + slot) * BP) * kMfR + wave * 64 + lane;
+  const int64_t row = int64_t(tile) * kMfR + wave * 64 + lane;
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-      *reinterpret_cast<mf_float4*>(t + r16 * kMfTStride + 16 * rb + 4 * g) =
-          mf_float4{acc[rb][0], acc[rb][1], acc[rb][2], acc[rb][3]};
-  }
-  if (shared) {
-    float* mine = a.partials + ((int64_t(blockIdx.x) * 2 + slot) * BP) * kMfR + wave * 64 + lane;
+  for (int b0 = 0; b0 < BP; b0 += TB) {
+    if (r16 >= b0 && r16 < b0 + TB) {
 #pragma unroll
-    for (int b = 0; b < BP; ++b)
-      __hip_atomic_store(mine + b * kMfR, t[b * kMfTStride + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  } else {
-    const int64_t row = int64_t(tile) * kMfR + wave * 64 + lane;
-    if (row < a.M) {
+      for (int rb = 0; rb < 4; ++rb)
+        *reinterpret_cast<mf_float4*>(t + (r16 - b0) * kMfTStride + 16 * rb + 4 * g) =
+            mf_float4{acc[rb][0], acc[rb][1], acc[rb][2], acc[rb][3]};
+    }
+    if (shared) {
 #pragma unroll
-      for (int b = 0; b < BP; ++b)
-        if (b < a.B) store_y(a, b, row, t[b * kMfTStride + lane]);
+      for (int b = b0; b < b0 + TB; ++b)
+        __hip_atomic_store(mine + b * kMfR, t[(b - b0) * kMfTStride + lane], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    } else if (row < a.M) {
+#pragma unroll
+      for (int b = b0; b < b0 + TB; ++b)
+        if (b < a.B) store_y(a, b, row, t[(b - b0) * kMfTStride + lane]);
     }
   }
 }
@@ -260,41 +277,47 @@ struct MfKernel {
 
   struct Lane {
     int t, lane, wave, r16, g;
-    uint32_t aw[2];   // word index, within a row's entry, of the first word holding the lane's canonical bits
+    uint32_t wa[2][2];   // scratch offsets of the two words holding the lane's canonical bits (see mf_unit)
     uint32_t sh;      // funnel shift
   };
 
   // Unit K of the workgroup (compile-time K < kMfMaxUnits; the launch plan keeps the range within that), with
   // register set K mod (D + 1). Fully unrolled, so no loads are carried through a loop header.
-  // Order: request unit K+D (activations, then signs and row scales) and the metadata of unit K+D+1; multiply unit K
-  // (waits only for its own data, requested D units ago); stage unit K+1 (requested D-1 units ago); end a tile.
+  // Order: request unit K+D (activations, then signs and row scales) and the metadata of unit K+D+1; stage unit K+1
+  // (requested D-1 units ago: activations to the workgroup's staging area, signs and row scales to the wavefront's
+  // scratch of K+1, so that its registers are free during the multiplication); multiply unit K (staged one unit ago);
+  // end a tile (transposing through unit K's scratch, now read).
   template <int K>
   __device__ static __forceinline__ void step(const GemmArgs& a, State& s, MfUnitRegs<BP> (&ur)[D + 1],
-                                              uint32_t& meta_next, const int* s_planes, uint32_t* sx, uint32_t* sa,
-                                              uint32_t* scr, const Lane& ln, const uint16_t* const (&xrow)[BP]) {
+                                              uint32_t (&meta_next)[2], const int* s_planes, uint32_t* sx,
+                                              uint32_t* sa, uint32_t* scr, const Lane& ln,
+                                              const __amdgpu_buffer_rsrc_t (&rx)[BP / 2]) {
     if constexpr (K < kMfMaxUnits) {
       if (K >= s.n) return;
-      constexpr int P = K % (D + 1);
       constexpr int PN = (K + D) % (D + 1);
       constexpr int PS = (K + 1) % (D + 1);
       {
         const int kd = K + D < s.n ? K + D : s.n - 1;
-        ur[PN].meta = meta_next;
-        mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kd], s_planes[2 * kd + 1], ln.wave, ln.lane, xrow, ur[PN]);
-        meta_next = mf_load_meta(a, s.stg_sc, ln.t);
+        ur[PN].meta[0] = meta_next[0];
+        ur[PN].meta[1] = meta_next[1];
+        mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kd], s_planes[2 * kd + 1], ln.wave, ln.lane, rx, ur[PN]);
+        mf_load_meta(a, s.stg_sc, ln.t, meta_next);
         if (K + D + 1 < s.n) mf_advance(a, s.nxt);
         if (K + D + 2 < s.n && ++s.stg_sc == a.steps) s.stg_sc = 0;
       }
       __builtin_amdgcn_sched_barrier(0);
-      // 64-bit shifts free VALU issue slots; with 16 batch rows their register pairs would spill
-      mf_unit<(BP <= 8)>(sx + (K & 1) * kMfXUnit, sa + (K & 1) * kMfAUnit, ur[P].e, ur[P].r, scr, ln.lane, ln.r16, ln.g, ln.aw,
+      if (K + 1 < s.n) {
+        mf_stage_write<BP>(ur[PS], sx + ((K + 1) & 1) * kMfXUnit, sa + ((K + 1) & 1) * kMfAUnit, ln.t);
+        mf_stage_signs<BP>(ur[PS], scr + ((K + 1) & 1) * kMfScrUnit, ln.lane);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mf_unit(sx + (K & 1) * kMfXUnit, sa + (K & 1) * kMfAUnit, scr + (K & 1) * kMfScrUnit, ln.r16, ln.g, ln.wa,
               ln.sh, s.acc);
-      if (K + 1 < s.n)
-        mf_stage_write<BP>(a, ur[PS], sx + ((K + 1) & 1) * kMfXUnit, sa + ((K + 1) & 1) * kMfAUnit, ln.t);
       if (s.cur.sc == a.steps - 1 || K + 1 == s.n) {
         const int tile = s.cur.tile;
         const bool shared = tile == s.first_tile ? s.first_shared : (tile == s.last_tile && s.last_shared);
-        mf_tile_end<BP>(a, tile, shared, tile == s.first_tile ? 0 : 1, ln.wave, ln.lane, ln.r16, ln.g, s.acc, scr);
+        mf_tile_end<BP>(a, tile, shared, tile == s.first_tile ? 0 : 1, ln.wave, ln.lane, ln.r16, ln.g, s.acc,
+                        scr + (K & 1) * kMfScrUnit);
         if (shared) ++s.n_pending;
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb)
@@ -303,13 +326,13 @@ struct MfKernel {
       }
       mf_advance(a, s.cur);
       __syncthreads();
-      step<K + 1>(a, s, ur, meta_next, s_planes, sx, sa, scr, ln, xrow);
+      step<K + 1>(a, s, ur, meta_next, s_planes, sx, sa, scr, ln, rx);
     }
   }
 };
 
 template <int BP, int MU, int D, bool R2>
-__global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
+__global__ void __launch_bounds__(kMfNT, (BP <= 4 && D == 2 && R2) ? 4 : 3) k_gemm_mfma(GemmArgs a) {
   using K = MfKernel<BP, MU, D>;
   __shared__ __attribute__((aligned(16))) uint32_t sx[2 * kMfXUnit];
   __shared__ __attribute__((aligned(16))) uint32_t sa[2 * kMfAUnit];
@@ -328,8 +351,11 @@ __global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
   {
     const int rot0 = MU == 8 ? 8 * ln.r16 : 4 * ln.r16;
 #pragma unroll
-    for (int par = 0; par < 2; ++par)
-      ln.aw[par] = uint32_t(((32 * ln.g - rot0 - (MU == 4 ? 64 * par : 0)) & 127) >> 5);
+    for (int par = 0; par < 2; ++par) {
+      const uint32_t aw = uint32_t(((32 * ln.g - rot0 - (MU == 4 ? 64 * par : 0)) & 127) >> 5);
+      ln.wa[par][0] = uint32_t(4 * ln.r16) + aw;
+      ln.wa[par][1] = uint32_t(4 * ln.r16) + ((aw + 1) & 3u);
+    }
     ln.sh = uint32_t((32 * ln.g - rot0) & 31);
   }
   uint32_t* scr = scr_all + ln.wave * kMfScrWave;
@@ -356,21 +382,23 @@ __global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
     while (sc >= a.steps) sc -= a.steps;
     s_planes[ln.t] = a.chunk_plane[2 * sc + (ln.t & 1)];
   }
-  // Batch rows of x (wave-uniform; rows >= B read row B-1, masked when staged).
-  const uint16_t* xrow[BP];
+  // Buffer resources of the thread's batch rows of x, each of range N columns: half t >> 7 of the padded batch
+  // (wave-uniform; rows >= B read row B-1).
+  __amdgpu_buffer_rsrc_t rx[BP / 2];
+  const int half = __builtin_amdgcn_readfirstlane(ln.t >> 7);
 #pragma unroll
-  for (int b = 0; b < BP; ++b) xrow[b] = a.x + int64_t(b < a.B ? b : a.B - 1) * a.ldx;
+  for (int i = 0; i < BP / 2; ++i) {
+    const int b = (BP / 2) * half + i;
+    rx[i] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.x + int64_t(b < a.B ? b : a.B - 1) * a.ldx), 0,
+                                              2 * a.N, 0x00020000);
+  }
   MfUnitRegs<BP> ur[D + 1];
-  uint32_t meta_next;
+  uint32_t meta_next[2];
   {
     int sc = s.cur.sc;
 #pragma unroll
     for (int k = 0; k <= D; ++k) {
-      const uint32_t m = mf_load_meta(a, sc, ln.t);
-      if (k < D)
-        ur[k].meta = m;
-      else
-        meta_next = m;
+      mf_load_meta(a, sc, ln.t, k < D ? ur[k].meta : meta_next);
       if (k + 1 < s.n && ++sc == a.steps) sc = 0;
     }
     s.stg_sc = sc;   // unit D + 1 (clamped)
@@ -382,12 +410,13 @@ __global__ void __launch_bounds__(kMfNT, 3) k_gemm_mfma(GemmArgs a) {
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int kk = k < s.n ? k : s.n - 1;
-    mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kk], s_planes[2 * kk + 1], ln.wave, ln.lane, xrow, ur[k]);
+    mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kk], s_planes[2 * kk + 1], ln.wave, ln.lane, rx, ur[k]);
     if (k + 1 < s.n) mf_advance(a, s.nxt);
   }
-  mf_stage_write<BP>(a, ur[0], sx, sa, ln.t);
+  mf_stage_write<BP>(ur[0], sx, sa, ln.t);
+  mf_stage_signs<BP>(ur[0], scr, ln.lane);
   __syncthreads();
-  K::template step<0>(a, s, ur, meta_next, s_planes, sx, sa, scr, ln, xrow);
+  K::template step<0>(a, s, ur, meta_next, s_planes, sx, sa, scr, ln, rx);
   if constexpr (!R2) {
     const int pend0 = s.first_shared ? s.first_tile : s.last_tile;
     publish_pending<kMfNT, 1, BP>(a, pend0, s.last_tile, s.n_pending, &s_flag);

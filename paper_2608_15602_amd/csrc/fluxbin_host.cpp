@@ -173,17 +173,18 @@ static fluxbin_tuning tuning_snapshot() {
 
 // Small-batch kernel choice (both kernels reduce split tiles with the second kernel). The matrix-core kernel's cost per
 // sign bit (decode) is the same for every B <= 16 (B <= 4 share one padded instance); the mu = 8 LUT batch kernel's
-// table work grows with B. Measured (us per call, up / down, LUT batch / matrix cores): 70B MLP layers B = 2 32.9 / 34.5
-// against 53.4 / 46.4, B = 4 42.1 / 42.4 against 51.9 / 48.0, B = 8 84.6 / 91.5 against 55.0 / 51.3; 7B MLP layers
-// (fewer than four 1024-row units per CU, where the LUT batch kernel's 1024-row workgroups do not fill the chip)
-// B = 2 14.4 / 17.4 against 15.3 / 17.8, B = 4 16.3 / 18.9 against 16.0 / 18.4. So mu = 8 uses the LUT batch kernel up
-// to B = 4 on large layers and at B = 2 on small ones, the matrix cores otherwise; mu = 4 (whose LUT path for B >= 2
-// is the generic kernel) always the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
+// table work grows with B. Measured (us per call, up / down, LUT batch against matrix cores, medians of interleaved
+// runs): 70B MLP layers B = 2 33.1 / 35.5 against 43.5 / 44.7, B = 4 41.0 / 42.2 against 43.3 / 44.1, B = 8 84.6 /
+// 91.5 against 47.3 / 47.6; 7B MLP layers (fewer than four 1024-row units per CU, where the LUT batch kernel's
+// 1024-row workgroups do not fill the chip) B = 2 14.8 / 17.7 against 13.8 / 14.9, B = 4 16.4 / 19.3 against 13.9 /
+// 15.0. So mu = 8 uses the LUT batch kernel up to B = 4 on large layers and the matrix cores otherwise; mu = 4 (whose
+// LUT path for B >= 2 is the generic kernel) always the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and
+// measurements).
 static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tuning& tu) {
   const int forced = tu.mfma;
   if (forced == 0 || forced == 1) return forced == 1;
   const bool small = ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
-  return L.shape.mu == 4 || B > 4 || (B > 2 && small);
+  return L.shape.mu == 4 || B > 4 || small;
 }
 
 static uint64_t layer_counter_bytes(int64_t M) {
@@ -321,6 +322,15 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   if (p->kernel == 0 && ceil_div(p->units, p->blocks) > b1_max_units(p->nt))
     p->blocks = ceil_div(p->units, int64_t(b1_max_units(p->nt)));
   if (p->kernel == 2 && ceil_div(p->units, p->blocks) > kBatMaxUnits) p->blocks = ceil_div(p->units, kBatMaxUnits);
+  // the matrix-core kernel: at least three units per workgroup (fewer split tiles to reduce, each workgroup's start-up
+  // amortized), as long as that leaves a workgroup for every CU. 7B MLP layers (about 1400 units), us per call up / down
+  // at 768 -> 512 -> 256 workgroups: B = 8 17.0 / 19.5 -> 14.7 / 16.7 -> 16.4 / 16.6, B = 16 22.6 / 24.7 -> 17.9 /
+  // 19.9 -> 18.8 / 18.8.
+  if (p->kernel == 3 && blocks_env <= 0 && ceil_div(p->units, p->blocks) < 3) {
+    const int64_t floor_blocks = p->units < cus ? p->units : int64_t(cus);
+    const int64_t b3 = ceil_div(p->units, 3);
+    p->blocks = b3 > floor_blocks ? b3 : floor_blocks;
+  }
   if (p->kernel == 3 && ceil_div(p->units, p->blocks) > kMfMaxUnits) p->blocks = ceil_div(p->units, kMfMaxUnits);
   // More workgroups than the chip holds at once (the caps above on large layers): whole waves of workgroups, each with
   // fewer units, instead of one full wave and a small second one that leaves most CUs idle (57344x8192 with 2 bases at
