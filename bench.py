@@ -336,6 +336,25 @@ def small_batch_us(specs, batches, launches=40, rounds=3):
     return out
 
 
+def prefill_us(specs, batches=(64, 256), launches=6):
+    """Per-call microseconds at prefill-size batches: B > 16 runs as 16-row batch tiles (one launch each, every tile
+    reading the packed weights again), graph-timed like the small-batch figures; TFLOP-eq counts 2 B M (N + S)."""
+    import torch
+    out = {}
+    for B in batches:
+        b = Bench(specs, B, COPIES_BYTES_PER_LAYER * len(specs))
+        us = b.per_launch_us(launches, 3)
+        for it, u in zip(b.items, us):
+            s = it["spec"]
+            plan = b.fb.fluxbin_plan_query(it["packs"][0], B)
+            out[f"{s.name}_B{B}"] = {"us_per_call": round(u, 2), "us_per_batch_row": round(u / B, 3),
+                                     "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (u * 1e-6) / 1e12, 2),
+                                     "batch_tiles": plan["batch_tiles"], "tile_kernel": plan["kernel_name"]}
+        del b
+        torch.cuda.empty_cache()
+    return out
+
+
 def decoder_layer_us(g_r: str, batches=(1, 4, 16), steps: int = 40):
     """A synthetic 70B decoder layer's linears in one HIP graph per step, for both hybrid variants (2 bases + 1%
     salient, 3 bases + 5% salient), at least three rotated copies of every layer; end-to-end microseconds per decoder
@@ -709,6 +728,7 @@ def main():
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
         out["config"]["small_batch"] = small_batch_us(specs, (2, 4, 8, 16))
         out["config"]["small_batch_mlp7b"] = small_batch_us(config_layers("c3_mlp7b", args.g_r), (2, 4, 8))
+        out["config"]["prefill_mlp70b"] = prefill_us(specs)
     if not args.no_grid:
         out["config"]["kernel_latency_grid"] = kernel_latency_grid_us()
     if not args.no_decoder:

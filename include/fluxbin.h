@@ -183,7 +183,7 @@ fluxbin_status fluxbin_layer_from_header(const void* header_host, void* d_packed
                                          fluxbin_layer* out);
 
 /*
- * Workspace for split reductions of one GEMV/GEMM call with batch B (1..16): partial sums of output rows and one
+ * Workspace for split reductions of one GEMV/GEMM call with batch B (1..8192): partial sums of output rows and one
  * 32-bit counter per row tile. Before its first use the workspace must be zero-filled (fluxbin_workspace_init); every
  * call leaves the counters at zero again. Calls sharing a workspace must not overlap in time.
  * The counters sit in a region of the same size for every batch size of a layer, so calls of one layer with any
@@ -203,9 +203,12 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
                                 void* d_workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
- * Y[b, :] = W-hat X[b, :] for b < B (1..16), reading every packed sign word once per call and using it for all B rows
- * (batch-independent reuse of the weights, Sec. 3.2 and App. E.2). d_x fp16 with row stride ldx >= N (elements); d_y
- * with row stride ldy >= M (elements of the output type). B = 1 gives the same result as fluxbin_lut_gemv.
+ * Y[b, :] = W-hat X[b, :] for b < B (1..8192). Up to 16 rows are one launch, which reads every packed sign word once
+ * and uses it for all its rows (batch-independent reuse of the weights, Sec. 3.2 and App. E.2); larger batches run as
+ * consecutive launches of 16-row batch tiles (the last with the remaining rows), each its own launch plan, one after
+ * another on the stream and sharing the workspace, so rows 16t..16t+15 give the same y as a call on those rows alone.
+ * d_x fp16 with row stride ldx >= N (elements); d_y with row stride ldy >= M (elements of the output type). B = 1
+ * gives the same result as fluxbin_lut_gemv.
  * Two kernels compute it: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4 on layers with at
  * least four 1024-row tiles of super-chunks per CU) and a matrix-core kernel (mu = 4, B > 4, or smaller layers) that
  * decodes the sign bits into fp16 +-alpha_c tiles and multiplies them with the activations on the MFMA units (the
@@ -257,10 +260,11 @@ fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
 /*
  * The launch plan a GEMV/GEMM call of batch B on this layer would use on the current device with the current tuning.
  *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel.
- * Host only apart from reading the device's CU count; launches nothing.
+ * For B > 16 the plan is that of the full 16-row batch tiles, batch_tiles the number of launches and workspace_bytes
+ * the call's workspace. Host only apart from reading the device's CU count; launches nothing.
  */
 typedef struct {
-  int32_t kernel, threads, rows_per_tile, depth, batch_groups, second_kernel_reduction, early, reserved;
+  int32_t kernel, threads, rows_per_tile, depth, batch_groups, second_kernel_reduction, early, batch_tiles;
   int64_t tiles, units, workgroups;
   uint64_t workspace_bytes;
 } fluxbin_plan_info;

@@ -508,16 +508,47 @@ fluxbin_status fluxbin_layer_from_header(const void* header_host, void* d_packed
   return FLUXBIN_OK;
 }
 
+}  // extern "C"
+
+// Batches larger than one launch's kMaxBatch rows run as consecutive launches of kMaxBatch-row batch tiles (the last
+// one with the remaining rows), each with its own launch plan, one after another on the caller's stream and sharing the
+// workspace (every launch leaves its counters at zero). Each tile reads the packed weights again: the batch dimension is
+// tiled with a fixed per-launch on-chip footprint.
+struct BatchTiles {
+  Plan full, tail;     // plans of a full tile and of the last tile (tail rows < kMaxBatch; unused if 0)
+  int n_full, tail_rows;
+  uint64_t ws_bytes;   // the larger of the two plans' workspaces
+};
+
+static fluxbin_status batch_tiles(const fluxbin_layer& L, int B, BatchTiles* bt) {
+  std::memset(bt, 0, sizeof(*bt));
+  bt->n_full = B / kMaxBatch;
+  bt->tail_rows = B % kMaxBatch;
+  if (bt->n_full > 0) {
+    const fluxbin_status st = make_plan(L, kMaxBatch, &bt->full);
+    if (st != FLUXBIN_OK) return st;
+    bt->ws_bytes = bt->full.ws_bytes;
+  }
+  if (bt->tail_rows > 0) {
+    const fluxbin_status st = make_plan(L, bt->tail_rows, &bt->tail);
+    if (st != FLUXBIN_OK) return st;
+    if (bt->tail.ws_bytes > bt->ws_bytes) bt->ws_bytes = bt->tail.ws_bytes;
+  }
+  return FLUXBIN_OK;
+}
+
+extern "C" {
+
 fluxbin_status fluxbin_workspace_query(const fluxbin_layer* layer, int32_t B, size_t* bytes) {
   g_msg[0] = 0;
   fluxbin_status st = check_layer(layer);
   if (st != FLUXBIN_OK) return st;
   if (!bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "bytes is NULL");
-  if (B < 1 || B > kMaxBatch) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, 16]", B);
-  Plan p;
-  st = make_plan(*layer, B, &p);
+  if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
+  BatchTiles bt;
+  st = batch_tiles(*layer, B, &bt);
   if (st != FLUXBIN_OK) return st;
-  *bytes = static_cast<size_t>(p.ws_bytes);
+  *bytes = static_cast<size_t>(bt.ws_bytes);
   return FLUXBIN_OK;
 }
 
@@ -534,7 +565,7 @@ static fluxbin_status gemm_common(const fluxbin_layer* layer, int32_t B, const u
   fluxbin_status st = check_layer(layer);
   if (st != FLUXBIN_OK) return st;
   const fluxbin_shape& s = layer->shape;
-  if (B < 1 || B > kMaxBatch) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, 16]", B);
+  if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
   if (!d_x || !d_y) return fail(FLUXBIN_ERR_INVALID_ARG, "x or y is NULL");
   if (y_is_fp32 != 0 && y_is_fp32 != 1) return fail(FLUXBIN_ERR_INVALID_ARG, "y_is_fp32 must be 0 or 1");
   if (ldx < s.N) return fail(FLUXBIN_ERR_INVALID_ARG, "ldx = %lld < N", (long long)ldx);
@@ -542,16 +573,25 @@ static fluxbin_status gemm_common(const fluxbin_layer* layer, int32_t B, const u
   const size_t xb = (size_t(B - 1) * ldx + s.N) * 2;
   const size_t yb = (size_t(B - 1) * ldy + s.M) * (y_is_fp32 ? 4 : 2);
   if (ranges_overlap(d_x, xb, d_y, yb)) return fail(FLUXBIN_ERR_INVALID_ARG, "x and y overlap");
-  Plan p;
-  st = make_plan(*layer, B, &p);
+  BatchTiles bt;
+  st = batch_tiles(*layer, B, &bt);
   if (st != FLUXBIN_OK) return st;
   if (!d_ws) return fail(FLUXBIN_ERR_INVALID_ARG, "workspace is NULL");
-  if (ws_bytes < p.ws_bytes)
+  if (ws_bytes < bt.ws_bytes)
     return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "workspace has %zu bytes, needs %llu", ws_bytes,
-                (unsigned long long)p.ws_bytes);
+                (unsigned long long)bt.ws_bytes);
   if (ranges_overlap(d_ws, ws_bytes, d_y, yb) || ranges_overlap(d_ws, ws_bytes, d_x, xb))
     return fail(FLUXBIN_ERR_INVALID_ARG, "workspace overlaps x or y");
-  return launch_gemm(*layer, p, B, d_x, ldx, d_y, ldy, y_is_fp32, d_ws, stream);
+  const size_t y_elt = y_is_fp32 ? 4 : 2;
+  for (int t = 0; t <= bt.n_full; ++t) {
+    const int rows = t < bt.n_full ? kMaxBatch : bt.tail_rows;
+    if (rows == 0) break;
+    const int64_t b0 = int64_t(t) * kMaxBatch;
+    st = launch_gemm(*layer, t < bt.n_full ? bt.full : bt.tail, rows, d_x + b0 * ldx, ldx,
+                     static_cast<uint8_t*>(d_y) + size_t(b0) * size_t(ldy) * y_elt, ldy, y_is_fp32, d_ws, stream);
+    if (st != FLUXBIN_OK) return st;
+  }
+  return FLUXBIN_OK;
 }
 
 fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x, void* d_y, int32_t y_is_fp32,
@@ -632,10 +672,11 @@ fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin
   fluxbin_status st = check_layer(layer);
   if (st != FLUXBIN_OK) return st;
   if (!out) return fail(FLUXBIN_ERR_INVALID_ARG, "out is NULL");
-  if (B < 1 || B > kMaxBatch) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, 16]", B);
-  Plan p;
-  st = make_plan(*layer, B, &p);
+  if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
+  BatchTiles bt;
+  st = batch_tiles(*layer, B, &bt);
   if (st != FLUXBIN_OK) return st;
+  const Plan& p = bt.n_full > 0 ? bt.full : bt.tail;
   std::memset(out, 0, sizeof(*out));
   out->kernel = p.kernel;
   out->threads = p.nt;
@@ -644,11 +685,11 @@ fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin
   out->batch_groups = p.n_groups;
   out->second_kernel_reduction = p.reduce2 ? 1 : 0;
   out->early = p.early ? 1 : 0;
-  out->reserved = 0;
+  out->batch_tiles = bt.n_full + (bt.tail_rows > 0 ? 1 : 0);
   out->tiles = p.n_tiles;
   out->units = p.units;
   out->workgroups = p.blocks;
-  out->workspace_bytes = p.ws_bytes;
+  out->workspace_bytes = bt.ws_bytes;
   return FLUXBIN_OK;
 }
 

@@ -10,7 +10,8 @@ namespace fluxbin {
 
 constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes of signs per row)
 constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
-constexpr int kMaxBatch = 16;
+constexpr int kMaxBatch = 16;          // batch rows of one launch (a batch tile)
+constexpr int kMaxBatchCall = 8192;     // batch rows of one call: larger batches run as 16-row batch tiles
 // Units per workgroup of the batch-1 kernel (its LDS staging capacity): 16 for 1024-thread workgroups (one per CU),
 // 12 for the smaller ones (two or more share a CU's LDS).
 constexpr int b1_max_units(int nt) { return nt == 1024 ? 16 : 12; }

@@ -69,7 +69,7 @@ class Tuning(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_int32), ("threads", ctypes.c_int32), ("rows_per_tile", ctypes.c_int32),
                 ("depth", ctypes.c_int32), ("batch_groups", ctypes.c_int32),
-                ("second_kernel_reduction", ctypes.c_int32), ("early", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("second_kernel_reduction", ctypes.c_int32), ("early", ctypes.c_int32), ("batch_tiles", ctypes.c_int32),
                 ("tiles", ctypes.c_int64), ("units", ctypes.c_int64), ("workgroups", ctypes.c_int64),
                 ("workspace_bytes", ctypes.c_uint64)]
 
@@ -368,6 +368,6 @@ def fluxbin_plan_query(layer: PackedLayer, B: int = 1) -> Dict[str, object]:
     """The launch plan a call with batch B would use (kernel name, workgroups, ...)."""
     p = PlanInfo()
     _check(lib().fluxbin_plan_query(ctypes.byref(layer.layer), int(B), ctypes.byref(p)))
-    out = {n: getattr(p, n) for n, _ in PlanInfo._fields_ if n != "reserved"}
+    out = {n: getattr(p, n) for n, _ in PlanInfo._fields_}
     out["kernel_name"] = KERNEL_NAMES.get(p.kernel, str(p.kernel))
     return out

@@ -193,7 +193,8 @@ def test_gemv_rejects_bad_arguments(L):
     assert g(ctypes.byref(lay), X, X + 100, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG   # x/y overlap
     gb = L.fluxbin_lut_gemm_smallbatch
     assert gb(ctypes.byref(lay), 0, X, 300, Y, 1000, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
-    assert gb(ctypes.byref(lay), 17, X, 300, Y, 1000, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
+    assert gb(ctypes.byref(lay), 8193, X, 300, Y, 1000, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
+    assert gb(ctypes.byref(lay), -1, X, 300, Y, 1000, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert gb(ctypes.byref(lay), 2, X, 299, Y, 1000, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert gb(ctypes.byref(lay), 2, X, 300, Y, 999, 0, WS, 1 << 20, None) == fb.FLUXBIN_ERR_INVALID_ARG
     assert L.fluxbin_stream_probe(ctypes.byref(lay), X, 1000, None) == fb.FLUXBIN_ERR_BUFFER_TOO_SMALL

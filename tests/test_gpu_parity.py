@@ -319,6 +319,31 @@ def test_batch_rows_equal_batch1(B, mu, kernel):
     _with_env(SMALL_BATCH_KERNELS[kernel], lambda: _parity(spec, B, out_fp32=True))
 
 
+PREFILL_SPECS = [
+    LayerSpec("prefill_mu8", M=1536, N=2048, Kb=2, Ks=1, mu=8, S=61, g_r=128, g_s=61, seed=23),
+    LayerSpec("prefill_mu4", M=700, N=1000, Kb=2, Ks=1, mu=4, S=40, g_r=128, g_s=40, seed=24),
+    LayerSpec("prefill_fine", M=333, N=300, Kb=3, Ks=2, mu=8, S=77, g_r=64, g_s=8, seed=25),
+]
+
+
+@pytest.mark.parametrize("B", [17, 40, 64])
+@pytest.mark.parametrize("spec", PREFILL_SPECS, ids=lambda s: s.name)
+def test_prefill_batch_tiles(spec, B):
+    """B > 16 runs as 16-row batch tiles, one launch each: every row matches the oracle, and each tile's rows are
+    bitwise those of a call on that tile's rows alone (a one-row tail runs the batch-1 kernel)."""
+    _, packed, x, y = _parity(spec, B, out_fp32=True)
+    for b0 in range(0, B, 16):
+        part = run_gemm(packed, x[b0:b0 + 16], out_fp32=True)
+        assert np.array_equal(part, y[b0:b0 + 16]), (B, b0)
+
+
+def test_prefill_batch_mlp70b_full_size():
+    """A 64-row batch on the 70B MLP up layer at full size (four 16-row tiles on the matrix cores): sampled rows
+    against the oracle."""
+    spec = config_layers("c4_mlp70b", "128")[0]
+    _parity(spec, 64, rows=sample_rows(spec.M, 96, seed=64))
+
+
 @pytest.mark.parametrize("B", [4, 16])
 def test_mfma_small_batch_mlp70b_full_size(B):
     """The matrix-core kernel on both 70B MLP layers at full size, in the launch configuration the benchmark times:
