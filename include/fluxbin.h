@@ -250,16 +250,19 @@ fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16
  *   generic        FLUXBIN_GENERIC        1: the generic kernel for every batch size
  *   mfma_r2        FLUXBIN_MFMA_R2        0: matrix-core split tiles reduced by tile counters, not a second kernel
  *   bat_r2         FLUXBIN_BAT_R2         0: LUT batch kernel split tiles reduced by tile counters
+ *   rows           FLUXBIN_ROWS           batch 1: 1 the row-complete kernel where the layer allows it, 0 never;
+ *                                         -1: chosen by layer size
  */
 typedef struct {
-  int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2;
+  int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2, rows;
 } fluxbin_tuning;
 fluxbin_status fluxbin_get_tuning(fluxbin_tuning* out);
 fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
 
 /*
  * The launch plan a GEMV/GEMM call of batch B on this layer would use on the current device with the current tuning.
- *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel.
+ *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel,
+ *           4: row-complete batch-1 kernel (layers with few rows).
  * For B > 16 the plan is that of the full 16-row batch tiles, batch_tiles the number of launches and workspace_bytes
  * the call's workspace. Host only apart from reading the device's CU count; launches nothing.
  */

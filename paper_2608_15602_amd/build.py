@@ -27,7 +27,8 @@ SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=und
              "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
 
 SOURCES = ["fluxbin_host.cpp", "fluxbin_pack.hip", "fluxbin_gemv.hip", "fluxbin_gemm_batch.hip",
-           "fluxbin_gemm_mfma.hip", "fluxbin_rc.hip", "fluxbin_noalloc.hip"]
+           "fluxbin_gemm_mfma.hip", "fluxbin_rc.hip", "fluxbin_noalloc.hip",
+           "fluxbin_gemv_rows.hip"]
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are kept out of the generated code (plain float code only).

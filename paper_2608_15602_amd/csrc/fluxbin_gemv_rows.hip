@@ -1,0 +1,229 @@
+// Batch-1 LUT-GEMV of libfluxbin for layers with few rows (the product of Eqs. 10-15, as the batch-1 kernel in
+// fluxbin_gemv.hip computes it): row-complete workgroups, so that no partial sum crosses a workgroup.
+//
+// Why a second batch-1 kernel. A layer of a few thousand rows carries a few MB of sign data, and spread over the
+// chip that is a handful of units per CU. There the split-tile kernel spends most of a call outside its steady state:
+// its start-up, then the cross-workgroup reduction of split tiles (partial-sum stores, a counter round trip, the
+// reducer's loads and the y stores), each a dependent round trip to memory. Here a workgroup owns 16 rows and every
+// super-chunk of them: its W wavefronts take every W-th super-chunk, build that unit's tables, look them up, and add
+// their partial sums through LDS in a fixed order at the end. The tables of a unit are built once per workgroup
+// instead of once per tile of 512-1024 rows; with mu = 4 tables that redundancy costs 20 adds and 16 LDS writes per
+// lane and unit.
+//
+// Tables. mu = 4 patterns for either packed mu (a mu = 8 sub-vector byte is two mu = 4 nibbles, and both packed
+// rotations move whole nibbles). Per unit 64 tables, one per (chunk h, canonical nibble s), of 16 fp32 entries, one
+// table built by each of the wavefront's 64 lanes: T[e] = sum_n xv[n] (2 bit_n(e) - 1) over the nibble's four folded
+// activations xv = x[xidx] * colscale (exact in fp32, Eq. 11; VCM gather through the index table, Eq. 13), formed as
+// (+-xv0 +-xv1) + (+-xv2 +-xv3). Entry e of table T is LDS float e*64 + T, so the 64 lanes of a table write hit 64
+// banks.
+//
+// Lookups. Lane (r, p) handles row r of the workgroup and dword p of its 16-byte entries: per chunk the eight stored
+// nibbles Q = 8p + j, whose canonical nibble is (Q + rot(i)) mod 32 (mu = 8: rot = 2i, and rows with i mod 32 >= 16
+// hold the chunk pair swapped; mu = 4: rot = i). The lane sums its eight lookups of a chunk and multiplies the sum by
+// the row's scale of that chunk (Eq. 15; layers whose row-scale groups are shorter than a chunk use the other
+// kernels). The four lanes of a row are then added pairwise (lane xor 1, then xor 2: each addition is commutative, so
+// both lanes of a pair hold the same bits), and the W wavefronts' sums in wavefront order.
+//
+// Activations. The whole x (N <= kRwMaxN fp16) is staged in LDS once per workgroup, one round trip at the start
+// that overlaps the first sign requests; every gather then reads LDS.
+#include <hip/hip_runtime.h>
+
+#include "fluxbin_device.h"
+
+namespace fluxbin {
+
+namespace {
+
+constexpr int kRwRows = 16;       // output rows per workgroup (kRwSteps, kRwMaxN: fluxbin_internal.h)
+
+// Requested data of one unit for one lane.
+struct RwRegs {
+  uint32_t w[2];    // dword p of the row's entries of chunks 2sc (w[0]) and 2sc + 1 (w[1])
+  uint32_t rs[2];   // fp16 row scales of the row for the two chunks
+  uint2 cs;         // fp16 column scales of the four columns of the lane's table
+  uint2 xi;         // their activation indices (0xFFFF: no source)
+};
+
+struct RwLane {
+  int t, lane, w, r, p;
+  uint32_t row;       // the lane's output row (< Mp)
+  int hb;             // mu = 8: the row holds the chunk pair of a super-chunk swapped
+  int tv;             // the lane's table: virtual column of its first column within a super-chunk (0..252)
+  uint32_t col[2][8]; // byte offset of the table column of lookup j of chunk h: (h*32 + canonical nibble) * 4
+};
+
+// Requests a unit's sign dwords, column scales and activation indices (addresses known from the unit alone).
+template <int MU>
+__device__ __forceinline__ void rw_issue(const GemmArgs& a, const RwLane& ln, int sc, RwRegs& u) {
+  const int64_t plane_bytes = int64_t(a.Mp) * 16;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int slot = MU == 8 ? (h ^ ln.hb) : h;
+    u.w[h] = *reinterpret_cast<const uint32_t*>(a.signs + int64_t(2 * sc + slot) * plane_bytes + ln.row * 16u +
+                                                4u * uint32_t(ln.p));
+  }
+  const int v0 = sc * 256 + ln.tv;
+  u.cs = *reinterpret_cast<const uint2*>(a.colscale + v0);
+  u.xi = *reinterpret_cast<const uint2*>(a.xidx + v0);
+}
+
+// Requests a unit's row scales (planes of its chunks from LDS: no load waits for another).
+__device__ __forceinline__ void rw_issue_rs(const GemmArgs& a, const RwLane& ln, int sc, const int* s_plane,
+                                           RwRegs& u) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h) u.rs[h] = a.rscale[int64_t(s_plane[2 * sc + h]) * a.Mp + ln.row];
+}
+
+// Builds the lane's table of a unit into tab (entry e at e*64 + lane).
+__device__ __forceinline__ void rw_build(const RwRegs& u, const uint16_t* xl, float* tab, int lane) {
+  float xv[4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) {
+    const uint32_t xi = ((n < 2 ? u.xi.x : u.xi.y) >> (16 * (n & 1))) & 0xFFFFu;
+    const uint32_t cs = ((n < 2 ? u.cs.x : u.cs.y) >> (16 * (n & 1))) & 0xFFFFu;
+    const uint16_t xb = xi == 0xFFFFu ? uint16_t(0) : xl[xi];
+    xv[n] = h2f(xb) * h2f(uint16_t(cs));
+  }
+  // pair sums: lo[e & 3] = +-xv0 +-xv1, hi[e >> 2] = +-xv2 +-xv3 (bit set: +)
+  const float s01 = xv[0] + xv[1], d01 = xv[0] - xv[1];
+  const float s23 = xv[2] + xv[3], d23 = xv[2] - xv[3];
+  const float lo[4] = {-s01, d01, -d01, s01};
+  const float hi[4] = {-s23, d23, -d23, s23};
+#pragma unroll
+  for (int e = 0; e < 16; ++e) tab[e * 64 + lane] = lo[e & 3] + hi[e >> 2];
+}
+
+// Looks up a unit for the lane's row: the two chunks' sums, each times its row scale, added to acc.
+__device__ __forceinline__ void rw_lookup(const RwRegs& u, const float* tab, const RwLane& ln, float& acc) {
+  const char* tb = reinterpret_cast<const char*>(tab);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t nib = (u.w[h] >> (4 * j)) & 15u;
+      s += *reinterpret_cast<const float*>(tb + ((nib << 8) | ln.col[h][j]));
+    }
+    acc = fmaf(h2f(uint16_t(u.rs[h])), s, acc);
+  }
+}
+
+template <int MU, int W, int D>
+struct RwKernel {
+  // Unit K of the wavefront (super-chunk w + K*W), with register set K mod (D + 1); fully unrolled, so that no load
+  // is carried through a loop header.
+  template <int K>
+  __device__ static __forceinline__ void step(const GemmArgs& a, const RwLane& ln, int n, RwRegs (&ur)[D + 1],
+                                              const int* s_plane, const uint16_t* xl, float* tab, float& acc) {
+    if constexpr (K < kRwSteps) {
+      if (K >= n) return;
+      if (K + D < n) {
+        RwRegs& nx = ur[(K + D) % (D + 1)];
+        rw_issue<MU>(a, ln, ln.w + (K + D) * W, nx);
+        rw_issue_rs(a, ln, ln.w + (K + D) * W, s_plane, nx);
+      }
+      rw_build(ur[K % (D + 1)], xl, tab, ln.lane);
+      rw_lookup(ur[K % (D + 1)], tab, ln, acc);
+      step<K + 1>(a, ln, n, ur, s_plane, xl, tab, acc);
+    }
+  }
+};
+
+template <int MU, int W, int D>
+__global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
+  constexpr int NT = 64 * W;
+  __shared__ __attribute__((aligned(16))) uint16_t xl[kRwMaxN];
+  __shared__ __attribute__((aligned(16))) float tabs[W * 16 * 64];
+  __shared__ float s_red[W * kRwRows];
+  __shared__ int s_plane[2 * 8 * kRwSteps];   // row-scale plane of every chunk (NCP <= 2 * 8 * kRwSteps)
+
+  RwLane ln;
+  ln.t = threadIdx.x;
+  ln.lane = ln.t & 63;
+  ln.w = __builtin_amdgcn_readfirstlane(ln.t >> 6);
+  ln.r = ln.lane >> 2;
+  ln.p = ln.lane & 3;
+  const int row0 = int(blockIdx.x) * kRwRows;
+  ln.row = uint32_t(row0 + ln.r);   // < Mp: Mp is a multiple of 64 and row0 < M
+  ln.hb = MU == 8 ? int((ln.row >> 4) & 1u) : 0;
+  ln.tv = (ln.lane >> 5) * 128 + 4 * (ln.lane & 31);
+  {
+    const int rot = MU == 8 ? int(2u * ln.row) : int(ln.row);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ln.col[h][j] = uint32_t((h * 32 + ((8 * ln.p + j + rot) & 31)) * 4);
+  }
+  const int n = ln.w < a.NSC ? (a.NSC - 1 - ln.w) / W + 1 : 0;   // super-chunks w, w + W, ...
+
+  // x to LDS (one round trip, overlapping the first sign requests below)
+  if ((reinterpret_cast<uintptr_t>(a.x) & 3u) == 0) {
+    const uint32_t* x32 = reinterpret_cast<const uint32_t*>(a.x);
+    uint32_t* xl32 = reinterpret_cast<uint32_t*>(xl);
+    for (int d = ln.t; d < (a.N >> 1); d += NT) xl32[d] = x32[d];
+    if ((a.N & 1) && ln.t == 0) xl[a.N - 1] = a.x[a.N - 1];
+  } else {
+    for (int d = ln.t; d < a.N; d += NT) xl[d] = a.x[d];
+  }
+  for (int c = ln.t; c < 2 * a.NSC; c += NT) s_plane[c] = a.chunk_plane[c];
+  RwRegs ur[D + 1];
+#pragma unroll
+  for (int k = 0; k < D; ++k)
+    if (k < n) rw_issue<MU>(a, ln, ln.w + k * W, ur[k]);
+  __syncthreads();   // x and the planes staged
+#pragma unroll
+  for (int k = 0; k < D; ++k)
+    if (k < n) rw_issue_rs(a, ln, ln.w + k * W, s_plane, ur[k]);
+
+  float acc = 0.f;
+  RwKernel<MU, W, D>::template step<0>(a, ln, n, ur, s_plane, xl, tabs + ln.w * (16 * 64), acc);
+
+  // the row's four lanes, then the wavefronts in order
+  acc += __shfl_xor(acc, 1);
+  acc += __shfl_xor(acc, 2);
+  if (ln.p == 0) s_red[ln.w * kRwRows + ln.r] = acc;
+  __syncthreads();
+  if (ln.t < kRwRows) {
+    float y = s_red[ln.t];
+#pragma unroll
+    for (int w = 1; w < W; ++w) y += s_red[w * kRwRows + ln.t];
+    const int64_t row = int64_t(row0) + ln.t;
+    if (row < a.M) store_y(a, 0, row, y);
+  }
+}
+
+template <int W, int D>
+bool launch_rows_wd(const GemmArgs& a, int mu, hipStream_t stream) {
+  const dim3 grid(unsigned((a.M + kRwRows - 1) / kRwRows)), block(64 * W);
+  if (mu == 8)
+    hipLaunchKernelGGL((k_gemv_rows<8, W, D>), grid, block, 0, stream, a);
+  else if (mu == 4)
+    hipLaunchKernelGGL((k_gemv_rows<4, W, D>), grid, block, 0, stream, a);
+  else
+    return false;
+  return true;
+}
+
+template <int W>
+bool launch_rows_w(const GemmArgs& a, int mu, int depth, hipStream_t stream) {
+  switch (depth) {
+    case 2: return launch_rows_wd<W, 2>(a, mu, stream);
+    case 4: return launch_rows_wd<W, 4>(a, mu, stream);
+    case 6: return launch_rows_wd<W, 6>(a, mu, stream);
+  }
+  return false;
+}
+
+}  // namespace
+
+bool launch_gemv_rows(const GemmArgs& a, int mu, int waves, int depth, hipStream_t stream) {
+  if (a.B != 1 || a.N > kRwMaxN || a.NSC > waves * kRwSteps || a.NSC > 8 * kRwSteps) return false;
+  switch (waves) {
+    case 4: return launch_rows_w<4>(a, mu, depth, stream);
+    case 8: return launch_rows_w<8>(a, mu, depth, stream);
+    case 16: return launch_rows_w<16>(a, mu, depth, stream);
+  }
+  return false;
+}
+
+}  // namespace fluxbin

@@ -133,6 +133,7 @@ static fluxbin_tuning tuning_defaults() {
   t.generic = 0;
   t.mfma_r2 = 1;
   t.bat_r2 = 1;
+  t.rows = -1;
   return t;
 }
 
@@ -161,6 +162,7 @@ static void tuning_init_locked() {
   t.generic = env_int("FLUXBIN_GENERIC", t.generic);
   t.mfma_r2 = env_int("FLUXBIN_MFMA_R2", t.mfma_r2);
   t.bat_r2 = env_int("FLUXBIN_BAT_R2", t.bat_r2);
+  t.rows = env_int("FLUXBIN_ROWS", t.rows);
   g_tuning = t;
   g_tuning_init = true;
 }
@@ -187,6 +189,18 @@ static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tunin
   return L.shape.mu == 4 || B > 4 || small;
 }
 
+// Row-complete batch-1 kernel: coarse row scales only, x staged in LDS (N <= kRwMaxN), at most kRwSteps super-chunks
+// per wavefront. Chosen for layers of at most one 16-row workgroup per CU with at most 56 super-chunks (3.5 per
+// wavefront of 16): us per call, split-tile kernel -> row-complete kernel (16 wavefronts, graph-timed): 4096x4096 2b
+// 7.61 -> 6.14, 7B attention 4096x4096 (2+1, 2%) 8.13 -> 6.28, 2048x4096 7.87 -> 5.62, 3072x4096 3+1 (49
+// super-chunks) 8.49 -> 7.65; slower with more super-chunks: 4096x4096 4b (64) 8.63 -> 9.12, 4096x11008 (86)
+// 9.47 -> 10.8. FLUXBIN_ROWS=1 / 0 forces the choice where the layer allows it.
+static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const fluxbin_tuning& tu) {
+  if (dv.Gcg != 1 || dv.Gcs != 1 || L.shape.N > kRwMaxN || L.NSC > 8 * kRwSteps) return false;
+  if (tu.rows == 0 || tu.rows == 1) return tu.rows == 1;
+  return ceil_div(L.shape.M, 16) <= cus && L.NSC <= 56;
+}
+
 static uint64_t layer_counter_bytes(int64_t M) {
   return round_up256(uint64_t(ceil_div(M, 256) + 4) * uint64_t(kCounterStride) * 4u);
 }
@@ -208,6 +222,25 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   // the batch-1 instances for fine groups: salient side only, 8 or 16 groups per chunk (s = 16 or 8 at mu = 8)
   const bool b1_fine_ok = L.shape.mu == 8 && dv.Gcg == 1 && (dv.Gcs == 8 || dv.Gcs == 16);
   p->nt = 256;
+  if (B == 1 && !force_generic && use_rows(L, dv, cus, tu)) {
+    // row-complete batch-1 kernel: 16 rows per workgroup, every super-chunk of them, no cross-workgroup reduction;
+    // 16 wavefronts, two units requested ahead (4 and 8 wavefronts, and 4 or 6 units ahead, measured slower or equal)
+    p->kernel = 4;
+    p->nt = (tu.nt == 256 && L.NSC <= 4 * kRwSteps) ? 256 : (tu.nt == 512 ? 512 : 1024);
+    p->rpt = 1;
+    p->rows = 16;
+    p->depth = (tu.depth == 4 || tu.depth == 6) ? tu.depth : 2;
+    p->bg = 1;
+    p->n_groups = 1;
+    p->bpad = 1;
+    p->n_tiles = ceil_div(L.shape.M, 16);
+    p->units = p->n_tiles * L.NSC;
+    p->blocks = p->n_tiles;
+    p->ws_counters_off = 0;
+    p->ws_partials_off = layer_counter_bytes(L.shape.M);
+    p->ws_bytes = p->ws_partials_off;   // no workspace of its own: the counter region every plan of the layer keeps
+    return FLUXBIN_OK;
+  }
   if (B == 1 && !force_generic && (!fine || b1_fine_ok)) {   // batch-1 kernel (mu = 8 or 4)
     p->kernel = 0;
     const int nt_env = tu.nt;

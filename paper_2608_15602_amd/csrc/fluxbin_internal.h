@@ -12,6 +12,8 @@ constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes o
 constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
 constexpr int kMaxBatch = 16;          // batch rows of one launch (a batch tile)
 constexpr int kMaxBatchCall = 8192;     // batch rows of one call: larger batches run as 16-row batch tiles
+constexpr int kRwMaxN = 16384;          // row-complete batch-1 kernel: input columns staged in LDS
+constexpr int kRwSteps = 16;            // row-complete batch-1 kernel: super-chunks per wavefront
 // Units per workgroup of the batch-1 kernel (its LDS staging capacity): 16 for 1024-thread workgroups (one per CU),
 // 12 for the smaller ones (two or more share a CU's LDS).
 constexpr int b1_max_units(int nt) { return nt == 1024 ? 16 : 12; }
@@ -107,7 +109,7 @@ fluxbin_status hip_fail(int hip_error, const char* what);
 // ---- launch plan of the GEMV/GEMM kernels ----
 struct Plan {
   int kernel;       // 0 = batch-1 super-chunk kernel (mu 8 or 4), 1 = generic (any mu, any batch), 2 = mu8 batch 2..16,
-                    // 3 = matrix-core small batch (mu 8 or 4, batch 2..16)
+                    // 3 = matrix-core small batch (mu 8 or 4, batch 2..16), 4 = row-complete batch-1 (few rows)
   int nt;           // threads per block
   int rpt;          // rows per thread
   int rows;         // rows per tile (nt * rpt)

@@ -253,8 +253,11 @@ EDGE_SPECS = [
 @pytest.mark.parametrize("spec", EDGE_SPECS, ids=lambda s: s.name)
 @pytest.mark.parametrize("B", [1, 3, 9])
 def test_edge_shapes(spec, B):
-    """B = 1: batch-1 kernels; B = 3: LUT batch kernel (mu = 8) or matrix cores (mu = 4); B = 9: matrix cores."""
+    """B = 1: batch-1 kernels (the plan's choice, and the split-tile kernel with the row-complete one switched off);
+    B = 3: LUT batch kernel (mu = 8) or matrix cores (mu = 4); B = 9: matrix cores."""
     _parity(spec, B)
+    if B == 1:
+        _with_env({"FLUXBIN_ROWS": "0"}, lambda: _parity(spec, B))
 
 
 @pytest.mark.parametrize("spec", kernel_latency_layers(), ids=lambda s: s.name)
@@ -264,6 +267,48 @@ def test_paper_kernel_latency_configs_full_size(spec):
     2b-s16-g128 and 4b-g128 at full size in the benchmark's launch configuration, sampled rows against the oracle."""
     rows = sample_rows(spec.M, 384, seed=spec.layer_id)
     _parity(spec, 1, rows=rows)
+
+
+ROWS_SPECS = [
+    LayerSpec("rows_mu8_ragged", M=333, N=300, Kb=3, Ks=2, mu=8, S=77, g_r=128, g_s=77, seed=60),
+    LayerSpec("rows_mu4_ragged", M=100, N=201, Kb=1, Ks=1, mu=4, S=130, g_r=201, g_s=128, seed=61),
+    LayerSpec("rows_no_salient", M=64, N=128, Kb=2, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=62),
+    LayerSpec("rows_mu8_wide", M=1000, N=5000, Kb=2, Ks=1, mu=8, S=100, g_r=5000, g_s=100, seed=63),
+    LayerSpec("rows_mu4_many", M=257, N=16384, Kb=1, Ks=1, mu=4, S=128, g_r=128, g_s=128, seed=64),
+]
+
+
+@pytest.mark.parametrize("nt,depth", [(1024, 2), (512, 4), (256, 6)])
+def test_rows_kernel_instances(nt, depth):
+    """Every workgroup size (4, 8, 16 wavefronts) and request depth of the row-complete kernel, both packed mu."""
+    for mu in (8, 4):
+        spec = LayerSpec(f"rows_inst_mu{mu}", M=500, N=1500, Kb=2, Ks=1, mu=mu, S=60, g_r=128, g_s=60, seed=65)
+        _with_env({"FLUXBIN_ROWS": "1", "FLUXBIN_NT": str(nt), "FLUXBIN_DEPTH": str(depth)},
+                  lambda: _parity(spec, 1, out_fp32=True))
+
+
+@pytest.mark.parametrize("spec", ROWS_SPECS, ids=lambda s: s.name)
+def test_rows_kernel_matches_oracle(spec):
+    """The row-complete batch-1 kernel (forced) on every row: both packed mu, ragged M and N, salient chunks, no
+    salient part, the widest N its activation staging takes, and more super-chunks than four wavefronts hold (its
+    512-thread instance); and it is the kernel the plan reports."""
+    from paper_2608_15602_amd import fluxbin as fb
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    with fb.tuning(rows=1):
+        assert fb.fluxbin_plan_query(packed, 1)["kernel_name"] == "rows"
+        _, _, x, y = _parity(spec, 1, out_fp32=True, packed=packed, L=L)
+        assert np.array_equal(run_gemm(packed, x, out_fp32=True), y), "repeat differs"
+    y16 = _with_env({"FLUXBIN_ROWS": "1"}, lambda: run_gemm(packed, x))
+    _check(y16, oracle.gemv_dense(L, x), "fp16 output")
+
+
+@pytest.mark.parametrize("spec", [sp for sp in kernel_latency_layers() if sp.name.endswith(("2b-g128", "4b-g128"))]
+                         + config_layers("c3_mlp7b", "128"), ids=lambda s: s.name)
+def test_rows_kernel_full_size(spec):
+    """The row-complete kernel (forced) on the coarse App. E.4 shapes and the 7B MLP layers at full size, sampled rows
+    against the oracle."""
+    _with_env({"FLUXBIN_ROWS": "1"}, lambda: _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=spec.M)))
 
 
 @pytest.mark.parametrize("B", [2, 4])
@@ -279,11 +324,13 @@ def test_paper_config_small_batch(B):
     LayerSpec("mu4_b1_c", M=64, N=300, Kb=1, Ks=0, mu=4, S=0, g_r=300, g_s=1, seed=53),
 ], ids=lambda s: s.name)
 def test_mu4_batch1_kernel_matches_oracle_and_generic(spec):
-    """mu = 4 at batch 1 runs the batch-1 kernel (16-entry tables); it matches the oracle on every row and the
-    generic kernel's result within the tolerance."""
-    L, packed, x, y = _parity(spec, 1, out_fp32=True)
+    """mu = 4 at batch 1: the split-tile batch-1 kernel (16-entry tables) matches the oracle on every row, and the
+    generic and row-complete kernels' results within the tolerance."""
+    L, packed, x, y = _with_env({"FLUXBIN_ROWS": "0"}, lambda: _parity(spec, 1, out_fp32=True))
     y_gen = _with_env({"FLUXBIN_GENERIC": "1"}, lambda: run_gemm(packed, x, out_fp32=True))
     _check(y, y_gen, "batch-1 kernel vs generic kernel")
+    y_rows = _with_env({"FLUXBIN_ROWS": "1"}, lambda: run_gemm(packed, x, out_fp32=True))
+    _check(y, y_rows, "batch-1 kernel vs row-complete kernel")
 
 
 def test_fp32_output_and_generic_kernel_at_batch1():
@@ -555,7 +602,7 @@ def _subnormal_case(which, mu):
     return L, x
 
 
-@pytest.mark.parametrize("kernel", ["batch1", "lut_batch", "mfma"])
+@pytest.mark.parametrize("kernel", ["batch1", "rows", "lut_batch", "mfma"])
 @pytest.mark.parametrize("which", ["colscale", "rowscale", "x"])
 def test_fp16_subnormals_are_honoured(which, kernel):
     """Subnormal fp16 column scales, row scales or activations (the reading that subnormals are honoured on both
@@ -564,8 +611,9 @@ def test_fp16_subnormals_are_honoured(which, kernel):
     against the fp64 oracle (fp32 output)."""
     L, x = _subnormal_case(which, 8)
     packed = pack_layer(L)
-    env = {"batch1": {}, "lut_batch": {"FLUXBIN_MFMA": "0"}, "mfma": {"FLUXBIN_MFMA": "1"}}[kernel]
-    for B in ((1,) if kernel == "batch1" else (3, 9) if kernel == "mfma" else (3,)):
+    env = {"batch1": {"FLUXBIN_ROWS": "0"}, "rows": {"FLUXBIN_ROWS": "1"}, "lut_batch": {"FLUXBIN_MFMA": "0"},
+           "mfma": {"FLUXBIN_MFMA": "1"}}[kernel]
+    for B in ((1,) if kernel in ("batch1", "rows") else (3, 9) if kernel == "mfma" else (3,)):
         log(f"case subnormal {which} kernel={kernel} B={B}")
         xb = x[:B]
         y = _with_env(env, lambda: run_gemm(packed, xb, out_fp32=True))

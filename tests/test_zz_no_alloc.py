@@ -26,7 +26,7 @@ def _gpu():
 
 LARGE = LayerSpec("na_large", M=28672, N=8192, Kb=3, Ks=1, mu=8, S=410, g_r=128, g_s=410, outlier_frac=0.001,
                   seed=61)
-SMALL = LayerSpec("na_small", M=3000, N=2048, Kb=2, Ks=1, mu=8, S=70, g_r=128, g_s=70, seed=62)
+SMALL = LayerSpec("na_small", M=6000, N=2048, Kb=2, Ks=1, mu=8, S=70, g_r=128, g_s=70, seed=62)
 MU4 = LayerSpec("na_mu4", M=1500, N=777, Kb=3, Ks=2, mu=4, S=300, g_r=256, g_s=128, seed=63)
 
 
