@@ -49,7 +49,9 @@ struct RwLane {
   uint32_t row;       // the lane's output row (< Mp)
   int hb;             // mu = 8: the row holds the chunk pair of a super-chunk swapped
   int tv;             // the lane's table: virtual column of its first column within a super-chunk (0..252)
-  uint32_t col[2][8]; // byte offset of the table column of lookup j of chunk h: (h*32 + canonical nibble) * 4
+  int hA;             // chunk of the lane's first eight lookups (rw_lookup)
+  uint32_t sh;        // rotation of its sign dwords before the lookups (0 or 4 bits)
+  uint32_t col[16];   // byte offset of the table column of lookup k: (chunk * 32 + canonical nibble) * 4
 };
 
 // Requests a unit's sign dwords, column scales and activation indices (addresses known from the unit alone).
@@ -93,18 +95,23 @@ __device__ __forceinline__ void rw_build(const RwRegs& u, const uint16_t* xl, fl
   for (int e = 0; e < 16; ++e) tab[e * 64 + lane] = lo[e & 3] + hi[e >> 2];
 }
 
-// Looks up a unit for the lane's row: the two chunks' sums, each times its row scale, added to acc.
+// Looks up a unit for the lane's row: the two chunks' sums, each times its row scale, added to acc. Lookup k of the
+// lane reads chunk hA (k < 8) or the other (k >= 8), and its dword rotated right by sh bits puts the nibble at bits
+// 4 (k mod 8) (see RwLane setup): the 64 lanes of every read then hit 64 different tables, i.e. 64 banks.
 __device__ __forceinline__ void rw_lookup(const RwRegs& u, const float* tab, const RwLane& ln, float& acc) {
   const char* tb = reinterpret_cast<const char*>(tab);
+  const uint32_t wa = ln.hA ? u.w[1] : u.w[0], wb = ln.hA ? u.w[0] : u.w[1];
+  const uint32_t w2[2] = {__builtin_amdgcn_alignbit(wa, wa, ln.sh), __builtin_amdgcn_alignbit(wb, wb, ln.sh)};
+  const uint32_t rs2[2] = {ln.hA ? u.rs[1] : u.rs[0], ln.hA ? u.rs[0] : u.rs[1]};
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int c = 0; c < 2; ++c) {
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const uint32_t nib = (u.w[h] >> (4 * j)) & 15u;
-      s += *reinterpret_cast<const float*>(tb + ((nib << 8) | ln.col[h][j]));
+      const uint32_t nib = (w2[c] >> (4 * j)) & 15u;
+      s += *reinterpret_cast<const float*>(tb + ((nib << 8) | ln.col[8 * c + j]));
     }
-    acc = fmaf(h2f(uint16_t(u.rs[h])), s, acc);
+    acc = fmaf(h2f(uint16_t(rs2[c])), s, acc);
   }
 }
 
@@ -132,7 +139,7 @@ struct RwKernel {
 template <int MU, int W, int D>
 __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   constexpr int NT = 64 * W;
-  __shared__ __attribute__((aligned(16))) uint16_t xl[kRwMaxN];
+  extern __shared__ __attribute__((aligned(16))) uint16_t xl[];   // x: N fp16 (dynamic size, at most kRwMaxN)
   __shared__ __attribute__((aligned(16))) float tabs[W * 16 * 64];
   __shared__ float s_red[W * kRwRows];
   __shared__ int s_plane[2 * 8 * kRwSteps];   // row-scale plane of every chunk (NCP <= 2 * 8 * kRwSteps)
@@ -147,12 +154,21 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   ln.row = uint32_t(row0 + ln.r);   // < Mp: Mp is a multiple of 64 and row0 < M
   ln.hb = MU == 8 ? int((ln.row >> 4) & 1u) : 0;
   ln.tv = (ln.lane >> 5) * 128 + 4 * (ln.lane & 31);
+  // Lookup order: at lookup k the lane reads chunk h_k = hA ^ (k >= 8) and its stored nibble 8p + j_k, canonical nibble
+  // s_k = (8p + j_k + rot) mod 32. mu = 8 (rot = 2i): hA = p >> 1, j_k = (k + (p & 1)) mod 8, so lanes p and p ^ 1 read
+  // nibbles of opposite parity and the 32 lanes of a chunk 32 different s; mu = 4 (rot = i): hA = p & 1, j_k = k mod
+  // 8, so lanes p and p ^ 2 read s and s + 16. The odd-p shift of j is a rotation of the dword by one nibble.
   {
     const int rot = MU == 8 ? int(2u * ln.row) : int(ln.row);
+    ln.hA = MU == 8 ? (ln.p >> 1) : (ln.p & 1);
+    const int jo = MU == 8 ? (ln.p & 1) : 0;
+    ln.sh = uint32_t(4 * jo);
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) ln.col[h][j] = uint32_t((h * 32 + ((8 * ln.p + j + rot) & 31)) * 4);
+    for (int k = 0; k < 16; ++k) {
+      const int h = ln.hA ^ (k >> 3);
+      const int j = ((k & 7) + jo) & 7;
+      ln.col[k] = uint32_t((h * 32 + ((8 * ln.p + j + rot) & 31)) * 4);
+    }
   }
   const int n = ln.w < a.NSC ? (a.NSC - 1 - ln.w) / W + 1 : 0;   // super-chunks w, w + W, ...
 
@@ -195,10 +211,11 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
 template <int W, int D>
 bool launch_rows_wd(const GemmArgs& a, int mu, hipStream_t stream) {
   const dim3 grid(unsigned((a.M + kRwRows - 1) / kRwRows)), block(64 * W);
+  const unsigned xl_bytes = unsigned((a.N * 2 + 15) & ~15);
   if (mu == 8)
-    hipLaunchKernelGGL((k_gemv_rows<8, W, D>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((k_gemv_rows<8, W, D>), grid, block, xl_bytes, stream, a);
   else if (mu == 4)
-    hipLaunchKernelGGL((k_gemv_rows<4, W, D>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((k_gemv_rows<4, W, D>), grid, block, xl_bytes, stream, a);
   else
     return false;
   return true;
