@@ -37,6 +37,8 @@ namespace {
 constexpr int kRwRows = 16;       // output rows per workgroup (kRwSteps, kRwMaxN: fluxbin_internal.h)
 
 // Requested data of one unit for one lane.
+typedef unsigned int mf_u32x2_rw __attribute__((ext_vector_type(2)));
+
 struct RwRegs {
   uint32_t w[2];    // dword p of the row's entries of chunks 2sc (w[0]) and 2sc + 1 (w[1])
   uint32_t rs[2];   // fp16 row scales of the row for the two chunks
@@ -51,39 +53,48 @@ struct RwLane {
   int tv;             // the lane's table: virtual column of its first column within a super-chunk (0..252)
   int hA;             // chunk of the lane's first eight lookups (rw_lookup)
   uint32_t sh;        // rotation of its sign dwords before the lookups (0 or 4 bits)
-  uint32_t col[16];   // byte offset of the table column of lookup k: (chunk * 32 + canonical nibble) * 4
+  uint32_t colp[4];   // byte k mod 4 of colp[k / 4]: byte offset of the table column of lookup k, (chunk*32 + s)*4
+  uint32_t wblk;      // (w << 4) in every byte: the wavefront's table block in bits 12..15 of a lookup address
+};
+
+// Buffer resources of the packed sections and per-lane byte offsets: every load is a buffer load with the unit's
+// offset in a scalar register (the launch plan keeps the sign and row-scale sections below 2^31 bytes).
+struct RwBufs {
+  __amdgpu_buffer_rsrc_t signs, rscale, colscale, xidx;
+  uint32_t voff_w[2];   // sign dword p of the lane's row in the slot holding chunk 2sc + h, super-chunk 0
+  uint32_t voff_rs;     // the lane's row in a row-scale plane
+  uint32_t voff_cv;     // the lane's table's four columns in a super-chunk's column tables
 };
 
 // Requests a unit's sign dwords, column scales and activation indices (addresses known from the unit alone).
-template <int MU>
-__device__ __forceinline__ void rw_issue(const GemmArgs& a, const RwLane& ln, int sc, RwRegs& u) {
-  const int64_t plane_bytes = int64_t(a.Mp) * 16;
+__device__ __forceinline__ void rw_issue(const GemmArgs& a, const RwBufs& bf, int sc, RwRegs& u) {
+  const int soff_w = 2 * sc * a.Mp * 16;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int slot = MU == 8 ? (h ^ ln.hb) : h;
-    u.w[h] = *reinterpret_cast<const uint32_t*>(a.signs + int64_t(2 * sc + slot) * plane_bytes + ln.row * 16u +
-                                                4u * uint32_t(ln.p));
-  }
-  const int v0 = sc * 256 + ln.tv;
-  u.cs = *reinterpret_cast<const uint2*>(a.colscale + v0);
-  u.xi = *reinterpret_cast<const uint2*>(a.xidx + v0);
+  for (int h = 0; h < 2; ++h) u.w[h] = __builtin_amdgcn_raw_buffer_load_b32(bf.signs, int(bf.voff_w[h]), soff_w, 0);
+  const mf_u32x2_rw cs = __builtin_amdgcn_raw_buffer_load_b64(bf.colscale, int(bf.voff_cv), sc * 512, 0);
+  const mf_u32x2_rw xi = __builtin_amdgcn_raw_buffer_load_b64(bf.xidx, int(bf.voff_cv), sc * 512, 0);
+  u.cs = make_uint2(cs[0], cs[1]);
+  u.xi = make_uint2(xi[0], xi[1]);
 }
 
 // Requests a unit's row scales (planes of its chunks from LDS: no load waits for another).
-__device__ __forceinline__ void rw_issue_rs(const GemmArgs& a, const RwLane& ln, int sc, const int* s_plane,
+__device__ __forceinline__ void rw_issue_rs(const GemmArgs& a, const RwBufs& bf, int sc, const int* s_plane,
                                            RwRegs& u) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h) u.rs[h] = a.rscale[int64_t(s_plane[2 * sc + h]) * a.Mp + ln.row];
+  for (int h = 0; h < 2; ++h) {
+    const int plane = __builtin_amdgcn_readfirstlane(s_plane[2 * sc + h]);
+    u.rs[h] = __builtin_amdgcn_raw_buffer_load_b16(bf.rscale, int(bf.voff_rs), plane * a.Mp * 2, 0);
+  }
 }
 
 // Builds the lane's table of a unit into tab (entry e at e*64 + lane).
-__device__ __forceinline__ void rw_build(const RwRegs& u, const uint16_t* xl, float* tab, int lane) {
+__device__ __forceinline__ void rw_build(const RwRegs& u, const uint16_t* xl, uint32_t n_x, float* tab, int lane) {
   float xv[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) {
     const uint32_t xi = ((n < 2 ? u.xi.x : u.xi.y) >> (16 * (n & 1))) & 0xFFFFu;
     const uint32_t cs = ((n < 2 ? u.cs.x : u.cs.y) >> (16 * (n & 1))) & 0xFFFFu;
-    const uint16_t xb = xi == 0xFFFFu ? uint16_t(0) : xl[xi];
+    const uint16_t xb = xl[xi < n_x ? xi : n_x];   // xl[N] = 0: a column with no source (index 0xFFFF)
     xv[n] = h2f(xb) * h2f(uint16_t(cs));
   }
   // pair sums: lo[e & 3] = +-xv0 +-xv1, hi[e >> 2] = +-xv2 +-xv3 (bit set: +)
@@ -98,18 +109,23 @@ __device__ __forceinline__ void rw_build(const RwRegs& u, const uint16_t* xl, fl
 // Looks up a unit for the lane's row: the two chunks' sums, each times its row scale, added to acc. Lookup k of the
 // lane reads chunk hA (k < 8) or the other (k >= 8), and its dword rotated right by sh bits puts the nibble at bits
 // 4 (k mod 8) (see RwLane setup): the 64 lanes of every read then hit 64 different tables, i.e. 64 banks.
-__device__ __forceinline__ void rw_lookup(const RwRegs& u, const float* tab, const RwLane& ln, float& acc) {
-  const char* tb = reinterpret_cast<const char*>(tab);
+__device__ __forceinline__ void rw_lookup(const RwRegs& u, const float* tabs, const RwLane& ln, float& acc) {
+  const char* tb = reinterpret_cast<const char*>(tabs);
   const uint32_t wa = ln.hA ? u.w[1] : u.w[0], wb = ln.hA ? u.w[0] : u.w[1];
   const uint32_t w2[2] = {__builtin_amdgcn_alignbit(wa, wa, ln.sh), __builtin_amdgcn_alignbit(wb, wb, ln.sh)};
   const uint32_t rs2[2] = {ln.hA ? u.rs[1] : u.rs[0], ln.hA ? u.rs[0] : u.rs[1]};
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
+    // even and odd nibbles in the low four bits of their bytes, the wavefront's table block (4 KB) in the high four;
+    // one v_perm_b32 then forms a lookup's byte address: byte 0 the table column, byte 1 block and pattern
+    const uint32_t ev = (w2[c] & 0x0F0F0F0Fu) | ln.wblk, od = ((w2[c] >> 4) & 0x0F0F0F0Fu) | ln.wblk;
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const uint32_t nib = (w2[c] >> (4 * j)) & 15u;
-      s += *reinterpret_cast<const float*>(tb + ((nib << 8) | ln.col[8 * c + j]));
+      const int k = 8 * c + j;
+      const uint32_t sel = 0x0C0C0000u | (uint32_t(4 + (j >> 1)) << 8) | uint32_t(k & 3);
+      const uint32_t addr = __builtin_amdgcn_perm((j & 1) ? od : ev, ln.colp[k >> 2], sel);
+      s += *reinterpret_cast<const float*>(tb + addr);
     }
     acc = fmaf(h2f(uint16_t(rs2[c])), s, acc);
   }
@@ -120,18 +136,19 @@ struct RwKernel {
   // Unit K of the wavefront (super-chunk w + K*W), with register set K mod (D + 1); fully unrolled, so that no load
   // is carried through a loop header.
   template <int K>
-  __device__ static __forceinline__ void step(const GemmArgs& a, const RwLane& ln, int n, RwRegs (&ur)[D + 1],
-                                              const int* s_plane, const uint16_t* xl, float* tab, float& acc) {
+  __device__ static __forceinline__ void step(const GemmArgs& a, const RwLane& ln, const RwBufs& bf, int n,
+                                              RwRegs (&ur)[D + 1], const int* s_plane, const uint16_t* xl, float* tab,
+                                              const float* tabs, float& acc) {
     if constexpr (K < kRwSteps) {
       if (K >= n) return;
       if (K + D < n) {
         RwRegs& nx = ur[(K + D) % (D + 1)];
-        rw_issue<MU>(a, ln, ln.w + (K + D) * W, nx);
-        rw_issue_rs(a, ln, ln.w + (K + D) * W, s_plane, nx);
+        rw_issue(a, bf, ln.w + (K + D) * W, nx);
+        rw_issue_rs(a, bf, ln.w + (K + D) * W, s_plane, nx);
       }
-      rw_build(ur[K % (D + 1)], xl, tab, ln.lane);
-      rw_lookup(ur[K % (D + 1)], tab, ln, acc);
-      step<K + 1>(a, ln, n, ur, s_plane, xl, tab, acc);
+      rw_build(ur[K % (D + 1)], xl, uint32_t(a.N), tab, ln.lane);
+      rw_lookup(ur[K % (D + 1)], tabs, ln, acc);
+      step<K + 1>(a, ln, bf, n, ur, s_plane, xl, tab, tabs, acc);
     }
   }
 };
@@ -163,11 +180,14 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
     ln.hA = MU == 8 ? (ln.p >> 1) : (ln.p & 1);
     const int jo = MU == 8 ? (ln.p & 1) : 0;
     ln.sh = uint32_t(4 * jo);
+    ln.wblk = uint32_t(ln.w << 4) * 0x01010101u;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) ln.colp[q] = 0u;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       const int h = ln.hA ^ (k >> 3);
       const int j = ((k & 7) + jo) & 7;
-      ln.col[k] = uint32_t((h * 32 + ((8 * ln.p + j + rot) & 31)) * 4);
+      ln.colp[k >> 2] |= uint32_t((h * 32 + ((8 * ln.p + j + rot) & 31)) * 4) << (8 * (k & 3));
     }
   }
   const int n = ln.w < a.NSC ? (a.NSC - 1 - ln.w) / W + 1 : 0;   // super-chunks w, w + W, ...
@@ -181,18 +201,31 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   } else {
     for (int d = ln.t; d < a.N; d += NT) xl[d] = a.x[d];
   }
+  if (ln.t == 0) xl[a.N] = 0;
   for (int c = ln.t; c < 2 * a.NSC; c += NT) s_plane[c] = a.chunk_plane[c];
+  RwBufs bf;
+  bf.signs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.signs), 0, a.NCP * a.Mp * 16, 0x00020000);
+  bf.rscale = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.rscale), 0, 0x7FFFFFFF, 0x00020000);
+  bf.colscale = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.colscale), 0, a.NCP * 256, 0x00020000);
+  bf.xidx = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.xidx), 0, a.NCP * 256, 0x00020000);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int slot = MU == 8 ? (h ^ ln.hb) : h;
+    bf.voff_w[h] = uint32_t(slot * a.Mp * 16) + ln.row * 16u + 4u * uint32_t(ln.p);
+  }
+  bf.voff_rs = ln.row * 2u;
+  bf.voff_cv = uint32_t(ln.tv) * 2u;
   RwRegs ur[D + 1];
 #pragma unroll
   for (int k = 0; k < D; ++k)
-    if (k < n) rw_issue<MU>(a, ln, ln.w + k * W, ur[k]);
+    if (k < n) rw_issue(a, bf, ln.w + k * W, ur[k]);
   __syncthreads();   // x and the planes staged
 #pragma unroll
   for (int k = 0; k < D; ++k)
-    if (k < n) rw_issue_rs(a, ln, ln.w + k * W, s_plane, ur[k]);
+    if (k < n) rw_issue_rs(a, bf, ln.w + k * W, s_plane, ur[k]);
 
   float acc = 0.f;
-  RwKernel<MU, W, D>::template step<0>(a, ln, n, ur, s_plane, xl, tabs + ln.w * (16 * 64), acc);
+  RwKernel<MU, W, D>::template step<0>(a, ln, bf, n, ur, s_plane, xl, tabs + ln.w * (16 * 64), tabs, acc);
 
   // the row's four lanes, then the wavefronts in order
   acc += __shfl_xor(acc, 1);
@@ -211,7 +244,7 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
 template <int W, int D>
 bool launch_rows_wd(const GemmArgs& a, int mu, hipStream_t stream) {
   const dim3 grid(unsigned((a.M + kRwRows - 1) / kRwRows)), block(64 * W);
-  const unsigned xl_bytes = unsigned((a.N * 2 + 15) & ~15);
+  const unsigned xl_bytes = unsigned(((a.N + 1) * 2 + 15) & ~15);   // x and one zero entry
   if (mu == 8)
     hipLaunchKernelGGL((k_gemv_rows<8, W, D>), grid, block, xl_bytes, stream, a);
   else if (mu == 4)

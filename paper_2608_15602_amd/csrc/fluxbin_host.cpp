@@ -190,15 +190,19 @@ static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tunin
 }
 
 // Row-complete batch-1 kernel: coarse row scales only, x staged in LDS (N <= kRwMaxN), at most kRwSteps super-chunks
-// per wavefront. Chosen for layers of at most one 16-row workgroup per CU with at most 56 super-chunks (3.5 per
-// wavefront of 16): us per call, split-tile kernel -> row-complete kernel (16 wavefronts, graph-timed): 4096x4096 2b
-// 7.61 -> 6.14, 7B attention 4096x4096 (2+1, 2%) 8.13 -> 6.28, 2048x4096 7.87 -> 5.62, 3072x4096 3+1 (49
-// super-chunks) 8.49 -> 7.65; slower with more super-chunks: 4096x4096 4b (64) 8.63 -> 9.12, 4096x11008 (86)
-// 9.47 -> 10.8. FLUXBIN_ROWS=1 / 0 forces the choice where the layer allows it.
+// per wavefront. Chosen for layers of at most one 16-row workgroup per CU with at most 64 super-chunks (four per
+// wavefront of 16), or 128 on layers of at most a quarter of that. us per call, split-tile kernel -> row-complete
+// kernel (16 wavefronts, graph-timed, medians of interleaved runs): 4096x4096 2b 7.63 -> 5.80, 4b 8.69 -> 8.26, 7B
+// attention 4096x4096 (2+1, 2%) 8.26 -> 5.98, 2048x4096 7.79 -> 5.31, 3072x4096 3+1 (49 super-chunks) 8.40 -> 7.00,
+// 1024x8192 2+1 (65) 8.36 -> 7.20, 1024x8192 3+1 (98) 9.35 -> 9.05; even or slower with more super-chunks per
+// wavefront: 4096x11008 2b (86) 9.47 -> 9.68. FLUXBIN_ROWS=1 / 0 forces the choice where the layer allows it.
 static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const fluxbin_tuning& tu) {
   if (dv.Gcg != 1 || dv.Gcs != 1 || L.shape.N > kRwMaxN || L.NSC > 8 * kRwSteps) return false;
+  // its buffer loads take 32-bit offsets into the sign and row-scale sections
+  if (dv.NCP * dv.Mp * 16 >= (int64_t(1) << 31) || dv.NRP * dv.Mp * 2 >= (int64_t(1) << 31)) return false;
   if (tu.rows == 0 || tu.rows == 1) return tu.rows == 1;
-  return ceil_div(L.shape.M, 16) <= cus && L.NSC <= 56;
+  const int64_t wgs = ceil_div(L.shape.M, 16);
+  return wgs <= cus && (L.NSC <= 64 || (L.NSC <= 128 && 4 * wgs <= cus));
 }
 
 static uint64_t layer_counter_bytes(int64_t M) {
