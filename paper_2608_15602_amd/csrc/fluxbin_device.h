@@ -244,8 +244,9 @@ void launch_reduce_split(const GemmArgs& a, int bp, int R, hipStream_t stream);
 bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, bool reduce2, hipStream_t stream);
 
 // Row-complete batch-1 kernel for layers with few rows (fluxbin_gemv_rows.hip): 16 rows per workgroup of `waves`
-// (4, 8 or 16) wavefronts, every super-chunk of them, `depth` (2, 4 or 6) units requested ahead, no workspace; false
-// if the layer is outside its limits (B = 1, N <= kRwMaxN, NSC <= min(waves, 8) * kRwSteps) or no instance exists.
-bool launch_gemv_rows(const GemmArgs& a, int mu, int waves, int depth, hipStream_t stream);
+// (4, 8 or 16) wavefronts, every super-chunk of them, `depth` (2, 4 or 6) units requested ahead, fg (0, or 8 / 16 fine
+// groups per salient chunk at mu = 8) as the batch-1 kernel's, no workspace; false if the layer is outside its limits
+// (B = 1, N <= kRwMaxN, NSC <= min(waves, 8) * kRwSteps) or no instance exists.
+bool launch_gemv_rows(const GemmArgs& a, int mu, int waves, int depth, int fg, hipStream_t stream);
 
 }  // namespace fluxbin

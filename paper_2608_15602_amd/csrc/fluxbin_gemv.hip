@@ -1208,7 +1208,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   } else if (p.kernel == 3) {
     ok = !fine && launch_gemm_mfma(a, p.bpad, int(L.shape.mu), p.depth, p.reduce2, stream);
   } else if (p.kernel == 4) {
-    ok = !fine && launch_gemv_rows(a, int(L.shape.mu), p.nt / 64, p.depth, stream);
+    ok = fg >= 0 && launch_gemv_rows(a, int(L.shape.mu), p.nt / 64, p.depth, fg, stream);
   } else if (L.shape.mu == 8) {
     ok = launch_gen_mu<8>(a, p, stream);
   } else {

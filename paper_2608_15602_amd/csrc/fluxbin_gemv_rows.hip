@@ -20,8 +20,9 @@
 // Lookups. Lane (r, p) handles row r of the workgroup and dword p of its 16-byte entries: per chunk the eight stored
 // nibbles Q = 8p + j, whose canonical nibble is (Q + rot(i)) mod 32 (mu = 8: rot = 2i, and rows with i mod 32 >= 16
 // hold the chunk pair swapped; mu = 4: rot = i). The lane sums its eight lookups of a chunk and multiplies the sum by
-// the row's scale of that chunk (Eq. 15; layers whose row-scale groups are shorter than a chunk use the other
-// kernels). The four lanes of a row are then added pairwise (lane xor 1, then xor 2: each addition is commutative, so
+// the row's scale of that chunk (Eq. 15). Salient chunks with FG = 8 or 16 fine row-scale groups (the paper's s16 /
+// s8 configurations at mu = 8) sum their lookups per stored position block and multiply each block's sum by its own
+// scale; other fine layouts use the other kernels. The four lanes of a row are then added pairwise (lane xor 1, then xor 2: each addition is commutative, so
 // both lanes of a pair hold the same bits), and the W wavefronts' sums in wavefront order.
 //
 // Activations. The whole x (N <= kRwMaxN fp16) is staged in LDS once per workgroup, one round trip at the start
@@ -39,9 +40,12 @@ constexpr int kRwRows = 16;       // output rows per workgroup (kRwSteps, kRwMax
 // Requested data of one unit for one lane.
 typedef unsigned int mf_u32x2_rw __attribute__((ext_vector_type(2)));
 
+template <int FG>
 struct RwRegs {
   uint32_t w[2];    // dword p of the row's entries of chunks 2sc (w[0]) and 2sc + 1 (w[1])
-  uint32_t rs[2];   // fp16 row scales of the row for the two chunks
+  // fp16 row scales of the row for the two chunks: one (low half of rs[h][0]), or for a chunk with FG fine groups the
+  // scales of the lane's position blocks (FG = 16: four, FG = 8: two)
+  uint32_t rs[2][FG == 16 ? 2 : 1];
   uint2 cs;         // fp16 column scales of the four columns of the lane's table
   uint2 xi;         // their activation indices (0xFFFF: no source)
 };
@@ -55,6 +59,7 @@ struct RwLane {
   uint32_t sh;        // rotation of its sign dwords before the lookups (0 or 4 bits)
   uint32_t colp[4];   // byte k mod 4 of colp[k / 4]: byte offset of the table column of lookup k, (chunk*32 + s)*4
   uint32_t wblk;      // (w << 4) in every byte: the wavefront's table block in bits 12..15 of a lookup address
+  uint32_t colf[4];   // the same for chunks with fine row-scale groups (their position rotation, no odd-p shift)
 };
 
 // Buffer resources of the packed sections and per-lane byte offsets: every load is a buffer load with the unit's
@@ -67,7 +72,8 @@ struct RwBufs {
 };
 
 // Requests a unit's sign dwords, column scales and activation indices (addresses known from the unit alone).
-__device__ __forceinline__ void rw_issue(const GemmArgs& a, const RwBufs& bf, int sc, RwRegs& u) {
+template <int FG>
+__device__ __forceinline__ void rw_issue(const GemmArgs& a, const RwBufs& bf, int sc, RwRegs<FG>& u) {
   const int soff_w = 2 * sc * a.Mp * 16;
 #pragma unroll
   for (int h = 0; h < 2; ++h) u.w[h] = __builtin_amdgcn_raw_buffer_load_b32(bf.signs, int(bf.voff_w[h]), soff_w, 0);
@@ -77,18 +83,33 @@ __device__ __forceinline__ void rw_issue(const GemmArgs& a, const RwBufs& bf, in
   u.xi = make_uint2(xi[0], xi[1]);
 }
 
-// Requests a unit's row scales (planes of its chunks from LDS: no load waits for another).
-__device__ __forceinline__ void rw_issue_rs(const GemmArgs& a, const RwBufs& bf, int sc, const int* s_plane,
-                                           RwRegs& u) {
+// Requests a unit's row scales (planes of its chunks from LDS: no load waits for another). A chunk with FG fine
+// groups owns FG planes read as [Mp][FG]: slot b of a row scales its stored position block b (16 / FG positions),
+// so the lane's blocks are contiguous: FG = 16 slots 4p..4p+3 (8 bytes), FG = 8 slots 2p, 2p+1 (4 bytes).
+template <int FG>
+__device__ __forceinline__ void rw_issue_rs(const GemmArgs& a, const RwBufs& bf, int sc, bool fine,
+                                           const int* s_plane, int p, RwRegs<FG>& u) {
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int plane = __builtin_amdgcn_readfirstlane(s_plane[2 * sc + h]);
-    u.rs[h] = __builtin_amdgcn_raw_buffer_load_b16(bf.rscale, int(bf.voff_rs), plane * a.Mp * 2, 0);
+    if (FG != 0 && fine) {
+      const int voff = int(bf.voff_rs) * FG + (FG == 16 ? 8 : 4) * p;
+      if constexpr (FG == 16) {
+        const mf_u32x2_rw v = __builtin_amdgcn_raw_buffer_load_b64(bf.rscale, voff, plane * a.Mp * 2, 0);
+        u.rs[h][0] = v[0];
+        u.rs[h][FG == 16 ? 1 : 0] = v[1];
+      } else {
+        u.rs[h][0] = __builtin_amdgcn_raw_buffer_load_b32(bf.rscale, voff, plane * a.Mp * 2, 0);
+      }
+    } else {
+      u.rs[h][0] = __builtin_amdgcn_raw_buffer_load_b16(bf.rscale, int(bf.voff_rs), plane * a.Mp * 2, 0);
+    }
   }
 }
 
 // Builds the lane's table of a unit into tab (entry e at e*64 + lane).
-__device__ __forceinline__ void rw_build(const RwRegs& u, const uint16_t* xl, uint32_t n_x, float* tab, int lane) {
+template <int FG>
+__device__ __forceinline__ void rw_build(const RwRegs<FG>& u, const uint16_t* xl, uint32_t n_x, float* tab, int lane) {
   float xv[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) {
@@ -108,53 +129,80 @@ __device__ __forceinline__ void rw_build(const RwRegs& u, const uint16_t* xl, ui
 
 // Looks up a unit for the lane's row: the two chunks' sums, each times its row scale, added to acc. Lookup k of the
 // lane reads chunk hA (k < 8) or the other (k >= 8), and its dword rotated right by sh bits puts the nibble at bits
-// 4 (k mod 8) (see RwLane setup): the 64 lanes of every read then hit 64 different tables, i.e. 64 banks.
-__device__ __forceinline__ void rw_lookup(const RwRegs& u, const float* tabs, const RwLane& ln, float& acc) {
+// 4 (k mod 8) (see RwLane setup): the 64 lanes of every read then hit 64 different tables, i.e. 64 banks. Units with
+// fine row-scale groups keep the stored nibble order (their lookups are summed per position block and each block
+// sum is multiplied by its own scale).
+template <int FG>
+__device__ __forceinline__ void rw_lookup(const RwRegs<FG>& u, bool fine, const float* tabs, const RwLane& ln,
+                                          float& acc) {
   const char* tb = reinterpret_cast<const char*>(tabs);
   const uint32_t wa = ln.hA ? u.w[1] : u.w[0], wb = ln.hA ? u.w[0] : u.w[1];
-  const uint32_t w2[2] = {__builtin_amdgcn_alignbit(wa, wa, ln.sh), __builtin_amdgcn_alignbit(wb, wb, ln.sh)};
-  const uint32_t rs2[2] = {ln.hA ? u.rs[1] : u.rs[0], ln.hA ? u.rs[0] : u.rs[1]};
+  const bool fu = FG != 0 && fine;
+  const uint32_t sh = fu ? 0u : ln.sh;
+  const uint32_t w2[2] = {__builtin_amdgcn_alignbit(wa, wa, sh), __builtin_amdgcn_alignbit(wb, wb, sh)};
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     // even and odd nibbles in the low four bits of their bytes, the wavefront's table block (4 KB) in the high four;
     // one v_perm_b32 then forms a lookup's byte address: byte 0 the table column, byte 1 block and pattern
     const uint32_t ev = (w2[c] & 0x0F0F0F0Fu) | ln.wblk, od = ((w2[c] >> 4) & 0x0F0F0F0Fu) | ln.wblk;
-    float s = 0.f;
+    float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int k = 8 * c + j;
       const uint32_t sel = 0x0C0C0000u | (uint32_t(4 + (j >> 1)) << 8) | uint32_t(k & 3);
-      const uint32_t addr = __builtin_amdgcn_perm((j & 1) ? od : ev, ln.colp[k >> 2], sel);
-      s += *reinterpret_cast<const float*>(tb + addr);
+      const uint32_t cols = fu ? ln.colf[k >> 2] : ln.colp[k >> 2];
+      v[j] = *reinterpret_cast<const float*>(tb + __builtin_amdgcn_perm((j & 1) ? od : ev, cols, sel));
     }
-    acc = fmaf(h2f(uint16_t(rs2[c])), s, acc);
+    const int h = ln.hA ^ c;
+    if (fu) {
+      // FG = 16: four blocks of two lookups (stored byte 4p + b); FG = 8: two blocks of four
+      constexpr int PER = FG == 16 ? 2 : 4;
+#pragma unroll
+      for (int b = 0; b < 8 / PER; ++b) {
+        float sb = v[PER * b];
+#pragma unroll
+        for (int q = 1; q < PER; ++q) sb += v[PER * b + q];
+        constexpr int NW = FG == 16 ? 2 : 1;
+        const int wi = FG == 16 ? (b >> 1) : 0;
+        const uint32_t word = h ? u.rs[1][wi < NW ? wi : 0] : u.rs[0][wi < NW ? wi : 0];
+        acc = fmaf(h2f(uint16_t(word >> (16 * (b & 1)))), sb, acc);
+      }
+    } else {
+      float sum = v[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) sum += v[j];
+      acc = fmaf(h2f(uint16_t(h ? u.rs[1][0] : u.rs[0][0])), sum, acc);
+    }
   }
 }
 
-template <int MU, int W, int D>
+template <int MU, int W, int D, int FG>
 struct RwKernel {
   // Unit K of the wavefront (super-chunk w + K*W), with register set K mod (D + 1); fully unrolled, so that no load
   // is carried through a loop header.
   template <int K>
   __device__ static __forceinline__ void step(const GemmArgs& a, const RwLane& ln, const RwBufs& bf, int n,
-                                              RwRegs (&ur)[D + 1], const int* s_plane, const uint16_t* xl, float* tab,
-                                              const float* tabs, float& acc) {
+                                              RwRegs<FG> (&ur)[D + 1], const int* s_plane, const uint16_t* xl,
+                                              float* tab, const float* tabs, float& acc) {
     if constexpr (K < kRwSteps) {
       if (K >= n) return;
       if (K + D < n) {
-        RwRegs& nx = ur[(K + D) % (D + 1)];
-        rw_issue(a, bf, ln.w + (K + D) * W, nx);
-        rw_issue_rs(a, bf, ln.w + (K + D) * W, s_plane, nx);
+        RwRegs<FG>& nx = ur[(K + D) % (D + 1)];
+        const int scn = ln.w + (K + D) * W;
+        rw_issue<FG>(a, bf, scn, nx);
+        rw_issue_rs<FG>(a, bf, scn, 2 * scn >= a.nfc, s_plane, ln.p, nx);
       }
-      rw_build(ur[K % (D + 1)], xl, uint32_t(a.N), tab, ln.lane);
-      rw_lookup(ur[K % (D + 1)], tabs, ln, acc);
+      const int sc = ln.w + K * W;
+      rw_build<FG>(ur[K % (D + 1)], xl, uint32_t(a.N), tab, ln.lane);
+      rw_lookup<FG>(ur[K % (D + 1)], 2 * sc >= a.nfc, tabs, ln, acc);
       step<K + 1>(a, ln, bf, n, ur, s_plane, xl, tab, tabs, acc);
     }
   }
 };
 
-template <int MU, int W, int D>
+template <int MU, int W, int D, int FG>
 __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
+  static_assert(FG == 0 || MU == 8, "fine row-scale groups: mu = 8 only");
   constexpr int NT = 64 * W;
   extern __shared__ __attribute__((aligned(16))) uint16_t xl[];   // x: N fp16 (dynamic size, at most kRwMaxN)
   __shared__ __attribute__((aligned(16))) float tabs[W * 16 * 64];
@@ -189,6 +237,22 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
       const int j = ((k & 7) + jo) & 7;
       ln.colp[k >> 2] |= uint32_t((h * 32 + ((8 * ln.p + j + rot) & 31)) * 4) << (8 * (k & 3));
     }
+    // fine chunks (mu = 8): stored byte q of row i holds sub-vector byte ((q/n + i/n) mod FG) n + ((q mod n) + i) mod n,
+    // n = 16 / FG; its low / high nibble is canonical nibble 2u / 2u + 1; nibble order j = k mod 8 (no shift)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) ln.colf[q] = 0u;
+    if constexpr (FG != 0) {
+      constexpr int NB = 16 / FG;
+      const int i = int(ln.row);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int h = ln.hA ^ (k >> 3);
+        const int j = k & 7;
+        const int q = 4 * ln.p + (j >> 1);
+        const int u = ((q / NB + i / NB) % FG) * NB + ((q % NB) + i) % NB;
+        ln.colf[k >> 2] |= uint32_t((h * 32 + 2 * u + (j & 1)) * 4) << (8 * (k & 3));
+      }
+    }
   }
   const int n = ln.w < a.NSC ? (a.NSC - 1 - ln.w) / W + 1 : 0;   // super-chunks w, w + W, ...
 
@@ -215,17 +279,17 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   }
   bf.voff_rs = ln.row * 2u;
   bf.voff_cv = uint32_t(ln.tv) * 2u;
-  RwRegs ur[D + 1];
+  RwRegs<FG> ur[D + 1];
 #pragma unroll
   for (int k = 0; k < D; ++k)
-    if (k < n) rw_issue(a, bf, ln.w + k * W, ur[k]);
+    if (k < n) rw_issue<FG>(a, bf, ln.w + k * W, ur[k]);
   __syncthreads();   // x and the planes staged
 #pragma unroll
   for (int k = 0; k < D; ++k)
-    if (k < n) rw_issue_rs(a, bf, ln.w + k * W, s_plane, ur[k]);
+    if (k < n) rw_issue_rs<FG>(a, bf, ln.w + k * W, 2 * (ln.w + k * W) >= a.nfc, s_plane, ln.p, ur[k]);
 
   float acc = 0.f;
-  RwKernel<MU, W, D>::template step<0>(a, ln, bf, n, ur, s_plane, xl, tabs + ln.w * (16 * 64), tabs, acc);
+  RwKernel<MU, W, D, FG>::template step<0>(a, ln, bf, n, ur, s_plane, xl, tabs + ln.w * (16 * 64), tabs, acc);
 
   // the row's four lanes, then the wavefronts in order
   acc += __shfl_xor(acc, 1);
@@ -242,36 +306,40 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
 }
 
 template <int W, int D>
-bool launch_rows_wd(const GemmArgs& a, int mu, hipStream_t stream) {
+bool launch_rows_wd(const GemmArgs& a, int mu, int fg, hipStream_t stream) {
   const dim3 grid(unsigned((a.M + kRwRows - 1) / kRwRows)), block(64 * W);
   const unsigned xl_bytes = unsigned(((a.N + 1) * 2 + 15) & ~15);   // x and one zero entry
-  if (mu == 8)
-    hipLaunchKernelGGL((k_gemv_rows<8, W, D>), grid, block, xl_bytes, stream, a);
-  else if (mu == 4)
-    hipLaunchKernelGGL((k_gemv_rows<4, W, D>), grid, block, xl_bytes, stream, a);
+  if (mu == 8 && fg == 0)
+    hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0>), grid, block, xl_bytes, stream, a);
+  else if (mu == 8 && fg == 8)
+    hipLaunchKernelGGL((k_gemv_rows<8, W, D, 8>), grid, block, xl_bytes, stream, a);
+  else if (mu == 8 && fg == 16)
+    hipLaunchKernelGGL((k_gemv_rows<8, W, D, 16>), grid, block, xl_bytes, stream, a);
+  else if (mu == 4 && fg == 0)
+    hipLaunchKernelGGL((k_gemv_rows<4, W, D, 0>), grid, block, xl_bytes, stream, a);
   else
     return false;
   return true;
 }
 
 template <int W>
-bool launch_rows_w(const GemmArgs& a, int mu, int depth, hipStream_t stream) {
+bool launch_rows_w(const GemmArgs& a, int mu, int depth, int fg, hipStream_t stream) {
   switch (depth) {
-    case 2: return launch_rows_wd<W, 2>(a, mu, stream);
-    case 4: return launch_rows_wd<W, 4>(a, mu, stream);
-    case 6: return launch_rows_wd<W, 6>(a, mu, stream);
+    case 2: return launch_rows_wd<W, 2>(a, mu, fg, stream);
+    case 4: return launch_rows_wd<W, 4>(a, mu, fg, stream);
+    case 6: return launch_rows_wd<W, 6>(a, mu, fg, stream);
   }
   return false;
 }
 
 }  // namespace
 
-bool launch_gemv_rows(const GemmArgs& a, int mu, int waves, int depth, hipStream_t stream) {
+bool launch_gemv_rows(const GemmArgs& a, int mu, int waves, int depth, int fg, hipStream_t stream) {
   if (a.B != 1 || a.N > kRwMaxN || a.NSC > waves * kRwSteps || a.NSC > 8 * kRwSteps) return false;
   switch (waves) {
-    case 4: return launch_rows_w<4>(a, mu, depth, stream);
-    case 8: return launch_rows_w<8>(a, mu, depth, stream);
-    case 16: return launch_rows_w<16>(a, mu, depth, stream);
+    case 4: return launch_rows_w<4>(a, mu, depth, fg, stream);
+    case 8: return launch_rows_w<8>(a, mu, depth, fg, stream);
+    case 16: return launch_rows_w<16>(a, mu, depth, fg, stream);
   }
   return false;
 }

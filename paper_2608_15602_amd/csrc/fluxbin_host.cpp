@@ -189,7 +189,7 @@ static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tunin
   return L.shape.mu == 4 || B > 4 || small;
 }
 
-// Row-complete batch-1 kernel: coarse row scales only, x staged in LDS (N <= kRwMaxN), at most kRwSteps super-chunks
+// Row-complete batch-1 kernel: coarse row scales, or 8 / 16 fine groups per salient chunk at mu = 8, x staged in LDS (N <= kRwMaxN), at most kRwSteps super-chunks
 // per wavefront. Chosen for layers of at most one 16-row workgroup per CU with at most 64 super-chunks (four per
 // wavefront of 16), or 128 on layers of at most a quarter of that. us per call, split-tile kernel -> row-complete
 // kernel (16 wavefronts, graph-timed, medians of interleaved runs): 4096x4096 2b 7.63 -> 5.80, 4b 8.69 -> 8.26, 7B
@@ -197,7 +197,8 @@ static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tunin
 // 1024x8192 2+1 (65) 8.36 -> 7.20, 1024x8192 3+1 (98) 9.35 -> 9.05; even or slower with more super-chunks per
 // wavefront: 4096x11008 2b (86) 9.47 -> 9.68. FLUXBIN_ROWS=1 / 0 forces the choice where the layer allows it.
 static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const fluxbin_tuning& tu) {
-  if (dv.Gcg != 1 || dv.Gcs != 1 || L.shape.N > kRwMaxN || L.NSC > 8 * kRwSteps) return false;
+  const bool fine_ok = dv.Gcg == 1 && (dv.Gcs == 1 || (L.shape.mu == 8 && (dv.Gcs == 8 || dv.Gcs == 16)));
+  if (!fine_ok || L.shape.N > kRwMaxN || L.NSC > 8 * kRwSteps) return false;
   // its buffer loads take 32-bit offsets into the sign and row-scale sections
   if (dv.NCP * dv.Mp * 16 >= (int64_t(1) << 31) || dv.NRP * dv.Mp * 2 >= (int64_t(1) << 31)) return false;
   if (tu.rows == 0 || tu.rows == 1) return tu.rows == 1;

@@ -275,14 +275,21 @@ ROWS_SPECS = [
     LayerSpec("rows_no_salient", M=64, N=128, Kb=2, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=62),
     LayerSpec("rows_mu8_wide", M=1000, N=5000, Kb=2, Ks=1, mu=8, S=100, g_r=5000, g_s=100, seed=63),
     LayerSpec("rows_mu4_many", M=257, N=16384, Kb=1, Ks=1, mu=4, S=128, g_r=128, g_s=128, seed=64),
+    # the paper's s8 / s16 configurations (16 / 8 fine row-scale groups per salient chunk), ragged M and N
+    paper_config("rows_2b-s8", 333, 1000, 2, 8, 128, seed=66),
+    paper_config("rows_2b-s16", 200, 2048, 2, 16, 128, seed=67),
+    paper_config("rows_3b-s8_separator", 300, 1100, 3, 8, 128, seed=68),   # 27 global chunks: an inert separator
 ]
 
 
 @pytest.mark.parametrize("nt,depth", [(1024, 2), (512, 4), (256, 6)])
 def test_rows_kernel_instances(nt, depth):
-    """Every workgroup size (4, 8, 16 wavefronts) and request depth of the row-complete kernel, both packed mu."""
-    for mu in (8, 4):
-        spec = LayerSpec(f"rows_inst_mu{mu}", M=500, N=1500, Kb=2, Ks=1, mu=mu, S=60, g_r=128, g_s=60, seed=65)
+    """Every workgroup size (4, 8, 16 wavefronts) and request depth of the row-complete kernel: both packed mu and both
+    fine salient group counts."""
+    specs = [LayerSpec(f"rows_inst_mu{mu}", M=500, N=1500, Kb=2, Ks=1, mu=mu, S=60, g_r=128, g_s=60, seed=65)
+             for mu in (8, 4)]
+    specs += [paper_config(f"rows_inst_s{sv}", 500, 1500, 2, sv, 128, seed=66) for sv in (8, 16)]
+    for spec in specs:
         _with_env({"FLUXBIN_ROWS": "1", "FLUXBIN_NT": str(nt), "FLUXBIN_DEPTH": str(depth)},
                   lambda: _parity(spec, 1, out_fp32=True))
 
@@ -303,11 +310,10 @@ def test_rows_kernel_matches_oracle(spec):
     _check(y16, oracle.gemv_dense(L, x), "fp16 output")
 
 
-@pytest.mark.parametrize("spec", [sp for sp in kernel_latency_layers() if sp.name.endswith(("2b-g128", "4b-g128"))]
-                         + config_layers("c3_mlp7b", "128"), ids=lambda s: s.name)
+@pytest.mark.parametrize("spec", kernel_latency_layers() + config_layers("c3_mlp7b", "128"), ids=lambda s: s.name)
 def test_rows_kernel_full_size(spec):
-    """The row-complete kernel (forced) on the coarse App. E.4 shapes and the 7B MLP layers at full size, sampled rows
-    against the oracle."""
+    """The row-complete kernel (forced where the layer allows it) on the App. E.4 shapes (2b, s8, s16, 4b) and the 7B
+    MLP layers at full size, sampled rows against the oracle."""
     _with_env({"FLUXBIN_ROWS": "1"}, lambda: _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=spec.M)))
 
 
