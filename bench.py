@@ -405,7 +405,9 @@ def kernel_variants_us(g_r: str, launches: int = 40):
 def mu_profile_us(g_r: str, launches: int = 40):
     """mu = 8 against mu = 4 (same shapes and seeds) at batch 1 (Sec. 3.2 trades table size against lookups; App. E.2
     profiles mu on the 7B model): the 7B attention and MLP layers, the 70B MLP layers, and the distinct shapes of the
-    70B decoder layer (q/o 8192x8192, k/v 1024x8192, gate/up 28672x8192, down 8192x28672) in both hybrid variants."""
+    70B decoder layer (q/o 8192x8192, k/v 1024x8192, gate/up 28672x8192, down 8192x28672) in both hybrid variants.
+    The split-tile batch-1 kernel for both (its tables follow the packed mu); where the launch plan picks the
+    row-complete kernel instead (its 16-entry tables serve either packing), that time is reported next to them."""
     import torch
     from synth import config_layers
     out = {}
@@ -417,9 +419,14 @@ def mu_profile_us(g_r: str, launches: int = 40):
             for mu in (8, 4):
                 sp = spec.with_(mu=mu, name=f"{spec.name}_mu{mu}")
                 b = Bench([sp], 1, COPIES_BYTES_PER_LAYER)
-                us = b.per_launch_us(launches, 3)[0]
+                it = b.items[0]
+                if mu == 8 and b.fb.fluxbin_plan_query(it["packs"][0], 1)["kernel_name"] == "rows":
+                    row["row_complete_kernel_us"] = round(b.per_launch_us(launches, 3)[0], 3)
+                with b.fb.tuning(rows=0):
+                    it["ws"] = b.fb.make_workspace(it["packs"][0], 1)
+                    us = b.per_launch_us(launches, 3)[0]
                 row[f"mu{mu}_us"] = round(us, 3)
-                row[f"mu{mu}_GBps"] = round(b.items[0]["bytes"] / (us * 1e-6) / 1e9, 1)
+                row[f"mu{mu}_GBps"] = round(it["bytes"] / (us * 1e-6) / 1e9, 1)
                 del b
                 torch.cuda.empty_cache()
             row["mu8_faster"] = row["mu8_us"] < row["mu4_us"]
