@@ -432,6 +432,27 @@ def test_strided_batch():
     _check(yc[:, :700], oracle.gemv_dense(L, x), "strided")
 
 
+def test_strided_prefill_batch():
+    """A 21-row batch (a 16-row tile and a 5-row tile) with row strides above N and M, fp16 and fp32 outputs: every
+    row against the oracle and nothing written between the rows."""
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    spec = LayerSpec("strided_prefill", M=700, N=512, Kb=2, Ks=1, mu=8, S=16, g_r=128, g_s=16, seed=24)
+    log("case strided prefill batch")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    x = make_activations(L, 21)
+    xt = torch.zeros(21, 601, dtype=torch.float16, device="cuda")
+    xt[:, :512] = x_tensor(x)
+    for fp32 in (True, False):
+        y = torch.full((21, 777), float("nan"), dtype=torch.float32 if fp32 else torch.float16, device="cuda")
+        fb.fluxbin_lut_gemm_smallbatch(packed, xt[:, :512], y=y[:, :700], out_fp32=fp32)
+        torch.cuda.synchronize()
+        yc = y.float().cpu().numpy().astype(np.float64)
+        assert np.all(np.isnan(yc[:, 700:]))
+        _check(yc[:, :700], oracle.gemv_dense(L, x), f"strided prefill fp32={fp32}")
+
+
 def test_deterministic_and_exact_power_of_two_scaling():
     import torch
     from paper_2608_15602_amd import fluxbin as fb
@@ -527,7 +548,8 @@ def test_workspace_shared_by_batch_sizes():
     L = make_layer(spec)
     packed = pack_layer(L)
     runs = [(1, {}), (3, {}), (2, {"FLUXBIN_MFMA": "0"}), (16, {}), (5, {"FLUXBIN_GENERIC": "1"}),
-            (4, {"FLUXBIN_MFMA": "0"}), (1, {"FLUXBIN_NT": "1024"}), (8, {"FLUXBIN_MFMA": "0"})]
+            (4, {"FLUXBIN_MFMA": "0"}), (1, {"FLUXBIN_NT": "1024", "FLUXBIN_ROWS": "0"}), (8, {"FLUXBIN_MFMA": "0"}),
+            (1, {"FLUXBIN_ROWS": "1"}), (37, {})]
     n = max(_with_env(env, lambda: fb.fluxbin_workspace_query(packed, B)) for B, env in runs)
     shared = torch.empty((n + 255) // 256 * 256, dtype=torch.uint8, device="cuda")
     fb.fluxbin_workspace_init(shared)
