@@ -83,15 +83,15 @@ __device__ __forceinline__ void rw_issue(const GemmArgs& a, const RwBufs& bf, in
   u.xi = make_uint2(xi[0], xi[1]);
 }
 
-// Requests a unit's row scales (planes of its chunks from LDS: no load waits for another). A chunk with FG fine
+// Requests a unit's row scales from the planes of its two chunks (wave-uniform). A chunk with FG fine
 // groups owns FG planes read as [Mp][FG]: slot b of a row scales its stored position block b (16 / FG positions),
 // so the lane's blocks are contiguous: FG = 16 slots 4p..4p+3 (8 bytes), FG = 8 slots 2p, 2p+1 (4 bytes).
 template <int FG>
-__device__ __forceinline__ void rw_issue_rs(const GemmArgs& a, const RwBufs& bf, int sc, bool fine,
-                                           const int* s_plane, int p, RwRegs<FG>& u) {
+__device__ __forceinline__ void rw_issue_rs(const GemmArgs& a, const RwBufs& bf, const int (&planes)[2], bool fine,
+                                           int p, RwRegs<FG>& u) {
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const int plane = __builtin_amdgcn_readfirstlane(s_plane[2 * sc + h]);
+    const int plane = planes[h];
     if (FG != 0 && fine) {
       const int voff = int(bf.voff_rs) * FG + (FG == 16 ? 8 : 4) * p;
       if constexpr (FG == 16) {
@@ -190,7 +190,10 @@ struct RwKernel {
         RwRegs<FG>& nx = ur[(K + D) % (D + 1)];
         const int scn = ln.w + (K + D) * W;
         rw_issue<FG>(a, bf, scn, nx);
-        rw_issue_rs<FG>(a, bf, scn, 2 * scn >= a.nfc, s_plane, ln.p, nx);
+        // planes from LDS (staged in the prologue): no load waits for another
+        const int planes[2] = {__builtin_amdgcn_readfirstlane(s_plane[2 * scn]),
+                               __builtin_amdgcn_readfirstlane(s_plane[2 * scn + 1])};
+        rw_issue_rs<FG>(a, bf, planes, 2 * scn >= a.nfc, ln.p, nx);
       }
       const int sc = ln.w + K * W;
       rw_build<FG>(ur[K % (D + 1)], xl, uint32_t(a.N), tab, ln.lane);
@@ -256,7 +259,8 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   }
   const int n = ln.w < a.NSC ? (a.NSC - 1 - ln.w) / W + 1 : 0;   // super-chunks w, w + W, ...
 
-  // x to LDS (one round trip, overlapping the first sign requests below)
+  // x and the row-scale planes to LDS first: x is a few KB that every workgroup reads (from L2 after the first), and
+  // its LDS writes would otherwise wait for the sign requests issued before them (vector loads complete in order)
   if ((reinterpret_cast<uintptr_t>(a.x) & 3u) == 0) {
     const uint32_t* x32 = reinterpret_cast<const uint32_t*>(a.x);
     uint32_t* xl32 = reinterpret_cast<uint32_t*>(xl);
@@ -283,10 +287,17 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
 #pragma unroll
   for (int k = 0; k < D; ++k)
     if (k < n) rw_issue<FG>(a, bf, ln.w + k * W, ur[k]);
-  __syncthreads();   // x and the planes staged
+  // the first units' row scales before the barrier (planes by scalar loads), so that their round trip overlaps the
+  // activation staging instead of following it
 #pragma unroll
-  for (int k = 0; k < D; ++k)
-    if (k < n) rw_issue_rs<FG>(a, bf, ln.w + k * W, 2 * (ln.w + k * W) >= a.nfc, s_plane, ln.p, ur[k]);
+  for (int k = 0; k < D; ++k) {
+    if (k < n) {
+      const int sc = ln.w + k * W;
+      const int planes[2] = {load_uniform_i32(a.chunk_plane, 2 * sc), load_uniform_i32(a.chunk_plane, 2 * sc + 1)};
+      rw_issue_rs<FG>(a, bf, planes, 2 * sc >= a.nfc, ln.p, ur[k]);
+    }
+  }
+  __syncthreads();   // x and the planes staged
 
   float acc = 0.f;
   RwKernel<MU, W, D, FG>::template step<0>(a, ln, bf, n, ur, s_plane, xl, tabs + ln.w * (16 * 64), tabs, acc);
