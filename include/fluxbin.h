@@ -203,10 +203,12 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
                                 void* d_workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
- * Y[b, :] = W-hat X[b, :] for b < B (1..8192). Up to 16 rows are one launch, which reads every packed sign word once
+ * Y[b, :] = W-hat X[b, :] for b < B (1..8192). Up to T rows are one launch, which reads every packed sign word once
  * and uses it for all its rows (batch-independent reuse of the weights, Sec. 3.2 and App. E.2); larger batches run as
- * consecutive launches of 16-row batch tiles (the last with the remaining rows), each its own launch plan, one after
- * another on the stream and sharing the workspace, so rows 16t..16t+15 give the same y as a call on those rows alone.
+ * consecutive launches of T-row batch tiles (the last with the remaining rows), each its own launch plan, one after
+ * another on the stream and sharing the workspace, so rows Tt..Tt+T-1 give the same y as a call on those rows alone.
+ * T = 32 on layers with one row scale per chunk (matrix-core kernel), else 16; also 16 where 15 row strides plus N
+ * elements of x reach 2^31 bytes. fluxbin_plan_query reports T as batch_tile_rows.
  * d_x fp16 with row stride ldx >= N (elements); d_y with row stride ldy >= M (elements of the output type). B = 1
  * gives the same result as fluxbin_lut_gemv.
  * Two kernels compute it: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4 on layers with at
@@ -252,9 +254,12 @@ fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16
  *   bat_r2         FLUXBIN_BAT_R2         0: LUT batch kernel split tiles reduced by tile counters
  *   rows           FLUXBIN_ROWS           batch 1: 1 the row-complete kernel where the layer allows it, 0 never;
  *                                         -1: chosen by layer size
+ *   batch_tile     FLUXBIN_BATCH_TILE     16: batch tiles of 16 rows on every layer; 0: 32 where the matrix-core
+ *                                         kernel takes the layer
  */
 typedef struct {
-  int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2, rows;
+  int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2, rows,
+      batch_tile;
 } fluxbin_tuning;
 fluxbin_status fluxbin_get_tuning(fluxbin_tuning* out);
 fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
@@ -263,11 +268,14 @@ fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
  * The launch plan a GEMV/GEMM call of batch B on this layer would use on the current device with the current tuning.
  *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel,
  *           4: row-complete batch-1 kernel (layers with few rows).
- * For B > 16 the plan is that of the full 16-row batch tiles, batch_tiles the number of launches and workspace_bytes
- * the call's workspace. Host only apart from reading the device's CU count; launches nothing.
+ * Batches of more than batch_tile_rows rows (32 on layers the matrix-core kernel takes, else 16; 16 also for an x row
+ * stride so large that 15 strides plus N elements reach 2^31 bytes) run as batch_tiles launches; the plan is then that
+ * of the full batch tiles, for an x of row stride N, and workspace_bytes the call's workspace. Host only apart from
+ * reading the device's CU count; launches nothing.
  */
 typedef struct {
   int32_t kernel, threads, rows_per_tile, depth, batch_groups, second_kernel_reduction, early, batch_tiles;
+  int32_t batch_tile_rows, reserved;
   int64_t tiles, units, workgroups;
   uint64_t workspace_bytes;
 } fluxbin_plan_info;

@@ -1,4 +1,4 @@
-// Small-batch (B = 2..16) product of libfluxbin on the gfx950 matrix cores (MFMA).
+// Small-batch (B = 2..32) product of libfluxbin on the gfx950 matrix cores (MFMA).
 //
 // What is computed is the same as the LUT kernels (Eqs. 10-11 and 15), for every batch row b < B:
 //   y[b, i] = sum_c rscale[plane(c)][i] * sum_{v in chunk c} s(i, v) * colscale[v] * x[b, xidx[v]],
@@ -6,7 +6,9 @@
 // cost grows with the batch (one table entry read and added per batch row and sub-vector). With B > 1 the same inner
 // sums are a dense contraction over the virtual columns: a (rows x 128) block of signed column scales times a
 // (128 x B) block of activations. Here every 32 columns of that contraction are one v_mfma_f32_16x16x32_f16, and the
-// cost per sign bit is the same for any B <= 16 (the batch occupies the 16 columns of the MFMA tile).
+// cost per sign bit is the same for any B <= 16 (the batch occupies the 16 columns of the MFMA tile). With 17..32 rows
+// each decoded operand feeds two MFMA tiles (batch rows 0..15 and 16..31): the decode per sign bit is paid once for
+// twice the rows.
 //
 // Exactness. The A operand is -s(i, v) * colscale[v], an fp16 value (the column scale with its sign bit flipped where
 // the sign bit is set), and the B operand is x[b, xidx[v]], also fp16. Their products are exact in the fp32
@@ -51,8 +53,11 @@ typedef unsigned short mf_u16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kMfNT = 256;                          // threads per workgroup: four wavefronts of 64 rows
 constexpr int kMfR = 256;                           // rows per tile
-constexpr int kMfXStride = 68;                      // dwords per (chunk, column group, K step) block: 64 + 4 pad
-constexpr int kMfXUnit = 2 * 4 * 4 * kMfXStride;    // dwords of staged activation pairs per unit
+// Batch rows per MFMA tile is 16; BP = 32 runs two batch tiles against each decoded sign operand.
+template <int BP> constexpr int mf_nbt() { return BP > 16 ? BP / 16 : 1; }
+// dwords per (chunk, column group, K step) block of staged activation pairs: 16 * mf_nbt rows x 4 pairs + 4 pad
+template <int BP> constexpr int mf_xstride() { return 64 * mf_nbt<BP>() + 4; }
+template <int BP> constexpr int mf_xunit() { return 2 * 4 * 4 * mf_xstride<BP>(); }   // dwords per unit
 constexpr int kMfAUnit = 2 * 4 * 16;                // dwords of column-scale pairs per unit
 constexpr int kMfScr = 2 * 64 * 4;                  // dwords of a wavefront's sign scratch: 2 chunks x 64 rows x 16 bytes
 constexpr int kMfScrUnit = kMfScr + 64;             // dwords of one unit's sign scratch and 64 words of row scales
@@ -70,6 +75,21 @@ struct MfUnitRegs {
   uint32_t r;
   uint32_t meta[2];     // xidx | colscale << 16 of the thread's columns c and c + 16 (see mf_pair_col)
   uint16_t xv[BP];      // x bits: xv[2i], xv[2i + 1] = columns c, c + 16 of batch row BP/2 * half + i (rows >= B: row B-1)
+};
+
+// Where the thread's BP/2 batch rows of x are read. BP <= 16: one buffer resource per row, of range the row's N
+// columns. BP = 32 (16 rows per thread, 64 scalar registers of resources otherwise): one resource from the first of
+// the thread's rows to the end of the last, and a byte offset per row (the host keeps that span below 2^31 bytes).
+template <int BP, bool ONE = (BP > 16)>
+struct MfXRows {
+  static constexpr bool kOne = false;
+  __amdgpu_buffer_rsrc_t r[BP / 2];
+};
+template <int BP>
+struct MfXRows<BP, true> {
+  static constexpr bool kOne = true;
+  __amdgpu_buffer_rsrc_t r[1];
+  int soff[BP / 2];
 };
 
 struct MfCursor {
@@ -111,18 +131,23 @@ __device__ __forceinline__ void mf_load_meta(const GemmArgs& a, int sc, int t, u
 }
 
 // Requests unit c's data into u: activations first (u.meta must hold the unit's metadata), then the sign entries and
-// row scales. p0, p1: row-scale planes of the unit's two chunks. rx: buffer resources of the thread's BP/2 batch rows
-// of x (range: the row's N columns). A padding column's load is given an offset outside every range (2^31), for which
-// the load returns zero without reading memory: x is never multiplied there, not even by a zero.
+// row scales. p0, p1: row-scale planes of the unit's two chunks. rx: the thread's BP/2 batch rows of x. A padding
+// column's load is given an offset outside every range (2^31), for which the load returns zero without reading memory:
+// x is never multiplied there, not even by a zero.
 template <int BP, int MU>
 __device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, int32_t p0, int32_t p1, int wave,
-                                         int lane, const __amdgpu_buffer_rsrc_t (&rx)[BP / 2], MfUnitRegs<BP>& u) {
+                                         int lane, const MfXRows<BP>& rx, MfUnitRegs<BP>& u) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const uint32_t xi = u.meta[i] & 0xFFFFu;
     const int voff = xi == 0xFFFFu ? int(0x80000000u) : int(2 * xi);
 #pragma unroll
-    for (int b = 0; b < BP / 2; ++b) u.xv[2 * b + i] = __builtin_amdgcn_raw_buffer_load_b16(rx[b], voff, 0, 0);
+    for (int b = 0; b < BP / 2; ++b) {
+      if constexpr (MfXRows<BP>::kOne)
+        u.xv[2 * b + i] = __builtin_amdgcn_raw_buffer_load_b16(rx.r[0], voff, rx.soff[b], 0);
+      else
+        u.xv[2 * b + i] = __builtin_amdgcn_raw_buffer_load_b16(rx.r[b], voff, 0, 0);
+    }
   }
   const int rbl = lane >> 4;
   const uint32_t row = mf_block_row(a, c.tile, wave, rbl) + uint32_t(lane & 15);
@@ -148,7 +173,7 @@ __device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, i
 template <int BP>
 __device__ __forceinline__ void mf_stage_write(const MfUnitRegs<BP>& u, uint32_t* sx, uint32_t* sa, int t) {
   const int p = t & 127, hg = p >> 4, j = p & 15, q = j >> 2, k = j & 3, half = t >> 7;
-  uint32_t* dst = sx + (hg * 4 + q) * kMfXStride + k + 4 * (BP / 2) * half;
+  uint32_t* dst = sx + (hg * 4 + q) * mf_xstride<BP>() + k + 4 * (BP / 2) * half;
 #pragma unroll
   for (int b = 0; b < BP / 2; ++b) dst[4 * b] = __builtin_bit_cast(uint32_t, mf_u16x2{u.xv[2 * b], u.xv[2 * b + 1]});
   if (half == 0) sa[hg * 16 + j] = (u.meta[0] >> 16) | (u.meta[1] & 0xFFFF0000u);
@@ -173,14 +198,17 @@ __device__ __forceinline__ void mf_stage_signs(const MfUnitRegs<BP>& u, uint32_t
   scr[kMfScr + lane] = u.r;
 }
 
-// Multiplies one staged unit into the accumulators. xs/as: the unit's staged activation and column-scale pairs;
+// Multiplies one staged unit into the accumulators of its NBT 16-row batch tiles. xs/as: the unit's staged activation
+// (batch tile bt at 64 bt dwords of each block) and column-scale pairs;
 // scr: the wavefront's scratch of the unit (mf_stage_signs). wa[par][c]: dword offset, within a chunk's entries, of
 // word c of the two a lane reads from its row of block 0 (row blocks of parity par; block rb adds 64 rb). Reading the
 // words separately, with the index wrapped within the entry, needs no copy of an entry's first words after it, and
 // the 64 lanes of one read hit 64 different banks: lane (r, g) reads bank 4r + (its word index), and the word indices
 // of one r are a permutation of 0..3 over g.
+template <int NBT>
 __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, const uint32_t* scr, int r16, int g,
-                                        const uint32_t (&wa)[2][2], uint32_t sh, float (&acc)[4][4]) {
+                                        const uint32_t (&wa)[2][2], uint32_t sh, float (&acc)[NBT][4][4]) {
+  constexpr int XS = 64 * NBT + 4;
   const uint32_t* srs = scr + kMfScr;
   uint32_t w[2][4];
 #pragma unroll
@@ -196,11 +224,14 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
     for (int rb = 0; rb < 4; ++rb) rs[rb] = *reinterpret_cast<const uint2*>(srs + h * 32 + 8 * rb + 2 * g);
     // the words of row blocks 2rp and 2rp + 1 as one 64-bit value (high: 2rp + 1), shifted together below
     const uint64_t w2[2] = {(uint64_t(w[h][1]) << 32) | w[h][0], (uint64_t(w[h][3]) << 32) | w[h][2]};
-    mf_float4 tmp[4];
+    mf_float4 tmp[NBT][4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const mf_u32x4 bx = *reinterpret_cast<const mf_u32x4*>(xs + ((h * 4 + g) * 4 + q) * kMfXStride + 4 * r16);
       const mf_u32x4 ac = *reinterpret_cast<const mf_u32x4*>(as + (h * 4 + g) * 16 + 4 * q);
+      mf_u32x4 bx[NBT];
+#pragma unroll
+      for (int bt = 0; bt < NBT; ++bt)
+        bx[bt] = *reinterpret_cast<const mf_u32x4*>(xs + ((h * 4 + g) * 4 + q) * XS + 64 * bt + 4 * r16);
 #pragma unroll
       for (int rp = 0; rp < 2; ++rp) {
         mf_u32x4 av0, av1;
@@ -210,21 +241,27 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
           av0[k] = (uint32_t(sft) & 0x80008000u) ^ ac[k];
           av1[k] = (uint32_t(sft >> 32) & 0x80008000u) ^ ac[k];
         }
-        const mf_float4 c0 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[2 * rp];
-        const mf_float4 c1 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[2 * rp + 1];
-        tmp[2 * rp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av0),
-                                                             __builtin_bit_cast(mf_half8, bx), c0, 0, 0, 0);
-        tmp[2 * rp + 1] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av1),
-                                                                 __builtin_bit_cast(mf_half8, bx), c1, 0, 0, 0);
+        // the decoded operands serve every batch tile
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+          const mf_float4 c0 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[bt][2 * rp];
+          const mf_float4 c1 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[bt][2 * rp + 1];
+          tmp[bt][2 * rp] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av0),
+                                                                   __builtin_bit_cast(mf_half8, bx[bt]), c0, 0, 0, 0);
+          tmp[bt][2 * rp + 1] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+              __builtin_bit_cast(mf_half8, av1), __builtin_bit_cast(mf_half8, bx[bt]), c1, 0, 0, 0);
+        }
       }
     }
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-      acc[rb][0] = fmaf(-h2f(uint16_t(rs[rb].x)), tmp[rb][0], acc[rb][0]);
-      acc[rb][1] = fmaf(-h2f(uint16_t(rs[rb].x >> 16)), tmp[rb][1], acc[rb][1]);
-      acc[rb][2] = fmaf(-h2f(uint16_t(rs[rb].y)), tmp[rb][2], acc[rb][2]);
-      acc[rb][3] = fmaf(-h2f(uint16_t(rs[rb].y >> 16)), tmp[rb][3], acc[rb][3]);
-    }
+    for (int bt = 0; bt < NBT; ++bt)
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        acc[bt][rb][0] = fmaf(-h2f(uint16_t(rs[rb].x)), tmp[bt][rb][0], acc[bt][rb][0]);
+        acc[bt][rb][1] = fmaf(-h2f(uint16_t(rs[rb].x >> 16)), tmp[bt][rb][1], acc[bt][rb][1]);
+        acc[bt][rb][2] = fmaf(-h2f(uint16_t(rs[rb].y)), tmp[bt][rb][2], acc[bt][rb][2]);
+        acc[bt][rb][3] = fmaf(-h2f(uint16_t(rs[rb].y >> 16)), tmp[bt][rb][3], acc[bt][rb][3]);
+      }
   }
 }
 
@@ -236,18 +273,23 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
 // lines: scattered 4-byte stores wrote each line several times).
 template <int BP>
 __device__ __forceinline__ void mf_tile_end(const GemmArgs& a, int tile, bool shared, int slot, int wave, int lane,
-                                            int r16, int g, const float (&acc)[4][4], uint32_t* scr) {
+                                            int r16, int g, const float (&acc)[mf_nbt<BP>()][4][4], uint32_t* scr) {
   constexpr int TB = BP < kMfTRows ? BP : kMfTRows;
   float* t = reinterpret_cast<float*>(scr);
   float* mine = a.partials + ((int64_t(blockIdx.x) * 2 + slot) * BP) * kMfR + wave * 64 + lane;
   const int64_t row = int64_t(tile) * kMfR + wave * 64 + lane;
 #pragma unroll
   for (int b0 = 0; b0 < BP; b0 += TB) {
-    if (r16 >= b0 && r16 < b0 + TB) {
+    constexpr int NBT = mf_nbt<BP>();
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-        *reinterpret_cast<mf_float4*>(t + (r16 - b0) * kMfTStride + 16 * rb + 4 * g) =
-            mf_float4{acc[rb][0], acc[rb][1], acc[rb][2], acc[rb][3]};
+    for (int bt = 0; bt < NBT; ++bt) {   // batch row 16 bt + r16 of the lane's accumulators
+      const int b = 16 * bt + r16;
+      if ((16 * bt + 16 > b0 && 16 * bt < b0 + TB) && b >= b0 && b < b0 + TB) {
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+          *reinterpret_cast<mf_float4*>(t + (b - b0) * kMfTStride + 16 * rb + 4 * g) =
+              mf_float4{acc[bt][rb][0], acc[bt][rb][1], acc[bt][rb][2], acc[bt][rb][3]};
+      }
     }
     if (shared) {
 #pragma unroll
@@ -272,7 +314,7 @@ struct MfKernel {
     MfCursor cur;    // unit K
     MfCursor nxt;    // unit K + D (clamped to the last unit of the range)
     int stg_sc;      // super-chunk of unit K + D + 1 (clamped), whose metadata is requested next
-    float acc[4][4];
+    float acc[mf_nbt<BP>()][4][4];
   };
 
   struct Lane {
@@ -291,7 +333,7 @@ struct MfKernel {
   __device__ static __forceinline__ void step(const GemmArgs& a, State& s, MfUnitRegs<BP> (&ur)[D + 1],
                                               uint32_t (&meta_next)[2], const int* s_planes, uint32_t* sx,
                                               uint32_t* sa, uint32_t* scr, const Lane& ln,
-                                              const __amdgpu_buffer_rsrc_t (&rx)[BP / 2]) {
+                                              const MfXRows<BP>& rx) {
     if constexpr (K < kMfMaxUnits) {
       if (K >= s.n) return;
       constexpr int PN = (K + D) % (D + 1);
@@ -307,11 +349,11 @@ struct MfKernel {
       }
       __builtin_amdgcn_sched_barrier(0);
       if (K + 1 < s.n) {
-        mf_stage_write<BP>(ur[PS], sx + ((K + 1) & 1) * kMfXUnit, sa + ((K + 1) & 1) * kMfAUnit, ln.t);
+        mf_stage_write<BP>(ur[PS], sx + ((K + 1) & 1) * mf_xunit<BP>(), sa + ((K + 1) & 1) * kMfAUnit, ln.t);
         mf_stage_signs<BP>(ur[PS], scr + ((K + 1) & 1) * kMfScrUnit, ln.lane);
       }
       __builtin_amdgcn_sched_barrier(0);
-      mf_unit(sx + (K & 1) * kMfXUnit, sa + (K & 1) * kMfAUnit, scr + (K & 1) * kMfScrUnit, ln.r16, ln.g, ln.wa,
+      mf_unit<mf_nbt<BP>()>(sx + (K & 1) * mf_xunit<BP>(), sa + (K & 1) * kMfAUnit, scr + (K & 1) * kMfScrUnit, ln.r16, ln.g, ln.wa,
               ln.sh, s.acc);
       if (s.cur.sc == a.steps - 1 || K + 1 == s.n) {
         const int tile = s.cur.tile;
@@ -320,9 +362,11 @@ struct MfKernel {
                         scr + (K & 1) * kMfScrUnit);
         if (shared) ++s.n_pending;
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
+        for (int bt = 0; bt < mf_nbt<BP>(); ++bt)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) s.acc[rb][v] = 0.f;
+          for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) s.acc[bt][rb][v] = 0.f;
       }
       mf_advance(a, s.cur);
       __syncthreads();
@@ -332,9 +376,9 @@ struct MfKernel {
 };
 
 template <int BP, int MU, int D, bool R2>
-__global__ void __launch_bounds__(kMfNT, (BP <= 4 && D == 2 && R2) ? 4 : 3) k_gemm_mfma(GemmArgs a) {
+__global__ void __launch_bounds__(kMfNT, BP > 16 ? 2 : ((BP <= 4 && D == 2 && R2) ? 4 : 3)) k_gemm_mfma(GemmArgs a) {
   using K = MfKernel<BP, MU, D>;
-  __shared__ __attribute__((aligned(16))) uint32_t sx[2 * kMfXUnit];
+  __shared__ __attribute__((aligned(16))) uint32_t sx[2 * mf_xunit<BP>()];
   __shared__ __attribute__((aligned(16))) uint32_t sa[2 * kMfAUnit];
   __shared__ __attribute__((aligned(16))) uint32_t scr_all[4 * kMfScrWave];
   __shared__ int s_planes[2 * kMfMaxUnits];
@@ -372,9 +416,11 @@ __global__ void __launch_bounds__(kMfNT, (BP <= 4 && D == 2 && R2) ? 4 : 3) k_ge
   s.last_shared = tile_is_shared(a, s.last_tile);
   s.n_pending = 0;
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int bt = 0; bt < mf_nbt<BP>(); ++bt)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) s.acc[rb][v] = 0.f;
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) s.acc[bt][rb][v] = 0.f;
 
   // Row-scale planes of the range's chunks (the launch plan keeps n <= kMfMaxUnits), and metadata of units 0..D.
   if (ln.t < 2 * s.n) {
@@ -382,15 +428,26 @@ __global__ void __launch_bounds__(kMfNT, (BP <= 4 && D == 2 && R2) ? 4 : 3) k_ge
     while (sc >= a.steps) sc -= a.steps;
     s_planes[ln.t] = a.chunk_plane[2 * sc + (ln.t & 1)];
   }
-  // Buffer resources of the thread's batch rows of x, each of range N columns: half t >> 7 of the padded batch
-  // (wave-uniform; rows >= B read row B-1).
-  __amdgpu_buffer_rsrc_t rx[BP / 2];
+  // The thread's batch rows of x: half t >> 7 of the padded batch (wave-uniform; rows >= B read row B-1).
+  MfXRows<BP> rx;
   const int half = __builtin_amdgcn_readfirstlane(ln.t >> 7);
+  if constexpr (MfXRows<BP>::kOne) {
+    const int b0 = (BP / 2) * half < a.B ? (BP / 2) * half : a.B - 1;
+    const int b1 = (BP / 2) * half + BP / 2 - 1 < a.B ? (BP / 2) * half + BP / 2 - 1 : a.B - 1;
+    rx.r[0] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.x + int64_t(b0) * a.ldx), 0,
+                                                int((int64_t(b1 - b0) * a.ldx + a.N) * 2), 0x00020000);
 #pragma unroll
-  for (int i = 0; i < BP / 2; ++i) {
-    const int b = (BP / 2) * half + i;
-    rx[i] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.x + int64_t(b < a.B ? b : a.B - 1) * a.ldx), 0,
-                                              2 * a.N, 0x00020000);
+    for (int i = 0; i < BP / 2; ++i) {
+      const int b = (BP / 2) * half + i;
+      rx.soff[i] = int(int64_t((b < a.B ? b : a.B - 1) - b0) * a.ldx * 2);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < BP / 2; ++i) {
+      const int b = (BP / 2) * half + i;
+      rx.r[i] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.x + int64_t(b < a.B ? b : a.B - 1) * a.ldx),
+                                                  0, 2 * a.N, 0x00020000);
+    }
   }
   MfUnitRegs<BP> ur[D + 1];
   uint32_t meta_next[2];
@@ -404,7 +461,7 @@ __global__ void __launch_bounds__(kMfNT, (BP <= 4 && D == 2 && R2) ? 4 : 3) k_ge
     s.stg_sc = sc;   // unit D + 1 (clamped)
   }
   // Staged rows of batch rows >= BP stay zero for the whole launch.
-  for (int i = ln.t; i < 2 * kMfXUnit; i += kMfNT) sx[i] = 0u;
+  for (int i = ln.t; i < 2 * mf_xunit<BP>(); i += kMfNT) sx[i] = 0u;
   __syncthreads();   // planes in LDS; zero fill done before any staged value is written
   s.nxt = s.cur;
 #pragma unroll
@@ -444,6 +501,7 @@ bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, bool reduc
       case 4: return launch_mfma_bp<4, 2, true>(a, mu, stream);
       case 8: return launch_mfma_bp<8, 2, true>(a, mu, stream);
       case 16: return launch_mfma_bp<16, 2, true>(a, mu, stream);
+      case 32: return launch_mfma_bp<32, 2, true>(a, mu, stream);
     }
     return false;
   }

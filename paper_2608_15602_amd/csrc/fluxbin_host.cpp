@@ -134,6 +134,7 @@ static fluxbin_tuning tuning_defaults() {
   t.mfma_r2 = 1;
   t.bat_r2 = 1;
   t.rows = -1;
+  t.batch_tile = 0;
   return t;
 }
 
@@ -163,6 +164,7 @@ static void tuning_init_locked() {
   t.mfma_r2 = env_int("FLUXBIN_MFMA_R2", t.mfma_r2);
   t.bat_r2 = env_int("FLUXBIN_BAT_R2", t.bat_r2);
   t.rows = env_int("FLUXBIN_ROWS", t.rows);
+  t.batch_tile = env_int("FLUXBIN_BATCH_TILE", t.batch_tile);
   g_tuning = t;
   g_tuning_init = true;
 }
@@ -210,11 +212,26 @@ static uint64_t layer_counter_bytes(int64_t M) {
   return round_up256(uint64_t(ceil_div(M, 256) + 4) * uint64_t(kCounterStride) * 4u);
 }
 
+// Rows of a full batch tile (calls with more batch rows run as several launches): 32 on layers the matrix-core kernel
+// takes (one row scale per chunk), whose sign decode then serves two 16-row MFMA tiles, else 16. The 32-row kernel
+// reads a thread's 16 batch rows of x through one buffer resource: the span of 15 rows of ldx elements plus N must stay
+// below 2^31 bytes (ldx < 0: not known yet). FLUXBIN_BATCH_TILE=16 keeps 16-row tiles.
+static int batch_tile_rows(const fluxbin_layer& L, int64_t ldx, const fluxbin_tuning& tu) {
+  const Derived dv = derive(L.shape);
+  if (tu.generic || dv.Gcg > 1 || dv.Gcs > 1 || tu.mfma == 0 || tu.mfma_depth == 3 || tu.mfma_r2 == 0 ||
+      tu.batch_tile == kMaxBatch)
+    return kMaxBatch;
+  if (ldx >= 0 && (int64_t(kMaxBatchMfma / 2 - 1) * ldx + L.shape.N) * 2 >= (int64_t(1) << 31)) return kMaxBatch;
+  return kMaxBatchMfma;
+}
+
 fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   const int cus = device_cu_count();
   if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
   std::memset(p, 0, sizeof(*p));
   const fluxbin_tuning tu = tuning_snapshot();
+  if (B < 1 || (B > kMaxBatch && batch_tile_rows(L, -1, tu) < B))
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "no launch plan for %d batch rows in one launch on this layer", B);
   const int force_generic = tu.generic;
   const int rpt_env = tu.rpt;
   int per_cu = tu.blocks_per_cu;
@@ -287,13 +304,17 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     // units of data requested ahead: two (measured 2-8 us faster than three on the 70B MLP layers at B = 2..16)
     const int depth_env = tu.mfma_depth;
     p->depth = depth_env == 3 ? 3 : 2;
-    p->bg = B <= 4 ? 4 : (B <= 8 ? 8 : 16);
+    p->bg = B <= 4 ? 4 : (B <= 8 ? 8 : (B <= 16 ? 16 : 32));
     p->n_groups = 1;
     // split tiles reduced by a second kernel (FLUXBIN_MFMA_R2=0: by the tile counters, as at batch 1): measured
     // on the 70B MLP layers, up / down, 58.6 / 78.7 -> 57.2 / 59.3 us at B = 16, 48.0 / 57.7 -> 46.5 / 47.1 at B = 8,
     // 45.5 / 48.8 -> 42.6 / 43.6 at B = 4; 7B MLP layers 18.8 / 19.0 -> 15.1 / 17.1 at B = 4
     p->reduce2 = p->depth == 2 && tu.mfma_r2 != 0;
-    if (per_cu < 1 || per_cu > 8) per_cu = 3;   // three 256-thread workgroups per CU (the kernel's occupancy)
+    // three 256-thread workgroups per CU (the kernel's occupancy); two with 32 batch rows (instantiated with two units
+    // ahead and the second-kernel reduction only)
+    if (per_cu < 1 || per_cu > 8) per_cu = p->bg == 32 ? 2 : 3;
+    if (p->bg == 32 && !(p->depth == 2 && p->reduce2))
+      return fail(FLUXBIN_ERR_UNSUPPORTED, "32-row matrix-core launches need two units ahead and the second kernel");
   } else if (L.shape.mu == 8 && B >= 2 && !force_generic && !fine) {
     // small batch: 1024-row tiles, one super-chunk per unit (the batch-1 sign stream), batch in groups of four rows
     // (two for B = 2: half the table entries and lookup additions of a padded group of four)
@@ -314,6 +335,8 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     if (p->n_groups == 3) p->n_groups = 4;  // instantiated batch paddings: 1, 2, 4, 8, 16
     if (per_cu < 1 || per_cu > 8) per_cu = 2;
   }
+  if (B > kMaxBatch && p->kernel != 3)
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "%d batch rows in one launch need the matrix-core kernel", B);
   const int blocks_env = tu.blocks;   // tuning override: grid size target
   const int64_t target = blocks_env > 0 ? blocks_env : int64_t(cus) * per_cu;
   p->bpad = p->bg * p->n_groups;
@@ -548,22 +571,23 @@ fluxbin_status fluxbin_layer_from_header(const void* header_host, void* d_packed
 
 }  // extern "C"
 
-// Batches larger than one launch's kMaxBatch rows run as consecutive launches of kMaxBatch-row batch tiles (the last
-// one with the remaining rows), each with its own launch plan, one after another on the caller's stream and sharing the
-// workspace (every launch leaves its counters at zero). Each tile reads the packed weights again: the batch dimension is
-// tiled with a fixed per-launch on-chip footprint.
+// Batches larger than one launch's rows (batch_tile_rows: 16 or 32) run as consecutive launches of full batch tiles
+// (the last one with the remaining rows), each with its own launch plan, one after another on the caller's stream and
+// sharing the workspace (every launch leaves its counters at zero). Each tile reads the packed weights again: the batch
+// dimension is tiled with a fixed per-launch on-chip footprint.
 struct BatchTiles {
-  Plan full, tail;     // plans of a full tile and of the last tile (tail rows < kMaxBatch; unused if 0)
-  int n_full, tail_rows;
+  Plan full, tail;     // plans of a full tile and of the last tile (tail rows < tile; unused if 0)
+  int tile, n_full, tail_rows;
   uint64_t ws_bytes;   // the larger of the two plans' workspaces
 };
 
-static fluxbin_status batch_tiles(const fluxbin_layer& L, int B, BatchTiles* bt) {
+static fluxbin_status batch_tiles(const fluxbin_layer& L, int B, int tile, BatchTiles* bt) {
   std::memset(bt, 0, sizeof(*bt));
-  bt->n_full = B / kMaxBatch;
-  bt->tail_rows = B % kMaxBatch;
+  bt->tile = tile;
+  bt->n_full = B / tile;
+  bt->tail_rows = B % tile;
   if (bt->n_full > 0) {
-    const fluxbin_status st = make_plan(L, kMaxBatch, &bt->full);
+    const fluxbin_status st = make_plan(L, tile, &bt->full);
     if (st != FLUXBIN_OK) return st;
     bt->ws_bytes = bt->full.ws_bytes;
   }
@@ -583,10 +607,18 @@ fluxbin_status fluxbin_workspace_query(const fluxbin_layer* layer, int32_t B, si
   if (st != FLUXBIN_OK) return st;
   if (!bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "bytes is NULL");
   if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
+  // the call's ldx decides the tile rows (batch_tile_rows): room for either choice
+  const fluxbin_tuning tu = tuning_snapshot();
   BatchTiles bt;
-  st = batch_tiles(*layer, B, &bt);
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, -1, tu), &bt);
   if (st != FLUXBIN_OK) return st;
-  *bytes = static_cast<size_t>(bt.ws_bytes);
+  uint64_t ws = bt.ws_bytes;
+  if (bt.tile != kMaxBatch) {
+    st = batch_tiles(*layer, B, kMaxBatch, &bt);
+    if (st != FLUXBIN_OK) return st;
+    if (bt.ws_bytes > ws) ws = bt.ws_bytes;
+  }
+  *bytes = static_cast<size_t>(ws);
   return FLUXBIN_OK;
 }
 
@@ -612,7 +644,7 @@ static fluxbin_status gemm_common(const fluxbin_layer* layer, int32_t B, const u
   const size_t yb = (size_t(B - 1) * ldy + s.M) * (y_is_fp32 ? 4 : 2);
   if (ranges_overlap(d_x, xb, d_y, yb)) return fail(FLUXBIN_ERR_INVALID_ARG, "x and y overlap");
   BatchTiles bt;
-  st = batch_tiles(*layer, B, &bt);
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, ldx, tuning_snapshot()), &bt);
   if (st != FLUXBIN_OK) return st;
   if (!d_ws) return fail(FLUXBIN_ERR_INVALID_ARG, "workspace is NULL");
   if (ws_bytes < bt.ws_bytes)
@@ -622,9 +654,9 @@ static fluxbin_status gemm_common(const fluxbin_layer* layer, int32_t B, const u
     return fail(FLUXBIN_ERR_INVALID_ARG, "workspace overlaps x or y");
   const size_t y_elt = y_is_fp32 ? 4 : 2;
   for (int t = 0; t <= bt.n_full; ++t) {
-    const int rows = t < bt.n_full ? kMaxBatch : bt.tail_rows;
+    const int rows = t < bt.n_full ? bt.tile : bt.tail_rows;
     if (rows == 0) break;
-    const int64_t b0 = int64_t(t) * kMaxBatch;
+    const int64_t b0 = int64_t(t) * bt.tile;
     st = launch_gemm(*layer, t < bt.n_full ? bt.full : bt.tail, rows, d_x + b0 * ldx, ldx,
                      static_cast<uint8_t*>(d_y) + size_t(b0) * size_t(ldy) * y_elt, ldy, y_is_fp32, d_ws, stream);
     if (st != FLUXBIN_OK) return st;
@@ -711,8 +743,8 @@ fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin
   if (st != FLUXBIN_OK) return st;
   if (!out) return fail(FLUXBIN_ERR_INVALID_ARG, "out is NULL");
   if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
-  BatchTiles bt;
-  st = batch_tiles(*layer, B, &bt);
+  BatchTiles bt;   // for contiguous x (ldx = N)
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, layer->shape.N, tuning_snapshot()), &bt);
   if (st != FLUXBIN_OK) return st;
   const Plan& p = bt.n_full > 0 ? bt.full : bt.tail;
   std::memset(out, 0, sizeof(*out));
@@ -724,6 +756,7 @@ fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin
   out->second_kernel_reduction = p.reduce2 ? 1 : 0;
   out->early = p.early ? 1 : 0;
   out->batch_tiles = bt.n_full + (bt.tail_rows > 0 ? 1 : 0);
+  out->batch_tile_rows = bt.tile;
   out->tiles = p.n_tiles;
   out->units = p.units;
   out->workgroups = p.blocks;

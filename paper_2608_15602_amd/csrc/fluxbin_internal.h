@@ -11,7 +11,8 @@ namespace fluxbin {
 constexpr int kChunk = 128;             // virtual columns per chunk (16 bytes of signs per row)
 constexpr uint32_t kMagic = 0x42584C46u;  // "FLXB"
 constexpr int kMaxBatch = 16;          // batch rows of one launch (a batch tile)
-constexpr int kMaxBatchCall = 8192;     // batch rows of one call: larger batches run as 16-row batch tiles
+constexpr int kMaxBatchMfma = 32;      // batch rows of one matrix-core launch on layers with one row scale per chunk
+constexpr int kMaxBatchCall = 8192;     // batch rows of one call: larger batches run as batch tiles
 constexpr int kRwMaxN = 16384;          // row-complete batch-1 kernel: input columns staged in LDS
 constexpr int kRwSteps = 16;            // row-complete batch-1 kernel: super-chunks per wavefront
 // Units per workgroup of the batch-1 kernel (its LDS staging capacity): 16 for 1024-thread workgroups (one per CU),

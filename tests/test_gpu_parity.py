@@ -379,19 +379,72 @@ PREFILL_SPECS = [
 ]
 
 
-@pytest.mark.parametrize("B", [17, 40, 64])
+@pytest.mark.parametrize("B", [17, 33, 40, 64, 65])
 @pytest.mark.parametrize("spec", PREFILL_SPECS, ids=lambda s: s.name)
 def test_prefill_batch_tiles(spec, B):
-    """B > 16 runs as 16-row batch tiles, one launch each: every row matches the oracle, and each tile's rows are
-    bitwise those of a call on that tile's rows alone (a one-row tail runs the batch-1 kernel)."""
+    """Batches above one launch's rows run as batch tiles (32 rows on layers with one row scale per chunk, else 16),
+    one launch each: every row matches the oracle, and each tile's rows are bitwise those of a call on that tile's rows
+    alone (a one-row tail runs a batch-1 kernel)."""
+    from paper_2608_15602_amd import fluxbin as fb
     _, packed, x, y = _parity(spec, B, out_fp32=True)
-    for b0 in range(0, B, 16):
-        part = run_gemm(packed, x[b0:b0 + 16], out_fp32=True)
-        assert np.array_equal(part, y[b0:b0 + 16]), (B, b0)
+    info = fb.fluxbin_plan_query(packed, B)
+    tile = info["batch_tile_rows"]
+    fine = (spec.g_r < 128 and spec.g_r < spec.N) or (spec.Ks > 0 and spec.S > 0 and spec.g_s < min(128, spec.S))
+    assert tile == (16 if fine else 32), info
+    assert info["batch_tiles"] == -(-B // tile), info
+    for b0 in range(0, B, tile):
+        part = run_gemm(packed, x[b0:b0 + tile], out_fp32=True)
+        assert np.array_equal(part, y[b0:b0 + tile]), (B, b0)
+
+
+TILE32_SPECS = [
+    LayerSpec("tile32_mu8", M=2000, N=3000, Kb=2, Ks=1, mu=8, S=90, g_r=128, g_s=90, seed=31),
+    LayerSpec("tile32_mu4", M=1100, N=2200, Kb=3, Ks=1, mu=4, S=33, g_r=128, g_s=33, seed=32),
+    LayerSpec("tile32_1base", M=300, N=700, Kb=1, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=33),
+]
+
+
+@pytest.mark.parametrize("B", [17, 24, 32])
+@pytest.mark.parametrize("spec", TILE32_SPECS, ids=lambda s: s.name)
+def test_mfma_32_row_launch(spec, B):
+    """17..32 batch rows in one matrix-core launch (two 16-row MFMA tiles per decoded sign operand): every row against
+    the oracle, bitwise repeatable, and within tolerance of the same batch run as 16-row tiles."""
+    from paper_2608_15602_amd import fluxbin as fb
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    info = fb.fluxbin_plan_query(packed, B)
+    assert (info["kernel"], info["batch_tile_rows"], info["batch_tiles"]) == (3, 32, 1), info
+    _, _, x, y = _parity(spec, B, packed=packed, L=L)
+    assert np.array_equal(run_gemm(packed, x), y), "repeat differs"
+    y16 = _with_env({"FLUXBIN_BATCH_TILE": "16"}, lambda: run_gemm(packed, x))
+    _check(y, y16, "32-row launch vs 16-row tiles")
+
+
+def test_mfma_32_row_launch_large_row_stride():
+    """An x row stride so large that 15 strides reach 2^31 bytes: the call runs 16-row tiles instead of one 32-row
+    launch (whose reads of x take 32-bit offsets), giving bitwise the 16-row tiles' result on a contiguous copy."""
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    spec = TILE32_SPECS[2]
+    log("case 32-row launch, large x row stride")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    B, ldx = 20, (1 << 30) // 15 + 64
+    x = make_activations(L, B)
+    flat = torch.zeros((B - 1) * ldx + spec.N, dtype=torch.float16, device="cuda")
+    xs = flat.as_strided((B, spec.N), (ldx, 1))
+    xs.copy_(x_tensor(x))
+    y = fb.fluxbin_lut_gemm_smallbatch(packed, xs, out_fp32=True)
+    torch.cuda.synchronize()
+    y = y.cpu().numpy().astype(np.float64)
+    del flat, xs
+    y16 = _with_env({"FLUXBIN_BATCH_TILE": "16"}, lambda: run_gemm(packed, x, out_fp32=True))
+    assert np.array_equal(y, y16)
+    _check(y, oracle.gemv_dense(L, x), "large row stride")
 
 
 def test_prefill_batch_mlp70b_full_size():
-    """A 64-row batch on the 70B MLP up layer at full size (four 16-row tiles on the matrix cores): sampled rows
+    """A 64-row batch on the 70B MLP up layer at full size (two 32-row tiles on the matrix cores): sampled rows
     against the oracle."""
     spec = config_layers("c4_mlp70b", "128")[0]
     _parity(spec, 64, rows=sample_rows(spec.M, 96, seed=64))
