@@ -207,8 +207,8 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
  * and uses it for all its rows (batch-independent reuse of the weights, Sec. 3.2 and App. E.2); larger batches run as
  * consecutive launches of T-row batch tiles (the last with the remaining rows), each its own launch plan, one after
  * another on the stream and sharing the workspace, so rows Tt..Tt+T-1 give the same y as a call on those rows alone.
- * T = 32 on layers with one row scale per chunk (matrix-core kernel), else 16; also 16 where 15 row strides plus N
- * elements of x reach 2^31 bytes. fluxbin_plan_query reports T as batch_tile_rows.
+ * T = 32 on layers with one row scale per chunk (matrix-core kernel), else 16. fluxbin_plan_query reports T as
+ * batch_tile_rows.
  * d_x fp16 with row stride ldx >= N (elements); d_y with row stride ldy >= M (elements of the output type). B = 1
  * gives the same result as fluxbin_lut_gemv.
  * Two kernels compute it: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4 on layers with at
@@ -268,10 +268,9 @@ fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
  * The launch plan a GEMV/GEMM call of batch B on this layer would use on the current device with the current tuning.
  *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel,
  *           4: row-complete batch-1 kernel (layers with few rows).
- * Batches of more than batch_tile_rows rows (32 on layers the matrix-core kernel takes, else 16; 16 also for an x row
- * stride so large that 15 strides plus N elements reach 2^31 bytes) run as batch_tiles launches; the plan is then that
- * of the full batch tiles, for an x of row stride N, and workspace_bytes the call's workspace. Host only apart from
- * reading the device's CU count; launches nothing.
+ * Batches of more than batch_tile_rows rows (32 on layers the matrix-core kernel takes, else 16) run as batch_tiles
+ * launches; the plan is then that of the full batch tiles, and workspace_bytes the call's workspace. Host only apart
+ * from reading the device's CU count; launches nothing.
  */
 typedef struct {
   int32_t kernel, threads, rows_per_tile, depth, batch_groups, second_kernel_reduction, early, batch_tiles;

@@ -18,6 +18,7 @@ struct GemmArgs {
   void* y;
   float* partials;
   uint32_t* counters;
+  uint32_t* img;     // matrix-core kernel: per-call activation images of every super-chunk (workspace)
   int64_t ldx, ldy;
   int32_t units, blocks;
   int32_t uq, ur;    // units per workgroup: uq + 1 for the first ur workgroups, uq for the others

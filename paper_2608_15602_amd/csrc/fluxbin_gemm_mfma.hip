@@ -32,12 +32,17 @@
 //
 // Memory pipeline. Each lane requests its row's whole 16-byte entries of a unit (one 16-byte load per chunk) and one
 // 32-bit word of row scales, D units ahead of the unit being multiplied (2 KB of signs per wavefront per unit, no
-// byte requested twice); a wavefront passes the entries to its MFMA lanes through its own LDS scratch. The
-// activations of a unit (gathered through the VCM index table) are requested together with its signs, because
-// vector loads complete in issue order: a load issued after the sign loads of a later unit could only be used once
-// those had arrived. Each thread gathers one column pair (the two halves of an operand dword) for half of the batch
-// rows and writes them, one unit before they are multiplied and before the multiplication of the current unit (so
-// that their registers are free during it), to a double-buffered LDS staging area as whole dwords, 64 banks per write.
+// byte requested twice); a wavefront passes the entries to its MFMA lanes through its own LDS scratch.
+// Activations. The B operands of a super-chunk (x gathered through the VCM index table, in the order the MFMA lanes
+// read them, as fp16 pairs) and its signed column-scale pairs do not depend on the row tile, so a first kernel
+// (k_mf_image) writes them once per call, for every super-chunk, to an image in the workspace laid out exactly like
+// the LDS staging area of one unit. The multiplying kernel copies a unit's image into its double-buffered staging
+// area with LDS-direct loads (global_load_lds_dwordx4: 16 bytes per lane written straight to LDS, no registers), one
+// unit ahead, issued before that step's sign requests. Vector memory operations complete in issue order, so waiting
+// until at most the three sign and row-scale requests issued after the copy are outstanding (s_waitcnt vmcnt(3)),
+// before the step's barrier, means the copy has landed while the later sign requests stay in flight. The copies are
+// written as instructions because the compiler, seeing an LDS-direct load in flight, drains every outstanding load
+// before each barrier, which would leave no sign request in flight across the steps.
 #include <hip/hip_runtime.h>
 
 #include "fluxbin_device.h"
@@ -56,8 +61,7 @@ constexpr int kMfR = 256;                           // rows per tile
 // Batch rows per MFMA tile is 16; BP = 32 runs two batch tiles against each decoded sign operand.
 template <int BP> constexpr int mf_nbt() { return BP > 16 ? BP / 16 : 1; }
 // dwords per (chunk, column group, K step) block of staged activation pairs: 16 * mf_nbt rows x 4 pairs + 4 pad
-template <int BP> constexpr int mf_xstride() { return 64 * mf_nbt<BP>() + 4; }
-template <int BP> constexpr int mf_xunit() { return 2 * 4 * 4 * mf_xstride<BP>(); }   // dwords per unit
+template <int BP> constexpr int mf_xunit() { return 2 * 4 * 4 * mf_xstride(BP); }   // dwords per unit
 constexpr int kMfAUnit = 2 * 4 * 16;                // dwords of column-scale pairs per unit
 constexpr int kMfScr = 2 * 64 * 4;                  // dwords of a wavefront's sign scratch: 2 chunks x 64 rows x 16 bytes
 constexpr int kMfScrUnit = kMfScr + 64;             // dwords of one unit's sign scratch and 64 words of row scales
@@ -66,30 +70,40 @@ constexpr int kMfTStride = 68;                      // dwords per batch row of a
 constexpr int kMfTRows = 8;                         // batch rows per pass of the transpose (in one unit's scratch)
 static_assert(kMfTRows * kMfTStride <= kMfScrUnit, "transpose pass larger than a unit's scratch");
 
+// dwords of a unit's activation image: the staged activation pairs, then the column-scale pairs; a whole number of
+// 1 KB LDS-direct requests (64 lanes x 16 bytes)
+template <int BP> constexpr int mf_img() { return mf_image_dwords(BP); }
+static_assert(mf_img<4>() >= mf_xunit<4>() + kMfAUnit && mf_img<16>() == mf_xunit<16>() + kMfAUnit &&
+              mf_img<32>() == mf_xunit<32>() + kMfAUnit, "image smaller than the staging area");
+
+// Activation staging: up to 8 batch rows each thread gathers its column pair of a unit itself (few rows: the loads
+// are cheap and a separate image kernel would cost more than it saves); 16 and 32 rows copy the unit's image.
+template <int BP> constexpr bool mf_gather() { return BP <= 8; }
+
 // Requested data of one unit: the lane's row entries of both chunks (lane l: row 16 (l >> 4) + (l & 15) of the
-// wavefront's 64 rows), one word of row scales (lane l: rows 2 (l & 31) and 2 (l & 31) + 1 of chunk l >> 5), and the
-// lane's staged column pair: the metadata of its two columns and their x in its half of the batch rows.
-template <int BP>
+// wavefront's 64 rows) and one word of row scales (lane l: rows 2 (l & 31) and 2 (l & 31) + 1 of chunk l >> 5);
+// gathering: also the thread's staged column pair, the metadata of its two columns and their x in its half of the
+// batch rows.
+template <int BP, bool G = mf_gather<BP>()>
 struct MfUnitRegs {
+  mf_u32x4 e[2];
+  uint32_t r;
+};
+template <int BP>
+struct MfUnitRegs<BP, true> {
   mf_u32x4 e[2];
   uint32_t r;
   uint32_t meta[2];     // xidx | colscale << 16 of the thread's columns c and c + 16 (see mf_pair_col)
   uint16_t xv[BP];      // x bits: xv[2i], xv[2i + 1] = columns c, c + 16 of batch row BP/2 * half + i (rows >= B: row B-1)
 };
 
-// Where the thread's BP/2 batch rows of x are read. BP <= 16: one buffer resource per row, of range the row's N
-// columns. BP = 32 (16 rows per thread, 64 scalar registers of resources otherwise): one resource from the first of
-// the thread's rows to the end of the last, and a byte offset per row (the host keeps that span below 2^31 bytes).
-template <int BP, bool ONE = (BP > 16)>
-struct MfXRows {
-  static constexpr bool kOne = false;
-  __amdgpu_buffer_rsrc_t r[BP / 2];
-};
+// Buffer resources of a gathering thread's BP/2 batch rows of x, each of range the row's N columns (empty when
+// copying images).
+template <int BP, bool G = mf_gather<BP>()>
+struct MfXRows {};
 template <int BP>
 struct MfXRows<BP, true> {
-  static constexpr bool kOne = true;
-  __amdgpu_buffer_rsrc_t r[1];
-  int soff[BP / 2];
+  __amdgpu_buffer_rsrc_t r[BP / 2];
 };
 
 struct MfCursor {
@@ -110,8 +124,9 @@ __device__ __forceinline__ uint32_t mf_block_row(const GemmArgs& a, int tile, in
   return uint32_t(r <= a.Mp - 16 ? r : a.Mp - 16);
 }
 
-// Staging ownership: thread t stages the column pair p = t & 127 of a unit, virtual columns c = 32 (p >> 4) + (p & 15)
-// and c + 16 (chunk c >> 7; the pair is one fp16 pair of the MFMA operands), for half t >> 7 of the batch rows.
+// Staging ownership when gathering: thread t stages the column pair p = t & 127 of a unit, virtual columns
+// c = 32 (p >> 4) + (p & 15) and c + 16 (chunk c >> 7; the pair is one fp16 pair of the MFMA operands), for half t >> 7
+// of the batch rows.
 __device__ __forceinline__ int mf_pair_col(int t) { return 32 * ((t & 127) >> 4) + (t & 15); }
 
 // Metadata of the thread's two columns of super-chunk sc, through buffer loads (byte offsets 32-bit: the host checks
@@ -130,25 +145,37 @@ __device__ __forceinline__ void mf_load_meta(const GemmArgs& a, int sc, int t, u
   }
 }
 
-// Requests unit c's data into u: activations first (u.meta must hold the unit's metadata), then the sign entries and
-// row scales. p0, p1: row-scale planes of the unit's two chunks. rx: the thread's BP/2 batch rows of x. A padding
-// column's load is given an offset outside every range (2^31), for which the load returns zero without reading memory:
-// x is never multiplied there, not even by a zero.
-template <int BP, int MU>
-__device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, int32_t p0, int32_t p1, int wave,
-                                         int lane, const MfXRows<BP>& rx, MfUnitRegs<BP>& u) {
+// Gathers the thread's activations of a unit into u (u.meta must hold the unit's metadata). A padding column's load
+// is given an offset outside every range (2^31), for which the load returns zero without reading memory: x is never
+// multiplied there, not even by a zero.
+template <int BP>
+__device__ __forceinline__ void mf_issue_x(const MfXRows<BP>& rx, MfUnitRegs<BP>& u) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const uint32_t xi = u.meta[i] & 0xFFFFu;
     const int voff = xi == 0xFFFFu ? int(0x80000000u) : int(2 * xi);
 #pragma unroll
-    for (int b = 0; b < BP / 2; ++b) {
-      if constexpr (MfXRows<BP>::kOne)
-        u.xv[2 * b + i] = __builtin_amdgcn_raw_buffer_load_b16(rx.r[0], voff, rx.soff[b], 0);
-      else
-        u.xv[2 * b + i] = __builtin_amdgcn_raw_buffer_load_b16(rx.r[b], voff, 0, 0);
-    }
+    for (int b = 0; b < BP / 2; ++b) u.xv[2 * b + i] = __builtin_amdgcn_raw_buffer_load_b16(rx.r[b], voff, 0, 0);
   }
+}
+
+// Writes a gathered unit to its staging buffer: the thread's activation pairs and, for half 0, its column-scale pair
+// (with sign), in the order the MFMA operands read them. Batch rows b >= B hold row B-1's values: MFMA output column b
+// depends on activation column b only, and columns >= B are never stored.
+template <int BP>
+__device__ __forceinline__ void mf_stage_write(const MfUnitRegs<BP>& u, uint32_t* sx, uint32_t* sa, int t) {
+  const int p = t & 127, hg = p >> 4, j = p & 15, q = j >> 2, k = j & 3, half = t >> 7;
+  uint32_t* dst = sx + (hg * 4 + q) * mf_xstride(BP) + k + 4 * (BP / 2) * half;
+#pragma unroll
+  for (int b = 0; b < BP / 2; ++b) dst[4 * b] = __builtin_bit_cast(uint32_t, mf_u16x2{u.xv[2 * b], u.xv[2 * b + 1]});
+  if (half == 0) sa[hg * 16 + j] = (u.meta[0] >> 16) | (u.meta[1] & 0xFFFF0000u);
+}
+
+// Requests unit c's sign entries and row scales into u (three vector loads per lane). p0, p1: row-scale planes of the
+// unit's two chunks.
+template <int BP, int MU>
+__device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, int32_t p0, int32_t p1, int wave,
+                                         int lane, MfUnitRegs<BP>& u) {
   const int rbl = lane >> 4;
   const uint32_t row = mf_block_row(a, c.tile, wave, rbl) + uint32_t(lane & 15);
   const int64_t plane_bytes = int64_t(a.Mp) * 16;
@@ -167,16 +194,28 @@ __device__ __forceinline__ void mf_issue(const GemmArgs& a, const MfCursor& c, i
                                            (int64_t(plane) * a.Mp + rrow) * 2);
 }
 
-// Writes a staged unit: the thread's activation pairs and, for half 0, its column-scale pair (with sign), in the order
-// the MFMA operands read them. Batch rows b >= B hold row B-1's values: MFMA output column b depends on activation
-// column b only, and columns >= B are never stored.
+// LDS address (bytes) of a pointer into the workgroup's LDS.
+__device__ __forceinline__ uint32_t mf_lds_addr(const uint32_t* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const uint32_t*)(p)));
+}
+
+// Copies the activation image of super-chunk sc (mf_img<BP>() dwords) into the LDS staging area dst, LDS-direct: the
+// image's 1 KB requests are dealt round-robin to the four wavefronts (request r: image dwords 256 r .. 256 r + 255,
+// lane l's 16 bytes written at dst + 256 r + 4 l). M0 holds the request's LDS address (one wait state between its
+// write and the load). Returns nothing to registers; the caller waits with vmcnt before the data is read.
 template <int BP>
-__device__ __forceinline__ void mf_stage_write(const MfUnitRegs<BP>& u, uint32_t* sx, uint32_t* sa, int t) {
-  const int p = t & 127, hg = p >> 4, j = p & 15, q = j >> 2, k = j & 3, half = t >> 7;
-  uint32_t* dst = sx + (hg * 4 + q) * mf_xstride<BP>() + k + 4 * (BP / 2) * half;
+__device__ __forceinline__ void mf_issue_image(const GemmArgs& a, int sc, uint32_t* dst, int wave, int lane) {
+  constexpr int NI = mf_img<BP>() / 256;
+  const uint32_t* src = a.img + int64_t(sc) * mf_img<BP>() + 4 * lane;
 #pragma unroll
-  for (int b = 0; b < BP / 2; ++b) dst[4 * b] = __builtin_bit_cast(uint32_t, mf_u16x2{u.xv[2 * b], u.xv[2 * b + 1]});
-  if (half == 0) sa[hg * 16 + j] = (u.meta[0] >> 16) | (u.meta[1] & 0xFFFF0000u);
+  for (int i = 0; i < (NI + 3) / 4; ++i) {
+    const int r = 4 * i + wave;
+    if (r < NI)
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                   :
+                   : "s"(mf_lds_addr(dst + 256 * r)), "v"(src + 256 * r)
+                   : "memory");
+  }
 }
 
 // 64-bit left shift by a constant, as one v_lshlrev_b64: it shifts two 32-bit words in the time a 32-bit shift takes
@@ -199,16 +238,18 @@ __device__ __forceinline__ void mf_stage_signs(const MfUnitRegs<BP>& u, uint32_t
 }
 
 // Multiplies one staged unit into the accumulators of its NBT 16-row batch tiles. xs/as: the unit's staged activation
-// (batch tile bt at 64 bt dwords of each block) and column-scale pairs;
+// (batch tile bt at 64 bt dwords of each block) and column-scale pairs. With BP < 16 a block holds BP rows, and lanes
+// of MFMA batch columns >= BP read the next block's dwords: those columns of the product are never stored, and each
+// column of an MFMA result depends on that column of its B operand only.
 // scr: the wavefront's scratch of the unit (mf_stage_signs). wa[par][c]: dword offset, within a chunk's entries, of
 // word c of the two a lane reads from its row of block 0 (row blocks of parity par; block rb adds 64 rb). Reading the
 // words separately, with the index wrapped within the entry, needs no copy of an entry's first words after it, and
 // the 64 lanes of one read hit 64 different banks: lane (r, g) reads bank 4r + (its word index), and the word indices
 // of one r are a permutation of 0..3 over g.
-template <int NBT>
+template <int BP, int NBT = mf_nbt<BP>()>
 __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, const uint32_t* scr, int r16, int g,
                                         const uint32_t (&wa)[2][2], uint32_t sh, float (&acc)[NBT][4][4]) {
-  constexpr int XS = 64 * NBT + 4;
+  constexpr int XS = mf_xstride(BP);
   const uint32_t* srs = scr + kMfScr;
   uint32_t w[2][4];
 #pragma unroll
@@ -306,6 +347,7 @@ __device__ __forceinline__ void mf_tile_end(const GemmArgs& a, int tile, bool sh
 
 template <int BP, int MU, int D>
 struct MfKernel {
+  static constexpr int IMG = mf_img<BP>();
   struct State {
     int n;
     int first_tile, last_tile;
@@ -313,7 +355,8 @@ struct MfKernel {
     int n_pending;
     MfCursor cur;    // unit K
     MfCursor nxt;    // unit K + D (clamped to the last unit of the range)
-    int stg_sc;      // super-chunk of unit K + D + 1 (clamped), whose metadata is requested next
+    int img_sc;      // copying images: super-chunk of unit K + 1, whose activation image is copied next
+    int stg_sc;      // gathering: super-chunk of unit K + D + 1 (clamped), whose metadata is requested next
     float acc[mf_nbt<BP>()][4][4];
   };
 
@@ -325,36 +368,54 @@ struct MfKernel {
 
   // Unit K of the workgroup (compile-time K < kMfMaxUnits; the launch plan keeps the range within that), with
   // register set K mod (D + 1). Fully unrolled, so no loads are carried through a loop header.
-  // Order: request unit K+D (activations, then signs and row scales) and the metadata of unit K+D+1; stage unit K+1
-  // (requested D-1 units ago: activations to the workgroup's staging area, signs and row scales to the wavefront's
-  // scratch of K+1, so that its registers are free during the multiplication); multiply unit K (staged one unit ago);
-  // end a tile (transposing through unit K's scratch, now read).
+  // Order: copy unit K+1's activation image into its staging buffer (free: unit K-1, its last reader, ended at the
+  // previous barrier); request unit K+D's signs and row scales; stage unit K+1's signs and row scales (requested D-1
+  // units ago) to the wavefront's scratch of K+1, so that their registers are free during the multiplication; multiply
+  // unit K; end a tile (transposing through unit K's scratch, now read); wait for this step's image copy, then meet at
+  // the barrier.
+  // Gathering: request unit K+D's activations (metadata requested one unit earlier), signs and row scales, and the
+  // metadata of unit K+D+1; stage unit K+1's activations, signs and row scales (requested D-1 units ago); multiply unit
+  // K; end a tile; meet at the barrier.
   template <int K>
   __device__ static __forceinline__ void step(const GemmArgs& a, State& s, MfUnitRegs<BP> (&ur)[D + 1],
-                                              uint32_t (&meta_next)[2], const int* s_planes, uint32_t* sx,
-                                              uint32_t* sa, uint32_t* scr, const Lane& ln,
-                                              const MfXRows<BP>& rx) {
+                                              uint32_t (&meta_next)[2], const int* s_planes, uint32_t* ubuf,
+                                              uint32_t* scr, const Lane& ln, const MfXRows<BP>& rx) {
     if constexpr (K < kMfMaxUnits) {
       if (K >= s.n) return;
       constexpr int PN = (K + D) % (D + 1);
       constexpr int PS = (K + 1) % (D + 1);
-      {
+      if constexpr (mf_gather<BP>()) {
         const int kd = K + D < s.n ? K + D : s.n - 1;
         ur[PN].meta[0] = meta_next[0];
         ur[PN].meta[1] = meta_next[1];
-        mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kd], s_planes[2 * kd + 1], ln.wave, ln.lane, rx, ur[PN]);
+        mf_issue_x<BP>(rx, ur[PN]);
+        mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kd], s_planes[2 * kd + 1], ln.wave, ln.lane, ur[PN]);
         mf_load_meta(a, s.stg_sc, ln.t, meta_next);
         if (K + D + 1 < s.n) mf_advance(a, s.nxt);
         if (K + D + 2 < s.n && ++s.stg_sc == a.steps) s.stg_sc = 0;
+        __builtin_amdgcn_sched_barrier(0);
+        if (K + 1 < s.n) {
+          uint32_t* nb = ubuf + ((K + 1) & 1) * IMG;
+          mf_stage_write<BP>(ur[PS], nb, nb + mf_xunit<BP>(), ln.t);
+          mf_stage_signs<BP>(ur[PS], scr + ((K + 1) & 1) * kMfScrUnit, ln.lane);
+        }
+      } else {
+        if (K + 1 < s.n) {
+          mf_issue_image<BP>(a, s.img_sc, ubuf + ((K + 1) & 1) * IMG, ln.wave, ln.lane);
+          if (++s.img_sc == a.steps) s.img_sc = 0;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        {
+          const int kd = K + D < s.n ? K + D : s.n - 1;
+          mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kd], s_planes[2 * kd + 1], ln.wave, ln.lane, ur[PN]);
+          if (K + D + 1 < s.n) mf_advance(a, s.nxt);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (K + 1 < s.n) mf_stage_signs<BP>(ur[PS], scr + ((K + 1) & 1) * kMfScrUnit, ln.lane);
       }
       __builtin_amdgcn_sched_barrier(0);
-      if (K + 1 < s.n) {
-        mf_stage_write<BP>(ur[PS], sx + ((K + 1) & 1) * mf_xunit<BP>(), sa + ((K + 1) & 1) * kMfAUnit, ln.t);
-        mf_stage_signs<BP>(ur[PS], scr + ((K + 1) & 1) * kMfScrUnit, ln.lane);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      mf_unit<mf_nbt<BP>()>(sx + (K & 1) * mf_xunit<BP>(), sa + (K & 1) * kMfAUnit, scr + (K & 1) * kMfScrUnit, ln.r16, ln.g, ln.wa,
-              ln.sh, s.acc);
+      const uint32_t* ub = ubuf + (K & 1) * IMG;
+      mf_unit<BP>(ub, ub + mf_xunit<BP>(), scr + (K & 1) * kMfScrUnit, ln.r16, ln.g, ln.wa, ln.sh, s.acc);
       if (s.cur.sc == a.steps - 1 || K + 1 == s.n) {
         const int tile = s.cur.tile;
         const bool shared = tile == s.first_tile ? s.first_shared : (tile == s.last_tile && s.last_shared);
@@ -369,17 +430,55 @@ struct MfKernel {
             for (int v = 0; v < 4; ++v) s.acc[bt][rb][v] = 0.f;
       }
       mf_advance(a, s.cur);
+      // copying images: every vector memory operation but the last three (unit K+D's sign and row-scale requests, or
+      // tile-end stores issued after them) has completed, so this step's image copy has landed
+      if constexpr (!mf_gather<BP>()) asm volatile("s_waitcnt vmcnt(3)" ::: "memory");
       __syncthreads();
-      step<K + 1>(a, s, ur, meta_next, s_planes, sx, sa, scr, ln, rx);
+      step<K + 1>(a, s, ur, meta_next, s_planes, ubuf, scr, ln, rx);
     }
   }
 };
 
+// Activation images of every super-chunk for one call (the first of the two kernels; grid IMG / 256 x NSC): image dword
+// d of super-chunk sc is what the staging area of a unit of sc holds at d. Activation part (d < mf_xunit): block
+// (h g, q) = d / XS, offset o = d mod XS; o < 4 BP is batch row o / 4, pair k = o mod 4 of K step q: the fp16 pair
+// (x[row][xidx[v]], x[row][xidx[v + 16]]) of virtual column v = 256 sc + 32 (h g) + 4 q + k, zero for a column with no
+// source or a row >= B; padding dwords are zero. Column-scale part: dword 16 (h g) + j holds the signed column scales
+// of columns 32 (h g) + j and that + 16.
+template <int BP>
+__global__ void __launch_bounds__(256) k_mf_image(GemmArgs a) {
+  constexpr int XS = mf_xstride(BP);
+  constexpr int XU = 2 * 4 * 4 * XS;
+  constexpr int IMG = mf_img<BP>();
+  const int sc = blockIdx.y;
+  const int d = blockIdx.x * 256 + threadIdx.x;
+  const int64_t v0 = int64_t(sc) * 256;
+  uint32_t v = 0u;
+  if (d < XU) {
+    const int blk = d / XS;
+    const int o = d - blk * XS;
+    const int row = o >> 2;
+    if (o < 4 * BP && row < a.B) {
+      const int c = 32 * (blk >> 2) + 4 * (blk & 3) + (o & 3);
+      const uint32_t i0 = a.xidx[v0 + c], i1 = a.xidx[v0 + c + 16];
+      const uint16_t* xr = a.x + int64_t(row) * a.ldx;
+      const uint32_t x0 = i0 == 0xFFFFu ? 0u : xr[i0];
+      const uint32_t x1 = i1 == 0xFFFFu ? 0u : xr[i1];
+      v = x0 | (x1 << 16);
+    }
+  } else if (d < XU + kMfAUnit) {
+    const int e = d - XU;
+    const int c = 32 * (e >> 4) + (e & 15);
+    v = uint32_t(a.colscale[v0 + c]) | (uint32_t(a.colscale[v0 + c + 16]) << 16);
+  }
+  a.img[int64_t(sc) * IMG + d] = v;
+}
+
 template <int BP, int MU, int D, bool R2>
-__global__ void __launch_bounds__(kMfNT, BP > 16 ? 2 : ((BP <= 4 && D == 2 && R2) ? 4 : 3)) k_gemm_mfma(GemmArgs a) {
+__global__ void __launch_bounds__(kMfNT, mf_gather<BP>() ? ((BP <= 4 && D == 2 && R2) ? 4 : 3) : (BP > 16 ? 2 : 4))
+    k_gemm_mfma(GemmArgs a) {
   using K = MfKernel<BP, MU, D>;
-  __shared__ __attribute__((aligned(16))) uint32_t sx[2 * mf_xunit<BP>()];
-  __shared__ __attribute__((aligned(16))) uint32_t sa[2 * kMfAUnit];
+  __shared__ __attribute__((aligned(16))) uint32_t ubuf[2 * K::IMG];
   __shared__ __attribute__((aligned(16))) uint32_t scr_all[4 * kMfScrWave];
   __shared__ int s_planes[2 * kMfMaxUnits];
   __shared__ int s_flag;
@@ -387,7 +486,7 @@ __global__ void __launch_bounds__(kMfNT, BP > 16 ? 2 : ((BP <= 4 && D == 2 && R2
   typename K::Lane ln;
   ln.t = threadIdx.x;
   ln.lane = ln.t & 63;
-  ln.wave = ln.t >> 6;
+  ln.wave = __builtin_amdgcn_readfirstlane(ln.t >> 6);
   ln.r16 = ln.lane & 15;
   ln.g = ln.lane >> 4;
   // Words of a row's entry that hold canonical bits 32g..32g+31: they start at stored bit (32g - R) mod 128;
@@ -422,36 +521,26 @@ __global__ void __launch_bounds__(kMfNT, BP > 16 ? 2 : ((BP <= 4 && D == 2 && R2
 #pragma unroll
       for (int v = 0; v < 4; ++v) s.acc[bt][rb][v] = 0.f;
 
-  // Row-scale planes of the range's chunks (the launch plan keeps n <= kMfMaxUnits), and metadata of units 0..D.
+  // Row-scale planes of the range's chunks (the launch plan keeps n <= kMfMaxUnits).
   if (ln.t < 2 * s.n) {
     int sc = s.cur.sc + (ln.t >> 1);
     while (sc >= a.steps) sc -= a.steps;
     s_planes[ln.t] = a.chunk_plane[2 * sc + (ln.t & 1)];
   }
-  // The thread's batch rows of x: half t >> 7 of the padded batch (wave-uniform; rows >= B read row B-1).
+  MfUnitRegs<BP> ur[D + 1];
+  uint32_t meta_next[2];
   MfXRows<BP> rx;
-  const int half = __builtin_amdgcn_readfirstlane(ln.t >> 7);
-  if constexpr (MfXRows<BP>::kOne) {
-    const int b0 = (BP / 2) * half < a.B ? (BP / 2) * half : a.B - 1;
-    const int b1 = (BP / 2) * half + BP / 2 - 1 < a.B ? (BP / 2) * half + BP / 2 - 1 : a.B - 1;
-    rx.r[0] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.x + int64_t(b0) * a.ldx), 0,
-                                                int((int64_t(b1 - b0) * a.ldx + a.N) * 2), 0x00020000);
-#pragma unroll
-    for (int i = 0; i < BP / 2; ++i) {
-      const int b = (BP / 2) * half + i;
-      rx.soff[i] = int(int64_t((b < a.B ? b : a.B - 1) - b0) * a.ldx * 2);
-    }
-  } else {
+  s.nxt = s.cur;
+  if constexpr (mf_gather<BP>()) {
+    // the thread's batch rows of x: half t >> 7 of the padded batch (wave-uniform; rows >= B read row B-1)
+    const int half = __builtin_amdgcn_readfirstlane(ln.t >> 7);
 #pragma unroll
     for (int i = 0; i < BP / 2; ++i) {
       const int b = (BP / 2) * half + i;
       rx.r[i] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.x + int64_t(b < a.B ? b : a.B - 1) * a.ldx),
                                                   0, 2 * a.N, 0x00020000);
     }
-  }
-  MfUnitRegs<BP> ur[D + 1];
-  uint32_t meta_next[2];
-  {
+    // metadata of units 0..D
     int sc = s.cur.sc;
 #pragma unroll
     for (int k = 0; k <= D; ++k) {
@@ -459,21 +548,35 @@ __global__ void __launch_bounds__(kMfNT, BP > 16 ? 2 : ((BP <= 4 && D == 2 && R2
       if (k + 1 < s.n && ++sc == a.steps) sc = 0;
     }
     s.stg_sc = sc;   // unit D + 1 (clamped)
-  }
-  // Staged rows of batch rows >= BP stay zero for the whole launch.
-  for (int i = ln.t; i < 2 * mf_xunit<BP>(); i += kMfNT) sx[i] = 0u;
-  __syncthreads();   // planes in LDS; zero fill done before any staged value is written
-  s.nxt = s.cur;
+    __syncthreads();   // planes in LDS
 #pragma unroll
-  for (int k = 0; k < D; ++k) {
-    const int kk = k < s.n ? k : s.n - 1;
-    mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kk], s_planes[2 * kk + 1], ln.wave, ln.lane, rx, ur[k]);
-    if (k + 1 < s.n) mf_advance(a, s.nxt);
+    for (int k = 0; k < D; ++k) {
+      const int kk = k < s.n ? k : s.n - 1;
+      mf_issue_x<BP>(rx, ur[k]);
+      mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kk], s_planes[2 * kk + 1], ln.wave, ln.lane, ur[k]);
+      if (k + 1 < s.n) mf_advance(a, s.nxt);
+    }
+    mf_stage_write<BP>(ur[0], ubuf, ubuf + mf_xunit<BP>(), ln.t);
+    mf_stage_signs<BP>(ur[0], scr, ln.lane);
+  } else {
+    __syncthreads();   // planes in LDS
+    // unit 0's image, then the signs and row scales of units 0..D-1
+    mf_issue_image<BP>(a, s.cur.sc, ubuf, ln.wave, ln.lane);
+    s.img_sc = s.cur.sc + 1 == a.steps ? 0 : s.cur.sc + 1;
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      const int kk = k < s.n ? k : s.n - 1;
+      mf_issue<BP, MU>(a, s.nxt, s_planes[2 * kk], s_planes[2 * kk + 1], ln.wave, ln.lane, ur[k]);
+      if (k + 1 < s.n) mf_advance(a, s.nxt);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mf_stage_signs<BP>(ur[0], scr, ln.lane);
+    // units 0..D-1 requested after the image: all but their last three requests complete means the image has landed
+    asm volatile("s_waitcnt vmcnt(3)" ::: "memory");
   }
-  mf_stage_write<BP>(ur[0], sx, sa, ln.t);
-  mf_stage_signs<BP>(ur[0], scr, ln.lane);
   __syncthreads();
-  K::template step<0>(a, s, ur, meta_next, s_planes, sx, sa, scr, ln, rx);
+  K::template step<0>(a, s, ur, meta_next, s_planes, ubuf, scr, ln, rx);
   if constexpr (!R2) {
     const int pend0 = s.first_shared ? s.first_tile : s.last_tile;
     publish_pending<kMfNT, 1, BP>(a, pend0, s.last_tile, s.n_pending, &s_flag);
@@ -482,6 +585,10 @@ __global__ void __launch_bounds__(kMfNT, BP > 16 ? 2 : ((BP <= 4 && D == 2 && R2
 
 template <int BP, int D, bool R2>
 bool launch_mfma_bp(const GemmArgs& a, int mu, hipStream_t stream) {
+  if (mu != 8 && mu != 4) return false;
+  if constexpr (!mf_gather<BP>())
+    hipLaunchKernelGGL((k_mf_image<BP>), dim3(unsigned(mf_img<BP>() / 256), unsigned(a.NSC)), dim3(256), 0, stream,
+                       a);
   const dim3 grid(unsigned(a.blocks)), block(kMfNT);
   if (mu == 8)
     hipLaunchKernelGGL((k_gemm_mfma<BP, 8, D, R2>), grid, block, 0, stream, a);

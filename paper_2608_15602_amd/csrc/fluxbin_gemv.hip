@@ -1169,6 +1169,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   a.y = d_y;
   a.counters = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + p.ws_counters_off);
   a.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(d_ws) + p.ws_partials_off);
+  a.img = p.kernel == 3 ? reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + p.ws_image_off) : nullptr;
   a.ldx = ldx;
   a.ldy = ldy;
   a.units = int32_t(p.units);

@@ -213,15 +213,13 @@ static uint64_t layer_counter_bytes(int64_t M) {
 }
 
 // Rows of a full batch tile (calls with more batch rows run as several launches): 32 on layers the matrix-core kernel
-// takes (one row scale per chunk), whose sign decode then serves two 16-row MFMA tiles, else 16. The 32-row kernel
-// reads a thread's 16 batch rows of x through one buffer resource: the span of 15 rows of ldx elements plus N must stay
-// below 2^31 bytes (ldx < 0: not known yet). FLUXBIN_BATCH_TILE=16 keeps 16-row tiles.
-static int batch_tile_rows(const fluxbin_layer& L, int64_t ldx, const fluxbin_tuning& tu) {
+// takes (one row scale per chunk), whose sign decode then serves two 16-row MFMA tiles, else 16.
+// FLUXBIN_BATCH_TILE=16 keeps 16-row tiles.
+static int batch_tile_rows(const fluxbin_layer& L, const fluxbin_tuning& tu) {
   const Derived dv = derive(L.shape);
   if (tu.generic || dv.Gcg > 1 || dv.Gcs > 1 || tu.mfma == 0 || tu.mfma_depth == 3 || tu.mfma_r2 == 0 ||
       tu.batch_tile == kMaxBatch)
     return kMaxBatch;
-  if (ldx >= 0 && (int64_t(kMaxBatchMfma / 2 - 1) * ldx + L.shape.N) * 2 >= (int64_t(1) << 31)) return kMaxBatch;
   return kMaxBatchMfma;
 }
 
@@ -230,7 +228,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
   std::memset(p, 0, sizeof(*p));
   const fluxbin_tuning tu = tuning_snapshot();
-  if (B < 1 || (B > kMaxBatch && batch_tile_rows(L, -1, tu) < B))
+  if (B < 1 || (B > kMaxBatch && batch_tile_rows(L, tu) < B))
     return fail(FLUXBIN_ERR_UNSUPPORTED, "no launch plan for %d batch rows in one launch on this layer", B);
   const int force_generic = tu.generic;
   const int rpt_env = tu.rpt;
@@ -413,6 +411,10 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     return fail(FLUXBIN_ERR_UNSUPPORTED, "launch plan needs %llu bytes of tile counters, the layer's region holds %llu",
                 (unsigned long long)counter_bytes, (unsigned long long)p->ws_partials_off);
   p->ws_bytes = p->ws_partials_off + uint64_t(p->blocks) * 2u * uint64_t(p->rows) * uint64_t(p->bpad) * 4u;
+  if (p->kernel == 3 && p->bpad > 8) {   // the activation images of every super-chunk, written by a first kernel
+    p->ws_image_off = round_up256(p->ws_bytes);
+    p->ws_bytes = p->ws_image_off + uint64_t(L.NSC) * uint64_t(mf_image_dwords(p->bpad)) * 4u;
+  }
   return FLUXBIN_OK;
 }
 
@@ -607,18 +609,10 @@ fluxbin_status fluxbin_workspace_query(const fluxbin_layer* layer, int32_t B, si
   if (st != FLUXBIN_OK) return st;
   if (!bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "bytes is NULL");
   if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
-  // the call's ldx decides the tile rows (batch_tile_rows): room for either choice
-  const fluxbin_tuning tu = tuning_snapshot();
   BatchTiles bt;
-  st = batch_tiles(*layer, B, batch_tile_rows(*layer, -1, tu), &bt);
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot()), &bt);
   if (st != FLUXBIN_OK) return st;
-  uint64_t ws = bt.ws_bytes;
-  if (bt.tile != kMaxBatch) {
-    st = batch_tiles(*layer, B, kMaxBatch, &bt);
-    if (st != FLUXBIN_OK) return st;
-    if (bt.ws_bytes > ws) ws = bt.ws_bytes;
-  }
-  *bytes = static_cast<size_t>(ws);
+  *bytes = static_cast<size_t>(bt.ws_bytes);
   return FLUXBIN_OK;
 }
 
@@ -644,7 +638,7 @@ static fluxbin_status gemm_common(const fluxbin_layer* layer, int32_t B, const u
   const size_t yb = (size_t(B - 1) * ldy + s.M) * (y_is_fp32 ? 4 : 2);
   if (ranges_overlap(d_x, xb, d_y, yb)) return fail(FLUXBIN_ERR_INVALID_ARG, "x and y overlap");
   BatchTiles bt;
-  st = batch_tiles(*layer, B, batch_tile_rows(*layer, ldx, tuning_snapshot()), &bt);
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot()), &bt);
   if (st != FLUXBIN_OK) return st;
   if (!d_ws) return fail(FLUXBIN_ERR_INVALID_ARG, "workspace is NULL");
   if (ws_bytes < bt.ws_bytes)
@@ -743,8 +737,8 @@ fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin
   if (st != FLUXBIN_OK) return st;
   if (!out) return fail(FLUXBIN_ERR_INVALID_ARG, "out is NULL");
   if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
-  BatchTiles bt;   // for contiguous x (ldx = N)
-  st = batch_tiles(*layer, B, batch_tile_rows(*layer, layer->shape.N, tuning_snapshot()), &bt);
+  BatchTiles bt;
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot()), &bt);
   if (st != FLUXBIN_OK) return st;
   const Plan& p = bt.n_full > 0 ? bt.full : bt.tail;
   std::memset(out, 0, sizeof(*out));

@@ -20,6 +20,12 @@ constexpr int kRwSteps = 16;            // row-complete batch-1 kernel: super-ch
 constexpr int b1_max_units(int nt) { return nt == 1024 ? 16 : 12; }
 constexpr int kBatMaxUnits = 12;        // units per workgroup of the small-batch mu = 8 kernel (its LDS index table)
 constexpr int kMfMaxUnits = 16;         // units per workgroup of the matrix-core small-batch kernel (unrolled steps)
+// Matrix-core kernel with bp padded batch rows (4, 8, 16 or 32): dwords per (chunk, column group, K step) block of a
+// unit's staged activation pairs (bp rows x 4 pairs, and 4 dwords of padding so that the 64 dwords one wavefront's
+// gathering threads write land in 64 different banks), and dwords of a super-chunk's activation image (the 32 blocks
+// and the 128 column-scale pairs, rounded up to whole 1 KB LDS-direct requests).
+constexpr int mf_xstride(int bp) { return 4 * bp + 4; }
+constexpr int mf_image_dwords(int bp) { return (32 * mf_xstride(bp) + 128 + 255) / 256 * 256; }
 // Tile counters of the split-tile reduction sit kCounterStride 32-bit words (256 bytes) apart: every workgroup
 // publishes at the end of a launch, and device-scope atomics on one memory line are serialized (densely packed
 // counters cost the batch-1 GEMV on 8192 x 28672 layers 0.3-0.5 us).
@@ -124,6 +130,7 @@ struct Plan {
   bool early;       // batch-1 kernel: request sign data before staging the activations (small layers)
   bool reduce2;     // matrix-core kernel: split tiles reduced by a second kernel over the whole chip
   uint64_t ws_counters_off, ws_partials_off, ws_bytes;
+  uint64_t ws_image_off;   // matrix-core kernel: activation images after the partial sums (0 for other kernels)
 };
 
 fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p);
