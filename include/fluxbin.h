@@ -183,9 +183,11 @@ fluxbin_status fluxbin_layer_from_header(const void* header_host, void* d_packed
                                          fluxbin_layer* out);
 
 /*
- * Workspace for split reductions of one GEMV/GEMM call with batch B (1..8192): partial sums of output rows and one
- * 32-bit counter per row tile. Before its first use the workspace must be zero-filled (fluxbin_workspace_init); every
- * call leaves the counters at zero again. Calls sharing a workspace must not overlap in time.
+ * Workspace of one GEMV/GEMM call with batch B (1..8192): partial sums of output rows and one 32-bit counter per row
+ * tile for split reductions, and for matrix-core launches of 16 or 32 rows the call's staged activations (one image
+ * per super-chunk, rewritten by every call). Before its first use the workspace must be zero-filled
+ * (fluxbin_workspace_init); every call leaves the counters at zero again. Calls sharing a workspace must not overlap
+ * in time.
  * The counters sit in a region of the same size for every batch size of a layer, so calls of one layer with any
  * B may share one workspace (of the size queried for the largest B). A workspace used for another layer must first
  * be zero-filled again: the other layer's partial sums may cover this layer's counters.

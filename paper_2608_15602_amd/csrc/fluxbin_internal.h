@@ -116,7 +116,7 @@ fluxbin_status hip_fail(int hip_error, const char* what);
 // ---- launch plan of the GEMV/GEMM kernels ----
 struct Plan {
   int kernel;       // 0 = batch-1 super-chunk kernel (mu 8 or 4), 1 = generic (any mu, any batch), 2 = mu8 batch 2..16,
-                    // 3 = matrix-core small batch (mu 8 or 4, batch 2..16), 4 = row-complete batch-1 (few rows)
+                    // 3 = matrix-core small batch (mu 8 or 4, batch 2..32), 4 = row-complete batch-1 (few rows)
   int nt;           // threads per block
   int rpt;          // rows per thread
   int rows;         // rows per tile (nt * rpt)
