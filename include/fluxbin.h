@@ -258,10 +258,12 @@ fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16
  *                                         -1: chosen by layer size
  *   batch_tile     FLUXBIN_BATCH_TILE     16: batch tiles of 16 rows on every layer; 0: 32 where the matrix-core
  *                                         kernel takes the layer
+ *   mfma_rows      FLUXBIN_MFMA_ROWS      B = 2..8: 1 the row-complete matrix-core kernel wherever it fits, 0 never;
+ *                                         -1: chosen by layer size
  */
 typedef struct {
   int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2, rows,
-      batch_tile;
+      batch_tile, mfma_rows;
 } fluxbin_tuning;
 fluxbin_status fluxbin_get_tuning(fluxbin_tuning* out);
 fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
@@ -269,7 +271,8 @@ fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
 /*
  * The launch plan a GEMV/GEMM call of batch B on this layer would use on the current device with the current tuning.
  *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel,
- *           4: row-complete batch-1 kernel (layers with few rows).
+ *           4: row-complete batch-1 kernel (layers with few rows), 5: row-complete matrix-core kernel (layers with few
+ *           rows, B = 2..8).
  * Batches of more than batch_tile_rows rows (32 on layers the matrix-core kernel takes, else 16) run as batch_tiles
  * launches; the plan is then that of the full batch tiles, and workspace_bytes the call's workspace. Host only apart
  * from reading the device's CU count; launches nothing.

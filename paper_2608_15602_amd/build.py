@@ -28,7 +28,7 @@ SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=und
 
 SOURCES = ["fluxbin_host.cpp", "fluxbin_pack.hip", "fluxbin_gemv.hip", "fluxbin_gemm_batch.hip",
            "fluxbin_gemm_mfma.hip", "fluxbin_rc.hip", "fluxbin_noalloc.hip",
-           "fluxbin_gemv_rows.hip"]
+           "fluxbin_gemv_rows.hip", "fluxbin_gemm_mfma_rows.hip"]
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are kept out of the generated code (plain float code only).

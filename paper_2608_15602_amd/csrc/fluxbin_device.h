@@ -243,6 +243,9 @@ void launch_reduce_split(const GemmArgs& a, int bp, int R, hipStream_t stream);
 // batch rows, data requested depth (2 or 3) units ahead; with reduce2 (depth 2) the split tiles are reduced by a
 // second kernel instead of the tile counters; false if no instance exists.
 bool launch_gemm_mfma(const GemmArgs& a, int bpad, int mu, int depth, bool reduce2, hipStream_t stream);
+// Row-complete small-batch kernel on the matrix cores (fluxbin_gemm_mfma_rows.hip): 16 rb rows per workgroup of
+// 64 waves threads, bpad = 4 or 8 padded batch rows; false if no instance exists or the layer exceeds its limits.
+bool launch_gemm_mfma_rows(const GemmArgs& a, int bpad, int mu, int waves, int rb, hipStream_t stream);
 
 // Row-complete batch-1 kernel for layers with few rows (fluxbin_gemv_rows.hip): 16 rows per workgroup of `waves`
 // (4, 8 or 16) wavefronts, every super-chunk of them, `depth` (2, 4 or 6) units requested ahead, fg (0, or 8 / 16 fine

@@ -34,9 +34,11 @@
 // 32-bit word of row scales, D units ahead of the unit being multiplied (2 KB of signs per wavefront per unit, no
 // byte requested twice); a wavefront passes the entries to its MFMA lanes through its own LDS scratch.
 // Activations. The B operands of a super-chunk (x gathered through the VCM index table, in the order the MFMA lanes
-// read them, as fp16 pairs) and its signed column-scale pairs do not depend on the row tile, so a first kernel
-// (k_mf_image) writes them once per call, for every super-chunk, to an image in the workspace laid out exactly like
-// the LDS staging area of one unit. The multiplying kernel copies a unit's image into its double-buffered staging
+// read them, as fp16 pairs) and its signed column-scale pairs do not depend on the row tile. Up to 8 batch rows each
+// thread gathers its column pair of a unit itself, with the unit's signs, and writes it to the double-buffered LDS
+// staging area one unit ahead. With 16 and 32 rows those gathers would hold 48 or 96 registers of loads in flight,
+// so a first kernel (k_mf_image) writes the activations once per call, for every super-chunk, to an image in the
+// workspace laid out exactly like the LDS staging area of one unit. The multiplying kernel copies a unit's image into its double-buffered staging
 // area with LDS-direct loads (global_load_lds_dwordx4: 16 bytes per lane written straight to LDS, no registers), one
 // unit ahead, issued before that step's sign requests. Vector memory operations complete in issue order, so waiting
 // until at most the three sign and row-scale requests issued after the copy are outstanding (s_waitcnt vmcnt(3)),

@@ -1169,7 +1169,8 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   a.y = d_y;
   a.counters = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + p.ws_counters_off);
   a.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(d_ws) + p.ws_partials_off);
-  a.img = p.kernel == 3 ? reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + p.ws_image_off) : nullptr;
+  a.img = (p.kernel == 3 || p.kernel == 5) ? reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + p.ws_image_off)
+                                           : nullptr;
   a.ldx = ldx;
   a.ldy = ldy;
   a.units = int32_t(p.units);
@@ -1208,6 +1209,8 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
     ok = !fine && launch_gemm_batch(a, p.n_groups, p.depth, p.bg, p.reduce2, stream);
   } else if (p.kernel == 3) {
     ok = !fine && launch_gemm_mfma(a, p.bpad, int(L.shape.mu), p.depth, p.reduce2, stream);
+  } else if (p.kernel == 5) {
+    ok = !fine && launch_gemm_mfma_rows(a, p.bpad, int(L.shape.mu), p.nt / 64, p.rows / 16, stream);
   } else if (p.kernel == 4) {
     ok = fg >= 0 && launch_gemv_rows(a, int(L.shape.mu), p.nt / 64, p.depth, fg, stream);
   } else if (L.shape.mu == 8) {

@@ -135,6 +135,7 @@ static fluxbin_tuning tuning_defaults() {
   t.bat_r2 = 1;
   t.rows = -1;
   t.batch_tile = 0;
+  t.mfma_rows = -1;
   return t;
 }
 
@@ -165,6 +166,7 @@ static void tuning_init_locked() {
   t.bat_r2 = env_int("FLUXBIN_BAT_R2", t.bat_r2);
   t.rows = env_int("FLUXBIN_ROWS", t.rows);
   t.batch_tile = env_int("FLUXBIN_BATCH_TILE", t.batch_tile);
+  t.mfma_rows = env_int("FLUXBIN_MFMA_ROWS", t.mfma_rows);
   g_tuning = t;
   g_tuning_init = true;
 }
@@ -206,6 +208,37 @@ static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const f
   if (tu.rows == 0 || tu.rows == 1) return tu.rows == 1;
   const int64_t wgs = ceil_div(L.shape.M, 16);
   return wgs <= cus && (L.NSC <= 64 || (L.NSC <= 128 && 4 * wgs <= cus));
+}
+
+// Row-complete matrix-core kernel for B = 2..8 (16 or 32 rows per workgroup, every super-chunk of them, no split
+// tiles): the first fitting shape of 16 wavefronts x 16 rows (one workgroup per CU), 8 wavefronts x 32 rows (two per
+// CU), 16 wavefronts x 32 rows; fitting: the grid within one wave of workgroups, LDS (activation blocks of every
+// column block, column-scale pairs of every chunk, sign scratch) within the CU's 160 KB, at most kMrSteps
+// super-chunks per wavefront, buffer offsets below 2^31. By default only the first shape, on layers of half a
+// workgroup to one workgroup per CU: 7B attention 4096x4096 at B = 2 / 4 / 8 11.1 / 11.3 / 11.6 -> 8.4 / 8.5 / 8.9 us
+// (split-tile matrix-core kernel -> this); the 32-row shapes were slower than the split-tile kernel (7B gate/up
+// 11008x4096 at B = 2: 13.2 -> 15.0 us: four to five units per wavefront, two in flight). FLUXBIN_MFMA_ROWS=0 never,
+// 1 wherever it fits.
+static bool use_mfma_rows(const fluxbin_layer& L, const Derived& dv, int B, int cus, const fluxbin_tuning& tu,
+                          int* waves, int* rb) {
+  if (tu.mfma_rows == 0 || tu.mfma == 0 || tu.generic) return false;
+  const int64_t wgs16 = ceil_div(L.shape.M, 16);
+  if (tu.mfma_rows != 1 && (wgs16 > cus || 2 * wgs16 < cus)) return false;
+  if (dv.NCP * dv.Mp * 16 >= (int64_t(1) << 31) || dv.NRP * dv.Mp * 2 >= (int64_t(1) << 31)) return false;
+  const int bp = B <= 4 ? 4 : 8;
+  const int64_t nblk = dv.ncg + (dv.NCP - L.shape.Kb * dv.ncg);
+  const int64_t dyn = mfma_rows_lds_bytes(dv.NCP, nblk, bp);
+  const int shapes[3][3] = {{16, 1, 1}, {8, 2, 2}, {16, 2, 1}};   // waves, row blocks, workgroups per CU
+  for (const auto& sh : shapes) {
+    const int64_t stat = int64_t(sh[0]) * sh[1] * 1024 + 2 * 2 * sh[0] * kMrSteps * 4;
+    if (L.NSC <= int64_t(sh[0]) * kMrSteps && (stat + dyn) * sh[2] <= 160 * 1024 &&
+        ceil_div(L.shape.M, 16 * sh[1]) <= int64_t(cus) * sh[2]) {
+      *waves = sh[0];
+      *rb = sh[1];
+      return true;
+    }
+  }
+  return false;
 }
 
 static uint64_t layer_counter_bytes(int64_t M) {
@@ -259,6 +292,27 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     p->ws_counters_off = 0;
     p->ws_partials_off = layer_counter_bytes(L.shape.M);
     p->ws_bytes = p->ws_partials_off;   // no workspace of its own: the counter region every plan of the layer keeps
+    return FLUXBIN_OK;
+  }
+  int mr_waves = 0, mr_rb = 0;
+  if (B >= 2 && B <= 8 && !force_generic && !fine && use_mfma_rows(L, dv, B, cus, tu, &mr_waves, &mr_rb)) {
+    // row-complete matrix-core kernel: no split tiles, no second kernel, activations staged once per workgroup
+    p->kernel = 5;
+    p->nt = 64 * mr_waves;
+    p->rpt = 1;
+    p->rows = 16 * mr_rb;
+    p->depth = 2;
+    p->bg = B <= 4 ? 4 : 8;
+    p->n_groups = 1;
+    p->bpad = p->bg;
+    p->n_tiles = ceil_div(L.shape.M, p->rows);
+    p->units = p->n_tiles * L.NSC;
+    p->blocks = p->n_tiles;
+    p->ws_counters_off = 0;
+    p->ws_partials_off = layer_counter_bytes(L.shape.M);
+    p->ws_image_off = p->ws_partials_off;   // no partial sums: the staging image follows the counter region
+    p->ws_bytes = p->ws_image_off +
+                  uint64_t(mfma_rows_image_dwords(dv.NCP, dv.ncg + (dv.NCP - L.shape.Kb * dv.ncg), p->bpad)) * 4u;
     return FLUXBIN_OK;
   }
   if (B == 1 && !force_generic && (!fine || b1_fine_ok)) {   // batch-1 kernel (mu = 8 or 4)

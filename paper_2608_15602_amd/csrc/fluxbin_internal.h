@@ -26,6 +26,20 @@ constexpr int kMfMaxUnits = 16;         // units per workgroup of the matrix-cor
 // and the 128 column-scale pairs, rounded up to whole 1 KB LDS-direct requests).
 constexpr int mf_xstride(int bp) { return 4 * bp + 4; }
 constexpr int mf_image_dwords(int bp) { return (32 * mf_xstride(bp) + 128 + 255) / 256 * 256; }
+// Row-complete matrix-core kernel (small layers, B = 2..8): super-chunks per wavefront (units unrolled), and its
+// dynamic LDS: column-scale pairs of every chunk (64 dwords each), then nblk activation blocks (16 per column block of
+// (4 bp + 4) dwords).
+// The staging image (column-scale pairs, then activation blocks) is copied in whole 1 KB requests, so the LDS holds
+// the image rounded up to 256 dwords, and at least 64 dwords past its end.
+constexpr int kMrSteps = 8;
+constexpr int64_t mfma_rows_image_dwords(int64_t ncp, int64_t nblk, int bp) {
+  return (ncp * 64 + nblk * 16 * (4 * bp + 4) + 255) / 256 * 256;
+}
+constexpr int64_t mfma_rows_lds_bytes(int64_t ncp, int64_t nblk, int bp) {
+  return (ncp * 64 + nblk * 16 * (4 * bp + 4) + 64 > mfma_rows_image_dwords(ncp, nblk, bp)
+              ? ncp * 64 + nblk * 16 * (4 * bp + 4) + 64
+              : mfma_rows_image_dwords(ncp, nblk, bp)) * 4;
+}
 // Tile counters of the split-tile reduction sit kCounterStride 32-bit words (256 bytes) apart: every workgroup
 // publishes at the end of a launch, and device-scope atomics on one memory line are serialized (densely packed
 // counters cost the batch-1 GEMV on 8192 x 28672 layers 0.3-0.5 us).
@@ -116,7 +130,8 @@ fluxbin_status hip_fail(int hip_error, const char* what);
 // ---- launch plan of the GEMV/GEMM kernels ----
 struct Plan {
   int kernel;       // 0 = batch-1 super-chunk kernel (mu 8 or 4), 1 = generic (any mu, any batch), 2 = mu8 batch 2..16,
-                    // 3 = matrix-core small batch (mu 8 or 4, batch 2..32), 4 = row-complete batch-1 (few rows)
+                    // 3 = matrix-core small batch (mu 8 or 4, batch 2..32), 4 = row-complete batch-1 (few rows),
+                    // 5 = row-complete matrix-core small batch (few rows, batch 2..8)
   int nt;           // threads per block
   int rpt;          // rows per thread
   int rows;         // rows per tile (nt * rpt)

@@ -31,7 +31,7 @@ EXPORTS = (
 )
 NOALLOC_SCRATCH_BYTES = 8 << 20
 
-KERNEL_NAMES = {0: "batch1", 1: "generic", 2: "lut_batch", 3: "mfma", 4: "rows"}
+KERNEL_NAMES = {0: "batch1", 1: "generic", 2: "lut_batch", 3: "mfma", 4: "rows", 5: "mfma_rows"}
 
 
 class FluxbinError(RuntimeError):
@@ -64,7 +64,7 @@ class Layer(ctypes.Structure):
 class Tuning(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("nt", "min_units", "blocks", "blocks_per_cu", "depth", "mfma_depth",
                                              "early", "rpt", "mfma", "generic", "mfma_r2", "bat_r2", "rows",
-                                             "batch_tile")]
+                                             "batch_tile", "mfma_rows")]
 
 
 class PlanInfo(ctypes.Structure):

@@ -346,10 +346,12 @@ def test_fp32_output_and_generic_kernel_at_batch1():
     _check(y2, oracle.gemv_dense(L, x), "generic kernel at batch 1")
 
 
-# Small-batch kernels: the matrix-core kernel (FLUXBIN_MFMA=1; the default for mu = 4 and for B > 4), the mu = 8 LUT
-# batch kernel (FLUXBIN_MFMA=0; the default for mu = 8 up to B = 4) and the generic LUT kernel (FLUXBIN_GENERIC=1; with
-# FLUXBIN_MFMA=0 also the mu = 4 small-batch path).
-SMALL_BATCH_KERNELS = {"mfma": {"FLUXBIN_MFMA": "1"}, "lut_batch": {"FLUXBIN_MFMA": "0"},
+# Small-batch kernels: the split-tile matrix-core kernel (FLUXBIN_MFMA=1, FLUXBIN_MFMA_ROWS=0; the default for mu = 4
+# and for B > 4 on larger layers), the row-complete matrix-core kernel (FLUXBIN_MFMA_ROWS=1: B = 2..8 where it fits;
+# the default on layers with few rows), the mu = 8 LUT batch kernel (FLUXBIN_MFMA=0; the default for mu = 8 up to B = 4
+# on large layers) and the generic LUT kernel (FLUXBIN_GENERIC=1; with FLUXBIN_MFMA=0 also the mu = 4 small-batch path).
+SMALL_BATCH_KERNELS = {"mfma": {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0"}, "mfma_rows": {"FLUXBIN_MFMA_ROWS": "1"},
+                       "lut_batch": {"FLUXBIN_MFMA": "0"},
                        "generic": {"FLUXBIN_GENERIC": "1"}}
 
 
@@ -370,6 +372,46 @@ def test_batch_rows_equal_batch1(B, mu, kernel):
     tile, B not a multiple of four)."""
     spec = LayerSpec("bat", M=1536, N=2048, Kb=2, Ks=1, mu=mu, S=61, g_r=128, g_s=61, seed=22)
     _with_env(SMALL_BATCH_KERNELS[kernel], lambda: _parity(spec, B, out_fp32=True))
+
+
+MR_SPECS = [
+    LayerSpec("mr_mu8", M=1000, N=1000, Kb=2, Ks=1, mu=8, S=40, g_r=128, g_s=40, seed=81),
+    LayerSpec("mr_mu4", M=700, N=2048, Kb=3, Ks=1, mu=4, S=33, g_r=128, g_s=33, seed=82),
+    LayerSpec("mr_1base_32rows", M=4100, N=640, Kb=1, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=83),
+    LayerSpec("mr_mu4_32rows", M=5000, N=700, Kb=2, Ks=1, mu=4, S=20, g_r=128, g_s=20, seed=84),
+]
+
+
+@pytest.mark.parametrize("B", [2, 3, 5, 8])
+@pytest.mark.parametrize("spec", MR_SPECS, ids=lambda s: s.name)
+def test_mfma_rows_kernel_matches_oracle(spec, B):
+    """The row-complete matrix-core kernel (16 or 32 rows per workgroup, every super-chunk of them): every row and
+    batch row against the oracle on ragged layers (M and N not multiples of the tiles, one and three bases, salient
+    columns or none, mu 8 and 4), bitwise repeatable, and within tolerance of the split-tile matrix-core kernel."""
+    from paper_2608_15602_amd import fluxbin as fb
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    env = SMALL_BATCH_KERNELS["mfma_rows"]
+    info = _with_env(env, lambda: fb.fluxbin_plan_query(packed, B))
+    assert info["kernel_name"] == "mfma_rows", info
+    assert info["rows_per_tile"] == (16 if -(-spec.M // 16) <= 256 else 32), info
+    _, _, x, y = _with_env(env, lambda: _parity(spec, B, packed=packed, L=L, out_fp32=True))
+    assert np.array_equal(_with_env(env, lambda: run_gemm(packed, x, out_fp32=True)), y), "repeat differs"
+    y_split = _with_env(SMALL_BATCH_KERNELS["mfma"], lambda: run_gemm(packed, x, out_fp32=True))
+    _check(y, y_split, "row-complete vs split-tile matrix-core kernel")
+
+
+@pytest.mark.parametrize("B", [2, 8])
+def test_mfma_rows_kernel_7b_layers_full_size(B):
+    """The 7B attention and MLP layers at full size with the default plan at B = 2 and 8 (the row-complete matrix-core
+    kernel where it fits): sampled rows against the oracle."""
+    from paper_2608_15602_amd import fluxbin as fb
+    for spec in config_layers("c2_attn7b", "128") + config_layers("c3_mlp7b", "128"):
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        log(f"plan {spec.name} B={B}: {fb.fluxbin_plan_query(packed, B)['kernel_name']}")
+        _parity(spec, B, rows=sample_rows(spec.M, 256, seed=B), packed=packed, L=L)
+        del packed
 
 
 PREFILL_SPECS = [
@@ -628,7 +670,7 @@ def test_mfma_second_kernel_reduction_equals_counters(B, mu):
     L = make_layer(spec)
     packed = pack_layer(L)
     x = make_activations(L, B)
-    env = {"FLUXBIN_MFMA": "1"}
+    env = {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0"}
     y_c = _with_env({**env, "FLUXBIN_MFMA_R2": "0"},
                     lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
     y_r = _with_env({**env, "FLUXBIN_MFMA_R2": "1"},
@@ -682,7 +724,7 @@ def _subnormal_case(which, mu):
     return L, x
 
 
-@pytest.mark.parametrize("kernel", ["batch1", "rows", "lut_batch", "mfma"])
+@pytest.mark.parametrize("kernel", ["batch1", "rows", "lut_batch", "mfma", "mfma_rows"])
 @pytest.mark.parametrize("which", ["colscale", "rowscale", "x"])
 def test_fp16_subnormals_are_honoured(which, kernel):
     """Subnormal fp16 column scales, row scales or activations (the reading that subnormals are honoured on both
@@ -692,8 +734,9 @@ def test_fp16_subnormals_are_honoured(which, kernel):
     L, x = _subnormal_case(which, 8)
     packed = pack_layer(L)
     env = {"batch1": {"FLUXBIN_ROWS": "0"}, "rows": {"FLUXBIN_ROWS": "1"}, "lut_batch": {"FLUXBIN_MFMA": "0"},
-           "mfma": {"FLUXBIN_MFMA": "1"}}[kernel]
-    for B in ((1,) if kernel in ("batch1", "rows") else (3, 9) if kernel == "mfma" else (3,)):
+           "mfma": {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0"}, "mfma_rows": {"FLUXBIN_MFMA_ROWS": "1"}}[kernel]
+    for B in ((1,) if kernel in ("batch1", "rows") else (3, 9) if kernel == "mfma" else (3, 8) if kernel == "mfma_rows"
+              else (3,)):
         log(f"case subnormal {which} kernel={kernel} B={B}")
         xb = x[:B]
         y = _with_env(env, lambda: run_gemm(packed, xb, out_fp32=True))
@@ -714,7 +757,7 @@ def test_fp16_subnormals_mu4(which):
 
 
 @pytest.mark.parametrize("kernel,B", [("lut_batch", 2), ("lut_batch", 4), ("mfma", 3), ("mfma", 16),
-                                      ("generic", 3)])
+                                      ("mfma_rows", 3), ("mfma_rows", 8), ("generic", 3)])
 def test_small_batch_power_of_two_scaling_is_exact(kernel, B):
     """y(2x) == 2 y(x) bit for bit on the small-batch kernels (scaling by two commutes with every fp32 rounding when
     nothing overflows or underflows), and repeated calls are bitwise equal."""
@@ -723,7 +766,8 @@ def test_small_batch_power_of_two_scaling_is_exact(kernel, B):
     packed = pack_layer(L)
     x = make_activations(L, B)
     x2 = (oracle.f16_to_f64(x) * 2).astype(np.float16).view(np.uint16)
-    env = {"lut_batch": {"FLUXBIN_MFMA": "0"}, "mfma": {"FLUXBIN_MFMA": "1"}, "generic": {"FLUXBIN_GENERIC": "1"}}[kernel]
+    env = {"lut_batch": {"FLUXBIN_MFMA": "0"}, "mfma": {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0"},
+           "mfma_rows": {"FLUXBIN_MFMA_ROWS": "1"}, "generic": {"FLUXBIN_GENERIC": "1"}}[kernel]
     log(f"case y(2x) == 2 y(x) {kernel} B={B}")
     y1 = _with_env(env, lambda: run_gemm(packed, x, out_fp32=True))
     y1b = _with_env(env, lambda: run_gemm(packed, x, out_fp32=True))
