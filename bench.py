@@ -306,19 +306,25 @@ def cpu_baseline(bench, budget_s: float):
 
 def small_batch_us(specs, batches, launches=40, rounds=3):
     """Per-call microseconds of the small-batch product on the same layers, graph-timed like the batch-1 figure, for
-    the default kernel choice and, on the same packed copies, each kernel forced: the matrix cores (the sign decode per
-    bit is shared by all batch rows) and the LUT batch kernel (batch-interleaved tables, each sign word read once for
-    all batch rows). The three are measured in turn, `rounds` times, and each figure is the median of its rounds (the
-    first measurement of a process runs at lower clocks)."""
+    the default kernel choice and, on the same packed copies, each kernel forced: the split-tile matrix-core kernel (the
+    sign decode per bit is shared by all batch rows), the LUT batch kernel (batch-interleaved tables, each sign word
+    read once for all batch rows) and, where a layer fits it, the row-complete matrix-core kernel. They are measured in
+    turn, `rounds` times, and each figure is the median of its rounds (the first measurement of a process runs at lower
+    clocks)."""
     import statistics
     import torch
     out = {}
     for B in batches:
         b = Bench(specs, B, COPIES_BYTES_PER_LAYER * len(specs))
-        runs = {"mfma": [], "lut": [], "default": []}
+        kernels = [("mfma", {"mfma": 1, "mfma_rows": 0}), ("lut", {"mfma": 0}), ("default", {})]
+        with b.fb.tuning(mfma_rows=1):
+            fits = [b.fb.fluxbin_plan_query(it["packs"][0], B)["kernel_name"] == "mfma_rows" for it in b.items]
+        if any(fits):
+            kernels.append(("mfma_rows", {"mfma_rows": 1}))
+        runs = {k: [] for k, _ in kernels}
         for _ in range(rounds):
-            for kern, flag in (("mfma", 1), ("lut", 0), ("default", None)):
-                with b.fb.tuning(**({} if flag is None else {"mfma": flag})):
+            for kern, tun in kernels:
+                with b.fb.tuning(**tun):
                     for it in b.items:
                         it["ws"] = b.fb.make_workspace(it["packs"][0], B)
                     runs[kern].append(b.per_launch_us(launches, 3))
@@ -327,17 +333,20 @@ def small_batch_us(specs, batches, launches=40, rounds=3):
             s = it["spec"]
             um, ul, us = us_k["mfma"][i], us_k["lut"][i], us_k["default"][i]
             plan = b.fb.fluxbin_plan_query(it["packs"][0], B)   # the launch plan's own choice (no forcing)
-            out[f"{s.name}_B{B}"] = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
-                                     "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
-                                     "matrix_core_kernel_us": round(um, 3), "lut_batch_kernel_us": round(ul, 3),
-                                     "default_kernel": plan["kernel_name"]}
+            row = {"us_per_call": round(us, 3), "GBps": round(it["bytes"] / (us * 1e-6) / 1e9, 1),
+                   "tflop_eq": round(2.0 * B * s.M * (s.N + s.S) / (us * 1e-6) / 1e12, 2),
+                   "matrix_core_kernel_us": round(um, 3), "lut_batch_kernel_us": round(ul, 3),
+                   "default_kernel": plan["kernel_name"]}
+            if "mfma_rows" in us_k and fits[i]:
+                row["row_complete_matrix_core_kernel_us"] = round(us_k["mfma_rows"][i], 3)
+            out[f"{s.name}_B{B}"] = row
         del b
         torch.cuda.empty_cache()
     return out
 
 
 def prefill_us(specs, batches=(64, 256), launches=6):
-    """Per-call microseconds at prefill-size batches: B > 16 runs as 16-row batch tiles (one launch each, every tile
+    """Per-call microseconds at prefill-size batches: B > 32 runs as 32-row batch tiles (one launch each, every tile
     reading the packed weights again), graph-timed like the small-batch figures; TFLOP-eq counts 2 B M (N + S)."""
     import torch
     out = {}
@@ -735,6 +744,7 @@ def main():
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
         out["config"]["small_batch"] = small_batch_us(specs, (2, 4, 8, 16))
         out["config"]["small_batch_mlp7b"] = small_batch_us(config_layers("c3_mlp7b", args.g_r), (2, 4, 8))
+        out["config"]["small_batch_attn7b"] = small_batch_us(config_layers("c2_attn7b", args.g_r), (2, 4, 8))
         out["config"]["prefill_mlp70b"] = prefill_us(specs)
     if not args.no_grid:
         out["config"]["kernel_latency_grid"] = kernel_latency_grid_us()
