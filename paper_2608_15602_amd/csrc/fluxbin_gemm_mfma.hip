@@ -267,6 +267,49 @@ __device__ __forceinline__ void mf_unit(const uint32_t* xs, const uint32_t* as, 
     for (int rb = 0; rb < 4; ++rb) rs[rb] = *reinterpret_cast<const uint2*>(srs + h * 32 + 8 * rb + 2 * g);
     // the words of row blocks 2rp and 2rp + 1 as one 64-bit value (high: 2rp + 1), shifted together below
     const uint64_t w2[2] = {(uint64_t(w[h][1]) << 32) | w[h][0], (uint64_t(w[h][3]) << 32) | w[h][2]};
+    if constexpr (NBT > 1) {
+      // two batch tiles: one pair of row blocks at a time (half the live partial products, the activation and
+      // column-scale rows read once per pair), which keeps the kernel within three waves per SIMD
+#pragma unroll
+      for (int rp = 0; rp < 2; ++rp) {
+        mf_float4 tmp[NBT][2];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const mf_u32x4 ac = *reinterpret_cast<const mf_u32x4*>(as + (h * 4 + g) * 16 + 4 * q);
+          mf_u32x4 bx[NBT];
+#pragma unroll
+          for (int bt = 0; bt < NBT; ++bt)
+            bx[bt] = *reinterpret_cast<const mf_u32x4*>(xs + ((h * 4 + g) * 4 + q) * XS + 64 * bt + 4 * r16);
+          mf_u32x4 av0, av1;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint64_t sft = mf_shl64(w2[rp], uint32_t(15 - (4 * q + k)));
+            av0[k] = (uint32_t(sft) & 0x80008000u) ^ ac[k];
+            av1[k] = (uint32_t(sft >> 32) & 0x80008000u) ^ ac[k];
+          }
+#pragma unroll
+          for (int bt = 0; bt < NBT; ++bt) {
+            const mf_float4 c0 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[bt][0];
+            const mf_float4 c1 = q == 0 ? mf_float4{0.f, 0.f, 0.f, 0.f} : tmp[bt][1];
+            tmp[bt][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av0),
+                                                                __builtin_bit_cast(mf_half8, bx[bt]), c0, 0, 0, 0);
+            tmp[bt][1] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(mf_half8, av1),
+                                                                __builtin_bit_cast(mf_half8, bx[bt]), c1, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt)
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            const int rb = 2 * rp + i;
+            acc[bt][rb][0] = fmaf(-h2f(uint16_t(rs[rb].x)), tmp[bt][i][0], acc[bt][rb][0]);
+            acc[bt][rb][1] = fmaf(-h2f(uint16_t(rs[rb].x >> 16)), tmp[bt][i][1], acc[bt][rb][1]);
+            acc[bt][rb][2] = fmaf(-h2f(uint16_t(rs[rb].y)), tmp[bt][i][2], acc[bt][rb][2]);
+            acc[bt][rb][3] = fmaf(-h2f(uint16_t(rs[rb].y >> 16)), tmp[bt][i][3], acc[bt][rb][3]);
+          }
+      }
+      continue;
+    }
     mf_float4 tmp[NBT][4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -477,7 +520,7 @@ __global__ void __launch_bounds__(256) k_mf_image(GemmArgs a) {
 }
 
 template <int BP, int MU, int D, bool R2>
-__global__ void __launch_bounds__(kMfNT, mf_gather<BP>() ? ((BP <= 4 && D == 2 && R2) ? 4 : 3) : (BP > 16 ? 2 : 4))
+__global__ void __launch_bounds__(kMfNT, mf_gather<BP>() ? ((BP <= 4 && D == 2 && R2) ? 4 : 3) : (BP > 16 ? 3 : 4))
     k_gemm_mfma(GemmArgs a) {
   using K = MfKernel<BP, MU, D>;
   __shared__ __attribute__((aligned(16))) uint32_t ubuf[2 * K::IMG];

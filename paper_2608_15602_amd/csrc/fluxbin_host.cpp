@@ -362,11 +362,9 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     // on the 70B MLP layers, up / down, 58.6 / 78.7 -> 57.2 / 59.3 us at B = 16, 48.0 / 57.7 -> 46.5 / 47.1 at B = 8,
     // 45.5 / 48.8 -> 42.6 / 43.6 at B = 4; 7B MLP layers 18.8 / 19.0 -> 15.1 / 17.1 at B = 4
     p->reduce2 = p->depth == 2 && tu.mfma_r2 != 0;
-    // three 256-thread workgroups per CU (the kernel's occupancy). 32 batch rows fit two per CU, but a grid target of
-    // four per CU (smaller unit ranges, better balance at the end) measured faster: 70B MLP up / down 79.5 / 81.4 ->
-    // 78.0 / 79.5 us, 7B MLP 25.6 / 27.2 -> 24.8 / 25.9 us. (Three units ahead, or four workgroups per CU at 16 rows:
-    // no faster.)
-    if (per_cu < 1 || per_cu > 8) per_cu = p->bg == 32 ? 4 : 3;
+    // three 256-thread workgroups per CU (the kernel's occupancy at 16 and 32 batch rows; three units ahead, or four
+    // workgroups per CU at 16 rows: no faster)
+    if (per_cu < 1 || per_cu > 8) per_cu = 3;
     if (p->bg == 32 && !p->reduce2)
       return fail(FLUXBIN_ERR_UNSUPPORTED, "32-row matrix-core launches need the second-kernel reduction");
   } else if (L.shape.mu == 8 && B >= 2 && !force_generic && !fine) {
