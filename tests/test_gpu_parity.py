@@ -401,6 +401,28 @@ def test_mfma_rows_kernel_matches_oracle(spec, B):
     _check(y, y_split, "row-complete vs split-tile matrix-core kernel")
 
 
+MR_EDGE_SPECS = [
+    LayerSpec("mr_one_row_one_col", M=1, N=1, Kb=1, Ks=0, mu=8, S=0, g_r=1, g_s=1, seed=85),
+    LayerSpec("mr_17x129_mu4", M=17, N=129, Kb=2, Ks=1, mu=4, S=3, g_r=128, g_s=3, seed=86),
+    LayerSpec("mr_33x300_salient_only_chunk", M=33, N=300, Kb=1, Ks=2, mu=8, S=130, g_r=128, g_s=130, seed=87),
+]
+
+
+@pytest.mark.parametrize("B", [2, 7])
+@pytest.mark.parametrize("spec", MR_EDGE_SPECS, ids=lambda s: s.name)
+def test_mfma_rows_kernel_edge_shapes(spec, B):
+    """Degenerate shapes on the row-complete matrix-core kernel (one row and one column; fewer super-chunks than
+    wavefronts; a ragged mu = 4 layer; two salient bases over more than one salient chunk) and on a 32-row matrix-core
+    launch of the same layers: every row against the oracle."""
+    from paper_2608_15602_amd import fluxbin as fb
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    env = SMALL_BATCH_KERNELS["mfma_rows"]
+    assert _with_env(env, lambda: fb.fluxbin_plan_query(packed, B))["kernel_name"] == "mfma_rows"
+    _with_env(env, lambda: _parity(spec, B, packed=packed, L=L, out_fp32=True))
+    _parity(spec, 16 + B, packed=packed, L=L, out_fp32=True)   # one 32-row matrix-core launch (17..32 rows)
+
+
 @pytest.mark.parametrize("B", [2, 8])
 def test_mfma_rows_kernel_7b_layers_full_size(B):
     """The 7B attention and MLP layers at full size with the default plan at B = 2 and 8 (the row-complete matrix-core
