@@ -18,9 +18,8 @@
 // these took a dependent round trip per element (4096 x 4096: 10.7 us at B = 2 against 6.0 without them); instead a
 // first kernel writes them once per call to an image in the workspace, which every workgroup copies into LDS with
 // LDS-direct loads, waited for with vmcnt before the first barrier while its first sign requests stay in flight.
-// MFMA lanes of batch
-// columns >= BP read past their block: those columns of the product are never stored, and each column of an MFMA
-// result depends on that column of its B operand only. The sign entries of a unit pass through the wavefront's own LDS
+// MFMA lanes of batch columns >= BP read past their block: those columns of the product are never stored, and each
+// column of an MFMA result depends on that column of its B operand only. The sign entries of a unit pass through the wavefront's own LDS
 // scratch to the MFMA lanes, and are decoded as in the split-tile kernel (the words of one row's two chunks shifted
 // together by one 64-bit shift).
 #include <hip/hip_runtime.h>
