@@ -32,6 +32,8 @@ struct GemmArgs {
   int32_t ngc;       // global chunks (Kb * ncg); chunks >= ngc are salient or padding
   int32_t nfc;       // first chunk with the salient chunks' row-scale layout
   int32_t Gcg, Gcs;  // row scales per chunk and row: global / salient layout (1, or 2..32 for fine groups)
+  int32_t kpt;       // matrix-core kernel: kpt > 0: workgroup b covers part b mod kpt of tile b / kpt (tile-aligned
+                     // ranges); 0: the balanced split of all units (first_unit)
 };
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

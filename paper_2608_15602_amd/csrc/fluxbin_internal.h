@@ -146,6 +146,7 @@ struct Plan {
   bool reduce2;     // matrix-core kernel: split tiles reduced by a second kernel over the whole chip
   uint64_t ws_counters_off, ws_partials_off, ws_bytes;
   uint64_t ws_image_off;   // matrix-core kernel: activation images after the partial sums (0 for other kernels)
+  int kpt;                 // matrix-core kernel: workgroups per tile with tile-aligned unit ranges (0: balanced split)
 };
 
 fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p);

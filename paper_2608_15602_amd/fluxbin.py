@@ -64,14 +64,14 @@ class Layer(ctypes.Structure):
 class Tuning(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("nt", "min_units", "blocks", "blocks_per_cu", "depth", "mfma_depth",
                                              "early", "rpt", "mfma", "generic", "mfma_r2", "bat_r2", "rows",
-                                             "batch_tile", "mfma_rows")]
+                                             "batch_tile", "mfma_rows", "mfma_align")]
 
 
 class PlanInfo(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_int32), ("threads", ctypes.c_int32), ("rows_per_tile", ctypes.c_int32),
                 ("depth", ctypes.c_int32), ("batch_groups", ctypes.c_int32),
                 ("second_kernel_reduction", ctypes.c_int32), ("early", ctypes.c_int32), ("batch_tiles", ctypes.c_int32),
-                ("batch_tile_rows", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("batch_tile_rows", ctypes.c_int32), ("workgroups_per_tile", ctypes.c_int32),
                 ("tiles", ctypes.c_int64), ("units", ctypes.c_int64), ("workgroups", ctypes.c_int64),
                 ("workspace_bytes", ctypes.c_uint64)]
 

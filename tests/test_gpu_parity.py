@@ -685,20 +685,26 @@ def test_workspace_shared_by_batch_sizes():
 def test_mfma_second_kernel_reduction_equals_counters(B, mu):
     """The matrix-core kernel's split tiles reduced by a second kernel (one workgroup per split tile and batch row) give
     the counter protocol's y bit for bit (same contributors, same order), on a layer with many contributors per tile,
-    and match the oracle."""
+    and match the oracle; so do workgroup ranges aligned to the row tiles (the default with the second kernel)."""
     from paper_2608_15602_amd import fluxbin as fb
     spec = LayerSpec("r2", M=3000, N=8192, Kb=3, Ks=1, mu=mu, S=100, g_r=128, g_s=100, seed=34)
     log(f"case second-kernel reduction B={B} mu={mu}")
     L = make_layer(spec)
     packed = pack_layer(L)
     x = make_activations(L, B)
-    env = {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0"}
+    env = {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0", "FLUXBIN_MFMA_ALIGN": "0"}
     y_c = _with_env({**env, "FLUXBIN_MFMA_R2": "0"},
                     lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
     y_r = _with_env({**env, "FLUXBIN_MFMA_R2": "1"},
                     lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
     assert np.array_equal(y_r, y_c), int(np.sum(y_r != y_c))
-    _check(y_r, oracle.gemv_dense(L, x), "second-kernel reduction vs oracle")
+    y_ref = oracle.gemv_dense(L, x)
+    _check(y_r, y_ref, "second-kernel reduction vs oracle")
+    info = _with_env({**env, "FLUXBIN_MFMA_ALIGN": "-1"}, lambda: fb.fluxbin_plan_query(packed, B))
+    assert info["workgroups_per_tile"] > 1, info
+    y_a = _with_env({**env, "FLUXBIN_MFMA_ALIGN": "-1"},
+                    lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
+    _check(y_a, y_ref, "tile-aligned ranges vs oracle")
 
 
 
