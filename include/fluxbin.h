@@ -262,13 +262,14 @@ fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16
  *                                         kernel takes the layer
  *   mfma_rows      FLUXBIN_MFMA_ROWS      B = 2..8: 1 the row-complete matrix-core kernel wherever it fits, 0 never;
  *                                         -1: chosen by layer size
- *   mfma_align     FLUXBIN_MFMA_ALIGN     0: matrix-core workgroups over balanced unit ranges; -1: ranges aligned to
- *                                         row tiles where that fits one wave of workgroups; k > 0: aligned ranges,
- *                                         k workgroups per tile (clamped to what the unit cap and the tile allow)
+ *   align          FLUXBIN_ALIGN          split-tile kernels (batch-1, LUT batch, matrix-core): 0 workgroups over
+ *                                         balanced unit ranges; -1 ranges aligned to row tiles where that fits one
+ *                                         wave of workgroups; k > 0 aligned ranges, k workgroups per tile (clamped to
+ *                                         what the unit cap and the tile allow)
  */
 typedef struct {
   int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2, rows,
-      batch_tile, mfma_rows, mfma_align;
+      batch_tile, mfma_rows, align;
 } fluxbin_tuning;
 fluxbin_status fluxbin_get_tuning(fluxbin_tuning* out);
 fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
@@ -280,8 +281,8 @@ fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
  *           rows, B = 2..8).
  * Batches of more than batch_tile_rows rows (32 on layers the matrix-core kernel takes, else 16) run as batch_tiles
  * launches; the plan is then that of the full batch tiles, and workspace_bytes the call's workspace.
- * workgroups_per_tile > 0: the matrix-core kernel's workgroups cover tile-aligned unit ranges, that many per row tile;
- * 0: balanced ranges over all units (or another kernel). Host only apart
+ * workgroups_per_tile > 0: the split-tile kernel's workgroups cover tile-aligned unit ranges, that many per row tile;
+ * 0: balanced ranges over all units (or a kernel without split tiles). Host only apart
  * from reading the device's CU count; launches nothing.
  */
 typedef struct {

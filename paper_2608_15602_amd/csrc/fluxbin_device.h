@@ -32,8 +32,8 @@ struct GemmArgs {
   int32_t ngc;       // global chunks (Kb * ncg); chunks >= ngc are salient or padding
   int32_t nfc;       // first chunk with the salient chunks' row-scale layout
   int32_t Gcg, Gcs;  // row scales per chunk and row: global / salient layout (1, or 2..32 for fine groups)
-  int32_t kpt;       // matrix-core kernel: kpt > 0: workgroup b covers part b mod kpt of tile b / kpt (tile-aligned
-                     // ranges); 0: the balanced split of all units (first_unit)
+  int32_t kpt;       // kpt > 0: workgroup b covers part b mod kpt of tile b / kpt (tile-aligned ranges); 0: the
+                     // balanced split of all units (first_unit)
 };
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -47,13 +47,27 @@ __device__ __forceinline__ uint4 load_stream16(const uint8_t* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// Balanced split of the units: workgroup b owns [first_unit(b), first_unit(b + 1)), uq + 1 units for b < ur and uq
-// units otherwise (uq >= 1).
-__device__ __forceinline__ int first_unit(const GemmArgs& a, int b) { return b * a.uq + (b < a.ur ? b : a.ur); }
+// Split of the units over the workgroups: workgroup b owns [first_unit(b), first_unit(b + 1)).
+// kpt == 0: balanced over all units, uq + 1 units for b < ur and uq otherwise (uq >= 1).
+// kpt > 0: aligned to tiles, workgroup b owns part j = b mod kpt of tile b / kpt, the steps units of a tile split as
+// uq + 1 units for j < ur and uq otherwise (uq = steps / kpt >= 1, ur = steps mod kpt).
+__device__ __forceinline__ int first_unit(const GemmArgs& a, int b) {
+  int t = 0;
+  if (a.kpt > 0) {
+    t = b / a.kpt;
+    b -= t * a.kpt;
+  }
+  return t * a.steps + b * a.uq + (b < a.ur ? b : a.ur);
+}
 
 __device__ __forceinline__ int owner_of(const GemmArgs& a, int u) {
+  int t = 0;
+  if (a.kpt > 0) {
+    t = u / a.steps;
+    u -= t * a.steps;
+  }
   const int big = a.ur * (a.uq + 1);
-  return u < big ? u / (a.uq + 1) : a.ur + (u - big) / a.uq;
+  return t * a.kpt + (u < big ? u / (a.uq + 1) : a.ur + (u - big) / a.uq);
 }
 
 __device__ __forceinline__ void store_y(const GemmArgs& a, int b, int64_t row, float v) {

@@ -548,26 +548,16 @@ __global__ void __launch_bounds__(kMfNT, mf_gather<BP>() ? ((BP <= 4 && D == 2 &
   }
   uint32_t* scr = scr_all + ln.wave * kMfScrWave;
 
-  // the workgroup's units: part blockIdx mod kpt of tile blockIdx / kpt (tile-aligned ranges), or its range of the
-  // balanced split over all units
-  int u0, u1;
-  if (a.kpt > 0) {
-    const int tile = blockIdx.x / a.kpt, j = blockIdx.x - tile * a.kpt;
-    const int sq = a.steps / a.kpt, sr = a.steps - sq * a.kpt;
-    u0 = tile * a.steps + j * sq + (j < sr ? j : sr);
-    u1 = u0 + sq + (j < sr ? 1 : 0);
-  } else {
-    u0 = first_unit(a, blockIdx.x);
-    u1 = first_unit(a, blockIdx.x + 1);
-  }
+  const int u0 = first_unit(a, blockIdx.x);
+  const int u1 = first_unit(a, blockIdx.x + 1);
   typename K::State s;
   s.n = u1 - u0;
   s.cur.tile = u0 / a.steps;
   s.cur.sc = u0 - s.cur.tile * a.steps;
   s.first_tile = s.cur.tile;
   s.last_tile = (u1 - 1) / a.steps;
-  s.first_shared = a.kpt > 0 ? a.kpt > 1 : tile_is_shared(a, s.first_tile);
-  s.last_shared = a.kpt > 0 ? a.kpt > 1 : tile_is_shared(a, s.last_tile);
+  s.first_shared = tile_is_shared(a, s.first_tile);
+  s.last_shared = tile_is_shared(a, s.last_tile);
   s.n_pending = 0;
 #pragma unroll
   for (int bt = 0; bt < mf_nbt<BP>(); ++bt)

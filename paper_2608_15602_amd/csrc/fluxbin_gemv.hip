@@ -730,14 +730,11 @@ __global__ void __launch_bounds__(256) k_reduce_split(GemmArgs a, int bp, int R)
   const int tile = int(blockIdx.x) / per_tile;
   const int rem = int(blockIdx.x) - tile * per_tile;
   const int b = rem / q;
-  // contributors of the tile: the workgroups of its tile-aligned parts (every one writes slot 0), or those of the
-  // balanced split whose ranges meet it (the first in slot 1 when its range starts in an earlier tile)
-  const bool aligned = a.kpt > 0;
-  if (b >= a.B || !(aligned ? a.kpt > 1 : tile_is_shared(a, tile))) return;   // unshared: stored by the owner
+  if (b >= a.B || !tile_is_shared(a, tile)) return;   // unshared tiles were stored by their owner
   const int r = (rem - b * q) * 256 + int(threadIdx.x);
-  const int b_first = aligned ? tile * a.kpt : owner_of(a, tile * a.steps);
-  const int n_c = aligned ? a.kpt : owner_of(a, (tile + 1) * a.steps - 1) - b_first + 1;
-  const bool first_in_slot1 = !aligned && first_unit(a, b_first) < tile * a.steps;
+  const int b_first = owner_of(a, tile * a.steps);
+  const int n_c = owner_of(a, (tile + 1) * a.steps - 1) - b_first + 1;
+  const bool first_in_slot1 = first_unit(a, b_first) < tile * a.steps;   // its range starts in an earlier tile
   float sum = 0.f;
   for (int c0 = 0; c0 < n_c; c0 += CH) {
     float v[CH];
@@ -1123,6 +1120,14 @@ static bool launch_gen_mu(const GemmArgs& a, const Plan& p, hipStream_t stream) 
   return false;
 }
 
+// The plan's split of the units over the workgroups (first_unit): aligned to tiles, kpt per tile, or balanced.
+static void set_split(const Plan& p, GemmArgs& a) {
+  a.kpt = p.kpt;
+  const int64_t steps = p.units / p.n_tiles;
+  a.uq = int32_t(p.kpt > 0 ? steps / p.kpt : p.units / p.blocks);
+  a.ur = int32_t(p.kpt > 0 ? steps % p.kpt : p.units % p.blocks);
+}
+
 fluxbin_status launch_stream_probe(const fluxbin_layer& L, const Plan& p, uint32_t* d_sink, hipStream_t stream) {
   GemmArgs a{};
   const uint8_t* base = static_cast<const uint8_t*>(L.d_base);
@@ -1131,8 +1136,7 @@ fluxbin_status launch_stream_probe(const fluxbin_layer& L, const Plan& p, uint32
   a.chunk_plane = reinterpret_cast<const int32_t*>(base + L.off_chunk_plane);
   a.units = int32_t(p.units);
   a.blocks = int32_t(p.blocks);
-  a.uq = int32_t(p.units / p.blocks);
-  a.ur = int32_t(p.units % p.blocks);
+  set_split(p, a);
   a.M = int32_t(L.shape.M);
   a.Mp = int32_t(L.Mp);
   a.NSC = int32_t(L.NSC);
@@ -1174,13 +1178,11 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   a.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(d_ws) + p.ws_partials_off);
   a.img = (p.kernel == 3 || p.kernel == 5) ? reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + p.ws_image_off)
                                            : nullptr;
-  a.kpt = p.kernel == 3 ? p.kpt : 0;
   a.ldx = ldx;
   a.ldy = ldy;
   a.units = int32_t(p.units);
   a.blocks = int32_t(p.blocks);
-  a.uq = int32_t(p.units / p.blocks);
-  a.ur = int32_t(p.units % p.blocks);
+  set_split(p, a);
   a.N = int32_t(L.shape.N);
   a.ncg = int32_t(L.Npad / kChunk);
   a.ngc = int32_t(L.shape.Kb * (L.Npad / kChunk));

@@ -136,7 +136,7 @@ static fluxbin_tuning tuning_defaults() {
   t.rows = -1;
   t.batch_tile = 0;
   t.mfma_rows = -1;
-  t.mfma_align = -1;
+  t.align = -1;
   return t;
 }
 
@@ -168,7 +168,7 @@ static void tuning_init_locked() {
   t.rows = env_int("FLUXBIN_ROWS", t.rows);
   t.batch_tile = env_int("FLUXBIN_BATCH_TILE", t.batch_tile);
   t.mfma_rows = env_int("FLUXBIN_MFMA_ROWS", t.mfma_rows);
-  t.mfma_align = env_int("FLUXBIN_MFMA_ALIGN", t.mfma_align);
+  t.align = env_int("FLUXBIN_ALIGN", t.align);
   g_tuning = t;
   g_tuning_init = true;
 }
@@ -455,24 +455,25 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
     const int64_t whole = ceil_div(p->blocks, resident) * resident;
     p->blocks = whole < p->units ? whole : p->units;
   }
-  // The matrix-core kernel with the second-kernel reduction: unit ranges aligned to tiles (kpt workgroups per tile,
-  // each a contiguous part of one tile) where that fits one wave of resident workgroups: about as many workgroups as
-  // the balanced split, and at most its most units per workgroup. A balanced range over a tile boundary ends two tiles
-  // (two transposes of the accumulators and two stores of partial sums), and such workgroups set the kernel's end:
-  // aligned ranges end one each. 70B MLP down projection (32 tiles of 342 units, 768 workgroups) 49.7 -> 45.6 us at
-  // B = 8, 73.9 -> 70.3 at B = 32; 7B MLP (43 and 16 tiles, about 470 workgroups) 2 to 8 % faster at B = 8..32. The
-  // 70B up projection (112 tiles of 98 units) needs 7 per tile, 784 workgroups: one wave of 768 and a tail, so it keeps
-  // the balanced split. FLUXBIN_MFMA_ALIGN=0 keeps the balanced split everywhere.
+  // Unit ranges aligned to tiles (kpt workgroups per tile, each a contiguous part of one tile) for the split-tile
+  // kernels, where that fits one wave of resident workgroups: about as many workgroups as the balanced split, and at
+  // most its most units per workgroup. A balanced range over a tile boundary ends two tiles (two transposes or stores
+  // of partial sums, two counter bumps), and such workgroups end last; an aligned range ends one. Matrix-core kernel,
+  // 70B MLP down projection (32 tiles of 342 units, 768 workgroups): 49.7 -> 45.6 us at B = 8, 73.9 -> 70.3 at B = 32;
+  // 7B MLP (43 and 16 tiles, about 470 workgroups) 2 to 8 % faster at B = 8..32. The 70B up projection's 112 tiles of
+  // 98 units need 7 per tile, 784 workgroups: one wave of 768 and a tail, so the matrix-core kernel keeps the balanced
+  // split there. FLUXBIN_ALIGN=0 keeps the balanced split everywhere; k > 0 forces k per tile.
   p->kpt = 0;
-  if (p->kernel == 3 && p->reduce2 && tu.mfma_align != 0 && blocks_env <= 0) {
-    const int64_t steps = L.NSC;
+  if ((p->kernel == 0 || p->kernel == 2 || p->kernel == 3) && tu.align != 0 && blocks_env <= 0 && p->n_tiles > 0) {
+    const int64_t steps = p->units / p->n_tiles;
+    const int64_t cap = p->kernel == 0 ? b1_max_units(p->nt) : (p->kernel == 2 ? kBatMaxUnits : kMfMaxUnits);
     const int64_t k_round = (p->blocks + p->n_tiles / 2) / p->n_tiles;
     const int64_t k_units = ceil_div(steps, ceil_div(p->units, p->blocks));
-    int64_t kpt = tu.mfma_align > 0 ? tu.mfma_align : (k_round > k_units ? k_round : k_units);
-    const int64_t kmin = ceil_div(steps, kMfMaxUnits);
+    int64_t kpt = tu.align > 0 ? tu.align : (k_round > k_units ? k_round : k_units);
+    const int64_t kmin = ceil_div(steps, cap);
     if (kpt < kmin) kpt = kmin;
     if (kpt > steps) kpt = steps;
-    if (tu.mfma_align > 0 || p->n_tiles * kpt <= resident) {
+    if (tu.align > 0 || p->n_tiles * kpt <= resident) {
       p->kpt = int(kpt);
       p->blocks = p->n_tiles * kpt;
     }

@@ -692,7 +692,7 @@ def test_mfma_second_kernel_reduction_equals_counters(B, mu):
     L = make_layer(spec)
     packed = pack_layer(L)
     x = make_activations(L, B)
-    env = {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0", "FLUXBIN_MFMA_ALIGN": "0"}
+    env = {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0", "FLUXBIN_ALIGN": "0"}
     y_c = _with_env({**env, "FLUXBIN_MFMA_R2": "0"},
                     lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
     y_r = _with_env({**env, "FLUXBIN_MFMA_R2": "1"},
@@ -700,11 +700,49 @@ def test_mfma_second_kernel_reduction_equals_counters(B, mu):
     assert np.array_equal(y_r, y_c), int(np.sum(y_r != y_c))
     y_ref = oracle.gemv_dense(L, x)
     _check(y_r, y_ref, "second-kernel reduction vs oracle")
-    info = _with_env({**env, "FLUXBIN_MFMA_ALIGN": "-1"}, lambda: fb.fluxbin_plan_query(packed, B))
+    info = _with_env({**env, "FLUXBIN_ALIGN": "-1"}, lambda: fb.fluxbin_plan_query(packed, B))
     assert info["workgroups_per_tile"] > 1, info
-    y_a = _with_env({**env, "FLUXBIN_MFMA_ALIGN": "-1"},
-                    lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
-    _check(y_a, y_ref, "tile-aligned ranges vs oracle")
+    y_a = {}
+    for r2 in ("0", "1"):
+        y_a[r2] = _with_env({**env, "FLUXBIN_ALIGN": "-1", "FLUXBIN_MFMA_R2": r2},
+                            lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
+    assert np.array_equal(y_a["1"], y_a["0"]), int(np.sum(y_a["1"] != y_a["0"]))
+    _check(y_a["1"], y_ref, "tile-aligned ranges vs oracle")
+
+
+# Unit ranges of the split-tile kernels: balanced over all units (FLUXBIN_ALIGN=0), aligned to row tiles where that
+# fits one wave (-1, the default), and forced counts of workgroups per tile (k > 0: 1 = no split tiles; 3; a count
+# that leaves some parts one unit longer than others).
+ALIGN_CASES = [("batch1", 1, {"FLUXBIN_ROWS": "0"}), ("lut_batch", 3, {"FLUXBIN_MFMA": "0"}),
+               ("lut_batch_r2", 2, {"FLUXBIN_MFMA": "0", "FLUXBIN_BAT_R2": "1"}),
+               ("mfma", 5, {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0"}),
+               ("mfma_counters", 9, {"FLUXBIN_MFMA": "1", "FLUXBIN_MFMA_ROWS": "0", "FLUXBIN_MFMA_R2": "0"})]
+
+
+@pytest.mark.parametrize("case", ALIGN_CASES, ids=[c[0] for c in ALIGN_CASES])
+@pytest.mark.parametrize("align", ["0", "-1", "1", "3", "7"])
+def test_split_tile_unit_ranges(case, align):
+    """Every split-tile kernel matches the oracle with balanced, tile-aligned and forced per-tile unit ranges (ragged
+    last tile, a tile's parts of unequal length), and the plan reports the aligned split."""
+    from paper_2608_15602_amd import fluxbin as fb
+    name, B, env = case
+    spec = LayerSpec("align", M=2600, N=1536, Kb=2, Ks=1, mu=8, S=150, g_r=128, g_s=150, seed=36)
+    log(f"case unit ranges {name} B={B} align={align}")
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    x = make_activations(L, B)
+    env = {**env, "FLUXBIN_ALIGN": align}
+    info = _with_env(env, lambda: fb.fluxbin_plan_query(packed, B))
+    if int(align) > 0:
+        assert info["workgroups_per_tile"] == min(int(align), info["units"] // info["tiles"]) or \
+            info["workgroups_per_tile"] > int(align), info   # raised to the kernel's unit cap
+        assert info["workgroups"] == info["tiles"] * info["workgroups_per_tile"], info
+    elif align == "0":
+        assert info["workgroups_per_tile"] == 0, info
+    y = _with_env(env, lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
+    _check(y, oracle.gemv_dense(L, x), f"{name} align {align}")
+    y2 = _with_env(env, lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
+    assert np.array_equal(y2, y), "repeat differs"
 
 
 
@@ -719,10 +757,11 @@ def test_lut_batch_second_kernel_reduction_equals_counters(B):
     packed = pack_layer(L)
     x = make_activations(L, B)
     y = {}
-    for r2 in ("0", "1"):
-        y[r2] = _with_env({"FLUXBIN_MFMA": "0", "FLUXBIN_BAT_R2": r2},
-                          lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
-    assert np.array_equal(y["1"], y["0"]), int(np.sum(y["1"] != y["0"]))
+    for align in ("0", "-1"):
+        for r2 in ("0", "1"):
+            y[r2] = _with_env({"FLUXBIN_MFMA": "0", "FLUXBIN_BAT_R2": r2, "FLUXBIN_ALIGN": align},
+                              lambda: run_gemm(packed, x, out_fp32=True, ws=fb.make_workspace(packed, B)))
+        assert np.array_equal(y["1"], y["0"]), (align, int(np.sum(y["1"] != y["0"])))
     _check(y["1"], oracle.gemv_dense(L, x), "LUT batch second-kernel reduction vs oracle")
 
 
