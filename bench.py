@@ -411,6 +411,35 @@ def kernel_variants_us(g_r: str, launches: int = 40):
     return out
 
 
+def small_layers_b1_us(g_r: str, launches: int = 60):
+    """Batch 1 on the 7B attention (4096x4096) and MLP (11008x4096, 4096x11008) layers: the default launch plan's time,
+    the split-tile kernel's (forced where the default is the row-complete kernel), and the stream probe, which issues
+    the split-tile kernel's sign and row-scale requests without the table work (the load-only time of that access
+    pattern on these small layers, start-up and end-of-grid included)."""
+    import torch
+    from synth import config_layers
+    out = {}
+    for cfg in ("c2_attn7b", "c3_mlp7b"):
+        specs = config_layers(cfg, g_r)
+        b = Bench(specs, 1, COPIES_BYTES_PER_LAYER * len(specs))
+        kinds = [b.fb.fluxbin_plan_query(it["packs"][0], 1)["kernel_name"] for it in b.items]
+        us = b.per_launch_us(launches, 3)
+        with b.fb.tuning(rows=0):
+            for it in b.items:
+                it["ws"] = b.fb.make_workspace(it["packs"][0], 1)
+            us_split = b.per_launch_us(launches, 3)
+        probe = b.stream_probe_us(launches, 3)
+        for it, kind, u, u2, pu in zip(b.items, kinds, us, us_split, probe):
+            s = it["spec"]
+            out[f"{cfg}_{s.name}"] = {"shape_out_x_in": f"{s.M}x{s.N}", "bytes": it["bytes"], "default_kernel": kind,
+                                      "us_per_gemv": round(u, 3), "split_tile_kernel_us": round(u2, 3),
+                                      "stream_probe_us": round(pu, 3), "us_over_probe": round(u / pu, 3),
+                                      "GBps": round(it["bytes"] / (u * 1e-6) / 1e9, 1)}
+        del b
+        torch.cuda.empty_cache()
+    return out
+
+
 def mu_profile_us(g_r: str, launches: int = 40):
     """mu = 8 against mu = 4 (same shapes and seeds) at batch 1 (Sec. 3.2 trades table size against lookups; App. E.2
     profiles mu on the 7B model): the 7B attention and MLP layers, the 70B MLP layers, and the distinct shapes of the
@@ -742,6 +771,7 @@ def main():
         us, b2 = small_layer_us(spec2)
         out["config"]["attn_4096x4096_us_per_gemv"] = round(us, 3)
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
+        out["config"]["batch1_7b_layers"] = small_layers_b1_us(args.g_r)
         out["config"]["small_batch"] = small_batch_us(specs, (2, 4, 8, 16))
         out["config"]["small_batch_mlp7b"] = small_batch_us(config_layers("c3_mlp7b", args.g_r), (2, 4, 8))
         out["config"]["small_batch_attn7b"] = small_batch_us(config_layers("c2_attn7b", args.g_r), (2, 4, 8))

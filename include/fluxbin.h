@@ -306,10 +306,12 @@ fluxbin_status fluxbin_unpack_canonical(const fluxbin_layer* layer, uint32_t* d_
 
 /*
  * Measurement support (no result of the method). fluxbin_stream_probe reads the sign words and row scales of a packed
- * layer exactly as the batch-1 GEMV does (same launch plan, units, per-thread addresses and request depth) but does no
- * table work, giving the bandwidth this access pattern can reach on the device; the benchmark reports the GEMV's
- * bandwidth against it. d_sink (device, at least 1024 bytes) receives meaningless checksums. Same validation and
- * stream semantics as fluxbin_lut_gemv.
+ * layer exactly as the split-tile batch-1 GEMV does (its launch plan, units, per-thread addresses and request depth,
+ * also on layers whose default batch-1 plan is the row-complete kernel) but does no table work, giving the bandwidth
+ * this access pattern can reach on the device; the benchmark reports the GEMV's bandwidth against it. d_sink (device,
+ * at least 1024 bytes) receives meaningless checksums. Same validation and stream semantics as fluxbin_lut_gemv;
+ * FLUXBIN_ERR_UNSUPPORTED for a layer the split-tile batch-1 kernel does not take (fine groups it has no instance
+ * for, or the generic kernel forced by the tuning).
  */
 fluxbin_status fluxbin_stream_probe(const fluxbin_layer* layer, uint32_t* d_sink, size_t sink_bytes,
                                     hipStream_t stream);

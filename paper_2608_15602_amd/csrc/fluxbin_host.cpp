@@ -258,7 +258,7 @@ static int batch_tile_rows(const fluxbin_layer& L, const fluxbin_tuning& tu) {
   return kMaxBatchMfma;
 }
 
-fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
+fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p, bool allow_rows) {
   const int cus = device_cu_count();
   if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
   std::memset(p, 0, sizeof(*p));
@@ -277,7 +277,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p) {
   // the batch-1 instances for fine groups: salient side only, 8 or 16 groups per chunk (s = 16 or 8 at mu = 8)
   const bool b1_fine_ok = L.shape.mu == 8 && dv.Gcg == 1 && (dv.Gcs == 8 || dv.Gcs == 16);
   p->nt = 256;
-  if (B == 1 && !force_generic && use_rows(L, dv, cus, tu)) {
+  if (B == 1 && !force_generic && allow_rows && use_rows(L, dv, cus, tu)) {
     // row-complete batch-1 kernel: 16 rows per workgroup, every super-chunk of them, no cross-workgroup reduction;
     // 16 wavefronts, two units requested ahead (4 and 8 wavefronts, and 4 or 6 units ahead, measured slower or equal)
     p->kernel = 4;
@@ -790,8 +790,11 @@ fluxbin_status fluxbin_stream_probe(const fluxbin_layer* layer, uint32_t* d_sink
   if (!d_sink) return fail(FLUXBIN_ERR_INVALID_ARG, "d_sink is NULL");
   if (sink_bytes < 1024) return fail(FLUXBIN_ERR_BUFFER_TOO_SMALL, "sink of %zu bytes < 1024", sink_bytes);
   Plan p;
-  st = make_plan(*layer, 1, &p);
+  st = make_plan(*layer, 1, &p, false);
   if (st != FLUXBIN_OK) return st;
+  if (p.kernel != 0)
+    return fail(FLUXBIN_ERR_UNSUPPORTED, "the stream probe follows the split-tile batch-1 kernel's launch plan, and "
+                                         "this layer runs kernel %d at batch 1", p.kernel);
   return launch_stream_probe(*layer, p, d_sink, stream);
 }
 

@@ -149,7 +149,8 @@ struct Plan {
   int kpt;                 // matrix-core kernel: workgroups per tile with tile-aligned unit ranges (0: balanced split)
 };
 
-fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p);
+// allow_rows = false: never the row-complete batch-1 kernel (the stream probe follows the split-tile kernel's plan)
+fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p, bool allow_rows = true);
 
 // ---- launchers (fluxbin_pack.hip, fluxbin_gemv.hip) ----
 fluxbin_status launch_pack(const fluxbin_layer& L, const fluxbin_weights& dev_w, const int32_t* d_sal_idx,

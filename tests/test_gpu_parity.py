@@ -614,6 +614,8 @@ def test_stream_probe_runs_and_leaves_results_alone():
         assert np.array_equal(run_gemm(packed, xb, out_fp32=True), y0)
     with pytest.raises(fb.FluxbinError):   # sink below 1024 bytes
         fb.fluxbin_stream_probe(packed, sink[:100])
+    with fb.tuning(generic=1), pytest.raises(fb.FluxbinError):   # no split-tile batch-1 plan to follow
+        fb.fluxbin_stream_probe(packed, sink)
 
 
 def test_graph_replays_match_eager():
