@@ -19,6 +19,7 @@ import math
 import os
 import sys
 import time
+from typing import Dict
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -440,6 +441,29 @@ def small_layers_b1_us(g_r: str, launches: int = 60):
     return out
 
 
+def shard_us(g_r: str, full_us: Dict[str, float], launches: int = 60):
+    """One rank's share of the 70B MLP layers at P = 2, 4, 8 ranks (up split by output rows, down by input columns),
+    batch 1: the kernel at the shard's real shape, against the full layer's time over P (what perfect splitting would
+    give; the cross-rank sum of the down projection's partial outputs is not included)."""
+    import torch
+    from synth import shard_layers
+    out = {}
+    for P in (2, 4, 8):
+        specs = shard_layers(P, g_r)
+        b = Bench(specs, 1, COPIES_BYTES_PER_LAYER * len(specs))
+        us = b.per_launch_us(launches, 3)
+        for it, u, full in zip(b.items, us, ("up", "down")):
+            s = it["spec"]
+            out[s.name] = {"shape_out_x_in": f"{s.M}x{s.N}", "bytes": it["bytes"], "us_per_gemv": round(u, 3),
+                           "GBps": round(it["bytes"] / (u * 1e-6) / 1e9, 1),
+                           "pct_of_8TBps": round(100 * it["bytes"] / (u * 1e-6) / 1e9 / HBM_PEAK_GBS, 1),
+                           "full_layer_us_over_P": round(full_us[full] / P, 3),
+                           "kernel": b.fb.fluxbin_plan_query(it["packs"][0], 1)["kernel_name"]}
+        del b
+        torch.cuda.empty_cache()
+    return out
+
+
 def mu_profile_us(g_r: str, launches: int = 40):
     """mu = 8 against mu = 4 (same shapes and seeds) at batch 1 (Sec. 3.2 trades table size against lookups; App. E.2
     profiles mu on the 7B model): the 7B attention and MLP layers, the 70B MLP layers, and the distinct shapes of the
@@ -772,6 +796,7 @@ def main():
         out["config"]["attn_4096x4096_us_per_gemv"] = round(us, 3)
         out["config"]["attn_4096x4096_GBps"] = round(b2 / (us * 1e-6) / 1e9, 1)
         out["config"]["batch1_7b_layers"] = small_layers_b1_us(args.g_r)
+        out["config"]["shards_mlp70b"] = shard_us(args.g_r, {it["spec"].name: u for it, u in zip(bench.items, kern_us)})
         out["config"]["small_batch"] = small_batch_us(specs, (2, 4, 8, 16))
         out["config"]["small_batch_mlp7b"] = small_batch_us(config_layers("c3_mlp7b", args.g_r), (2, 4, 8))
         out["config"]["small_batch_attn7b"] = small_batch_us(config_layers("c2_attn7b", args.g_r), (2, 4, 8))

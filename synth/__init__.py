@@ -13,6 +13,7 @@ from .layers import (  # noqa: F401
     salient_count,
     kernel_variant_layers,
     fused_decoder_layers,
+    shard_layers,
     make_weight_matrix,
     vcm_off_equivalent,
     paper_config,

@@ -217,6 +217,17 @@ def kernel_variant_layers(g_r: str = "128") -> List[LayerSpec]:
     return [s.with_(g_r=s.N) if g_r == "N" else s for s in out]
 
 
+def shard_layers(P: int, g_r: str = "128") -> List[LayerSpec]:
+    """One rank's share of the 70B MLP layers when P ranks split them: the up projection by output rows
+    (28672 / P x 8192, every input column, the same 5% salient columns) and the down projection by input columns
+    (8192 x 28672 / P, the salient columns that fall in the rank's column range: 5% of them, drawn like any other
+    layer's). These are the layers one GPU runs when the path is sharded; their partial outputs would then be
+    concatenated (up) or summed across ranks (down)."""
+    out = [_attn_mlp(f"up_p{P}", 28672 // P, 8192, 3, 0.05, seed=6, layer_id=200 + 2 * P, outlier_frac=0.001),
+           _attn_mlp(f"down_p{P}", 8192, 28672 // P, 3, 0.05, seed=6, layer_id=201 + 2 * P, outlier_frac=0.001)]
+    return [s.with_(g_r=s.N) if g_r == "N" else s for s in out]
+
+
 def fused_decoder_layers(g_r: str = "128") -> List[LayerSpec]:
     """The 70B decoder layer's linears with the launches that share an input fused by stacking output rows: q, k and v
     as one 10240 x 8192 layer, gate and up as one 57344 x 8192 layer, then o and down. A fused layer has one salient

@@ -207,6 +207,21 @@ def test_kernel_variants_full_size():
         torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("P", [2, 4, 8])
+def test_shard_layers_full_size(P):
+    """One rank's share of the 70B MLP layers at P ranks (up by output rows, down by input columns), sampled rows at
+    full size in the launch configuration the benchmark uses, at batch 1 and 16."""
+    import torch
+    from synth import shard_layers
+    for spec in shard_layers(P, "128"):
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        for B in (1, 16):
+            _parity(spec, B, rows=sample_rows(spec.M, 256, seed=P), packed=packed, L=L)
+        del packed
+        torch.cuda.empty_cache()
+
+
 def test_mu4_profile_layers_full_size():
     """The 7B attention and MLP layers at mu = 4 (the benchmark's mu profile), sampled rows at full size."""
     for cfg in ("c2_attn7b", "c3_mlp7b"):
