@@ -333,6 +333,47 @@ def test_effective_tflops_matches_paper_table():
         assert abs(oracle.effective_tflops(M, N, 0, lat4 * 1e-6) - tf4) <= g["tolerance"]
 
 
+def test_effective_tflops_salient_term_matches_paper_table():
+    """The N_sal term: the paper's hybrid-base TFLOPS (App. E.3) are reproduced with its salient columns counted
+    (dropping the term misses most entries), at the salient width the table's figures follow (see the fixture)."""
+    g = _golden("tile_saliency_tflops.json")
+    miss = miss_without = total = 0
+    for shape in g["shapes"]:
+        M, N = shape["M"], shape["N"]
+        for lat8, tf8, lat16, tf16 in shape["rows"]:
+            for lat, tf in ((lat8, tf8), (lat16, tf16)):
+                total += 1
+                err = abs(oracle.effective_tflops(M, N, g["N_sal"], lat * 1e-6) - tf)
+                assert err <= g["max_error"], (M, N, lat, tf, err)
+                miss += err > g["tolerance"]
+                miss_without += abs(oracle.effective_tflops(M, N, 0, lat * 1e-6) - tf) > g["tolerance"]
+    assert total == 72 and miss <= g["max_mismatches"], miss
+    assert miss_without > total // 2, miss_without
+
+
+def test_effective_tflops_batch_factor():
+    """Batch B (this library's small-batch figures; the paper defines the metric for one vector): B vectors in B
+    times the latency are the batch-1 throughput, and B vectors in the batch-1 latency are B times it."""
+    v1 = oracle.effective_tflops(4096, 4096, 128, 50e-6)
+    assert np.isclose(oracle.effective_tflops(4096, 4096, 128, 8 * 50e-6, B=8), v1)
+    assert np.isclose(oracle.effective_tflops(4096, 4096, 128, 50e-6, B=8), 8 * v1)
+
+
+@pytest.mark.parametrize("mu,N,S,Kb,Ks", [(8, 256, 64, 2, 1), (4, 128, 24, 3, 2), (8, 512, 0, 1, 0)])
+def test_complexity_counts_the_lut_algorithm(mu, N, S, Kb, Ks):
+    """App. C.1's counts against the oracle's own LUT algorithm on a small layer: one table read per (base, row,
+    sub-vector) the lookup path forms an index for, and 2^mu entries per (base, sub-vector) table."""
+    M = 48
+    spec = LayerSpec("cplx", M=M, N=N, Kb=Kb, Ks=Ks, mu=mu, S=S, g_r=N, g_s=max(S, 1), seed=9)
+    L = make_layer(spec)
+    idx = oracle.lut_indices(L)
+    reads = idx["global"].size + idx["salient"].size
+    tables = idx["global"].shape[0] * idx["global"].shape[2] + idx["salient"].shape[0] * idx["salient"].shape[2]
+    c = oracle.complexity(M, N, S, Kb, Ks, mu)
+    assert reads == c["read"], (reads, c)
+    assert tables * 2 ** mu == c["build"], (tables, c)
+
+
 def test_complexity_ratio():
     c = oracle.complexity(M=4096, N=4096, N_sal=256, Kb=2, Ks=2, mu=8)
     assert c["read"] / c["build"] == 4096 / 256
