@@ -255,6 +255,8 @@ EDGE_SPECS = [
     LayerSpec("four_bases", M=513, N=1024, Kb=4, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=16),
     LayerSpec("mu4_ragged", M=777, N=260, Kb=2, Ks=1, mu=4, S=20, g_r=260, g_s=20, seed=17),
     LayerSpec("tiny_N", M=70, N=7, Kb=2, Ks=1, mu=4, S=3, g_r=7, g_s=3, seed=18),
+    LayerSpec("one_col", M=100, N=1, Kb=2, Ks=1, mu=8, S=1, g_r=1, g_s=1, seed=25),
+    LayerSpec("one_by_one", M=1, N=1, Kb=1, Ks=0, mu=8, S=0, g_r=1, g_s=1, seed=26),
     # fine row-scale groups (group shorter than a 128-column chunk) on the global side, the salient side or both
     LayerSpec("fine_g64_s8", M=1000, N=300, Kb=3, Ks=2, mu=8, S=77, g_r=64, g_s=8, seed=19),
     LayerSpec("fine_g8_s16", M=700, N=512, Kb=2, Ks=1, mu=8, S=100, g_r=8, g_s=16, seed=20),
