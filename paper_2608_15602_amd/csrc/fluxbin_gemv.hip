@@ -40,13 +40,15 @@ namespace fluxbin {
 // =====================================================================================================================
 
 
-template <int NT, int RPT>
+// XU: most units a workgroup stages (the launch plan keeps every workgroup within it): b1_max_units(NT), or
+// kB1BigUnits for the 1024-thread instance of layers that would otherwise need a second wave of workgroups.
+template <int NT, int RPT, int XU = b1_max_units(NT)>
 struct B1 {
   static constexpr int R = NT * RPT;
   static constexpr int NHI = NT / 32;                                   // pattern ranges per (slot, s) in the build
   static constexpr int LO = NHI == 4 ? 6 : (NHI == 8 ? 5 : (NHI == 16 ? 4 : 3));
   static constexpr int E = 1 << LO;                                     // entries per thread per build
-  static constexpr int XV = b1_max_units(NT);                            // units staged in LDS (1 KB each)
+  static constexpr int XV = XU;                                         // units staged in LDS (1 KB each)
   static constexpr int KPT = XV / (NT / 256);                           // staged units per thread
 };
 
@@ -79,11 +81,11 @@ __device__ __forceinline__ int wrap_sc(int v, int steps) {
 // chunk and whether it is salient are wavefront-uniform (scalar) values; only the column within the chunk is per lane.
 // All 16 wavefronts of a workgroup run this prologue at once, so it is kept free of divisions and loops: its scalar
 // instructions, issued for every wavefront, delay the first sign requests of the last wavefronts.
-template <int NT>
+template <int NT, int XU>
 struct Staged {
-  uint32_t v[B1<NT, 1>::KPT];    // x bits (global column) or the index (salient column)
-  uint32_t cs[B1<NT, 1>::KPT];   // column scale bits
-  uint32_t g[B1<NT, 1>::KPT];    // gathered x bits of salient columns
+  uint32_t v[B1<NT, 1, XU>::KPT];    // x bits (global column) or the index (salient column)
+  uint32_t cs[B1<NT, 1, XU>::KPT];   // column scale bits
+  uint32_t g[B1<NT, 1, XU>::KPT];    // gathered x bits of salient columns
   uint32_t sal;                  // bit m: the wavefront's chunk of its m-th staged unit is salient (or padding)
   uint32_t pad;                  // bit m: this lane's column of a global chunk is past the N input columns
   int32_t plane;                 // threads t < 2*XV: row-scale plane of chunk 2*sc(t/2) + (t&1)
@@ -95,9 +97,9 @@ __device__ __forceinline__ int staged_unit(int m) {
   return (__builtin_amdgcn_readfirstlane(int(threadIdx.x)) >> 8) + m * (NT / 256);
 }
 
-template <int NT>
-__device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, const int2* s_unit) {
-  using P = B1<NT, 1>;
+template <int NT, int XU>
+__device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT, XU>& sg, const int2* s_unit) {
+  using P = B1<NT, 1, XU>;
   const int t = threadIdx.x;
   const int col = t & 255;
   const int half = (__builtin_amdgcn_readfirstlane(t) >> 7) & 1;   // chunk of the super-chunk this wavefront covers
@@ -123,10 +125,10 @@ __device__ __forceinline__ void stage_issue(const GemmArgs& a, Staged<NT>& sg, c
   if (t < 2 * P::XV) sg.plane = a.chunk_plane[s_unit[t].y];
 }
 
-template <int NT>
-__device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT>& sg, float* xs, int64_t* s_roff,
+template <int NT, int XU>
+__device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT, XU>& sg, float* xs, int64_t* s_roff,
                                                    int sc0, int n) {
-  using P = B1<NT, 1>;
+  using P = B1<NT, 1, XU>;
   const int t = threadIdx.x;
   const int col = t & 255;
   if (t < 2 * P::XV) s_roff[t] = int64_t(sg.plane) * a.Mp * 2;
@@ -140,10 +142,10 @@ __device__ __forceinline__ void stage_write_global(const GemmArgs& a, Staged<NT>
   }
 }
 
-template <int NT>
-__device__ __forceinline__ void stage_write_salient(const GemmArgs& a, const Staged<NT>& sg, float* xs, int sc0,
+template <int NT, int XU>
+__device__ __forceinline__ void stage_write_salient(const GemmArgs& a, const Staged<NT, XU>& sg, float* xs, int sc0,
                                                     int n, int k_begin, int k_end) {
-  using P = B1<NT, 1>;
+  using P = B1<NT, 1, XU>;
   const int t = threadIdx.x;
   const int col = t & 255;
 #pragma unroll
@@ -532,12 +534,12 @@ __device__ __forceinline__ void issue_rscale_any(const GemmArgs& a, const Cursor
   }
 }
 
-template <int MU, int NT, int RPT, int D, int K, int FG>
+template <int MU, int NT, int RPT, int D, int K, int FG, int XU>
 __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st, Cursor<NT, RPT>& cur,
                                          Ring<RPT, FG> (&ring)[D + 1], float* lut, float* xs,
                                          const LaneConsts<FG>& lc, bool hb, const int64_t* s_roff,
-                                         const Staged<NT>& sg, int sc0) {
-  constexpr int XV = B1<NT, 1>::XV;
+                                         const Staged<NT, XU>& sg, int sc0) {
+  constexpr int XV = XU;
   if constexpr (K < XV) {
     if (K >= st.n) return;
     constexpr int BUF = K & 1;
@@ -553,7 +555,7 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
       else
         build_b1_mu4<NT, BUF ^ 1>(lut, xs + (K + 1) * 256);
     }
-    if constexpr (K == 0) stage_write_salient<NT>(a, sg, xs, sc0, st.n, 2, XV);   // built from step 1 on
+    if constexpr (K == 0) stage_write_salient<NT, XU>(a, sg, xs, sc0, st.n, 2, XV);   // built from step 1 on
     if constexpr (MU == 8 && FG > 0) {
       if (2 * st.sc >= a.nfc) {
         if constexpr (FG == 16)
@@ -584,7 +586,7 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
       st.sc = 0;
       ++st.tile;
     }
-    steps_b1<MU, NT, RPT, D, K + 1, FG>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
+    steps_b1<MU, NT, RPT, D, K + 1, FG, XU>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
   }
 }
 
@@ -592,12 +594,12 @@ __device__ __forceinline__ void steps_b1(const GemmArgs& a, B1State<NT, RPT>& st
 // columns per group, their global chunks one scale per chunk); mu = 8 only. Such layers need at most 128 VGPRs for
 // four waves per SIMD (one 1024- or two 512-thread workgroups per CU), which the second launch bound (minimum waves
 // per SIMD) asks of the compiler.
-template <int MU, int NT, int RPT, int D, bool EARLY, int FG>
+template <int MU, int NT, int RPT, int D, bool EARLY, int FG, int XU = b1_max_units(NT)>
 __global__ void __launch_bounds__(NT, FG ? 4 : 1) k_gemv_b1(GemmArgs a) {
   static_assert(FG == 0 || MU == 8, "fine row-scale groups: mu = 8 only (mu = 4 layers with them run the generic kernel)");
   // mu = 8: 64 KB, two buffers interleaved per pattern; mu = 4: two buffers of 8 KB
   __shared__ __attribute__((aligned(16))) float lut[MU == 8 ? 256 * 64 : 2 * 2048];
-  constexpr int XV = B1<NT, 1>::XV;
+  constexpr int XV = XU;
   __shared__ __attribute__((aligned(16))) float xs[XV * 256];  // staged folded activations
   __shared__ __attribute__((aligned(16))) int64_t s_roff[2 * XV];   // row-scale plane byte offsets, staged units
   __shared__ int s_flag;
@@ -663,20 +665,20 @@ __global__ void __launch_bounds__(NT, FG ? 4 : 1) k_gemv_b1(GemmArgs a) {
   // scales of units 0..D-1 are requested after the first barrier, from the plane offsets staged in LDS (a unit's row
   // scales are used last, after all its lookups), and the tables of unit 0 are built right after.
   const bool hb = ((t >> 4) & 1) != 0;
-  Staged<NT> sg;
+  Staged<NT, XU> sg;
   const int sc0 = st.sc;
-  stage_issue<NT>(a, sg, s_unit);
+  stage_issue<NT, XU>(a, sg, s_unit);
   Cursor<NT, RPT> cur;
   cursor_init<NT, RPT>(a, cur, st.tile, st.sc);
   Ring<RPT, FG> ring[D + 1];
   Cursor<NT, RPT> cur0 = cur;
-  if constexpr (!EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);   // n <= XV (launch plan)
+  if constexpr (!EARLY) stage_write_global<NT, XU>(a, sg, xs, s_roff, sc0, st.n);   // n <= XV (launch plan)
 #pragma unroll
   for (int k = 0; k < D; ++k) {   // units 0..D-1 (the dummy region past the end)
     issue_signs<NT, RPT, FG>(a, cur, ring[k]);
     cursor_advance<NT, RPT>(a, cur, k + 1 < st.n);
   }
-  if constexpr (EARLY) stage_write_global<NT>(a, sg, xs, s_roff, sc0, st.n);
+  if constexpr (EARLY) stage_write_global<NT, XU>(a, sg, xs, s_roff, sc0, st.n);
 
   // Per-lane byte offsets of the table columns read at step q: rows are congruent to t modulo 32. Byte bb of c1[m] is
   // (hb << 6) | (s << 2) with s = (t + 4m + bb) mod 16 (the four bytes at once: no byte exceeds 18 before the mask).
@@ -696,7 +698,7 @@ __global__ void __launch_bounds__(NT, FG ? 4 : 1) k_gemv_b1(GemmArgs a) {
   }
   if constexpr (FG == 8) rotation_consts(t, FG, hb, lc.fs1, lc.fs2);
 
-  stage_write_salient<NT>(a, sg, xs, sc0, st.n, 0, 2);
+  stage_write_salient<NT, XU>(a, sg, xs, sc0, st.n, 0, 2);
   __syncthreads();
   // the row scales of units 0..D-1, from the plane offsets just staged (they are used last in a unit's lookups)
 #pragma unroll
@@ -711,7 +713,7 @@ __global__ void __launch_bounds__(NT, FG ? 4 : 1) k_gemv_b1(GemmArgs a) {
   else
     build_b1_mu4<NT, 0>(lut, xs);
   __syncthreads();
-  steps_b1<MU, NT, RPT, D, 0, FG>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
+  steps_b1<MU, NT, RPT, D, 0, FG, XU>(a, st, cur, ring, lut, xs, lc, hb, s_roff, sg, sc0);
   const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
   publish_pending<NT, RPT, 1>(a, pend0, st.last_tile, st.n_pending, &s_flag);
 }
@@ -757,7 +759,7 @@ void launch_reduce_split(const GemmArgs& a, int bp, int R, hipStream_t stream) {
 
 // Stream probe: the batch-1 kernel's sign and row-scale requests (same plan, cursor, ring depth and per-unit barrier)
 // without the table work; each unit's words are folded into a checksum so the loads are not removed.
-template <int NT, int D>
+template <int NT, int D, int XU = b1_max_units(NT)>
 __global__ void __launch_bounds__(NT) k_stream_probe(GemmArgs a, uint32_t* sink) {
   const int u0 = first_unit(a, blockIdx.x);
   const int u1 = first_unit(a, blockIdx.x + 1);
@@ -779,7 +781,7 @@ __global__ void __launch_bounds__(NT) k_stream_probe(GemmArgs a, uint32_t* sink)
     if (++sck == a.steps) sck = 0;
   }
 #pragma unroll
-  for (int k = 0; k < B1<NT, 1>::XV; ++k) {   // n <= XV (launch plan); unrolled so the ring stays in registers
+  for (int k = 0; k < XU; ++k) {   // n <= XU (launch plan); unrolled so the ring stays in registers
     if (k < n) {
       Ring<1>& nx = ring[(k + D) % (D + 1)];
       issue_signs<NT, 1, 0>(a, cur, nx);
@@ -1090,7 +1092,16 @@ static bool launch_b1_d(const GemmArgs& a, int depth, int fg, hipStream_t stream
 }
 
 template <int MU, int NT, int RPT>
-static bool launch_b1(const GemmArgs& a, int depth, bool early, int fg, hipStream_t stream) {
+static bool launch_b1(const GemmArgs& a, int depth, bool early, int fg, int xv, hipStream_t stream) {
+  if (xv == kB1BigUnits) {   // the launch plan takes it for mu = 8, 1024 threads, one unit ahead, staged first only
+    if constexpr (MU == 8 && NT == 1024 && RPT == 1) {
+      if (depth != 1 || early || fg) return false;
+      hipLaunchKernelGGL((k_gemv_b1<8, 1024, 1, 1, false, 0, kB1BigUnits>), dim3(unsigned(a.blocks)), dim3(1024), 0,
+                         stream, a);
+      return true;
+    }
+    return false;
+  }
   return early ? launch_b1_d<MU, NT, RPT, true>(a, depth, fg, stream)
                : launch_b1_d<MU, NT, RPT, false>(a, depth, fg, stream);
 }
@@ -1145,7 +1156,8 @@ fluxbin_status launch_stream_probe(const fluxbin_layer& L, const Plan& p, uint32
   a.n_tiles = int32_t(p.n_tiles);
   const dim3 grid(unsigned(p.blocks));
   bool ok = true;
-  switch (p.nt * 10 + p.depth) {
+  switch (p.xv == kB1BigUnits ? -1 : p.nt * 10 + p.depth) {
+    case -1: hipLaunchKernelGGL((k_stream_probe<1024, 1, kB1BigUnits>), grid, dim3(1024), 0, stream, a, d_sink); break;
     case 10241: hipLaunchKernelGGL((k_stream_probe<1024, 1>), grid, dim3(1024), 0, stream, a, d_sink); break;
     case 10242: hipLaunchKernelGGL((k_stream_probe<1024, 2>), grid, dim3(1024), 0, stream, a, d_sink); break;
     case 10243: hipLaunchKernelGGL((k_stream_probe<1024, 3>), grid, dim3(1024), 0, stream, a, d_sink); break;
@@ -1203,12 +1215,12 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   const int fg = fine ? (d.Gcg == 1 ? int(d.Gcs) : -1) : 0;   // batch-1 fine instances: salient groups only
   if (p.kernel == 0) {
     switch (p.nt) {   // one row per thread (the launch plan's only choice for this kernel)
-      case 256: ok = L.shape.mu == 8 ? launch_b1<8, 256, 1>(a, p.depth, p.early, fg, stream)
-                                     : launch_b1<4, 256, 1>(a, p.depth, p.early, fg, stream); break;
-      case 512: ok = L.shape.mu == 8 ? launch_b1<8, 512, 1>(a, p.depth, p.early, fg, stream)
-                                     : launch_b1<4, 512, 1>(a, p.depth, p.early, fg, stream); break;
-      case 1024: ok = L.shape.mu == 8 ? launch_b1<8, 1024, 1>(a, p.depth, p.early, fg, stream)
-                                      : launch_b1<4, 1024, 1>(a, p.depth, p.early, fg, stream); break;
+      case 256: ok = L.shape.mu == 8 ? launch_b1<8, 256, 1>(a, p.depth, p.early, fg, p.xv, stream)
+                                     : launch_b1<4, 256, 1>(a, p.depth, p.early, fg, p.xv, stream); break;
+      case 512: ok = L.shape.mu == 8 ? launch_b1<8, 512, 1>(a, p.depth, p.early, fg, p.xv, stream)
+                                     : launch_b1<4, 512, 1>(a, p.depth, p.early, fg, p.xv, stream); break;
+      case 1024: ok = L.shape.mu == 8 ? launch_b1<8, 1024, 1>(a, p.depth, p.early, fg, p.xv, stream)
+                                      : launch_b1<4, 1024, 1>(a, p.depth, p.early, fg, p.xv, stream); break;
       default: ok = false;
     }
   } else if (p.kernel == 2) {
