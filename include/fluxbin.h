@@ -266,12 +266,12 @@ fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16
  *                                         balanced unit ranges; -1 ranges aligned to row tiles where that fits one
  *                                         wave of workgroups; k > 0 aligned ranges, k workgroups per tile (clamped to
  *                                         what the unit cap and the tile allow)
- *   b1_big         FLUXBIN_B1_BIG         batch 1: 0 at most 16 units per 1024-thread workgroup; -1 up to 24 where
- *                                         that fits a layer into one wave of workgroups
+ *   big_units      FLUXBIN_BIG_UNITS      batch-1 and LUT batch kernels: 0 at most 16 / 12 units per 1024-thread
+ *                                         workgroup; -1 up to 24 where that fits a layer into one wave of workgroups
  */
 typedef struct {
   int32_t nt, min_units, blocks, blocks_per_cu, depth, mfma_depth, early, rpt, mfma, generic, mfma_r2, bat_r2, rows,
-      batch_tile, mfma_rows, align, b1_big;
+      batch_tile, mfma_rows, align, big_units;
 } fluxbin_tuning;
 fluxbin_status fluxbin_get_tuning(fluxbin_tuning* out);
 fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);

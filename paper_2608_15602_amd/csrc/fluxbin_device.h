@@ -249,7 +249,8 @@ __device__ __forceinline__ int32_t load_uniform_i32(const int32_t* p, int i) {
 // Small-batch mu = 8 kernel (fluxbin_gemm_batch.hip): launches k_gemm_mu8_batch with n_groups groups of nb (2 or 4)
 // batch rows and depth units of sign data requested ahead; with reduce2 (one group, depth 1) the split tiles are
 // reduced by a second kernel instead of the tile counters; false if no instance exists.
-bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, bool reduce2, hipStream_t stream);
+// mx: kBigUnits for the instance staging up to that many units per workgroup (launch plan), else 0
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, bool reduce2, int mx, hipStream_t stream);
 
 // Split tiles of a launch whose kernel stored every contributor's partial sums and skipped the tile counters, reduced
 // by a second kernel over the whole chip (fluxbin_gemv.hip): bp padded batch rows, R rows per tile (a multiple of 256).

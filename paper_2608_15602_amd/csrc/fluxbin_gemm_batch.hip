@@ -254,30 +254,33 @@ struct BatState {
   float acc[1][NB];
 };
 
-// Row-scale plane of chunk 2*sc(k) + half of unit k (clamped), from the table staged in LDS.
+// Row-scale plane of chunk 2*sc(k) + half of unit k (clamped to the MX staged units), from the table staged in LDS.
+template <int MX>
 __device__ __forceinline__ int32_t bat_plane(const int* s_planes, int k, int half) {
-  return __builtin_amdgcn_readfirstlane(s_planes[2 * (k < kBatMaxUnits ? k : kBatMaxUnits - 1) + half]);
+  return __builtin_amdgcn_readfirstlane(s_planes[2 * (k < MX ? k : MX - 1) + half]);
 }
 
-// Unit K of the workgroup (compile-time K, at most kBatMaxUnits units), in two sub-steps.
+// Unit K of the workgroup (compile-time K, at most MX units: kBatMaxUnits, or kBigUnits for the instance of layers
+// that would otherwise need a second wave of workgroups), in two sub-steps.
 // Sub-step 0: request unit K+4's activations into a free set of staging registers and unit K+D's signs into the ring
 // slot unit K-1 used (D+1 units of sign data in flight at every wait); build chunk 1's tables into buffer 1; look up
 // chunk 0 (buffer 0).
 // Sub-step 1: write unit K+2's activations (requested two units earlier) into the staging slot unit K no longer
 // needs; build unit K+1's chunk 0 into buffer 0; look up chunk 1. Each wait covers loads that the step needs anyway:
 // the staging loads waited for were issued before the sign loads of unit K+D-2.
-template <int D, int K, int NB>
+template <int D, int K, int NB, int MX>
 __device__ __forceinline__ void bat_units(const GemmArgs& a, BatState<NB>& st, BatCursor& cur, BatRing (&ring)[D + 1],
                                           BatStageCursor& scur, BatStage (&sr)[3], uint32_t xrow, float* tbl,
                                           float* xs, const uint16_t* s_xidx, const int* s_planes,
                                           const uint32_t (&cq)[4], bool swap) {
-  if constexpr (K < kBatMaxUnits) {
+  if constexpr (K < MX) {
     if (K >= st.n) return;
     // sub-step 0
     bat_stage_load(a, s_xidx, scur, st.n, xrow, sr[(K + 4) % 3]);   // unit K+4
     bat_stage_cursor_next(a, scur);
     bat_issue_signs(a, cur, ring[(K + D) % (D + 1)]);
-    bat_issue_rscale(a, cur, bat_plane(s_planes, K + D, 0), bat_plane(s_planes, K + D, 1), ring[(K + D) % (D + 1)]);
+    bat_issue_rscale(a, cur, bat_plane<MX>(s_planes, K + D, 0), bat_plane<MX>(s_planes, K + D, 1),
+                     ring[(K + D) % (D + 1)]);
     bat_cursor_advance(a, cur, K + D + 1 < st.n);
     bat_build<NB>(tbl + Bat::TBL, xs + (K & 1) * Bat::XS + Bat::XC);
     bat_lookup<0, NB>(tbl, ring[K % (D + 1)], cq, swap, st.acc);
@@ -302,16 +305,16 @@ __device__ __forceinline__ void bat_units(const GemmArgs& a, BatState<NB>& st, B
       st.sc = 0;
       ++st.tile;
     }
-    bat_units<D, K + 1, NB>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
+    bat_units<D, K + 1, NB, MX>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
   }
 }
 
-template <int D, int NB, bool R2>
+template <int D, int NB, bool R2, int MX = kBatMaxUnits>
 __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   __shared__ __attribute__((aligned(16))) float tbl[2 * Bat::TBL];   // 128 KB: buffer 0 chunk 0, buffer 1 chunk 1
   __shared__ __attribute__((aligned(16))) float xs[2 * Bat::XS];      // staged activations, two units
-  __shared__ uint16_t s_xidx[kBatMaxUnits * 256];                      // VCM indices of the workgroup's units
-  __shared__ int s_planes[2 * kBatMaxUnits];                           // row-scale planes of their chunks
+  __shared__ uint16_t s_xidx[MX * 256];                                // VCM indices of the workgroup's units
+  __shared__ int s_planes[2 * MX];                                     // row-scale planes of their chunks
   __shared__ int s_flag;
 
   // This workgroup's group of NB batch rows, with its own slice of the workspace (counters, then partial sums).
@@ -348,7 +351,7 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
     if (++sc == a.steps) sc = 0;
   }
   if (has_sal) {
-    constexpr int PER = kBatMaxUnits * 256 / 1024;
+    constexpr int PER = MX * 256 / 1024;
     uint16_t xi[PER];
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
@@ -363,14 +366,14 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   }
 
   // Prologue order: the row-scale planes of the workgroup's chunks (lane 2k+h of a register loads unit k's chunk
-  // 2sc+h; units past the range repeat valid chunks; the launch plan keeps n <= kBatMaxUnits), the activations of
+  // 2sc+h; units past the range repeat valid chunks; the launch plan keeps n <= MX), the activations of
   // units 0 and 1, the sign data of units 0..D-1, then (each wait covering only older loads) their row scales once the
   // planes are in, the staging of units 0 and 1, and units 2 and 3's activations into the staging registers. The
   // planes reach LDS for the steps through the barrier before the first table build.
   int32_t planes;
   {
     const int lane = t & 63;
-    int sc = st.sc + (lane >> 1) % kBatMaxUnits;
+    int sc = st.sc + (lane >> 1) % MX;
     while (sc >= a.steps) sc -= a.steps;
     planes = a.chunk_plane[2 * sc + (lane & 1)];
   }
@@ -398,7 +401,7 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
                      ring[k]);
     bat_cursor_advance(a, cur0, k + 1 < st.n);
   }
-  if (t < 2 * kBatMaxUnits) s_planes[t] = planes;
+  if (t < 2 * MX) s_planes[t] = planes;
   bat_stage_write(xs, r0);
   bat_stage_write(xs + Bat::XS, r1);
   BatStage sr[3];
@@ -417,7 +420,7 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
   __syncthreads();
   bat_build<NB>(tbl, xs);   // unit 0, chunk 0
   __syncthreads();
-  bat_units<D, 0, NB>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
+  bat_units<D, 0, NB, MX>(a, st, cur, ring, scur, sr, xrow, tbl, xs, s_xidx, s_planes, cq, swap);
   if constexpr (!R2) {   // else the split tiles are reduced by k_reduce_split after this kernel
     const int pend0 = st.first_shared ? st.first_tile : st.last_tile;
     publish_pending<1024, 1, NB>(a, pend0, st.last_tile, st.n_pending, &s_flag);
@@ -425,8 +428,14 @@ __global__ void __launch_bounds__(1024) k_gemm_mu8_batch(GemmArgs args) {
 }
 
 template <int NB>
-static bool launch_batch_nb(const GemmArgs& a, int n_groups, int depth, bool reduce2, hipStream_t stream) {
+static bool launch_batch_nb(const GemmArgs& a, int n_groups, int depth, bool reduce2, int mx, hipStream_t stream) {
   const dim3 grid(unsigned(a.blocks), unsigned(n_groups));
+  if (mx == kBigUnits) {   // the launch plan takes it with the second-kernel reduction only
+    if (!reduce2 || n_groups != 1 || depth != 1) return false;
+    hipLaunchKernelGGL((k_gemm_mu8_batch<1, NB, true, kBigUnits>), grid, dim3(1024), 0, stream, a);
+    launch_reduce_split(a, NB, 1024, stream);
+    return true;
+  }
   if (reduce2) {   // one batch group, depth 1 (launch plan): the partial sums are laid out as k_reduce_split reads them
     if (n_groups != 1 || depth != 1) return false;
     hipLaunchKernelGGL((k_gemm_mu8_batch<1, NB, true>), grid, dim3(1024), 0, stream, a);
@@ -441,10 +450,10 @@ static bool launch_batch_nb(const GemmArgs& a, int n_groups, int depth, bool red
   return false;
 }
 
-bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, bool reduce2, hipStream_t stream) {
+bool launch_gemm_batch(const GemmArgs& a, int n_groups, int depth, int nb, bool reduce2, int mx, hipStream_t stream) {
   if (n_groups < 1 || n_groups > 4) return false;
-  if (nb == 2) return n_groups == 1 && launch_batch_nb<2>(a, n_groups, depth, reduce2, stream);
-  if (nb == 4) return launch_batch_nb<4>(a, n_groups, depth, reduce2, stream);
+  if (nb == 2) return n_groups == 1 && launch_batch_nb<2>(a, n_groups, depth, reduce2, mx, stream);
+  if (nb == 4) return launch_batch_nb<4>(a, n_groups, depth, reduce2, mx, stream);
   return false;
 }
 

@@ -41,7 +41,7 @@ namespace fluxbin {
 
 
 // XU: most units a workgroup stages (the launch plan keeps every workgroup within it): b1_max_units(NT), or
-// kB1BigUnits for the 1024-thread instance of layers that would otherwise need a second wave of workgroups.
+// kBigUnits for the 1024-thread instance of layers that would otherwise need a second wave of workgroups.
 template <int NT, int RPT, int XU = b1_max_units(NT)>
 struct B1 {
   static constexpr int R = NT * RPT;
@@ -1093,10 +1093,10 @@ static bool launch_b1_d(const GemmArgs& a, int depth, int fg, hipStream_t stream
 
 template <int MU, int NT, int RPT>
 static bool launch_b1(const GemmArgs& a, int depth, bool early, int fg, int xv, hipStream_t stream) {
-  if (xv == kB1BigUnits) {   // the launch plan takes it for mu = 8, 1024 threads, one unit ahead, staged first only
+  if (xv == kBigUnits) {   // the launch plan takes it for mu = 8, 1024 threads, one unit ahead, staged first only
     if constexpr (MU == 8 && NT == 1024 && RPT == 1) {
       if (depth != 1 || early || fg) return false;
-      hipLaunchKernelGGL((k_gemv_b1<8, 1024, 1, 1, false, 0, kB1BigUnits>), dim3(unsigned(a.blocks)), dim3(1024), 0,
+      hipLaunchKernelGGL((k_gemv_b1<8, 1024, 1, 1, false, 0, kBigUnits>), dim3(unsigned(a.blocks)), dim3(1024), 0,
                          stream, a);
       return true;
     }
@@ -1156,8 +1156,8 @@ fluxbin_status launch_stream_probe(const fluxbin_layer& L, const Plan& p, uint32
   a.n_tiles = int32_t(p.n_tiles);
   const dim3 grid(unsigned(p.blocks));
   bool ok = true;
-  switch (p.xv == kB1BigUnits ? -1 : p.nt * 10 + p.depth) {
-    case -1: hipLaunchKernelGGL((k_stream_probe<1024, 1, kB1BigUnits>), grid, dim3(1024), 0, stream, a, d_sink); break;
+  switch (p.xv == kBigUnits ? -1 : p.nt * 10 + p.depth) {
+    case -1: hipLaunchKernelGGL((k_stream_probe<1024, 1, kBigUnits>), grid, dim3(1024), 0, stream, a, d_sink); break;
     case 10241: hipLaunchKernelGGL((k_stream_probe<1024, 1>), grid, dim3(1024), 0, stream, a, d_sink); break;
     case 10242: hipLaunchKernelGGL((k_stream_probe<1024, 2>), grid, dim3(1024), 0, stream, a, d_sink); break;
     case 10243: hipLaunchKernelGGL((k_stream_probe<1024, 3>), grid, dim3(1024), 0, stream, a, d_sink); break;
@@ -1224,7 +1224,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
       default: ok = false;
     }
   } else if (p.kernel == 2) {
-    ok = !fine && launch_gemm_batch(a, p.n_groups, p.depth, p.bg, p.reduce2, stream);
+    ok = !fine && launch_gemm_batch(a, p.n_groups, p.depth, p.bg, p.reduce2, p.xv, stream);
   } else if (p.kernel == 3) {
     ok = !fine && launch_gemm_mfma(a, p.bpad, int(L.shape.mu), p.depth, p.reduce2, stream);
   } else if (p.kernel == 5) {

@@ -137,7 +137,7 @@ static fluxbin_tuning tuning_defaults() {
   t.batch_tile = 0;
   t.mfma_rows = -1;
   t.align = -1;
-  t.b1_big = -1;
+  t.big_units = -1;
   return t;
 }
 
@@ -170,7 +170,7 @@ static void tuning_init_locked() {
   t.batch_tile = env_int("FLUXBIN_BATCH_TILE", t.batch_tile);
   t.mfma_rows = env_int("FLUXBIN_MFMA_ROWS", t.mfma_rows);
   t.align = env_int("FLUXBIN_ALIGN", t.align);
-  t.b1_big = env_int("FLUXBIN_B1_BIG", t.b1_big);
+  t.big_units = env_int("FLUXBIN_BIG_UNITS", t.big_units);
   g_tuning = t;
   g_tuning_init = true;
 }
@@ -438,15 +438,21 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p, bool allow_rows
   // The batch-1 kernel stages the folded activations of all its units at once: at most b1_max_units(nt) per
   // workgroup. 1024-thread mu = 8 plans whose units need 17..24 per workgroup to fit one wave of workgroups (the fused
   // 57344x8192 gate|up layer with 3 bases: 5488 units, 21.4 per workgroup) take the instance that stages up to
-  // kB1BigUnits, one wave instead of two: 41.9 -> 39.3 us. FLUXBIN_B1_BIG=0 keeps them at 16 units.
+  // kBigUnits, one wave instead of two: 41.9 -> 39.3 us. FLUXBIN_BIG_UNITS=0 keeps them at 16 units.
   p->xv = 0;
-  if (p->kernel == 0 && p->nt == 1024 && L.shape.mu == 8 && !fine && p->depth == 1 && !p->early && tu.b1_big != 0 &&
+  if (p->kernel == 0 && p->nt == 1024 && L.shape.mu == 8 && !fine && p->depth == 1 && !p->early && tu.big_units != 0 &&
       blocks_env <= 0 && ceil_div(p->units, p->blocks) > b1_max_units(1024) &&
-      ceil_div(p->units, int64_t(cus) * per_cu) <= kB1BigUnits)
-    p->xv = kB1BigUnits;
+      ceil_div(p->units, int64_t(cus) * per_cu) <= kBigUnits)
+    p->xv = kBigUnits;
   const int64_t b1_cap = p->xv ? p->xv : b1_max_units(p->nt);
   if (p->kernel == 0 && ceil_div(p->units, p->blocks) > b1_cap) p->blocks = ceil_div(p->units, b1_cap);
-  if (p->kernel == 2 && ceil_div(p->units, p->blocks) > kBatMaxUnits) p->blocks = ceil_div(p->units, kBatMaxUnits);
+  // The same for the LUT batch kernel with the second-kernel reduction (one batch group, one unit ahead): up to
+  // kBigUnits instead of kBatMaxUnits where that fits the layer into one wave (fused gate|up, 4-base layers).
+  if (p->kernel == 2 && p->reduce2 && p->n_groups == 1 && p->depth == 1 && tu.big_units != 0 && blocks_env <= 0 &&
+      ceil_div(p->units, p->blocks) > kBatMaxUnits && ceil_div(p->units, int64_t(cus) * per_cu) <= kBigUnits)
+    p->xv = kBigUnits;
+  const int64_t bat_cap = p->kernel == 2 && p->xv ? p->xv : kBatMaxUnits;
+  if (p->kernel == 2 && ceil_div(p->units, p->blocks) > bat_cap) p->blocks = ceil_div(p->units, bat_cap);
   // the matrix-core kernel: at least three units per workgroup (fewer split tiles to reduce, each workgroup's start-up
   // amortized), as long as that leaves a workgroup for every CU. 7B MLP layers (about 1400 units), us per call up / down
   // at 768 -> 512 -> 256 workgroups: B = 8 17.0 / 19.5 -> 14.7 / 16.7 -> 16.4 / 16.6, B = 16 22.6 / 24.7 -> 17.9 /
@@ -476,7 +482,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p, bool allow_rows
   p->kpt = 0;
   if ((p->kernel == 0 || p->kernel == 2 || p->kernel == 3) && tu.align != 0 && blocks_env <= 0 && p->n_tiles > 0) {
     const int64_t steps = p->units / p->n_tiles;
-    const int64_t cap = p->kernel == 0 ? b1_cap : (p->kernel == 2 ? kBatMaxUnits : kMfMaxUnits);
+    const int64_t cap = p->kernel == 0 ? b1_cap : (p->kernel == 2 ? bat_cap : kMfMaxUnits);
     const int64_t k_round = (p->blocks + p->n_tiles / 2) / p->n_tiles;
     const int64_t k_units = ceil_div(steps, ceil_div(p->units, p->blocks));
     int64_t kpt = tu.align > 0 ? tu.align : (k_round > k_units ? k_round : k_units);

@@ -18,10 +18,10 @@ constexpr int kRwSteps = 16;            // row-complete batch-1 kernel: super-ch
 // Units per workgroup of the batch-1 kernel (its LDS staging capacity): 16 for 1024-thread workgroups (one per CU),
 // 12 for the smaller ones (two or more share a CU's LDS).
 constexpr int b1_max_units(int nt) { return nt == 1024 ? 16 : 12; }
-// The 1024-thread mu = 8 instance that stages up to 24 units, for layers with 17..24 units per workgroup in one wave of
-// workgroups (with 16 they would need a second wave). A separate instance: its prologue issues six staging loads per
-// thread instead of four, which costs the layers that fit 16.
-constexpr int kB1BigUnits = 24;
+// The instances that stage up to 24 units per 1024-thread workgroup (batch-1 mu = 8 kernel, LUT batch kernel), for
+// layers that then fit one wave of workgroups (with 16 or 12 units they would need a second wave). Separate instances:
+// the batch-1 prologue then issues six staging loads per thread instead of four, which costs the layers that fit 16.
+constexpr int kBigUnits = 24;
 constexpr int kBatMaxUnits = 12;        // units per workgroup of the small-batch mu = 8 kernel (its LDS index table)
 constexpr int kMfMaxUnits = 16;         // units per workgroup of the matrix-core small-batch kernel (unrolled steps)
 // Matrix-core kernel with bp padded batch rows (4, 8, 16 or 32): dwords per (chunk, column group, K step) block of a
@@ -151,7 +151,7 @@ struct Plan {
   uint64_t ws_counters_off, ws_partials_off, ws_bytes;
   uint64_t ws_image_off;   // matrix-core kernel: activation images after the partial sums (0 for other kernels)
   int kpt;                 // split-tile kernels: workgroups per tile with tile-aligned unit ranges (0: balanced split)
-  int xv;                  // batch-1 kernel: kB1BigUnits for the instance staging that many units, else 0
+  int xv;                  // batch-1 and LUT batch kernels: kBigUnits for the instance staging that many units, else 0
 };
 
 // allow_rows = false: never the row-complete batch-1 kernel (the stream probe follows the split-tile kernel's plan)

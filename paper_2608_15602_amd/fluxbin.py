@@ -64,7 +64,7 @@ class Layer(ctypes.Structure):
 class Tuning(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("nt", "min_units", "blocks", "blocks_per_cu", "depth", "mfma_depth",
                                              "early", "rpt", "mfma", "generic", "mfma_r2", "bat_r2", "rows",
-                                             "batch_tile", "mfma_rows", "align", "b1_big")]
+                                             "batch_tile", "mfma_rows", "align", "big_units")]
 
 
 class PlanInfo(ctypes.Structure):

@@ -197,28 +197,30 @@ def test_fused_decoder_layers_full_size():
         torch.cuda.empty_cache()
 
 
-def test_batch1_24_unit_instance_full_size():
-    """The fused 3 bases + 5% gate|up layer (57344 x 8192, 5488 units) at batch 1 on the instance that stages up to 24
-    units per 1024-thread workgroup (one wave of 256 workgroups, the default) and with the 16-unit cap (two waves of
-    256), sampled rows at full size, and determinism of the first."""
+@pytest.mark.parametrize("B", [1, 2, 4])
+def test_24_unit_instances_full_size(B):
+    """The fused 3 bases + 5% gate|up layer (57344 x 8192, 5488 units) on the instances that stage up to 24 units per
+    1024-thread workgroup (batch-1 kernel at B = 1, LUT batch kernel at B = 2 and 4: one wave of 256 workgroups, the
+    default) and with the 16 / 12-unit caps (two waves), sampled rows at full size, and determinism of the first."""
     import torch
     from paper_2608_15602_amd import fluxbin as fb
     from synth import fused_decoder_layers
     spec = [s for s in fused_decoder_layers("128") if s.name == "3b5pct_gate_up"][0]
     L = make_layer(spec)
     packed = pack_layer(L)
-    rows = sample_rows(spec.M, 256, seed=24)
-    x = make_activations(L, 1)
+    rows = sample_rows(spec.M, 256, seed=24 + B)
+    x = make_activations(L, B)
     y_ref = oracle.gemv_dense(L, x, rows=rows)
+    kernel = "batch1" if B == 1 else "lut_batch"
     for big, wgs in (("-1", 256), ("0", 512)):
-        log(f"case 57344x8192 batch 1, b1_big={big}")
-        with fb.tuning(b1_big=int(big)):
-            info = fb.fluxbin_plan_query(packed, 1)
-            assert info["kernel_name"] == "batch1" and info["workgroups"] == wgs, info
+        log(f"case 57344x8192 B={B}, big_units={big}")
+        with fb.tuning(big_units=int(big)):
+            info = fb.fluxbin_plan_query(packed, B)
+            assert info["kernel_name"] == kernel and info["workgroups"] == wgs, info
             y = run_gemm(packed, x, out_fp32=True)
             if big == "-1":
                 assert np.array_equal(run_gemm(packed, x, out_fp32=True), y), "repeat differs"
-        _check(y[:, rows], y_ref, f"b1_big={big}")
+        _check(y[:, rows], y_ref, f"big_units={big}")
     del packed
     torch.cuda.empty_cache()
 
