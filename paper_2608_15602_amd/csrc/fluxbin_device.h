@@ -268,6 +268,7 @@ bool launch_gemm_mfma_rows(const GemmArgs& a, int bpad, int mu, int waves, int r
 // (4, 8 or 16) wavefronts, every super-chunk of them, `depth` (2, 4 or 6) units requested ahead, fg (0, or 8 / 16 fine
 // groups per salient chunk at mu = 8) as the batch-1 kernel's, no workspace; false if the layer is outside its limits
 // (B = 1, N <= kRwMaxN, NSC <= min(waves, 8) * kRwSteps) or no instance exists.
-bool launch_gemv_rows(const GemmArgs& a, int mu, int waves, int depth, int fg, hipStream_t stream);
+// rb: 1 (16 rows per workgroup) or 2 (32 rows: each lane two rows; mu = 8 without fine groups)
+bool launch_gemv_rows(const GemmArgs& a, int mu, int waves, int depth, int fg, int rb, hipStream_t stream);
 
 }  // namespace fluxbin

@@ -1230,7 +1230,7 @@ fluxbin_status launch_gemm(const fluxbin_layer& L, const Plan& p, int B, const u
   } else if (p.kernel == 5) {
     ok = !fine && launch_gemm_mfma_rows(a, p.bpad, int(L.shape.mu), p.nt / 64, p.rows / 16, stream);
   } else if (p.kernel == 4) {
-    ok = fg >= 0 && launch_gemv_rows(a, int(L.shape.mu), p.nt / 64, p.depth, fg, stream);
+    ok = fg >= 0 && launch_gemv_rows(a, int(L.shape.mu), p.nt / 64, p.depth, fg, p.rows / 16, stream);
   } else if (L.shape.mu == 8) {
     ok = launch_gen_mu<8>(a, p, stream);
   } else {

@@ -204,14 +204,32 @@ static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tunin
 // attention 4096x4096 (2+1, 2%) 8.26 -> 5.98, 2048x4096 7.79 -> 5.31, 3072x4096 3+1 (49 super-chunks) 8.40 -> 7.00,
 // 1024x8192 2+1 (65) 8.36 -> 7.20, 1024x8192 3+1 (98) 9.35 -> 9.05; even or slower with more super-chunks per
 // wavefront: 4096x11008 2b (86) 9.47 -> 9.68. FLUXBIN_ROWS=1 / 0 forces the choice where the layer allows it.
-static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const fluxbin_tuning& tu) {
+// *rb: rows per lane, 1 (16 rows per workgroup) or 2 (32 rows, mu = 8 without fine groups).
+static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const fluxbin_tuning& tu, int* rb) {
   const bool fine_ok = dv.Gcg == 1 && (dv.Gcs == 1 || (L.shape.mu == 8 && (dv.Gcs == 8 || dv.Gcs == 16)));
+  *rb = 1;
   if (!fine_ok || L.shape.N > kRwMaxN || L.NSC > 8 * kRwSteps) return false;
   // its buffer loads take 32-bit offsets into the sign and row-scale sections
   if (dv.NCP * dv.Mp * 16 >= (int64_t(1) << 31) || dv.NRP * dv.Mp * 2 >= (int64_t(1) << 31)) return false;
+  const bool rb2_ok = L.shape.mu == 8 && dv.Gcg == 1 && dv.Gcs == 1;
+  if (tu.rows == 2) {
+    *rb = 2;
+    return rb2_ok;
+  }
   if (tu.rows == 0 || tu.rows == 1) return tu.rows == 1;
   const int64_t wgs = ceil_div(L.shape.M, 16);
-  return wgs <= cus && (L.NSC <= 64 || (L.NSC <= 128 && 4 * wgs <= cus));
+  if (wgs <= cus) return L.NSC <= 64 || (L.NSC <= 128 && 4 * wgs <= cus);
+  // Two rows per lane where 32-row workgroups fill the CUs once (more than half of them, at most one each) and each
+  // workgroup's table work stays small: 8192 x 8192 with 2 bases + 1% (65 super-chunks, 256 workgroups) 12.2 -> 11.0
+  // us against the split-tile kernel. With more workgroups than CUs the second workgroups on a CU double its time
+  // (11008 rows: 344 workgroups, no faster), with fewer the idle CUs cost more than the reduction saved (4096 rows:
+  // 5.7 -> 6.6 us), and 98 super-chunks (3 bases + 5%) were slower.
+  const int64_t wgs32 = ceil_div(L.shape.M, 32);
+  if (rb2_ok && 2 * wgs32 > cus && wgs32 <= cus && L.NSC <= 80) {
+    *rb = 2;
+    return true;
+  }
+  return false;
 }
 
 // Row-complete matrix-core kernel for B = 2..8 (16 or 32 rows per workgroup, every super-chunk of them, no split
@@ -279,18 +297,20 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p, bool allow_rows
   // the batch-1 instances for fine groups: salient side only, 8 or 16 groups per chunk (s = 16 or 8 at mu = 8)
   const bool b1_fine_ok = L.shape.mu == 8 && dv.Gcg == 1 && (dv.Gcs == 8 || dv.Gcs == 16);
   p->nt = 256;
-  if (B == 1 && !force_generic && allow_rows && use_rows(L, dv, cus, tu)) {
-    // row-complete batch-1 kernel: 16 rows per workgroup, every super-chunk of them, no cross-workgroup reduction;
-    // 16 wavefronts, two units requested ahead (4 and 8 wavefronts, and 4 or 6 units ahead, measured slower or equal)
+  int rw_rb = 1;
+  if (B == 1 && !force_generic && allow_rows && use_rows(L, dv, cus, tu, &rw_rb)) {
+    // row-complete batch-1 kernel: 16 rows per workgroup (32 with two rows per lane), every super-chunk of them, no
+    // cross-workgroup reduction; 16 wavefronts, two units requested ahead (4 and 8 wavefronts, and 4 or 6 units ahead,
+    // measured slower or equal)
     p->kernel = 4;
-    p->nt = (tu.nt == 256 && L.NSC <= 4 * kRwSteps) ? 256 : (tu.nt == 512 ? 512 : 1024);
+    p->nt = rw_rb == 2 ? 1024 : ((tu.nt == 256 && L.NSC <= 4 * kRwSteps) ? 256 : (tu.nt == 512 ? 512 : 1024));
     p->rpt = 1;
-    p->rows = 16;
-    p->depth = (tu.depth == 4 || tu.depth == 6) ? tu.depth : 2;
+    p->rows = 16 * rw_rb;
+    p->depth = rw_rb == 2 ? 2 : ((tu.depth == 4 || tu.depth == 6) ? tu.depth : 2);
     p->bg = 1;
     p->n_groups = 1;
     p->bpad = 1;
-    p->n_tiles = ceil_div(L.shape.M, 16);
+    p->n_tiles = ceil_div(L.shape.M, p->rows);
     p->units = p->n_tiles * L.NSC;
     p->blocks = p->n_tiles;
     p->ws_counters_off = 0;
