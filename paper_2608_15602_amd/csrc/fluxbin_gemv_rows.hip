@@ -53,7 +53,7 @@ struct RwRegs {
 template <int RB>
 struct RwLane {
   int t, lane, w, r, p;
-  uint32_t row[RB];   // the lane's output rows (< Mp): r and, with RB = 2, r + 16 of the workgroup
+  uint32_t row[RB];   // the lane's rows r, r + 16, ... of the workgroup (clamped to Mp - 1; rows >= M are not stored)
   int hb[RB];         // mu = 8: the row holds the chunk pair of a super-chunk swapped
   int tv;             // the lane's table: virtual column of its first column within a super-chunk (0..252)
   int hA;             // chunk of the lane's first eight lookups (rw_lookup)
@@ -221,12 +221,13 @@ struct RwKernel {
   }
 };
 
-// RB = 2: each lane also handles the row 16 further (32 rows per workgroup, the tables of a unit serving twice the
-// rows); mu = 8 without fine groups only, where the second row's table columns are the first row's.
+// RB > 1: each lane also handles the rows 16, 32 further (16 RB rows per workgroup, the tables of a unit serving RB
+// times the rows); mu = 8 without fine groups only, where those rows' table columns are the first row's (rotation 2i
+// mod 32).
 template <int MU, int W, int D, int FG, int RB>
 __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   static_assert(FG == 0 || MU == 8, "fine row-scale groups: mu = 8 only");
-  static_assert(RB == 1 || (RB == 2 && MU == 8 && FG == 0), "two rows per lane: mu = 8, no fine groups");
+  static_assert(RB == 1 || ((RB == 2 || RB == 3) && MU == 8 && FG == 0), "several rows per lane: mu = 8, no fine groups");
   constexpr int NT = 64 * W;
   constexpr int ROWS = kRwRows * RB;
   extern __shared__ __attribute__((aligned(16))) uint16_t xl[];   // x: N fp16 (dynamic size, at most kRwMaxN)
@@ -243,9 +244,11 @@ __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   const int row0 = int(blockIdx.x) * ROWS;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    // < Mp: Mp is a multiple of 64, row0 < M and ROWS divides 64, so row0 + ROWS <= Mp
-    ln.row[rb] = uint32_t(row0 + ln.r + kRwRows * rb);
-    ln.hb[rb] = MU == 8 ? int((ln.row[rb] >> 4) & 1u) : 0;
+    // Mp is a multiple of 64 and row0 < M: with 16 or 32 rows per workgroup every row is below Mp; with 48 the last
+    // workgroup's rows past Mp - 1 read row Mp - 1 (same rotation parity, never stored)
+    const int r_raw = row0 + ln.r + kRwRows * rb;
+    ln.row[rb] = uint32_t(r_raw < a.Mp ? r_raw : a.Mp - 1);
+    ln.hb[rb] = MU == 8 ? int((uint32_t(row0 + ln.r + kRwRows * rb) >> 4) & 1u) : 0;
   }
   ln.tv = (ln.lane >> 5) * 128 + 4 * (ln.lane & 31);
   // Lookup order: at lookup k the lane reads chunk h_k = hA ^ (k >= 8) and its stored nibble 8p + j_k, canonical nibble
@@ -354,10 +357,13 @@ template <int W, int D>
 bool launch_rows_wd(const GemmArgs& a, int mu, int fg, int rb, hipStream_t stream) {
   const dim3 grid(unsigned((a.M + kRwRows * rb - 1) / (kRwRows * rb))), block(64 * W);
   const unsigned xl_bytes = unsigned(((a.N + 1) * 2 + 15) & ~15);   // x and one zero entry
-  if (rb == 2) {   // launch plan: mu = 8 without fine groups, 16 wavefronts, two units ahead
+  if (rb == 2 || rb == 3) {   // launch plan: mu = 8 without fine groups, 16 wavefronts, two units ahead
     if constexpr (W == 16 && D == 2) {
       if (mu != 8 || fg != 0) return false;
-      hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0, 2>), grid, block, xl_bytes, stream, a);
+      if (rb == 2)
+        hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0, 2>), grid, block, xl_bytes, stream, a);
+      else
+        hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0, 3>), grid, block, xl_bytes, stream, a);
       return true;
     }
     return false;

@@ -369,30 +369,33 @@ ROWS32_SPECS = [s for s in ROWS_SPECS if s.mu == 8 and "-s" not in s.name] + [
 ]
 
 
+@pytest.mark.parametrize("rb", [2, 3])
 @pytest.mark.parametrize("spec", ROWS32_SPECS, ids=lambda s: s.name)
-def test_rows_kernel_32_rows_matches_oracle(spec):
-    """The row-complete kernel's 32-row workgroups (two rows per lane, forced) on every row: ragged M below, across and
-    above 32, salient chunks or none, wide N; deterministic, the plan reports it; and a mu = 4 or fine-group layer,
-    which it does not take, keeps another kernel."""
+def test_rows_kernel_32_rows_matches_oracle(spec, rb):
+    """The row-complete kernel's 32- and 48-row workgroups (two or three rows per lane, forced) on every row: ragged M
+    below, across and above them (48-row workgroups past the padded rows), salient chunks or none, wide N;
+    deterministic, the plan reports it; and a mu = 4 or fine-group layer, which it does not take, keeps another
+    kernel."""
     from paper_2608_15602_amd import fluxbin as fb
     L = make_layer(spec)
     packed = pack_layer(L)
-    with fb.tuning(rows=2):
+    with fb.tuning(rows=rb):
         info = fb.fluxbin_plan_query(packed, 1)
-        assert info["kernel_name"] == "rows" and info["rows_per_tile"] == 32, info
+        assert info["kernel_name"] == "rows" and info["rows_per_tile"] == 16 * rb, info
         _, _, x, y = _parity(spec, 1, out_fp32=True, packed=packed, L=L)
         assert np.array_equal(run_gemm(packed, x, out_fp32=True), y), "repeat differs"
     other = LayerSpec("rows32_mu4", M=100, N=300, Kb=1, Ks=1, mu=4, S=20, g_r=128, g_s=20, seed=72)
-    with fb.tuning(rows=2):
+    with fb.tuning(rows=rb):
         assert fb.fluxbin_plan_query(pack_layer(make_layer(other)), 1)["kernel_name"] != "rows"
 
 
 @pytest.mark.parametrize("spec", [s for s in kernel_latency_layers() + config_layers("c3_mlp7b", "128")
                                   if "-s" not in s.name], ids=lambda s: s.name)
-def test_rows_kernel_32_rows_full_size(spec):
-    """The 32-row workgroups of the row-complete kernel (forced) on the App. E.4 shapes without fine groups and the 7B
-    MLP layers at full size, sampled rows against the oracle."""
-    _with_env({"FLUXBIN_ROWS": "2"}, lambda: _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=spec.M + 1)))
+@pytest.mark.parametrize("rb", [2, 3])
+def test_rows_kernel_32_rows_full_size(spec, rb):
+    """The 32- and 48-row workgroups of the row-complete kernel (forced) on the App. E.4 shapes without fine groups and
+    the 7B MLP layers at full size, sampled rows (the last ones included) against the oracle."""
+    _with_env({"FLUXBIN_ROWS": str(rb)}, lambda: _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=spec.M + rb)))
 
 
 @pytest.mark.parametrize("B", [2, 4])
