@@ -218,7 +218,9 @@ static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const f
   }
   if (tu.rows == 0 || tu.rows == 1) return tu.rows == 1;
   const int64_t wgs = ceil_div(L.shape.M, 16);
-  if (wgs <= cus) return L.NSC <= 64 || (L.NSC <= 128 && 4 * wgs <= cus);
+  // up to one 16-row workgroup per CU: App. E.4 4096x11008 (86-97 super-chunks) 2b 10.1 -> 9.3, s8 11.6 -> 10.7, s16
+  // 13.5 -> 11.2 us against the split-tile kernel; 4096x4096 8.2 -> 5.6
+  if (wgs <= cus) return L.NSC <= 128;
   // Two rows per lane where 32-row workgroups fill the CUs once (more than half of them, at most one each) and each
   // workgroup's table work stays small: 8192 x 8192 with 2 bases + 1% (65 super-chunks, 256 workgroups) 12.2 -> 11.0
   // us against the split-tile kernel. With more workgroups than CUs the second workgroups on a CU double its time
