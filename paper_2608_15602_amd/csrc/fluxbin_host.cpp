@@ -231,10 +231,11 @@ static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const f
     *rb = 2;
     return true;
   }
-  // three rows per lane (48-row workgroups) where 32-row ones would be more than the CUs and 48-row ones still keep
-  // three quarters of them busy
+  // three rows per lane (48-row workgroups) where 32-row ones would be more than the CUs, 48-row ones still keep
+  // three quarters of them busy and the super-chunks are few: 11008x4096 (33 super-chunks) 9.5 -> 8.7 us; the fused
+  // 10240x8192 q|k|v layer with 2 bases + 1% (65) was slower, 13.0 -> 13.9
   const int64_t wgs48 = ceil_div(L.shape.M, 48);
-  if (rb2_ok && wgs32 > cus && wgs48 <= cus && 4 * wgs48 > 3 * cus && L.NSC <= 80) {
+  if (rb2_ok && wgs32 > cus && wgs48 <= cus && 4 * wgs48 > 3 * cus && L.NSC <= 48) {
     *rb = 3;
     return true;
   }
