@@ -255,7 +255,12 @@ static bool use_mfma_rows(const fluxbin_layer& L, const Derived& dv, int B, int 
                           int* waves, int* rb) {
   if (tu.mfma_rows == 0 || tu.mfma == 0 || tu.generic) return false;
   const int64_t wgs16 = ceil_div(L.shape.M, 16);
-  if (tu.mfma_rows != 1 && (wgs16 > cus || 2 * wgs16 < cus)) return false;
+  // Taken where 16-row workgroups fill between half and all of the CUs, or where the shape's workgroups are at most
+  // one per CU and the layer has at most 88 super-chunks (B = 2 / 4, µs against the split-tile matrix-core kernel:
+  // 5120x5120 12.9 / 13.0 -> 10.1 / 10.2, 8192x8192 with 2 bases + 1% 16.8 / 17.2 -> 15.6 / 15.6, 1024x8192 11.8 /
+  // 11.8 -> 10.4 / 10.4, 8192x7168 (86 super-chunks) 19.1 / 19.0 -> 17.8 / 17.9; with more workgroups than CUs (11008
+  // rows: 344 of 32 rows) or 98 super-chunks it was slower)
+  const bool fill = wgs16 <= cus && 2 * wgs16 >= cus;
   if (dv.NCP * dv.Mp * 16 >= (int64_t(1) << 31) || dv.NRP * dv.Mp * 2 >= (int64_t(1) << 31)) return false;
   const int bp = B <= 4 ? 4 : 8;
   const int64_t nblk = dv.ncg + (dv.NCP - L.shape.Kb * dv.ncg);
@@ -263,8 +268,9 @@ static bool use_mfma_rows(const fluxbin_layer& L, const Derived& dv, int B, int 
   const int shapes[3][3] = {{16, 1, 1}, {8, 2, 2}, {16, 2, 1}};   // waves, row blocks, workgroups per CU
   for (const auto& sh : shapes) {
     const int64_t stat = int64_t(sh[0]) * sh[1] * 1024 + 2 * 2 * sh[0] * kMrSteps * 4;
-    if (L.NSC <= int64_t(sh[0]) * kMrSteps && (stat + dyn) * sh[2] <= 160 * 1024 &&
-        ceil_div(L.shape.M, 16 * sh[1]) <= int64_t(cus) * sh[2]) {
+    const int64_t wgs = ceil_div(L.shape.M, 16 * sh[1]);
+    if (L.NSC <= int64_t(sh[0]) * kMrSteps && (stat + dyn) * sh[2] <= 160 * 1024 && wgs <= int64_t(cus) * sh[2] &&
+        (tu.mfma_rows == 1 || fill || (wgs <= cus && L.NSC <= 88))) {
       *waves = sh[0];
       *rb = sh[1];
       return true;
