@@ -525,7 +525,11 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p, bool allow_rows
     const int64_t kmin = ceil_div(steps, cap);
     if (kpt < kmin) kpt = kmin;
     if (kpt > steps) kpt = steps;
-    if (tu.align > 0 || p->n_tiles * kpt <= resident) {
+    // batch-1 kernel with more workgroups than CUs and at most three units each: the tiles' parts one unit longer
+    // than the rest then share CUs (App. E.4 5120x13824: 10 tiles of 51 parts, 13.0 / 15.2 / 14.4 us balanced against
+    // 13.9 / 16.0 / 15.3 aligned for 2b / s8 / s16), so the balanced split stays
+    const bool short_parts = p->kernel == 0 && p->n_tiles * kpt > cus && ceil_div(steps, kpt) <= 3;
+    if (tu.align > 0 || (p->n_tiles * kpt <= resident && !short_parts)) {
       p->kpt = int(kpt);
       p->blocks = p->n_tiles * kpt;
     }
