@@ -280,8 +280,8 @@ fluxbin_status fluxbin_set_tuning(const fluxbin_tuning* t);
 /*
  * The launch plan a GEMV/GEMM call of batch B on this layer would use on the current device with the current tuning.
  *   kernel  0: batch-1 super-chunk kernel, 1: generic kernel, 2: LUT batch kernel (mu = 8), 3: matrix-core kernel,
- *           4: row-complete batch-1 kernel (layers with few rows), 5: row-complete matrix-core kernel (layers with few
- *           rows, B = 2..8).
+ *           4: row-complete batch-1 kernel (layers with few rows; rows_per_tile 16, 32 or 48 rows per workgroup),
+ *           5: row-complete matrix-core kernel (layers with few rows, B = 2..8).
  * Batches of more than batch_tile_rows rows (32 on layers the matrix-core kernel takes, else 16) run as batch_tiles
  * launches; the plan is then that of the full batch tiles, and workspace_bytes the call's workspace.
  * workgroups_per_tile > 0: the split-tile kernel's workgroups cover tile-aligned unit ranges, that many per row tile;
