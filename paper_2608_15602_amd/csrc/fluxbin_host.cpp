@@ -188,12 +188,19 @@ static fluxbin_tuning tuning_snapshot() {
 // 91.5 against 47.3 / 47.6; 7B MLP layers (fewer than four 1024-row units per CU, where the LUT batch kernel's
 // 1024-row workgroups do not fill the chip) B = 2 14.8 / 17.7 against 13.8 / 14.9, B = 4 16.4 / 19.3 against 13.9 /
 // 15.0. So mu = 8 uses the LUT batch kernel up to B = 4 on large layers and the matrix cores otherwise; mu = 4 (whose
-// LUT path for B >= 2 is the generic kernel) always the matrix cores. FLUXBIN_MFMA=1 / 0 forces the choice (tests and
-// measurements).
+// LUT path for B >= 2 is the generic kernel) always the matrix cores. The crossover, in 1024-row units U = ceil(M /
+// 1024) x super-chunks, moves with B. At B = 2 the LUT batch kernel wins from U = 650 (us, matrix cores -> LUT batch:
+// 10240x8192 with 2 bases + 1% (U = 650) 19.3 -> 17.3; with 3 bases + 5%: 7168x8192 (686) 20.2 -> 18.1, 8192x7168
+// (688, row-complete matrix cores) 17.9 -> 17.1, 8192x8192 (784) 20.9 -> 19.9, 10240x8192 (980) 23.9 -> 19.6;
+// 4096x11008 with 4 bases (688) 21.0 -> 19.2) and loses up to U = 540 (5120x13824 with 2 bases 18.3 -> 18.6, 8192x8192
+// with 2 bases + 1% (520) 15.9 -> 16.9, 7B MLP (363, 352) 13.7 -> 14.5, 14.3 -> 16.8). At B = 3 and 4 it wins at U =
+// 980 (24.0 -> 22.3, 24.2 -> 22.9) and loses at U = 784 and below (21.3 -> 22.1, 20.9 -> 22.3). Thresholds: U >= 2.25
+// units per CU at B = 2, >= 3.5 at B = 3 and 4. FLUXBIN_MFMA=1 / 0 forces the choice (tests and measurements).
 static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tuning& tu) {
   const int forced = tu.mfma;
   if (forced == 0 || forced == 1) return forced == 1;
-  const bool small = ceil_div(L.shape.M, 1024) * L.NSC < 4 * int64_t(cus);
+  const int quarters = B == 2 ? 9 : 14;   // LUT batch kernel from U >= quarters / 4 units per CU
+  const bool small = 4 * ceil_div(L.shape.M, 1024) * L.NSC < int64_t(quarters) * cus;
   return L.shape.mu == 4 || B > 4 || small;
 }
 
@@ -254,6 +261,7 @@ static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const f
 static bool use_mfma_rows(const fluxbin_layer& L, const Derived& dv, int B, int cus, const fluxbin_tuning& tu,
                           int* waves, int* rb) {
   if (tu.mfma_rows == 0 || tu.mfma == 0 || tu.generic) return false;
+  if (tu.mfma_rows != 1 && !use_mfma(L, B, cus, tu)) return false;   // sizes where the LUT batch kernel is faster
   const int64_t wgs16 = ceil_div(L.shape.M, 16);
   // Taken where 16-row workgroups fill between half and all of the CUs, or where the shape's workgroups are at most
   // one per CU and the layer has at most 88 super-chunks (B = 2 / 4, µs against the split-tile matrix-core kernel:
