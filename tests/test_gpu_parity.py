@@ -182,7 +182,7 @@ def test_config5_layer70b(g_r):
 
 
 def test_fused_decoder_layers_full_size():
-    """The fused launches of the decoder layer (q|k|v as 10240 x 8192, gate|up as 57344 x 8192) at batch 1, 4 and 16,
+    """The fused launches of the decoder layer (q|k|v as 10240 x 8192, gate|up as 57344 x 8192) at batch 1, 2, 4 and 16,
     sampled rows at full size, in the launch configuration the benchmark times."""
     import torch
     from synth import fused_decoder_layers
@@ -191,8 +191,39 @@ def test_fused_decoder_layers_full_size():
             continue
         L = make_layer(spec)
         packed = pack_layer(L)
-        for B in (1, 4, 16):
+        for B in (1, 2, 4, 16):
             _parity(spec, B, rows=sample_rows(spec.M, 128, seed=B), packed=packed, L=L)
+        del packed
+        torch.cuda.empty_cache()
+
+
+def test_small_batch_kernel_choice_by_size():
+    """The default small-batch kernel (mu = 8) moves from the matrix cores to the LUT batch kernel at 2.25 (B = 2) and
+    3.5 (B = 3, 4) 1024-row units per CU, on a 256-CU device: 10240 x 8192 with 3 bases + 5% (980 units) takes the LUT
+    batch kernel at B = 2..4 and the matrix cores at B = 8; 8192 x 8192 with 3 bases + 5% (784) the LUT batch kernel at
+    B = 2 only; 8192 x 7168 (688) the LUT batch kernel at B = 2 and the row-complete matrix-core kernel at B = 3; the 7B
+    gate/up layer (363) the matrix cores. Each choice also runs against the oracle on sampled rows."""
+    import torch
+    from paper_2608_15602_amd import fluxbin as fb
+    from synth import fused_decoder_layers, shard_layers
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("thresholds are stated for a 256-CU device")
+    fused = {s.name: s for s in fused_decoder_layers("128")}
+    c5 = {s.name: s for s in config_layers("c5_layer70b", "128")}
+    down_p4 = [s for s in shard_layers(4, "128") if s.name == "down_p4"][0]
+    gate_up7b = [s for s in config_layers("c3_mlp7b", "128") if s.name == "gate_up"][0]
+    cases = [(fused["3b5pct_qkv"], {2: "lut_batch", 3: "lut_batch", 4: "lut_batch", 8: "mfma"}),
+             (c5["3b5pct_q"], {2: "lut_batch", 3: "mfma", 4: "mfma"}),
+             (down_p4, {2: "lut_batch", 3: "mfma_rows"}),
+             (gate_up7b, {2: "mfma", 4: "mfma"})]
+    for spec, want in cases:
+        L = make_layer(spec)
+        packed = pack_layer(L)
+        for B, kernel in want.items():
+            got = fb.fluxbin_plan_query(packed, B)["kernel_name"]
+            log(f"plan {spec.name} {spec.M}x{spec.N} B={B}: {got}")
+            assert got == kernel, (spec.name, B, got)
+            _parity(spec, B, rows=sample_rows(spec.M, 64, seed=B), packed=packed, L=L)
         del packed
         torch.cuda.empty_cache()
 
