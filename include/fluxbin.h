@@ -213,12 +213,13 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
  * batch_tile_rows.
  * d_x fp16 with row stride ldx >= N (elements); d_y with row stride ldy >= M (elements of the output type). B = 1
  * gives the same result as fluxbin_lut_gemv.
- * Kernels: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4 on layers with at least four
- * 1024-row tiles of super-chunks per CU) and a matrix-core kernel (mu = 4, B > 4, or smaller layers) that decodes the
- * sign bits into fp16 +-alpha_c tiles and multiplies them with the activations on the MFMA units (the products are
- * exact in the fp32 accumulation, as in the LUT path; the row scale is applied per 128-column chunk); on layers of
- * 2048 to 4096 rows (on a 256-CU device) at B <= 8 the matrix-core kernel runs row-complete (every super-chunk of 16
- * rows in one workgroup, no split reduction). Layers with fine row-scale groups (g_r or g_s below 128) run the generic
+ * Kernels: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4 on layers with at least 2.25 (B = 2)
+ * or 3.5 (B = 3, 4) 1024-row tiles of super-chunks per CU) and a matrix-core kernel (mu = 4, B > 4, or smaller
+ * layers) that decodes the sign bits into fp16 +-alpha_c tiles and multiplies them with the activations on the MFMA
+ * units (the products are exact in the fp32 accumulation, as in the LUT path; the row scale is applied per 128-column
+ * chunk); on layers of 2048 to 4096 rows, or of at most 8192 rows with at most 88 super-chunks (on a 256-CU device),
+ * at B <= 8 the matrix-core kernel runs row-complete (every super-chunk of 16 or 32 rows in one workgroup, no split
+ * reduction). Layers with fine row-scale groups (g_r or g_s below 128) run the generic
  * LUT kernel for B >= 2. All are deterministic; their results differ only by fp32 summation order.
  */
 fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx,
