@@ -258,8 +258,8 @@ fluxbin_status fluxbin_lut_gemv_noalloc(const fluxbin_layer* layer, const uint16
  *   mfma_r2        FLUXBIN_MFMA_R2        0: matrix-core split tiles reduced by tile counters, not a second kernel
  *   bat_r2         FLUXBIN_BAT_R2         0: LUT batch kernel split tiles reduced by tile counters
  *   rows           FLUXBIN_ROWS           batch 1: 1 the row-complete kernel where the layer allows it, 0 never;
- *                                         2 / 3 its 32- / 48-row workgroups (two / three rows per lane; mu = 8 without
- *                                         fine row-scale groups); -1: chosen by layer size
+ *                                         2 / 3 its 32- / 48-row workgroups (two / three rows per lane; mu = 8, on
+ *                                         layers the kernel takes); -1: chosen by layer size
  *   batch_tile     FLUXBIN_BATCH_TILE     16: batch tiles of 16 rows on every layer; 0: 32 where the matrix-core
  *                                         kernel takes the layer
  *   mfma_rows      FLUXBIN_MFMA_ROWS      B = 2..8: 1 the row-complete matrix-core kernel wherever it fits, 0 never;

@@ -222,12 +222,12 @@ struct RwKernel {
 };
 
 // RB > 1: each lane also handles the rows 16, 32 further (16 RB rows per workgroup, the tables of a unit serving RB
-// times the rows); mu = 8 without fine groups only, where those rows' table columns are the first row's (rotation 2i
-// mod 32).
+// times the rows); mu = 8 only, where those rows' table columns are the first row's: the rotation 2i is the same mod
+// 32, and a fine chunk's stored byte order (colf) depends on i mod 16 only.
 template <int MU, int W, int D, int FG, int RB>
 __global__ void __launch_bounds__(64 * W) k_gemv_rows(GemmArgs a) {
   static_assert(FG == 0 || MU == 8, "fine row-scale groups: mu = 8 only");
-  static_assert(RB == 1 || ((RB == 2 || RB == 3) && MU == 8 && FG == 0), "several rows per lane: mu = 8, no fine groups");
+  static_assert(RB == 1 || ((RB == 2 || RB == 3) && MU == 8), "several rows per lane: mu = 8");
   constexpr int NT = 64 * W;
   constexpr int ROWS = kRwRows * RB;
   extern __shared__ __attribute__((aligned(16))) uint16_t xl[];   // x: N fp16 (dynamic size, at most kRwMaxN)
@@ -357,13 +357,18 @@ template <int W, int D>
 bool launch_rows_wd(const GemmArgs& a, int mu, int fg, int rb, hipStream_t stream) {
   const dim3 grid(unsigned((a.M + kRwRows * rb - 1) / (kRwRows * rb))), block(64 * W);
   const unsigned xl_bytes = unsigned(((a.N + 1) * 2 + 15) & ~15);   // x and one zero entry
-  if (rb == 2 || rb == 3) {   // launch plan: mu = 8 without fine groups, 16 wavefronts, two units ahead
+  if (rb == 2 || rb == 3) {   // launch plan: mu = 8, 16 wavefronts, two units ahead
     if constexpr (W == 16 && D == 2) {
-      if (mu != 8 || fg != 0) return false;
-      if (rb == 2)
-        hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0, 2>), grid, block, xl_bytes, stream, a);
-      else
-        hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0, 3>), grid, block, xl_bytes, stream, a);
+      if (mu != 8 || (fg != 0 && fg != 8 && fg != 16)) return false;
+      if (rb == 2) {
+        if (fg == 0) hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0, 2>), grid, block, xl_bytes, stream, a);
+        if (fg == 8) hipLaunchKernelGGL((k_gemv_rows<8, W, D, 8, 2>), grid, block, xl_bytes, stream, a);
+        if (fg == 16) hipLaunchKernelGGL((k_gemv_rows<8, W, D, 16, 2>), grid, block, xl_bytes, stream, a);
+      } else {
+        if (fg == 0) hipLaunchKernelGGL((k_gemv_rows<8, W, D, 0, 3>), grid, block, xl_bytes, stream, a);
+        if (fg == 8) hipLaunchKernelGGL((k_gemv_rows<8, W, D, 8, 3>), grid, block, xl_bytes, stream, a);
+        if (fg == 16) hipLaunchKernelGGL((k_gemv_rows<8, W, D, 16, 3>), grid, block, xl_bytes, stream, a);
+      }
       return true;
     }
     return false;

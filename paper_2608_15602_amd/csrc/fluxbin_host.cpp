@@ -211,14 +211,14 @@ static bool use_mfma(const fluxbin_layer& L, int B, int cus, const fluxbin_tunin
 // attention 4096x4096 (2+1, 2%) 8.26 -> 5.98, 2048x4096 7.79 -> 5.31, 3072x4096 3+1 (49 super-chunks) 8.40 -> 7.00,
 // 1024x8192 2+1 (65) 8.36 -> 7.20, 1024x8192 3+1 (98) 9.35 -> 9.05; even or slower with more super-chunks per
 // wavefront: 4096x11008 2b (86) 9.47 -> 9.68. FLUXBIN_ROWS=1 / 0 forces the choice where the layer allows it.
-// *rb: rows per lane, 1 (16 rows per workgroup), 2 or 3 (32 or 48 rows; mu = 8 without fine groups).
+// *rb: rows per lane, 1 (16 rows per workgroup), 2 or 3 (32 or 48 rows; mu = 8).
 static bool use_rows(const fluxbin_layer& L, const Derived& dv, int cus, const fluxbin_tuning& tu, int* rb) {
   const bool fine_ok = dv.Gcg == 1 && (dv.Gcs == 1 || (L.shape.mu == 8 && (dv.Gcs == 8 || dv.Gcs == 16)));
   *rb = 1;
   if (!fine_ok || L.shape.N > kRwMaxN || L.NSC > 8 * kRwSteps) return false;
   // its buffer loads take 32-bit offsets into the sign and row-scale sections
   if (dv.NCP * dv.Mp * 16 >= (int64_t(1) << 31) || dv.NRP * dv.Mp * 2 >= (int64_t(1) << 31)) return false;
-  const bool rb2_ok = L.shape.mu == 8 && dv.Gcg == 1 && dv.Gcs == 1;
+  const bool rb2_ok = L.shape.mu == 8;   // with coarse row scales or 8 / 16 fine groups per salient chunk (fine_ok)
   if (tu.rows == 2 || tu.rows == 3) {
     *rb = tu.rows;
     return rb2_ok;

@@ -393,10 +393,13 @@ def test_rows_kernel_full_size(spec):
     _with_env({"FLUXBIN_ROWS": "1"}, lambda: _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=spec.M)))
 
 
-ROWS32_SPECS = [s for s in ROWS_SPECS if s.mu == 8 and "-s" not in s.name] + [
+ROWS32_SPECS = [s for s in ROWS_SPECS if s.mu == 8] + [
     LayerSpec("rows32_one_row", M=1, N=256, Kb=2, Ks=1, mu=8, S=20, g_r=128, g_s=20, seed=69),
     LayerSpec("rows32_17_rows", M=17, N=640, Kb=1, Ks=1, mu=8, S=200, g_r=640, g_s=200, seed=70),
     LayerSpec("rows32_ragged_47", M=47, N=1300, Kb=3, Ks=0, mu=8, S=0, g_r=128, g_s=1, seed=71),
+    # fine salient groups on rows 16 and 32 apart (same stored byte order), M across and past 48-row workgroups
+    paper_config("rows32_2b-s16_ragged_101", 101, 700, 2, 16, 128, seed=73),
+    paper_config("rows32_3b-s8_ragged_50", 50, 2304, 3, 8, 128, seed=74),
 ]
 
 
@@ -404,9 +407,9 @@ ROWS32_SPECS = [s for s in ROWS_SPECS if s.mu == 8 and "-s" not in s.name] + [
 @pytest.mark.parametrize("spec", ROWS32_SPECS, ids=lambda s: s.name)
 def test_rows_kernel_32_rows_matches_oracle(spec, rb):
     """The row-complete kernel's 32- and 48-row workgroups (two or three rows per lane, forced) on every row: ragged M
-    below, across and above them (48-row workgroups past the padded rows), salient chunks or none, wide N;
-    deterministic, the plan reports it; and a mu = 4 or fine-group layer, which it does not take, keeps another
-    kernel."""
+    below, across and above them (48-row workgroups past the padded rows), salient chunks or none, coarse or 8 / 16
+    fine salient row-scale groups, wide N; deterministic, the plan reports it; and a mu = 4 layer, which it does not
+    take, keeps another kernel."""
     from paper_2608_15602_amd import fluxbin as fb
     L = make_layer(spec)
     packed = pack_layer(L)
@@ -420,11 +423,10 @@ def test_rows_kernel_32_rows_matches_oracle(spec, rb):
         assert fb.fluxbin_plan_query(pack_layer(make_layer(other)), 1)["kernel_name"] != "rows"
 
 
-@pytest.mark.parametrize("spec", [s for s in kernel_latency_layers() + config_layers("c3_mlp7b", "128")
-                                  if "-s" not in s.name], ids=lambda s: s.name)
+@pytest.mark.parametrize("spec", kernel_latency_layers() + config_layers("c3_mlp7b", "128"), ids=lambda s: s.name)
 @pytest.mark.parametrize("rb", [2, 3])
 def test_rows_kernel_32_rows_full_size(spec, rb):
-    """The 32- and 48-row workgroups of the row-complete kernel (forced) on the App. E.4 shapes without fine groups and
+    """The 32- and 48-row workgroups of the row-complete kernel (forced) on the App. E.4 shapes (2b, s8, s16, 4b) and
     the 7B MLP layers at full size, sampled rows (the last ones included) against the oracle."""
     _with_env({"FLUXBIN_ROWS": str(rb)}, lambda: _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=spec.M + rb)))
 
