@@ -209,8 +209,9 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
  * and uses it for all its rows (batch-independent reuse of the weights, Sec. 3.2 and App. E.2); larger batches run as
  * consecutive launches of T-row batch tiles (the last with the remaining rows), each its own launch plan, one after
  * another on the stream and sharing the workspace, so rows Tt..Tt+T-1 give the same y as a call on those rows alone.
- * T = 32 on layers with one row scale per chunk (matrix-core kernel), else 16. fluxbin_plan_query reports T as
- * batch_tile_rows.
+ * T = 32 on layers with one row scale per chunk (matrix-core kernel), else 16; T = 1 (B launches of the batch-1
+ * kernels) for B <= 8 on mu = 8 layers with 8 or 16 fine salient row-scale groups per chunk (the s16 / s8
+ * configurations), unless the batch_tile tuning asks for 16. fluxbin_plan_query reports T as batch_tile_rows.
  * d_x fp16 with row stride ldx >= N (elements); d_y with row stride ldy >= M (elements of the output type). B = 1
  * gives the same result as fluxbin_lut_gemv.
  * Kernels: the LUT batch kernel (one set of tables per batch row; mu = 8, B <= 4 on layers with at least 2.25 (B = 2)
@@ -219,8 +220,8 @@ fluxbin_status fluxbin_lut_gemv(const fluxbin_layer* layer, const uint16_t* d_x,
  * units (the products are exact in the fp32 accumulation, as in the LUT path; the row scale is applied per 128-column
  * chunk); on layers of 2048 to 4096 rows, or of at most 8192 rows with at most 88 super-chunks (on a 256-CU device),
  * at B <= 8 the matrix-core kernel runs row-complete (every super-chunk of 16 or 32 rows in one workgroup, no split
- * reduction). Layers with fine row-scale groups (g_r or g_s below 128) run the generic
- * LUT kernel for B >= 2. All are deterministic; their results differ only by fp32 summation order.
+ * reduction). Other layers with fine row-scale groups (g_r or g_s below 128), and those above at B > 8, run the
+ * generic LUT kernel for B >= 2. All are deterministic; their results differ only by fp32 summation order.
  */
 fluxbin_status fluxbin_lut_gemm_smallbatch(const fluxbin_layer* layer, int32_t B, const uint16_t* d_x, int64_t ldx,
                                            void* d_y, int64_t ldy, int32_t y_is_fp32, void* d_workspace,

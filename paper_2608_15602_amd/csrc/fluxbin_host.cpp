@@ -292,10 +292,16 @@ static uint64_t layer_counter_bytes(int64_t M) {
 }
 
 // Rows of a full batch tile (calls with more batch rows run as several launches): 32 on layers the matrix-core kernel
-// takes (one row scale per chunk), whose sign decode then serves two 16-row MFMA tiles, else 16.
-// FLUXBIN_BATCH_TILE=16 keeps 16-row tiles.
-static int batch_tile_rows(const fluxbin_layer& L, const fluxbin_tuning& tu) {
+// takes (one row scale per chunk), whose sign decode then serves two 16-row MFMA tiles, else 16. Layers with 8 or 16
+// fine salient row-scale groups at mu = 8 (the paper's s16 / s8 configurations), which only the generic kernel takes at
+// B >= 2, run B <= 8 rows as B launches of the batch-1 kernels instead: faster on all eight App. E.4 s8 / s16 layers
+// at B = 2, 4 and 8 (us per call, generic kernel -> per-row batch-1 launches: 4096x4096 s8 B = 2 15.1 -> 12.1, B = 8
+// 59.5 -> 46.4; 5120x13824 s8 B = 2 55.7 -> 30.1, B = 8 139.5 -> 115.3). FLUXBIN_BATCH_TILE=16 keeps 16-row tiles.
+static int batch_tile_rows(const fluxbin_layer& L, const fluxbin_tuning& tu, int B) {
   const Derived dv = derive(L.shape);
+  if (!tu.generic && tu.batch_tile != kMaxBatch && B <= 8 && L.shape.mu == 8 && dv.Gcg == 1 &&
+      (dv.Gcs == 8 || dv.Gcs == 16))
+    return 1;
   if (tu.generic || dv.Gcg > 1 || dv.Gcs > 1 || tu.mfma == 0 || tu.mfma_depth == 3 || tu.mfma_r2 == 0 ||
       tu.batch_tile == kMaxBatch)
     return kMaxBatch;
@@ -307,7 +313,7 @@ fluxbin_status make_plan(const fluxbin_layer& L, int B, Plan* p, bool allow_rows
   if (cus <= 0) return fail(FLUXBIN_ERR_HIP, "cannot query the current HIP device");
   std::memset(p, 0, sizeof(*p));
   const fluxbin_tuning tu = tuning_snapshot();
-  if (B < 1 || (B > kMaxBatch && batch_tile_rows(L, tu) < B))
+  if (B < 1 || (B > kMaxBatch && batch_tile_rows(L, tu, B) < B))
     return fail(FLUXBIN_ERR_UNSUPPORTED, "no launch plan for %d batch rows in one launch on this layer", B);
   const int force_generic = tu.generic;
   const int rpt_env = tu.rpt;
@@ -753,7 +759,7 @@ fluxbin_status fluxbin_workspace_query(const fluxbin_layer* layer, int32_t B, si
   if (!bytes) return fail(FLUXBIN_ERR_INVALID_ARG, "bytes is NULL");
   if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
   BatchTiles bt;
-  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot()), &bt);
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot(), B), &bt);
   if (st != FLUXBIN_OK) return st;
   *bytes = static_cast<size_t>(bt.ws_bytes);
   return FLUXBIN_OK;
@@ -781,7 +787,7 @@ static fluxbin_status gemm_common(const fluxbin_layer* layer, int32_t B, const u
   const size_t yb = (size_t(B - 1) * ldy + s.M) * (y_is_fp32 ? 4 : 2);
   if (ranges_overlap(d_x, xb, d_y, yb)) return fail(FLUXBIN_ERR_INVALID_ARG, "x and y overlap");
   BatchTiles bt;
-  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot()), &bt);
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot(), B), &bt);
   if (st != FLUXBIN_OK) return st;
   if (!d_ws) return fail(FLUXBIN_ERR_INVALID_ARG, "workspace is NULL");
   if (ws_bytes < bt.ws_bytes)
@@ -884,7 +890,7 @@ fluxbin_status fluxbin_plan_query(const fluxbin_layer* layer, int32_t B, fluxbin
   if (!out) return fail(FLUXBIN_ERR_INVALID_ARG, "out is NULL");
   if (B < 1 || B > kMaxBatchCall) return fail(FLUXBIN_ERR_INVALID_ARG, "B = %d out of range [1, %d]", B, kMaxBatchCall);
   BatchTiles bt;
-  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot()), &bt);
+  st = batch_tiles(*layer, B, batch_tile_rows(*layer, tuning_snapshot(), B), &bt);
   if (st != FLUXBIN_OK) return st;
   const Plan& p = bt.n_full > 0 ? bt.full : bt.tail;
   std::memset(out, 0, sizeof(*out));

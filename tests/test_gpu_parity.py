@@ -431,11 +431,31 @@ def test_rows_kernel_32_rows_full_size(spec, rb):
     _with_env({"FLUXBIN_ROWS": str(rb)}, lambda: _parity(spec, 1, rows=sample_rows(spec.M, 256, seed=spec.M + rb)))
 
 
-@pytest.mark.parametrize("B", [2, 4])
-def test_paper_config_small_batch(B):
-    """A paper-configuration layer (fine salient row-scale groups) at small batch: the generic kernel."""
-    spec = paper_config("2b-s8-g128_small", 1536, 2048, 2, 8, 128)
-    _parity(spec, B, out_fp32=True)
+@pytest.mark.parametrize("B", [2, 4, 8])
+@pytest.mark.parametrize("spec", [paper_config("2b-s8-g128_small", 1536, 2048, 2, 8, 128),
+                                  paper_config("3b-s16-g128_ragged", 1000, 1100, 3, 16, 128, seed=9)],
+                         ids=lambda s: s.name)
+def test_paper_config_small_batch(spec, B):
+    """Paper-configuration layers (8 or 16 fine salient row-scale groups per chunk) at B <= 8: B launches of the batch-1
+    kernels (the plan reports one-row batch tiles), every row against the oracle, and within tolerance of the generic
+    kernel that 16-row tiles run (FLUXBIN_BATCH_TILE=16)."""
+    from paper_2608_15602_amd import fluxbin as fb
+    L = make_layer(spec)
+    packed = pack_layer(L)
+    info = fb.fluxbin_plan_query(packed, B)
+    assert (info["batch_tile_rows"], info["batch_tiles"]) == (1, B), info
+    assert info["kernel_name"] in ("batch1", "rows"), info
+    _, _, x, y = _parity(spec, B, out_fp32=True, packed=packed, L=L)
+    env = {"FLUXBIN_BATCH_TILE": "16"}
+    assert _with_env(env, lambda: fb.fluxbin_plan_query(packed, B))["kernel_name"] == "generic"
+    _check(y, _with_env(env, lambda: run_gemm(packed, x, out_fp32=True)), "per-row batch-1 launches vs generic kernel")
+
+
+def test_paper_config_small_batch_full_size():
+    """The App. E.4 5120 x 13824 s8 and s16 layers at B = 3 (three batch-1 launches), sampled rows at full size."""
+    for spec in kernel_latency_layers():
+        if spec.M == 5120 and spec.N == 13824 and "-s" in spec.name:
+            _parity(spec, 3, rows=sample_rows(spec.M, 128, seed=3))
 
 
 @pytest.mark.parametrize("spec", [
